@@ -1,0 +1,252 @@
+"""Plain CPU oracle for HTAM's hierarchical transition-attended retrieval.
+
+TEST INFRASTRUCTURE ONLY: only ``tests/``, ``__graft_entry__.smoke()`` and the
+CPU-baseline leg of ``bench.py`` may import this package. The GPU library never
+calls it, and it shares no code with the GPU library.
+
+The arithmetic lives in ``htam_oracle.c`` (fp64, OpenMP over rows); this module
+loads it with ctypes and composes its steps in the order the paper gives them
+(arXiv 2605.29734, Sec. 4.3 and Alg. 1):
+
+  O0  bf16 operand quantisation when the bank computes in bf16;
+  O1  coarse scores <q, c_g>          (Eq. score with a one-term prefix and the
+                                       linear scorer of App. B.6);
+  O2  top-c clusters, ties to the lower id (greedy limit of Eq. global direction);
+  O3  candidates = the selected clusters' segments (Eq. local nodes);
+  O4  fine scores <q, k_j>            (Eq. local policy with an inner product);
+  O5  temperature softmax over the candidates;
+  O6  top-k by (-score, caller id), padded with (-1, -inf, 0).
+
+Every result here is computed in double from the stored fp32 / bf16 values.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "htam_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+
+def build(force: bool = False) -> str:
+    """Compile the C oracle with gcc (OpenMP) into oracle/liboracle.so."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp"
+        subprocess.check_call(["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-std=c11",
+                               "-o", tmp, _SRC, "-lm"])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        build()
+        lib = ctypes.CDLL(_LIB)
+        P = ctypes.c_void_p
+        i32, i64, f64 = ctypes.c_int32, ctypes.c_int64, ctypes.c_double
+        lib.htam_oracle_round_bf16.argtypes = [P, P, i64]
+        lib.htam_oracle_scores.argtypes = [i32, i64, i32, P, P, P]
+        lib.htam_oracle_coarse.argtypes = [i32, i32, i32, P, P, i32, P, P]
+        lib.htam_oracle_attend.argtypes = [i64, P, P, f64, i32, P, P, P, P, P, P]
+        lib.htam_oracle_attend_rows.argtypes = [i64, P, P, P, f64, i32, P, P, P, P, P]
+        lib.htam_oracle_build.argtypes = [i64, i32, P, P, P]
+        lib.htam_oracle_build.restype = ctypes.c_int
+        _lib = lib
+    return _lib
+
+
+def _p(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _f32(a) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(a, dtype=np.float32))
+
+
+# ---------------------------------------------------------------------------
+# single steps
+# ---------------------------------------------------------------------------
+def round_bf16(x) -> np.ndarray:
+    """O0: fp32 -> bf16 (round to nearest, ties to even), returned as fp32 values."""
+    x = _f32(x)
+    y = np.empty_like(x)
+    _load().htam_oracle_round_bf16(_p(x), _p(y), x.size)
+    return y
+
+
+def scores(q, k) -> np.ndarray:
+    """O1/O4: double inner products, out[i][j] = <q_i, k_j>."""
+    q, k = _f32(q), _f32(k)
+    nq, d = q.shape
+    nk = k.shape[0]
+    out = np.empty((nq, nk), dtype=np.float64)
+    if nq and nk:
+        _load().htam_oracle_scores(nq, nk, d, _p(q), _p(k), _p(out))
+    return out
+
+
+def coarse(q, c, top_c: int):
+    """O1 + O2: the top_c clusters per query by (-score, cluster id)."""
+    q, c = _f32(q), _f32(c)
+    B, d = q.shape
+    G = c.shape[0]
+    sel = np.empty((B, top_c), dtype=np.int32)
+    sel_score = np.empty((B, top_c), dtype=np.float64)
+    if B:
+        _load().htam_oracle_coarse(B, G, d, _p(q), _p(c), top_c, _p(sel), _p(sel_score))
+    return sel, sel_score
+
+
+def attend(s, ids, tau: float, top_k: int, full_weights: bool = False) -> dict:
+    """O5 + O6 over one candidate set (scores s, caller ids)."""
+    s = np.ascontiguousarray(np.asarray(s, dtype=np.float64))
+    ids = np.ascontiguousarray(np.asarray(ids, dtype=np.int32))
+    n = s.size
+    out_id = np.empty(top_k, dtype=np.int32)
+    out_s = np.empty(top_k, dtype=np.float64)
+    out_w = np.empty(top_k, dtype=np.float64)
+    m = np.zeros(1, dtype=np.float64)
+    Z = np.zeros(1, dtype=np.float64)
+    w_full = np.empty(max(n, 1), dtype=np.float64) if full_weights else None
+    _load().htam_oracle_attend(n, _p(s), _p(ids), float(tau), top_k, _p(out_id), _p(out_s),
+                               _p(out_w), _p(m), _p(Z),
+                               _p(w_full) if full_weights else None)
+    r = dict(id=out_id, score=out_s, weight=out_w, m=float(m[0]), Z=float(Z[0]),
+             count=min(top_k, n))
+    if full_weights:
+        r["w_full"] = w_full[:n]
+    return r
+
+
+def attend_rows(offsets, s, ids, tau: float, top_k: int) -> dict:
+    """O5 + O6 over many independent candidate sets (rows r = s[off[r]:off[r+1]])."""
+    off = np.ascontiguousarray(np.asarray(offsets, dtype=np.int64))
+    s = np.ascontiguousarray(np.asarray(s, dtype=np.float64))
+    ids = np.ascontiguousarray(np.asarray(ids, dtype=np.int32))
+    rows = off.size - 1
+    out_id = np.empty((rows, top_k), dtype=np.int32)
+    out_s = np.empty((rows, top_k), dtype=np.float64)
+    out_w = np.empty((rows, top_k), dtype=np.float64)
+    m = np.empty(rows, dtype=np.float64)
+    Z = np.empty(rows, dtype=np.float64)
+    if rows:
+        _load().htam_oracle_attend_rows(rows, _p(off), _p(s), _p(ids), float(tau), top_k,
+                                        _p(out_id), _p(out_s), _p(out_w), _p(m), _p(Z))
+    count = np.minimum(np.diff(off), top_k).astype(np.int32)
+    return dict(id=out_id, score=out_s, weight=out_w, m=m, Z=Z, count=count)
+
+
+def build_bank(cluster_of, n_clusters: int):
+    """Memory build: stable counting sort of records by parent cluster.
+
+    Returns (seg_offsets int64 [G+1], transition_id int32 [N]).
+    """
+    cl = np.ascontiguousarray(np.asarray(cluster_of, dtype=np.int32))
+    off = np.empty(n_clusters + 1, dtype=np.int64)
+    tid = np.empty(cl.size, dtype=np.int32)
+    rc = _load().htam_oracle_build(cl.size, n_clusters, _p(cl), _p(off), _p(tid))
+    if rc != 0:
+        raise ValueError("cluster id out of range")
+    return off, tid
+
+
+# ---------------------------------------------------------------------------
+# the whole retrieval, composed in the paper's order
+# ---------------------------------------------------------------------------
+def retrieve(q, c, seg_offsets, top_c: int, top_k: int, tau: float, compute: str,
+             fetch_keys=None, keys=None, transition_id=None, sel=None, rows=None,
+             chunk_rows: int = 65536) -> dict:
+    """Hierarchical retrieval for the queries ``rows`` (default: all).
+
+    q [B][d], c [G][d]: stored query / coarse-key values (fp32 arrays; bf16
+    storage is passed widened to fp32, which is exact).
+    seg_offsets [G+1]: segment bounds of the segment-contiguous bank.
+    keys [N][d] or fetch_keys(start, stop) -> fp32 array [stop-start][d]: the
+    bank rows (the callback lets a caller stream a large bank cluster by cluster).
+    transition_id [N]: bank position -> caller id (None = identity).
+    compute: "f32" or "bf16" (O0 applies to q, c and the keys for "bf16").
+    sel: if given ([len(rows)][top_c]), the coarse selection to use instead of
+    the oracle's own O2 (used to check a fine stage on another implementation's
+    selection); the oracle's own selection is returned too.
+
+    Returns per-row outputs (id, score, weight, m, Z, count) over the union of
+    the selected segments, and per-slot outputs (slot_m, slot_Z, slot_id,
+    slot_score, slot_count) over each selected segment alone.
+    """
+    q = _f32(q)
+    c = _f32(c)
+    off = np.asarray(seg_offsets, dtype=np.int64)
+    if rows is None:
+        rows = np.arange(q.shape[0])
+    rows = np.asarray(rows, dtype=np.int64)
+    if compute == "bf16":
+        quant = round_bf16
+    elif compute == "f32":
+        def quant(x):
+            return _f32(x)
+    else:
+        raise ValueError(compute)
+    if fetch_keys is None:
+        kk = _f32(keys)
+
+        def fetch_keys(a, b):
+            return kk[a:b]
+
+    qh = quant(q[rows])
+    ch = quant(c)
+    own_sel, own_sel_score = coarse(qh, ch, top_c)                    # O1, O2
+    use_sel = own_sel if sel is None else np.asarray(sel, dtype=np.int32)
+    R = rows.size
+
+    # O3 + O4, cluster-major so that a large bank is streamed once.
+    slot_s = [[None] * top_c for _ in range(R)]
+    slot_ids = [[None] * top_c for _ in range(R)]
+    users = {}
+    for r in range(R):
+        for j in range(top_c):
+            users.setdefault(int(use_sel[r, j]), []).append((r, j))
+    for g, lst in users.items():
+        a, b = int(off[g]), int(off[g + 1])
+        rr = np.array([u[0] for u in lst], dtype=np.int64)
+        parts = []
+        for s0 in range(a, b, chunk_rows):
+            s1 = min(b, s0 + chunk_rows)
+            kh = quant(fetch_keys(s0, s1))
+            parts.append(scores(qh[rr], kh))
+        sc = np.concatenate(parts, axis=1) if parts else np.zeros((rr.size, 0))
+        ids = (np.arange(a, b, dtype=np.int64) if transition_id is None
+               else np.asarray(transition_id[a:b], dtype=np.int64)).astype(np.int32)
+        for t, (r, j) in enumerate(lst):
+            slot_s[r][j] = sc[t]
+            slot_ids[r][j] = ids
+
+    # O5 + O6 per slot (one selected segment) and per row (union of segments).
+    def pack(seq_s, seq_i):
+        lens = [x.size for x in seq_s]
+        o = np.zeros(len(lens) + 1, dtype=np.int64)
+        o[1:] = np.cumsum(lens)
+        s_all = np.concatenate(seq_s) if seq_s else np.zeros(0)
+        i_all = np.concatenate(seq_i) if seq_i else np.zeros(0, dtype=np.int32)
+        return o, s_all, i_all
+
+    o, s_all, i_all = pack([slot_s[r][j] for r in range(R) for j in range(top_c)],
+                           [slot_ids[r][j] for r in range(R) for j in range(top_c)])
+    per_slot = attend_rows(o, s_all, i_all, tau, top_k)
+    o, s_all, i_all = pack([np.concatenate(slot_s[r]) for r in range(R)],
+                           [np.concatenate(slot_ids[r]) for r in range(R)])
+    per_row = attend_rows(o, s_all, i_all, tau, top_k)
+
+    out = dict(rows=rows, sel=use_sel, own_sel=own_sel, own_sel_score=own_sel_score,
+               slot_m=per_slot["m"].reshape(R, top_c), slot_Z=per_slot["Z"].reshape(R, top_c),
+               slot_id=per_slot["id"].reshape(R, top_c, top_k),
+               slot_score=per_slot["score"].reshape(R, top_c, top_k),
+               slot_count=per_slot["count"].reshape(R, top_c))
+    out.update(per_row)
+    out["qh"] = qh
+    return out

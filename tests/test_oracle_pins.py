@@ -1,0 +1,358 @@
+"""Pins of the CPU oracle against facts that do not come from the oracle itself.
+
+Each test fixes the oracle to something independent: a hand-derived worked
+example, closed forms of the temperature softmax, a brute-force flat retrieval
+(the top_c = G special case, computed with numpy's own sort), numpy's stable
+argsort for the memory build, bit-level bf16 rounding cases, torch's bf16
+conversion, planted matches and invariances. A plausible slip in the oracle
+(a dropped term, a wrong sign or index, a transposed operand, a missing mask)
+fails at least one of them.
+"""
+import json
+import math
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _num(x):
+    if isinstance(x, str):
+        if x == "-inf":
+            return -math.inf
+        return float(Fraction(x))
+    return float(x)
+
+
+def _arr(x):
+    return np.vectorize(_num, otypes=[np.float64])(np.array(x, dtype=object))
+
+
+def _unit(rng, n, d):
+    x = rng.standard_normal((n, d))
+    return (x / np.linalg.norm(x, axis=1, keepdims=True)).astype(np.float32)
+
+
+def _bank(rng, G, sizes, d):
+    """Random segment-contiguous bank: offsets, keys, and shuffled caller ids."""
+    off = np.zeros(G + 1, dtype=np.int64)
+    off[1:] = np.cumsum(sizes)
+    N = int(off[-1])
+    keys = _unit(rng, N, d) if N else np.zeros((0, d), np.float32)
+    tid = rng.permutation(N).astype(np.int32)
+    return off, keys, tid
+
+
+# ---------------------------------------------------------------------------
+# hand-derived worked example (tests/golden/worked_example.json)
+# ---------------------------------------------------------------------------
+def test_worked_example_exact():
+    ex = json.load(open(os.path.join(GOLDEN, "worked_example.json")))
+    G = len(ex["coarse_keys"])
+    off, tid = oracle.build_bank(ex["cluster_of"], G)
+    keys = np.asarray(ex["keys"], np.float32)[tid]
+    r = oracle.retrieve(np.asarray(ex["queries"], np.float32), np.asarray(ex["coarse_keys"], np.float32),
+                        off, ex["top_c"], ex["top_k"], ex["tau"], "f32", keys=keys,
+                        transition_id=tid)
+    e = ex["expect"]
+    np.testing.assert_array_equal(r["own_sel"], e["sel"])
+    np.testing.assert_allclose(r["own_sel_score"], _arr(e["sel_score"]), rtol=0, atol=1e-12)
+    np.testing.assert_array_equal(r["id"], e["id"])
+    np.testing.assert_allclose(r["score"], _arr(e["score"]), rtol=0, atol=1e-12)
+    np.testing.assert_allclose(r["weight"], _arr(e["weight"]), rtol=1e-12, atol=1e-15)
+    np.testing.assert_allclose(r["m"], _arr(e["m"]), rtol=0, atol=1e-12)
+    np.testing.assert_allclose(r["Z"], _arr(e["Z"]), rtol=1e-12)
+    np.testing.assert_array_equal(r["count"], e["count"])
+    np.testing.assert_array_equal(r["slot_id"], e["slot_id"])
+    np.testing.assert_allclose(r["slot_score"], _arr(e["slot_score"]), rtol=0, atol=1e-12)
+    np.testing.assert_allclose(r["slot_m"], _arr(e["slot_m"]), rtol=0, atol=1e-12)
+    np.testing.assert_allclose(r["slot_Z"], _arr(e["slot_Z"]), rtol=1e-12)
+
+
+# ---------------------------------------------------------------------------
+# O0: bf16 rounding
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("bits,expect", [
+    (0x3F800000, 0x3F800000),   # exact
+    (0x3F808000, 0x3F800000),   # halfway, even below -> down
+    (0x3F818000, 0x3F820000),   # halfway, odd below -> up
+    (0x3F808001, 0x3F810000),   # above halfway -> up
+    (0x3F807FFF, 0x3F800000),   # below halfway -> down
+    (0xBF818000, 0xBF820000),   # negative, halfway, odd -> away from zero
+    (0xBF808000, 0xBF800000),   # negative, halfway, even -> toward zero
+    (0x7F7FFFFF, 0x7F800000),   # largest float rounds to +inf
+    (0x00008000, 0x00000000),   # subnormal halfway, even -> zero
+    (0x00018000, 0x00020000),   # subnormal halfway, odd -> up
+    (0x80000000, 0x80000000),   # -0 stays -0
+])
+def test_bf16_rounding_bits(bits, expect):
+    x = np.array([bits], dtype=np.uint32).view(np.float32)
+    y = oracle.round_bf16(x).view(np.uint32)[0]
+    assert int(y) == expect, f"{bits:#x} -> {int(y):#x}, expected {expect:#x}"
+
+
+def test_bf16_rounding_matches_torch():
+    rng = np.random.default_rng(1)
+    x = (rng.standard_normal(1 << 16) * np.exp2(rng.integers(-20, 20, 1 << 16))).astype(np.float32)
+    ref = torch.from_numpy(x).to(torch.bfloat16).to(torch.float32).numpy()
+    np.testing.assert_array_equal(oracle.round_bf16(x).view(np.uint32), ref.view(np.uint32))
+
+
+# ---------------------------------------------------------------------------
+# O1 + O2: coarse selection
+# ---------------------------------------------------------------------------
+def test_coarse_matches_full_sort():
+    rng = np.random.default_rng(2)
+    B, G, d, c = 9, 37, 24, 5
+    q, C = _unit(rng, B, d), _unit(rng, G, d)
+    C[7] = C[3]                       # exact duplicate keys -> exact ties
+    sel, sc = oracle.coarse(q, C, c)
+    S = q.astype(np.float64) @ C.astype(np.float64).T
+    for b in range(B):
+        order = np.lexsort((np.arange(G), -S[b]))      # -score, then id
+        np.testing.assert_array_equal(sel[b], order[:c])
+        np.testing.assert_allclose(sc[b], S[b, order[:c]], rtol=0, atol=1e-12)
+
+
+def test_coarse_argmax_and_ties_to_lower_id():
+    rng = np.random.default_rng(3)
+    d = 16
+    C = _unit(rng, 6, d)
+    C[4] = C[1]
+    q = C[[1, 2]].copy()              # query 0 ties clusters 1 and 4 exactly
+    sel, _ = oracle.coarse(q, C, 1)
+    assert sel[0, 0] == 1
+    assert sel[1, 0] == int(np.argmax(q[1].astype(np.float64) @ C.astype(np.float64).T))
+    sel2, _ = oracle.coarse(q, C, 2)
+    np.testing.assert_array_equal(sel2[0], [1, 4])
+
+
+# ---------------------------------------------------------------------------
+# O5: closed forms of the temperature softmax
+# ---------------------------------------------------------------------------
+def test_softmax_single_candidate():
+    r = oracle.attend([0.3], [7], 0.07, 3)
+    assert r["Z"] == 1.0 and r["m"] == 0.3
+    np.testing.assert_array_equal(r["id"], [7, -1, -1])
+    np.testing.assert_array_equal(r["weight"], [1.0, 0.0, 0.0])
+    assert r["score"][1] == -np.inf and r["count"] == 1
+
+
+def test_softmax_equal_scores_uniform():
+    n = 11
+    r = oracle.attend(np.full(n, 0.25), np.arange(n)[::-1], 0.5, n, full_weights=True)
+    np.testing.assert_allclose(r["w_full"], 1.0 / n, rtol=1e-14)
+    np.testing.assert_array_equal(r["id"], np.arange(n))    # ties: ascending id
+
+
+@pytest.mark.parametrize("tau", [0.07, 1.0, 3.0])
+def test_softmax_two_candidates_logistic(tau):
+    s1, s2 = 0.41, 0.17
+    r = oracle.attend([s2, s1], [0, 1], tau, 2)
+    w1 = 1.0 / (1.0 + math.exp(-(s1 - s2) / tau))
+    np.testing.assert_allclose(r["weight"], [w1, 1 - w1], rtol=1e-13)
+    np.testing.assert_array_equal(r["id"], [1, 0])
+
+
+def test_softmax_scale_invariance_and_large_tau():
+    rng = np.random.default_rng(4)
+    s = rng.standard_normal(50)
+    ids = np.arange(50)
+    a = oracle.attend(s, ids, 0.3, 50, full_weights=True)
+    b = oracle.attend(4.0 * s, ids, 1.2, 50, full_weights=True)
+    np.testing.assert_allclose(a["w_full"], b["w_full"], rtol=1e-12)
+    u = oracle.attend(s, ids, 1e12, 50, full_weights=True)
+    np.testing.assert_allclose(u["w_full"], 1 / 50, rtol=1e-9)
+    np.testing.assert_allclose(a["w_full"].sum(), 1.0, rtol=1e-13)
+    # ordering by weight agrees with ordering by score for tau > 0
+    assert np.all(np.diff(a["weight"]) <= 0)
+
+
+def test_empty_row():
+    r = oracle.attend([], [], 1.0, 4)
+    assert r["m"] == -np.inf and r["Z"] == 0.0 and r["count"] == 0
+    np.testing.assert_array_equal(r["id"], [-1] * 4)
+    np.testing.assert_array_equal(r["weight"], [0.0] * 4)
+
+
+# ---------------------------------------------------------------------------
+# whole path: brute-force flat retrieval when every cluster is selected
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("tau", [0.07, 1.0])
+def test_top_c_equal_G_is_flat_retrieval(tau):
+    rng = np.random.default_rng(5)
+    B, G, d, k = 7, 6, 32, 9
+    sizes = rng.integers(0, 12, G)
+    off, keys, tid = _bank(rng, G, sizes, d)
+    q, C = _unit(rng, B, d), _unit(rng, G, d)
+    r = oracle.retrieve(q, C, off, G, k, tau, "f32", keys=keys, transition_id=tid)
+    S = q.astype(np.float64) @ keys.astype(np.float64).T       # every record
+    N = keys.shape[0]
+    for b in range(B):
+        order = np.lexsort((tid, -S[b]))
+        m = S[b].max()
+        e = np.exp((S[b] - m) / tau)
+        w = e / e.sum()
+        kk = min(k, N)
+        np.testing.assert_array_equal(r["id"][b, :kk], tid[order[:kk]])
+        np.testing.assert_allclose(r["score"][b, :kk], S[b, order[:kk]], rtol=0, atol=1e-12)
+        np.testing.assert_allclose(r["weight"][b, :kk], w[order[:kk]], rtol=1e-12)
+        np.testing.assert_allclose(r["Z"][b], e.sum(), rtol=1e-12)
+        assert r["m"][b] == pytest.approx(m, abs=1e-12)
+
+
+def test_hierarchy_masks_unselected_clusters():
+    """The best record overall sits in a cluster that is not selected: it must not appear."""
+    rng = np.random.default_rng(6)
+    d = 16
+    q = _unit(rng, 1, d)
+    C = np.stack([q[0], -q[0], _unit(rng, 1, d)[0]]).astype(np.float32)
+    keys = _unit(rng, 9, d)
+    keys[7] = q[0]                    # perfect match, placed in cluster 1 (anti-aligned key)
+    off = np.array([0, 4, 8, 9], dtype=np.int64)
+    r = oracle.retrieve(q, C, off, 1, 9, 1.0, "f32", keys=keys)
+    assert r["own_sel"][0, 0] == 0
+    assert 7 not in r["id"][0]
+    np.testing.assert_array_equal(np.sort(r["id"][0, :4]), [0, 1, 2, 3])
+    assert r["count"][0] == 4
+    S = (q.astype(np.float64) @ keys[:4].astype(np.float64).T)[0]
+    w = np.exp(S - S.max())
+    np.testing.assert_allclose(r["weight"][0, :4], np.sort(w / w.sum())[::-1], rtol=1e-12)
+
+
+def test_planted_match_is_top1():
+    rng = np.random.default_rng(7)
+    B, G, d = 5, 10, 64
+    sizes = rng.integers(3, 9, G)
+    off, keys, tid = _bank(rng, G, sizes, d)
+    C = _unit(rng, G, d)
+    q = _unit(rng, B, d)
+    clusters = rng.choice(G, B, replace=False)      # one planted record per distinct cluster
+    targets = [int(off[g] + rng.integers(0, off[g + 1] - off[g])) for g in clusters]
+    for b, j in enumerate(targets):
+        g = int(np.searchsorted(off, j, side="right") - 1)
+        q[b] = keys[j]
+        C[g] = keys[j]                # the cluster key equals the query: score 1 (unit norm)
+    r = oracle.retrieve(q, C, off, 2, 4, 0.07, "f32", keys=keys, transition_id=tid)
+    for b, j in enumerate(targets):
+        g = int(np.searchsorted(off, j, side="right") - 1)
+        assert r["own_sel"][b, 0] == g
+        assert r["id"][b, 0] == tid[j]
+        exact = float(np.dot(keys[j].astype(np.float64), keys[j].astype(np.float64)))
+        assert r["score"][b, 0] == pytest.approx(exact, abs=1e-12)
+
+
+def test_permutation_invariance():
+    """Relabelling clusters and reordering records inside segments leaves every output unchanged."""
+    rng = np.random.default_rng(8)
+    B, G, d, c, k = 6, 12, 48, 3, 10
+    sizes = rng.integers(0, 15, G)
+    off, keys, tid = _bank(rng, G, sizes, d)
+    q, C = _unit(rng, B, d), _unit(rng, G, d)
+    base = oracle.retrieve(q, C, off, c, k, 0.5, "bf16", keys=keys, transition_id=tid)
+
+    perm = rng.permutation(G)                          # new cluster i = old cluster perm[i]
+    new_keys, new_tid, new_sizes = [], [], []
+    for g in perm:
+        a, b = off[g], off[g + 1]
+        inner = rng.permutation(b - a)
+        new_keys.append(keys[a:b][inner])
+        new_tid.append(tid[a:b][inner])
+        new_sizes.append(b - a)
+    off2 = np.zeros(G + 1, dtype=np.int64)
+    off2[1:] = np.cumsum(new_sizes)
+    r = oracle.retrieve(q, C[perm], off2, c, k, 0.5, "bf16", keys=np.concatenate(new_keys),
+                        transition_id=np.concatenate(new_tid))
+    np.testing.assert_array_equal(perm[r["own_sel"]], base["own_sel"])
+    for f in ("id", "count"):
+        np.testing.assert_array_equal(r[f], base[f])
+    for f in ("score", "weight", "m", "Z"):
+        np.testing.assert_allclose(r[f], base[f], rtol=1e-12, atol=1e-15)
+
+
+def test_rows_are_independent():
+    rng = np.random.default_rng(9)
+    B, G, d = 10, 8, 32
+    off, keys, tid = _bank(rng, G, rng.integers(1, 20, G), d)
+    q, C = _unit(rng, B, d), _unit(rng, G, d)
+    full = oracle.retrieve(q, C, off, 3, 5, 1.0, "f32", keys=keys, transition_id=tid)
+    sub = oracle.retrieve(q, C, off, 3, 5, 1.0, "f32", keys=keys, transition_id=tid,
+                          rows=[7, 2, 5])
+    for f in ("id", "score", "weight", "m", "Z", "count"):
+        np.testing.assert_array_equal(sub[f], full[f][[7, 2, 5]])
+
+
+def test_empty_clusters_and_short_rows():
+    rng = np.random.default_rng(10)
+    d = 16
+    C = _unit(rng, 4, d)
+    q = C[[0, 2]].copy()
+    keys = _unit(rng, 3, d)
+    off = np.array([0, 0, 3, 3, 3], dtype=np.int64)   # only cluster 1 holds records
+    r = oracle.retrieve(q, C, off, 1, 4, 1.0, "f32", keys=keys)
+    assert r["own_sel"][0, 0] == 0 and r["own_sel"][1, 0] == 2
+    for b in range(2):                                  # both rows select an empty cluster
+        assert r["count"][b] == 0 and r["m"][b] == -np.inf and r["Z"][b] == 0
+        np.testing.assert_array_equal(r["id"][b], [-1] * 4)
+    r2 = oracle.retrieve(q, C, off, 2, 4, 1.0, "f32", keys=keys, sel=[[0, 1], [1, 2]])
+    np.testing.assert_array_equal(r2["count"], [3, 3])
+    assert r2["id"][0, 3] == -1 and r2["weight"][0, 3] == 0.0
+    np.testing.assert_allclose(r2["weight"][0, :3].sum(), 1.0, rtol=1e-13)
+
+
+def test_weights_sum_to_one_and_slots_combine():
+    """Row weights sum to 1 over the candidate set; slot (m, Z) combine to the row's (m, Z)."""
+    rng = np.random.default_rng(11)
+    B, G, d, c = 8, 10, 40, 4
+    sizes = rng.integers(1, 30, G)
+    off, keys, tid = _bank(rng, G, sizes, d)
+    q, C = _unit(rng, B, d), _unit(rng, G, d)
+    N = keys.shape[0]
+    r = oracle.retrieve(q, C, off, c, N, 0.07, "bf16", keys=keys, transition_id=tid)
+    for b in range(B):
+        n = r["count"][b]
+        assert n == sum(sizes[g] for g in r["own_sel"][b])
+        np.testing.assert_allclose(r["weight"][b, :n].sum(), 1.0, rtol=1e-12)
+        M = r["slot_m"][b].max()
+        Z = np.sum(r["slot_Z"][b] * np.exp((r["slot_m"][b] - M) / 0.07))
+        assert r["m"][b] == M
+        np.testing.assert_allclose(r["Z"][b], Z, rtol=1e-12)
+
+
+def test_bf16_compute_quantises_every_operand():
+    rng = np.random.default_rng(12)
+    B, G, d = 4, 5, 24
+    off, keys, tid = _bank(rng, G, np.full(G, 6), d)
+    q, C = _unit(rng, B, d), _unit(rng, G, d)
+    r = oracle.retrieve(q, C, off, 2, 3, 1.0, "bf16", keys=keys, transition_id=tid)
+    qb = torch.from_numpy(q).bfloat16().double().numpy()
+    kb = torch.from_numpy(keys).bfloat16().double().numpy()
+    for b in range(B):
+        for t in range(3):
+            j = int(np.nonzero(tid == r["id"][b, t])[0][0])
+            assert r["score"][b, t] == pytest.approx(float(qb[b] @ kb[j]), abs=1e-12)
+
+
+# ---------------------------------------------------------------------------
+# memory build
+# ---------------------------------------------------------------------------
+def test_build_is_stable_counting_sort():
+    rng = np.random.default_rng(13)
+    G = 17
+    cl = rng.integers(0, G, 500).astype(np.int32)
+    cl[cl == 5] = 6                     # an empty cluster
+    off, tid = oracle.build_bank(cl, G)
+    np.testing.assert_array_equal(tid, np.argsort(cl, kind="stable"))
+    np.testing.assert_array_equal(np.diff(off), np.bincount(cl, minlength=G))
+    assert off[0] == 0 and off[-1] == cl.size
+
+
+def test_build_rejects_bad_cluster_id():
+    with pytest.raises(ValueError):
+        oracle.build_bank([0, 3, 1], 3)
