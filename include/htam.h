@@ -1,0 +1,233 @@
+/*
+ * htam.h -- C ABI of the MI355X (gfx950) library for HTAM's hierarchical
+ * transition-attended memory retrieval.
+ *
+ * Paper: "HTAM: Hierarchical Transition-Attended Memory for Operator
+ * Optimization" (arXiv 2605.29734). The memory is a two-level graph
+ * M = (V_G, V_GL, E_G) (Sec. 4.1, Eq. HTG): coarse global nodes, and local
+ * records grouped under a parent global node. One retrieval step (Alg. 1,
+ * Steps 2-3) scores every global node against the current state, picks a
+ * direction (Eq. global direction), restricts the candidates to that node's
+ * children (Eq. local nodes) and keeps the best-scoring children
+ * (Eq. local policy), whose memories are injected into the next generation
+ * (Eq. generation). This library runs that read path batched and in
+ * embedding space: a state is a query vector, a global node a coarse key, a
+ * local record (a before-state -> after-state transition, Eq. memory_update)
+ * a fine key, and every score an inner product (the linear scorer
+ * phi = w^T z of App. B.6).
+ *
+ * Conventions for every call:
+ *   - Array arguments are DEVICE pointers (memory of the current HIP device)
+ *     unless a comment says "host". Matrices are row-major and contiguous.
+ *   - The caller owns every buffer, including the workspace; the library
+ *     never allocates or frees device memory and keeps no pointer after a
+ *     call returns.
+ *   - Every call validates its arguments on the host first. On an invalid
+ *     argument it returns a negative status and enqueues nothing. Otherwise it
+ *     enqueues its kernels on `stream` (NULL = the null stream) and returns
+ *     without waiting (htam_memory_build excepted, see there). Outputs are
+ *     valid once the stream has reached that point.
+ *   - HTAM_ERR_DEVICE reports a HIP error seen while enqueueing; the message
+ *     is available from htam_last_error() on the calling thread.
+ *   - Inputs must be finite. NaN or infinite scores give unspecified rankings.
+ *   - Calls are stateless: concurrent calls on distinct streams with
+ *     distinct output and workspace buffers are safe.
+ */
+#ifndef HTAM_H
+#define HTAM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+struct ihipStream_t;
+typedef struct ihipStream_t *hipStream_t;
+
+/* Element types. */
+typedef enum { HTAM_F32 = 0, HTAM_BF16 = 1 } htam_dtype;
+
+typedef enum {
+    HTAM_OK = 0,
+    HTAM_ERR_NULL = -1,      /* a required pointer is NULL                        */
+    HTAM_ERR_SHAPE = -2,     /* a size or count is out of its documented range    */
+    HTAM_ERR_DTYPE = -3,     /* unsupported dtype or dtype combination            */
+    HTAM_ERR_VALUE = -4,     /* bad value: tau, or invalid records found in build */
+    HTAM_ERR_WORKSPACE = -5, /* workspace NULL or smaller than the size asked for */
+    HTAM_ERR_ALIGN = -6,     /* a pointer is not 16-byte aligned                  */
+    HTAM_ERR_DEVICE = -7     /* HIP runtime error (see htam_last_error)           */
+} htam_status;
+
+/* Limits checked by the calls. */
+#define HTAM_MAX_TOP_K 256   /* 1 <= top_k <= HTAM_MAX_TOP_K                      */
+#define HTAM_MAX_TOP_C 256   /* 1 <= top_c <= min(n_clusters, HTAM_MAX_TOP_C)     */
+#define HTAM_MAX_DIM 8192    /* 8 <= d <= HTAM_MAX_DIM, d % 8 == 0                */
+
+/*
+ * A built memory bank: the two-level memory of Sec. 4.1 (Eq. HTG) as flat
+ * device arrays. Plain descriptor filled by the caller; the library reads it
+ * during a call and keeps no reference.
+ *
+ *   d              embedding width.
+ *   n_clusters     G, the number of coarse keys (global nodes V_G).
+ *   n_transitions  N, the number of fine keys (local records V_GL), N < 2^31.
+ *   key_dtype      storage type of coarse_keys and fine_keys.
+ *   compute_dtype  arithmetic of the scores: HTAM_F32 (requires key_dtype
+ *                  HTAM_F32) or HTAM_BF16 (fp32 inputs are rounded to bf16,
+ *                  to nearest even, as they are loaded). Products are
+ *                  accumulated in fp32 either way.
+ *   coarse_keys    [G][d]  one key per cluster.
+ *   fine_keys      [N][d]  records grouped by cluster: the records of cluster
+ *                  g occupy rows seg_offsets[g] .. seg_offsets[g+1]-1.
+ *   seg_offsets    [G+1] int64, seg_offsets[0] = 0, nondecreasing,
+ *                  seg_offsets[G] = N (the children sets of Eq. local nodes).
+ *   transition_id  [N] int32 caller id of each row of fine_keys, or NULL for
+ *                  the row index itself. Outputs report these ids, and ties
+ *                  between equal scores go to the lower id.
+ */
+typedef struct htam_bank {
+    int32_t d;
+    int32_t n_clusters;
+    int64_t n_transitions;
+    int32_t key_dtype;
+    int32_t compute_dtype;
+    const void *coarse_keys;
+    const void *fine_keys;
+    const int64_t *seg_offsets;
+    const int32_t *transition_id;
+} htam_bank;
+
+/*
+ * htam_memory_build -- group transition records under their parent cluster.
+ *
+ * Follows Eq. HTG (each local record belongs to one global node, par(l) in
+ * Eq. local nodes) and the memory append of Sec. 3 / Eq. memory_update: the
+ * records arrive in any order and are laid out cluster by cluster so that a
+ * cluster's children form one contiguous segment. The sort is stable: within
+ * a cluster, records keep their input order.
+ *
+ *   n            number of records, 0 <= n < 2^31.
+ *   n_clusters   G >= 1.
+ *   d            key width (ignored when keys_in is NULL).
+ *   key_dtype    element type of keys_in / keys_out.
+ *   cluster_of   [n] int32 parent cluster of each input record, in [0, G).
+ *   keys_in      [n][d] input keys in record order, or NULL to build only the
+ *                offsets and ids.
+ *   keys_out     [n][d] receives the keys in segment order (required iff
+ *                keys_in is given; must not overlap keys_in).
+ *   seg_offsets  [G+1] int64 out: segment bounds.
+ *   transition_id [n] int32 out: input record index of each output row.
+ *   ws, ws_bytes workspace of at least htam_memory_build_workspace_size(n, G)
+ *                bytes, 256-byte aligned.
+ *
+ * Unlike the other calls this one waits for the stream before returning, so
+ * that it can report records whose cluster id is out of range
+ * (HTAM_ERR_VALUE; those records are left out of the outputs).
+ */
+htam_status htam_memory_build(int64_t n, int32_t n_clusters, int32_t d, int32_t key_dtype,
+                              const int32_t *cluster_of, const void *keys_in, void *keys_out,
+                              int64_t *seg_offsets, int32_t *transition_id, void *ws,
+                              size_t ws_bytes, hipStream_t stream);
+size_t htam_memory_build_workspace_size(int64_t n, int32_t n_clusters);
+
+/*
+ * htam_retrieve_coarse -- score every cluster and keep the best top_c.
+ *
+ * Alg. 1, Step 2: the score of each global node for the current state
+ * (Eq. score, with a one-term prefix and the linear scorer of App. B.6, so
+ * score = <q_b, c_g>), followed by the direction choice of Eq. global
+ * direction in its greedy limit (epsilon = 0), widened from one direction to
+ * the top_c best.
+ *
+ *   q            [n_queries][d] query embeddings, element type q_dtype
+ *                (HTAM_BF16 queries require compute_dtype HTAM_BF16).
+ *   top_c        1 <= top_c <= min(G, HTAM_MAX_TOP_C).
+ *   sel_cluster  [n_queries][top_c] int32 out: cluster ids by descending
+ *                score, ties to the lower cluster id.
+ *   sel_score    [n_queries][top_c] fp32 out (may be NULL): their scores.
+ *   ws, ws_bytes workspace of htam_retrieve_coarse_workspace_size() bytes.
+ */
+htam_status htam_retrieve_coarse(const htam_bank *bank, const void *q, int32_t q_dtype,
+                                 int32_t n_queries, int32_t top_c, int32_t *sel_cluster,
+                                 float *sel_score, void *ws, size_t ws_bytes, hipStream_t stream);
+size_t htam_retrieve_coarse_workspace_size(const htam_bank *bank, int32_t n_queries, int32_t top_c);
+
+/*
+ * htam_attend_transitions -- stream the selected clusters' transition
+ * segments, with softmax statistics and top-k per selected cluster.
+ *
+ * Alg. 1, Step 3: the candidates of a query are the children of its selected
+ * clusters (Eq. local nodes). Each candidate is scored by <q_b, k_j> (the
+ * preference score of Eq. local policy, as an inner product), and for every
+ * (query b, slot s) with cluster g = sel_cluster[b][s] this call returns:
+ *   slot_max[b][s]  m = max of the scores over segment g (-inf if empty);
+ *   slot_sum[b][s]  Z = sum over segment g of exp((score - m) / tau)
+ *                   (0 if empty): the temperature softmax of Eq. global
+ *                   direction applied to the transitions, in a form that
+ *                   merges across slots;
+ *   cand_score[b][s][0..top_k-1], cand_id[b][s][...]: the top_k records of
+ *                   segment g by descending score, ties to the lower caller
+ *                   id; padded with score -inf and id -1 when the segment is
+ *                   shorter than top_k.
+ * Scores are raw inner products (not divided by tau).
+ *
+ *   sel_cluster  [n_queries][top_c] int32, each in [0, G) (as produced by
+ *                htam_retrieve_coarse; a query's clusters must be distinct
+ *                for the union of htam_topk to be a set).
+ *   tau          temperature, finite and > 0.
+ *   top_k        1 <= top_k <= HTAM_MAX_TOP_K.
+ *   ws, ws_bytes workspace of htam_attend_transitions_workspace_size() bytes.
+ */
+htam_status htam_attend_transitions(const htam_bank *bank, const void *q, int32_t q_dtype,
+                                    int32_t n_queries, const int32_t *sel_cluster, int32_t top_c,
+                                    float tau, int32_t top_k, float *slot_max, float *slot_sum,
+                                    float *cand_score, int32_t *cand_id, void *ws,
+                                    size_t ws_bytes, hipStream_t stream);
+size_t htam_attend_transitions_workspace_size(const htam_bank *bank, int32_t n_queries,
+                                              int32_t top_c, int32_t top_k);
+
+/*
+ * htam_topk -- merge candidate lists into the memories to inject.
+ *
+ * The argmax of Eq. local policy widened to top_k injected memories, taken
+ * over the union of a query's selected segments (the weights are the
+ * temperature softmax over that union). With the App. B.7 fallback read as:
+ * a row with fewer than top_k candidates is padded, an empty row is invalid
+ * (count 0, row_max -inf, row_sum 0).
+ *
+ * Row b's candidates are the n_lists * k_in entries cand_score[b][..][..] with
+ * cand_id >= 0 (entries with id < 0 are padding and are skipped). If cand_id
+ * is NULL, every entry is a candidate and its id is its position
+ * 0 .. n_lists*k_in-1 within the row (a plain row-wise top-k over a dense
+ * score matrix). Entries need not be sorted.
+ *
+ *   slot_max, slot_sum  [n_rows][n_lists] per-list softmax statistics as
+ *                returned by htam_attend_transitions, or both NULL. When given,
+ *                the row's statistics are merged from them:
+ *                row_max = max_l m_l, row_sum = sum_l Z_l exp((m_l - row_max)/tau),
+ *                and out_weight = exp((score - row_max)/tau) / row_sum.
+ *                When NULL, row_max, row_sum and out_weight must be NULL too.
+ *   out_id, out_score [n_rows][top_k] out: by descending score, ties to the
+ *                lower id, padded with (-1, -inf).
+ *   out_weight   [n_rows][top_k] out or NULL (padding weight 0).
+ *   row_max, row_sum [n_rows] out or NULL.
+ *   out_count    [n_rows] out or NULL: min(top_k, number of candidates).
+ *   tau          finite and > 0 (unused without slot statistics).
+ *   top_k        1 <= top_k <= HTAM_MAX_TOP_K.
+ */
+htam_status htam_topk(int32_t n_rows, int32_t n_lists, int32_t k_in, const float *cand_score,
+                      const int32_t *cand_id, const float *slot_max, const float *slot_sum,
+                      float tau, int32_t top_k, int32_t *out_id, float *out_score,
+                      float *out_weight, float *row_max, float *row_sum, int32_t *out_count,
+                      hipStream_t stream);
+
+/* Human-readable name of a status, and the last error message of the calling thread. */
+const char *htam_status_string(htam_status status);
+const char *htam_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* HTAM_H */

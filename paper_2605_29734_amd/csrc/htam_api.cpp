@@ -1,0 +1,274 @@
+// Host side of the C ABI declared in include/htam.h: argument validation
+// (before anything is enqueued), workspace sizing, and kernel sequencing.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+
+#include "../../include/htam.h"
+#include "internal.hpp"
+
+#define HTAM_API extern "C" __attribute__((visibility("default")))
+
+namespace {
+
+thread_local std::string g_last_error;
+
+htam_status fail(htam_status st, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
+htam_status fail(htam_status st, const char *fmt, ...) {
+    char msg[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(msg, sizeof msg, fmt, ap);
+    va_end(ap);
+    g_last_error = msg;
+    return st;
+}
+
+htam_status ok() {
+    g_last_error.clear();
+    return HTAM_OK;
+}
+
+htam_status device_status(hipError_t e, const char *where) {
+    if (e == hipSuccess) return ok();
+    return fail(HTAM_ERR_DEVICE, "%s: %s", where, hipGetErrorString(e));
+}
+
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+bool aligned256(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 255u) == 0; }
+int dtype_bytes(int32_t t) { return t == HTAM_BF16 ? 2 : 4; }
+bool valid_dtype(int32_t t) { return t == HTAM_F32 || t == HTAM_BF16; }
+
+htam_status check_bank(const htam_bank *b) {
+    if (!b) return fail(HTAM_ERR_NULL, "bank is NULL");
+    if (b->d < 8 || b->d > HTAM_MAX_DIM || b->d % 8 != 0)
+        return fail(HTAM_ERR_SHAPE, "d = %d: need 8 <= d <= %d and d %% 8 == 0", b->d, HTAM_MAX_DIM);
+    if (b->n_clusters < 1) return fail(HTAM_ERR_SHAPE, "n_clusters = %d < 1", b->n_clusters);
+    if (b->n_transitions < 0 || b->n_transitions >= (int64_t(1) << 31))
+        return fail(HTAM_ERR_SHAPE, "n_transitions = %lld out of [0, 2^31)",
+                    (long long)b->n_transitions);
+    if (!valid_dtype(b->key_dtype) || !valid_dtype(b->compute_dtype))
+        return fail(HTAM_ERR_DTYPE, "unknown dtype (key %d, compute %d)", b->key_dtype,
+                    b->compute_dtype);
+    if (b->key_dtype == HTAM_BF16 && b->compute_dtype == HTAM_F32)
+        return fail(HTAM_ERR_DTYPE, "bf16 keys with fp32 compute is not supported");
+    if (!b->coarse_keys) return fail(HTAM_ERR_NULL, "bank->coarse_keys is NULL");
+    if (!b->seg_offsets) return fail(HTAM_ERR_NULL, "bank->seg_offsets is NULL");
+    if (b->n_transitions > 0 && !b->fine_keys) return fail(HTAM_ERR_NULL, "bank->fine_keys is NULL");
+    if (!aligned16(b->coarse_keys) || !aligned16(b->fine_keys))
+        return fail(HTAM_ERR_ALIGN, "bank key arrays must be 16-byte aligned");
+    return HTAM_OK;
+}
+
+htam_status check_query(const htam_bank *b, const void *q, int32_t q_dtype, int32_t B) {
+    if (B < 0) return fail(HTAM_ERR_SHAPE, "n_queries = %d < 0", B);
+    if (!valid_dtype(q_dtype)) return fail(HTAM_ERR_DTYPE, "unknown q_dtype %d", q_dtype);
+    if (q_dtype != b->key_dtype)
+        return fail(HTAM_ERR_DTYPE, "q_dtype %d differs from the bank's key_dtype %d", q_dtype,
+                    b->key_dtype);
+    if (B > 0 && !q) return fail(HTAM_ERR_NULL, "q is NULL");
+    if (!aligned16(q)) return fail(HTAM_ERR_ALIGN, "q must be 16-byte aligned");
+    return HTAM_OK;
+}
+
+htam_status check_ws(void *ws, size_t have, size_t need) {
+    if (!ws) return fail(HTAM_ERR_WORKSPACE, "workspace is NULL (%zu bytes needed)", need);
+    if (have < need)
+        return fail(HTAM_ERR_WORKSPACE, "workspace of %zu bytes is smaller than %zu", have, need);
+    if (!aligned256(ws)) return fail(HTAM_ERR_ALIGN, "workspace must be 256-byte aligned");
+    return HTAM_OK;
+}
+
+htam_status check_tau(float tau) {
+    if (!std::isfinite(tau) || !(tau > 0.0f))
+        return fail(HTAM_ERR_VALUE, "tau = %g: need a finite tau > 0", (double)tau);
+    return HTAM_OK;
+}
+
+// Compute units of the current device (cached per device).
+int device_cus(int *dev_out) {
+    static int cached[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return -1;
+    if (dev_out) *dev_out = dev;
+    if (dev >= 0 && dev < 64 && cached[dev] > 0) return cached[dev];
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return -1;
+    if (dev >= 0 && dev < 64) cached[dev] = n;
+    return n;
+}
+
+}  // namespace
+
+#define HTAM_TRY(x)                                    \
+    do {                                               \
+        htam_status _st = (x);                         \
+        if (_st != HTAM_OK) return _st;                \
+    } while (0)
+
+// ---------------------------------------------------------------------------
+HTAM_API size_t htam_memory_build_workspace_size(int64_t n, int32_t n_clusters) {
+    if (n < 0 || n_clusters < 1) return 0;
+    size_t bytes = 0;
+    htam::build_layout(nullptr, n, n_clusters, &bytes);
+    return bytes;
+}
+
+HTAM_API htam_status htam_memory_build(int64_t n, int32_t n_clusters, int32_t d, int32_t key_dtype,
+                                       const int32_t *cluster_of, const void *keys_in,
+                                       void *keys_out, int64_t *seg_offsets,
+                                       int32_t *transition_id, void *ws, size_t ws_bytes,
+                                       hipStream_t stream) {
+    if (n < 0 || n >= (int64_t(1) << 31)) return fail(HTAM_ERR_SHAPE, "n = %lld out of [0, 2^31)", (long long)n);
+    if (n_clusters < 1) return fail(HTAM_ERR_SHAPE, "n_clusters = %d < 1", n_clusters);
+    if (!seg_offsets) return fail(HTAM_ERR_NULL, "seg_offsets is NULL");
+    if (n > 0 && (!cluster_of || !transition_id))
+        return fail(HTAM_ERR_NULL, "cluster_of / transition_id is NULL");
+    if (keys_in) {
+        if (!keys_out) return fail(HTAM_ERR_NULL, "keys_out is NULL while keys_in is given");
+        if (!valid_dtype(key_dtype)) return fail(HTAM_ERR_DTYPE, "unknown key_dtype %d", key_dtype);
+        if (d < 8 || d > HTAM_MAX_DIM || d % 8 != 0)
+            return fail(HTAM_ERR_SHAPE, "d = %d: need 8 <= d <= %d and d %% 8 == 0", d, HTAM_MAX_DIM);
+        if (!aligned16(keys_in) || !aligned16(keys_out))
+            return fail(HTAM_ERR_ALIGN, "key arrays must be 16-byte aligned");
+        const char *a = static_cast<const char *>(keys_in), *b = static_cast<const char *>(keys_out);
+        const size_t bytes = (size_t)n * d * dtype_bytes(key_dtype);
+        if (n > 0 && a < b + bytes && b < a + bytes)
+            return fail(HTAM_ERR_VALUE, "keys_in and keys_out overlap");
+    }
+    HTAM_TRY(check_ws(ws, ws_bytes, htam_memory_build_workspace_size(n, n_clusters)));
+
+    const htam::BuildWs w = htam::build_layout(ws, n, n_clusters, nullptr);
+    hipError_t e = htam::launch_build(n, n_clusters, keys_in ? d * dtype_bytes(key_dtype) : 0,
+                                      cluster_of, keys_in, keys_out, seg_offsets, transition_id, w,
+                                      stream);
+    if (e != hipSuccess) return device_status(e, "htam_memory_build launch");
+    int32_t bad = 0;
+    e = hipMemcpyAsync(&bad, w.err, sizeof bad, hipMemcpyDeviceToHost, stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(stream);
+    if (e != hipSuccess) return device_status(e, "htam_memory_build");
+    if (bad) return fail(HTAM_ERR_VALUE, "%d records have a cluster id outside [0, %d)", bad, n_clusters);
+    return ok();
+}
+
+// ---------------------------------------------------------------------------
+HTAM_API size_t htam_retrieve_coarse_workspace_size(const htam_bank *bank, int32_t n_queries,
+                                                    int32_t top_c) {
+    (void)top_c;
+    if (!bank || n_queries < 0 || bank->n_clusters < 1) return 0;
+    size_t bytes = 0;
+    htam::coarse_layout(nullptr, n_queries, bank->n_clusters, &bytes);
+    return bytes;
+}
+
+HTAM_API htam_status htam_retrieve_coarse(const htam_bank *bank, const void *q, int32_t q_dtype,
+                                          int32_t n_queries, int32_t top_c, int32_t *sel_cluster,
+                                          float *sel_score, void *ws, size_t ws_bytes,
+                                          hipStream_t stream) {
+    HTAM_TRY(check_bank(bank));
+    HTAM_TRY(check_query(bank, q, q_dtype, n_queries));
+    const int32_t cmax = bank->n_clusters < HTAM_MAX_TOP_C ? bank->n_clusters : HTAM_MAX_TOP_C;
+    if (top_c < 1 || top_c > cmax)
+        return fail(HTAM_ERR_SHAPE, "top_c = %d out of [1, %d]", top_c, cmax);
+    if (n_queries > 0 && !sel_cluster) return fail(HTAM_ERR_NULL, "sel_cluster is NULL");
+    if (n_queries == 0) return ok();
+    HTAM_TRY(check_ws(ws, ws_bytes, htam_retrieve_coarse_workspace_size(bank, n_queries, top_c)));
+    const htam::CoarseWs w = htam::coarse_layout(ws, n_queries, bank->n_clusters, nullptr);
+    return device_status(htam::launch_coarse(bank->key_dtype, bank->compute_dtype, bank->d,
+                                             bank->n_clusters, bank->coarse_keys, q, n_queries,
+                                             top_c, sel_cluster, sel_score, w, stream),
+                         "htam_retrieve_coarse");
+}
+
+// ---------------------------------------------------------------------------
+HTAM_API size_t htam_attend_transitions_workspace_size(const htam_bank *bank, int32_t n_queries,
+                                                       int32_t top_c, int32_t top_k) {
+    if (!bank || n_queries < 0 || top_c < 1 || top_k < 1 || bank->n_clusters < 1 || bank->d < 8)
+        return 0;
+    size_t bytes = 0;
+    htam::attend_layout(nullptr, bank->d, bank->n_clusters, bank->n_transitions,
+                        dtype_bytes(bank->key_dtype), n_queries, top_c, top_k, &bytes);
+    return bytes;
+}
+
+HTAM_API htam_status htam_attend_transitions(const htam_bank *bank, const void *q, int32_t q_dtype,
+                                             int32_t n_queries, const int32_t *sel_cluster,
+                                             int32_t top_c, float tau, int32_t top_k,
+                                             float *slot_max, float *slot_sum, float *cand_score,
+                                             int32_t *cand_id, void *ws, size_t ws_bytes,
+                                             hipStream_t stream) {
+    HTAM_TRY(check_bank(bank));
+    HTAM_TRY(check_query(bank, q, q_dtype, n_queries));
+    const int32_t cmax = bank->n_clusters < HTAM_MAX_TOP_C ? bank->n_clusters : HTAM_MAX_TOP_C;
+    if (top_c < 1 || top_c > cmax)
+        return fail(HTAM_ERR_SHAPE, "top_c = %d out of [1, %d]", top_c, cmax);
+    if (top_k < 1 || top_k > HTAM_MAX_TOP_K)
+        return fail(HTAM_ERR_SHAPE, "top_k = %d out of [1, %d]", top_k, HTAM_MAX_TOP_K);
+    HTAM_TRY(check_tau(tau));
+    if ((int64_t)n_queries * top_c >= (int64_t(1) << 31))
+        return fail(HTAM_ERR_SHAPE, "n_queries * top_c must be < 2^31");
+    if (n_queries == 0) return ok();
+    if (!sel_cluster || !slot_max || !slot_sum || !cand_score || !cand_id)
+        return fail(HTAM_ERR_NULL, "an output or sel_cluster is NULL");
+    HTAM_TRY(check_ws(ws, ws_bytes,
+                      htam_attend_transitions_workspace_size(bank, n_queries, top_c, top_k)));
+    const int n_cu = device_cus(nullptr);
+    if (n_cu <= 0) return fail(HTAM_ERR_DEVICE, "no HIP device");
+    const htam::AttendWs w =
+        htam::attend_layout(ws, bank->d, bank->n_clusters, bank->n_transitions,
+                            dtype_bytes(bank->key_dtype), n_queries, top_c, top_k, nullptr);
+    return device_status(
+        htam::launch_attend(bank->key_dtype, bank->compute_dtype, bank->d, bank->n_clusters,
+                            bank->n_transitions, bank->fine_keys, bank->seg_offsets,
+                            bank->transition_id, q, n_queries, sel_cluster, top_c, tau, top_k,
+                            slot_max, slot_sum, cand_score, cand_id, w, n_cu, stream),
+        "htam_attend_transitions");
+}
+
+// ---------------------------------------------------------------------------
+HTAM_API htam_status htam_topk(int32_t n_rows, int32_t n_lists, int32_t k_in,
+                               const float *cand_score, const int32_t *cand_id,
+                               const float *slot_max, const float *slot_sum, float tau,
+                               int32_t top_k, int32_t *out_id, float *out_score,
+                               float *out_weight, float *row_max, float *row_sum,
+                               int32_t *out_count, hipStream_t stream) {
+    if (n_rows < 0 || n_lists < 1 || k_in < 1)
+        return fail(HTAM_ERR_SHAPE, "n_rows %d, n_lists %d, k_in %d: need n_rows >= 0, n_lists >= 1, k_in >= 1",
+                    n_rows, n_lists, k_in);
+    if ((int64_t)n_lists * k_in >= (int64_t(1) << 31))
+        return fail(HTAM_ERR_SHAPE, "n_lists * k_in must be < 2^31");
+    if (top_k < 1 || top_k > HTAM_MAX_TOP_K)
+        return fail(HTAM_ERR_SHAPE, "top_k = %d out of [1, %d]", top_k, HTAM_MAX_TOP_K);
+    if ((slot_max == nullptr) != (slot_sum == nullptr))
+        return fail(HTAM_ERR_NULL, "slot_max and slot_sum must be given together");
+    if (!slot_max && (out_weight || row_max || row_sum))
+        return fail(HTAM_ERR_VALUE, "out_weight / row_max / row_sum need slot_max and slot_sum");
+    if (slot_max) HTAM_TRY(check_tau(tau));
+    if (n_rows == 0) return ok();
+    if (!cand_score || !out_id || !out_score) return fail(HTAM_ERR_NULL, "an input or output is NULL");
+    return device_status(htam::launch_topk(n_rows, n_lists, k_in, cand_score, cand_id, slot_max,
+                                           slot_sum, slot_max ? tau : 1.0f, top_k, out_id,
+                                           out_score, out_weight, row_max, row_sum, out_count,
+                                           stream),
+                         "htam_topk");
+}
+
+// ---------------------------------------------------------------------------
+HTAM_API const char *htam_status_string(htam_status st) {
+    switch (st) {
+        case HTAM_OK: return "HTAM_OK";
+        case HTAM_ERR_NULL: return "HTAM_ERR_NULL";
+        case HTAM_ERR_SHAPE: return "HTAM_ERR_SHAPE";
+        case HTAM_ERR_DTYPE: return "HTAM_ERR_DTYPE";
+        case HTAM_ERR_VALUE: return "HTAM_ERR_VALUE";
+        case HTAM_ERR_WORKSPACE: return "HTAM_ERR_WORKSPACE";
+        case HTAM_ERR_ALIGN: return "HTAM_ERR_ALIGN";
+        case HTAM_ERR_DEVICE: return "HTAM_ERR_DEVICE";
+    }
+    return "HTAM_UNKNOWN_STATUS";
+}
+
+HTAM_API const char *htam_last_error(void) { return g_last_error.c_str(); }

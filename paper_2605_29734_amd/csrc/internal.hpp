@@ -1,0 +1,90 @@
+// Internal interface between the host API (htam_api.cpp) and the kernel
+// translation units: workspace layouts and kernel launchers.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace htam {
+
+enum DType : int32_t { kF32 = 0, kBF16 = 1 };
+
+// Routing plan written on the device by the planning kernel of the fine stage.
+struct Plan {
+    int64_t chunk;     // rows per work item (chunk of a segment)
+    int64_t n_items;   // work items (cluster, chunk) with at least one query
+    int64_t n_parts;   // partial results (query, chunk)
+    int32_t next;      // dynamic work counter of the streaming kernel
+    int32_t bad_sel;   // count of selected cluster ids out of range
+};
+
+// Carves a workspace into 256-byte aligned pieces; with base == nullptr it
+// only measures.
+struct Carve {
+    char *base;
+    size_t off = 0;
+    explicit Carve(void *b) : base(static_cast<char *>(b)) {}
+    template <typename T>
+    T *take(size_t count) {
+        off = (off + 255) & ~size_t(255);
+        T *p = base ? reinterpret_cast<T *>(base + off) : nullptr;
+        off += count * sizeof(T);
+        return p;
+    }
+};
+
+// ---- memory build --------------------------------------------------------
+struct BuildWs {
+    int64_t chunk, n_chunks;
+    int32_t *cnt;      // [n_chunks][G] per-chunk cluster counts, then exclusive column prefix
+    int64_t *len;      // [G] segment lengths
+    int32_t *err;      // [1] count of out-of-range cluster ids
+};
+BuildWs build_layout(void *ws, int64_t n, int32_t G, size_t *bytes);
+hipError_t launch_build(int64_t n, int32_t G, int32_t row_bytes, const int32_t *cluster_of,
+                        const void *keys_in, void *keys_out, int64_t *seg_offsets,
+                        int32_t *transition_id, const BuildWs &w, hipStream_t s);
+
+// ---- coarse scoring --------------------------------------------------------
+struct CoarseWs {
+    float *scores;     // [B][G]
+};
+CoarseWs coarse_layout(void *ws, int32_t B, int32_t G, size_t *bytes);
+hipError_t launch_coarse(int32_t key_dtype, int32_t compute_dtype, int32_t d, int32_t G,
+                         const void *coarse_keys, const void *q, int32_t B, int32_t top_c,
+                         int32_t *sel, float *sel_score, const CoarseWs &w, hipStream_t s);
+
+// ---- fine stage (routing + bank stream + per-slot merge) ----------------------
+struct AttendWs {
+    int32_t *cnt;      // [G] queries per cluster
+    int32_t *cursor;   // [G]
+    int32_t *qoff;     // [G+1]
+    int32_t *wstart;   // [G+1] first work item of each cluster
+    int64_t *pbase;    // [G]   first partial of each cluster
+    int32_t *qlist;    // [B*c] (query, slot) entries grouped by cluster
+    int32_t *pos;      // [B*c] position of each entry inside its cluster's list
+    Plan *plan;
+    float *pm;         // [P] partial max
+    float *pz;         // [P] partial sum
+    int32_t *pc;       // [P] partial kept count
+    uint64_t *pk;      // [P][k] partial keys, descending
+    int64_t p_cap;
+    int64_t chunk_min;
+    int64_t w_max;
+};
+AttendWs attend_layout(void *ws, int32_t d, int32_t G, int64_t N, int32_t key_bytes, int32_t B,
+                       int32_t c, int32_t k, size_t *bytes);
+hipError_t launch_attend(int32_t key_dtype, int32_t compute_dtype, int32_t d, int32_t G,
+                         int64_t N, const void *fine_keys, const int64_t *seg_offsets,
+                         const int32_t *transition_id, const void *q, int32_t B,
+                         const int32_t *sel, int32_t c, float tau, int32_t k, float *slot_max,
+                         float *slot_sum, float *cand_score, int32_t *cand_id, const AttendWs &w,
+                         int n_cu, hipStream_t s);
+
+// ---- top-k merge -----------------------------------------------------------
+hipError_t launch_topk(int32_t rows, int32_t lists, int32_t k_in, const float *score,
+                       const int32_t *id, const float *slot_max, const float *slot_sum, float tau,
+                       int32_t top_k, int32_t *out_id, float *out_score, float *out_weight,
+                       float *row_max, float *row_sum, int32_t *out_count, hipStream_t s);
+
+}  // namespace htam

@@ -1,0 +1,258 @@
+"""Python binding of libhtam.so (the C ABI of include/htam.h).
+
+Argument marshalling only: every step of retrieval runs in the library's HIP
+kernels. PyTorch supplies device memory (outputs and workspaces are torch
+tensors on the queries' device) and the stream (the current torch stream).
+If the library has not been built, importing this module raises ImportError:
+there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import dataclasses
+import os
+
+import torch
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libhtam.so")
+
+HTAM_F32 = 0
+HTAM_BF16 = 1
+HTAM_MAX_TOP_K = 256
+HTAM_MAX_TOP_C = 256
+HTAM_MAX_DIM = 8192
+
+STATUS = {0: "HTAM_OK", -1: "HTAM_ERR_NULL", -2: "HTAM_ERR_SHAPE", -3: "HTAM_ERR_DTYPE",
+          -4: "HTAM_ERR_VALUE", -5: "HTAM_ERR_WORKSPACE", -6: "HTAM_ERR_ALIGN",
+          -7: "HTAM_ERR_DEVICE"}
+
+
+class HtamError(RuntimeError):
+    def __init__(self, where: str, status: int, message: str):
+        super().__init__(f"{where}: {STATUS.get(status, status)}: {message}")
+        self.status = status
+
+
+class BankStruct(ctypes.Structure):
+    """Mirror of struct htam_bank."""
+    _fields_ = [("d", ctypes.c_int32), ("n_clusters", ctypes.c_int32),
+                ("n_transitions", ctypes.c_int64), ("key_dtype", ctypes.c_int32),
+                ("compute_dtype", ctypes.c_int32), ("coarse_keys", ctypes.c_void_p),
+                ("fine_keys", ctypes.c_void_p), ("seg_offsets", ctypes.c_void_p),
+                ("transition_id", ctypes.c_void_p)]
+
+
+def _load():
+    if not os.path.exists(_LIB_PATH):
+        raise ImportError(f"{_LIB_PATH} is missing: build it with "
+                          "`python -m paper_2605_29734_amd.build_lib` (hipcc, gfx950)")
+    lib = ctypes.CDLL(_LIB_PATH)
+    P, i32, i64, f32, sz = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float,
+                            ctypes.c_size_t)
+    BP = ctypes.POINTER(BankStruct)
+    sig = {
+        "htam_memory_build": ([i64, i32, i32, i32, P, P, P, P, P, P, sz, P], i32),
+        "htam_memory_build_workspace_size": ([i64, i32], sz),
+        "htam_retrieve_coarse": ([BP, P, i32, i32, i32, P, P, P, sz, P], i32),
+        "htam_retrieve_coarse_workspace_size": ([BP, i32, i32], sz),
+        "htam_attend_transitions": ([BP, P, i32, i32, P, i32, f32, i32, P, P, P, P, P, sz, P], i32),
+        "htam_attend_transitions_workspace_size": ([BP, i32, i32, i32], sz),
+        "htam_topk": ([i32, i32, i32, P, P, P, P, f32, i32, P, P, P, P, P, P, P], i32),
+        "htam_status_string": ([i32], ctypes.c_char_p),
+        "htam_last_error": ([], ctypes.c_char_p),
+    }
+    for name, (args, res) in sig.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = res
+    return lib
+
+
+lib = _load()
+
+
+def _check(where: str, status: int):
+    if status < 0:
+        raise HtamError(where, status, lib.htam_last_error().decode())
+    return status
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(device) -> ctypes.c_void_p:
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def dtype_code(dt: torch.dtype) -> int:
+    if dt == torch.float32:
+        return HTAM_F32
+    if dt == torch.bfloat16:
+        return HTAM_BF16
+    raise TypeError(f"unsupported dtype {dt}")
+
+
+def _workspace(nbytes: int, device) -> torch.Tensor:
+    # torch's caching allocator returns blocks aligned to at least 512 bytes
+    return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
+
+
+@dataclasses.dataclass
+class Bank:
+    """A built two-level memory bank (device tensors) and its descriptor."""
+    coarse_keys: torch.Tensor       # [G][d]
+    fine_keys: torch.Tensor         # [N][d], segment-contiguous
+    seg_offsets: torch.Tensor       # [G+1] int64
+    transition_id: torch.Tensor | None   # [N] int32 or None (= row index)
+    compute: str = "bf16"           # "f32" | "bf16"
+
+    def __post_init__(self):
+        self._s = BankStruct(
+            d=self.coarse_keys.shape[1], n_clusters=self.coarse_keys.shape[0],
+            n_transitions=self.fine_keys.shape[0], key_dtype=dtype_code(self.fine_keys.dtype),
+            compute_dtype=HTAM_BF16 if self.compute == "bf16" else HTAM_F32,
+            coarse_keys=self.coarse_keys.data_ptr(), fine_keys=self.fine_keys.data_ptr(),
+            seg_offsets=self.seg_offsets.data_ptr(),
+            transition_id=None if self.transition_id is None else self.transition_id.data_ptr())
+
+    @property
+    def struct(self) -> BankStruct:
+        return self._s
+
+    @property
+    def device(self):
+        return self.fine_keys.device
+
+
+# ---------------------------------------------------------------------------
+# the four calls
+# ---------------------------------------------------------------------------
+def htam_memory_build(cluster_of: torch.Tensor, keys_in: torch.Tensor | None, n_clusters: int):
+    """Group records by parent cluster. Returns (keys_out, seg_offsets, transition_id)."""
+    dev = cluster_of.device
+    n = cluster_of.numel()
+    keys_out = None if keys_in is None else torch.empty_like(keys_in)
+    off = torch.empty(n_clusters + 1, dtype=torch.int64, device=dev)
+    tid = torch.empty(n, dtype=torch.int32, device=dev)
+    ws = _workspace(lib.htam_memory_build_workspace_size(n, n_clusters), dev)
+    d = 0 if keys_in is None else keys_in.shape[1]
+    kd = HTAM_F32 if keys_in is None else dtype_code(keys_in.dtype)
+    _check("htam_memory_build",
+           lib.htam_memory_build(n, n_clusters, d, kd, _ptr(cluster_of), _ptr(keys_in),
+                                 _ptr(keys_out), _ptr(off), _ptr(tid), _ptr(ws), ws.numel(),
+                                 _stream(dev)))
+    return keys_out, off, tid
+
+
+def htam_retrieve_coarse(bank: Bank, q: torch.Tensor, top_c: int, out=None, ws=None):
+    """Top-c clusters per query. Returns (sel_cluster int32 [B][c], sel_score fp32 [B][c])."""
+    B = q.shape[0]
+    dev = q.device
+    if out is None:
+        out = (torch.empty(B, top_c, dtype=torch.int32, device=dev),
+               torch.empty(B, top_c, dtype=torch.float32, device=dev))
+    if ws is None:
+        ws = _workspace(lib.htam_retrieve_coarse_workspace_size(ctypes.byref(bank.struct), B,
+                                                                top_c), dev)
+    _check("htam_retrieve_coarse",
+           lib.htam_retrieve_coarse(ctypes.byref(bank.struct), _ptr(q), dtype_code(q.dtype), B,
+                                    top_c, _ptr(out[0]), _ptr(out[1]), _ptr(ws), ws.numel(),
+                                    _stream(dev)))
+    return out
+
+
+def htam_attend_transitions(bank: Bank, q: torch.Tensor, sel: torch.Tensor, tau: float,
+                            top_k: int, out=None, ws=None):
+    """Per (query, slot): (slot_max, slot_sum, cand_score [B][c][k], cand_id [B][c][k])."""
+    B, c = sel.shape
+    dev = q.device
+    if out is None:
+        out = (torch.empty(B, c, dtype=torch.float32, device=dev),
+               torch.empty(B, c, dtype=torch.float32, device=dev),
+               torch.empty(B, c, top_k, dtype=torch.float32, device=dev),
+               torch.empty(B, c, top_k, dtype=torch.int32, device=dev))
+    if ws is None:
+        ws = _workspace(lib.htam_attend_transitions_workspace_size(ctypes.byref(bank.struct), B,
+                                                                   c, top_k), dev)
+    _check("htam_attend_transitions",
+           lib.htam_attend_transitions(ctypes.byref(bank.struct), _ptr(q), dtype_code(q.dtype), B,
+                                       _ptr(sel), c, float(tau), top_k, _ptr(out[0]), _ptr(out[1]),
+                                       _ptr(out[2]), _ptr(out[3]), _ptr(ws), ws.numel(),
+                                       _stream(dev)))
+    return out
+
+
+def htam_topk(cand_score: torch.Tensor, cand_id: torch.Tensor | None, top_k: int,
+              slot_max: torch.Tensor | None = None, slot_sum: torch.Tensor | None = None,
+              tau: float = 1.0, out=None):
+    """Merge [rows][lists][k_in] candidates. Returns (id, score, weight, row_max, row_sum, count);
+    the softmax outputs are None without slot statistics."""
+    if cand_score.dim() == 2:
+        cand_score = cand_score.unsqueeze(1)
+        cand_id = None if cand_id is None else cand_id.unsqueeze(1)
+    rows, lists, k_in = cand_score.shape
+    dev = cand_score.device
+    stats = slot_max is not None
+    if out is None:
+        out = (torch.empty(rows, top_k, dtype=torch.int32, device=dev),
+               torch.empty(rows, top_k, dtype=torch.float32, device=dev),
+               torch.empty(rows, top_k, dtype=torch.float32, device=dev) if stats else None,
+               torch.empty(rows, dtype=torch.float32, device=dev) if stats else None,
+               torch.empty(rows, dtype=torch.float32, device=dev) if stats else None,
+               torch.empty(rows, dtype=torch.int32, device=dev))
+    _check("htam_topk",
+           lib.htam_topk(rows, lists, k_in, _ptr(cand_score), _ptr(cand_id), _ptr(slot_max),
+                         _ptr(slot_sum), float(tau), top_k, _ptr(out[0]), _ptr(out[1]),
+                         _ptr(out[2]), _ptr(out[3]), _ptr(out[4]), _ptr(out[5]), _stream(dev)))
+    return out
+
+
+# ---------------------------------------------------------------------------
+# a whole retrieval with preallocated buffers
+# ---------------------------------------------------------------------------
+class Retriever:
+    """Preallocates outputs and workspaces for a fixed (bank, batch, top_c, top_k, tau),
+    so that ``run`` only enqueues the three retrieval calls on the current stream."""
+
+    def __init__(self, bank: Bank, n_queries: int, top_c: int, top_k: int, tau: float):
+        self.bank, self.B, self.c, self.k, self.tau = bank, n_queries, top_c, top_k, tau
+        dev = bank.device
+        e = lambda *s, dt=torch.float32: torch.empty(*s, dtype=dt, device=dev)  # noqa: E731
+        self.sel = (e(n_queries, top_c, dt=torch.int32), e(n_queries, top_c))
+        self.slots = (e(n_queries, top_c), e(n_queries, top_c), e(n_queries, top_c, top_k),
+                      e(n_queries, top_c, top_k, dt=torch.int32))
+        self.rows = (e(n_queries, top_k, dt=torch.int32), e(n_queries, top_k),
+                     e(n_queries, top_k), e(n_queries), e(n_queries),
+                     e(n_queries, dt=torch.int32))
+        bs = ctypes.byref(bank.struct)
+        self.ws_coarse = _workspace(lib.htam_retrieve_coarse_workspace_size(bs, n_queries, top_c), dev)
+        self.ws_attend = _workspace(
+            lib.htam_attend_transitions_workspace_size(bs, n_queries, top_c, top_k), dev)
+
+    def run(self, q: torch.Tensor) -> dict:
+        htam_retrieve_coarse(self.bank, q, self.c, out=self.sel, ws=self.ws_coarse)
+        htam_attend_transitions(self.bank, q, self.sel[0], self.tau, self.k, out=self.slots,
+                                ws=self.ws_attend)
+        htam_topk(self.slots[2], self.slots[3], self.k, self.slots[0], self.slots[1], self.tau,
+                  out=self.rows)
+        return self.outputs()
+
+    def outputs(self) -> dict:
+        return dict(sel=self.sel[0], sel_score=self.sel[1], slot_max=self.slots[0],
+                    slot_sum=self.slots[1], slot_score=self.slots[2], slot_id=self.slots[3],
+                    id=self.rows[0], score=self.rows[1], weight=self.rows[2], m=self.rows[3],
+                    Z=self.rows[4], count=self.rows[5])
+
+
+def build_bank(cluster_of: torch.Tensor, keys_in: torch.Tensor, coarse_keys: torch.Tensor,
+               compute: str) -> Bank:
+    """Run htam_memory_build on records in arrival order and wrap the result as a Bank."""
+    keys_out, off, tid = htam_memory_build(cluster_of, keys_in, coarse_keys.shape[0])
+    return Bank(coarse_keys=coarse_keys, fine_keys=keys_out, seg_offsets=off, transition_id=tid,
+                compute=compute)
+
+
+def retrieve(bank: Bank, q: torch.Tensor, top_c: int, top_k: int, tau: float) -> dict:
+    """One hierarchical retrieval: coarse top-c, segment attention, top-k."""
+    return Retriever(bank, q.shape[0], top_c, top_k, tau).run(q)

@@ -1,0 +1,113 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle, on seeded
+workloads small enough for the oracle to finish in seconds, spanning several
+tiles, chunks and ragged tails, plus the method's degenerate cases."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_cases import run_case, say, to_np
+from paper_2605_29734_amd import synth
+
+pytestmark = pytest.mark.gpu
+S = synth.SPECS
+
+
+@pytest.mark.parametrize("tau", [1.0, 0.07])
+def test_paper_shaped_memory(tau):
+    """Five global nodes with 4/3/3/3/3 children, one direction, the best child (k = 1)."""
+    run_case(S["paper_htg"], tau=tau, determinism=True)
+
+
+def test_tiny_f32():
+    run_case(S["tiny_f32"], determinism=True)
+
+
+def test_zipf_bf16_full():
+    run_case(S["zipf_bf16"])
+
+
+def test_mixture_bf16_reduced():
+    run_case(synth.scaled(S["mixture_bf16"], B=128, G=64, N=65536))
+
+
+def test_zipf_large_bf16_reduced():
+    run_case(synth.scaled(S["zipf_large_bf16"], B=256, G=256, N=262144))
+
+
+def test_before_after_reduced():
+    run_case(synth.scaled(S["before_after_f32"], B=96, G=256, N=65536))
+
+
+@pytest.mark.parametrize("compute", ["bf16", "f32"])
+def test_ragged_shapes_and_tail_dim(compute):
+    """B, G not multiples of a tile; d not a multiple of the MFMA K step."""
+    st = "bf16" if compute == "bf16" else "f32"
+    run_case(synth.Spec("ragged", B=37, d=72, G=13, N=1000, top_c=3, top_k=7, tau=0.5, storage=st,
+                        compute=compute, sizes="zipf", zipf_s=1.0, min_size=1), determinism=True)
+
+
+def test_many_queries_per_cluster():
+    """More queries select one cluster than one pass over a chunk holds."""
+    run_case(synth.Spec("crowded", B=300, d=128, G=4, N=4000, top_c=2, top_k=16, tau=1.0,
+                        storage="bf16", compute="bf16", sizes="uniform"))
+
+
+def test_flat_retrieval_top_c_equals_G():
+    run_case(synth.Spec("flat", B=24, d=64, G=6, N=3000, top_c=6, top_k=32, tau=0.2,
+                        storage="bf16", compute="bf16", sizes="zipf", zipf_s=1.5, min_size=2))
+
+
+def test_short_and_empty_segments():
+    """k larger than most segments; empty clusters selected; one segment > half the bank."""
+    sizes = tuple([1100] + [0] * 10 + [30] * 29)
+    spec = synth.Spec("sparse", B=50, d=64, G=len(sizes), N=sum(sizes), top_c=4, top_k=100,
+                      tau=1.0, storage="f32", compute="f32", sizes="fixed", fixed_sizes=sizes,
+                      shuffled=True)
+    run_case(spec)
+
+
+def test_large_k():
+    run_case(synth.Spec("bigk", B=20, d=256, G=8, N=20000, top_c=3, top_k=256, tau=1.0,
+                        storage="bf16", compute="bf16", sizes="uniform"))
+
+
+def test_topk_merge_standalone():
+    """htam_topk on unsorted lists with padding and exact ties, against the oracle's sort."""
+    from paper_2605_29734_amd import htam
+    say("[case] htam_topk standalone")
+    rng = np.random.default_rng(0)
+    rows, lists, kin, k, tau = 33, 5, 40, 24, 0.3
+    sc = rng.standard_normal((rows, lists, kin)).astype(np.float32)
+    sc[:, 1, :10] = sc[:, 0, :10]                      # exact score ties, distinct ids
+    ids = rng.permutation(rows * lists * kin).reshape(rows, lists, kin).astype(np.int32) % 100000
+    ids[:, 2, 5:] = -1                                 # padding
+    ids[3] = -1                                        # an empty row
+    sm = np.where(ids >= 0, sc, -np.inf).max(2).astype(np.float32)   # max over real entries
+    ss = np.array([[np.exp((sc[r, l][ids[r, l] >= 0] - sm[r, l]) / tau).sum() if np.isfinite(sm[r, l])
+                    else 0.0 for l in range(lists)] for r in range(rows)], np.float32)
+    dev = torch.device("cuda:0")
+    t = lambda a: torch.from_numpy(a).to(dev)           # noqa: E731
+    out = htam.htam_topk(t(sc), t(ids), k, t(sm), t(ss), tau)
+    torch.cuda.synchronize()
+    oid, osc, ow, om, oz, oc = (to_np(x) for x in out)
+    for r in range(rows):
+        m = ids[r] >= 0
+        ref = oracle.attend(sc[r][m].astype(np.float64), ids[r][m], tau, k)
+        assert oc[r] == ref["count"]
+        np.testing.assert_array_equal(oid[r], ref["id"])          # fp32 inputs: exact ranking
+        np.testing.assert_array_equal(osc[r], ref["score"].astype(np.float32))
+        if ref["count"]:
+            np.testing.assert_allclose(ow[r], ref["weight"], rtol=1e-5, atol=1e-30)
+            np.testing.assert_allclose(np.log(oz[r]), np.log(ref["Z"]), rtol=0, atol=1e-5)
+            assert om[r] == np.float32(ref["m"])
+        else:
+            assert om[r] == -np.inf and oz[r] == 0 and np.all(ow[r] == 0)
+    # dense rows with implicit ids (the coarse selection path)
+    dense = rng.standard_normal((17, 1000)).astype(np.float32)
+    dense[:, 500] = dense[:, 20]
+    o2 = htam.htam_topk(t(dense), None, 50)
+    torch.cuda.synchronize()
+    for r in range(17):
+        order = np.lexsort((np.arange(1000), -dense[r].astype(np.float64)))[:50]
+        np.testing.assert_array_equal(to_np(o2[0])[r], order)
