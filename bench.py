@@ -1,0 +1,207 @@
+"""Throughput of hierarchical transition-attended retrieval on one MI355X.
+
+One step = one batch of queries through the whole retrieval path on the GPU:
+coarse scoring and top-c selection (htam_retrieve_coarse), the bank stream
+over the selected clusters' segments with softmax statistics and per-slot
+top-k (htam_attend_transitions), and the final merge into the top-k memories
+and their weights (htam_topk). Inputs (bank, queries) are resident in HBM
+before the timed region; the bank build is offline and untimed.
+
+Prints one JSON line: queries/s for the workload, the roofline position of the
+dominant kernel (the bank stream, HBM-bound), measured with HIP events around
+that kernel inside the timed region, and the CPU oracle timed on a sample of the
+same workload on the host's cores.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--gpus 1]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "retrieval queries/sec at fixed bank size; % HBM roofline and % MFMA peak"
+HBM_PEAK_GBS = 8000.0           # MI355X HBM3E
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
+DEFAULT_WORKLOAD = "zipf_bf16"  # 256 queries, d = 512, 256 clusters, 65,536 records
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def stream_kernel_traffic(workload: str):
+    """Measured HBM bytes per launch of the bank-stream kernel from a committed
+    rocprofv3 counter summary, valid only while the kernel source is unchanged."""
+    path = os.path.join(ROOT, "profiles", "fine_stream_traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        rec = json.load(open(path))
+        src = open(os.path.join(ROOT, "paper_2605_29734_amd", "csrc", "fine.hip"), "rb").read()
+        if rec.get("source_sha256") != hashlib.sha256(src).hexdigest():
+            return None
+        return rec.get("workloads", {}).get(workload, {}).get("bytes_per_launch")
+    except Exception:
+        return None
+
+
+def cpu_baseline(spec, w, bank, target_s: float):
+    """Time the CPU oracle on a sample of the workload's queries (host copies excluded)."""
+    import oracle
+    cores = int(os.environ.get("OMP_NUM_THREADS") or len(os.sched_getaffinity(0)))
+    q = w.queries.float().cpu().numpy()
+    c = w.coarse_keys.float().cpu().numpy()
+    off = bank.seg_offsets.cpu().numpy()
+    tid = bank.transition_id.cpu().numpy()
+    # sample: as many queries as keep the touched bank rows near 2^20
+    head = min(spec.B, 256)
+    qh = oracle.round_bf16(q[:head]) if spec.compute == "bf16" else q[:head]
+    ch = oracle.round_bf16(c) if spec.compute == "bf16" else c
+    sel, _ = oracle.coarse(qh, ch, spec.top_c)
+    lens = np.diff(off)
+    per_query = lens[sel].sum(1)
+    n = int(np.searchsorted(np.cumsum(per_query), 1 << 20)) + 1
+    rows = np.arange(min(head, max(n, 1)))
+    touched = np.unique(sel[rows])
+    seg = {}
+    for g in touched:                      # host copies of the touched segments, untimed
+        a, b = int(off[g]), int(off[g + 1])
+        seg[int(g)] = (a, bank.fine_keys[a:b].float().cpu().numpy())
+
+
+    def fetch(a, b):
+        g = int(np.searchsorted(off, a, side="right") - 1)
+        s0, arr = seg[g]
+        return arr[a - s0:b - s0]
+
+    done, t0 = 0, time.perf_counter()
+    while True:
+        oracle.retrieve(q, c, off, spec.top_c, spec.top_k, spec.tau, spec.compute,
+                        fetch_keys=fetch, transition_id=tid, rows=rows)
+        done += rows.size
+        el = time.perf_counter() - t0
+        if el >= target_s:
+            break
+    return {"value": done / el, "unit": "queries/s", "cores": cores, "kind": "oracle",
+            "sample": f"{rows.size} of {spec.B} queries x {done // rows.size} passes "
+                      f"({el:.1f} s; coarse scores over all {spec.G} clusters, fine stage over "
+                      f"the selected segments, fp64)"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py runs on exactly one GPU: multi-GPU runs are not part of this build "
+              "(how the path would shard is described in DESIGN.md)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2605_29734_amd import htam, synth
+    spec = synth.SPECS[args.workload]
+    dev = torch.device("cuda:0")
+    log(f"[bench] workload {spec.name}: generating on {dev}")
+    w = synth.make(spec, device=dev, seed=args.seed)
+    bank = htam.build_bank(w.cluster_of, w.keys_in, w.coarse_keys, spec.compute)
+    torch.cuda.synchronize()
+    del w.keys_in
+    q = w.queries
+    r = htam.Retriever(bank, spec.B, spec.top_c, spec.top_k, spec.tau)
+    log(f"[bench] warmup {args.warmup}")
+    for _ in range(args.warmup):
+        r.run(q)
+    torch.cuda.synchronize()
+
+    K = args.steps
+    mk = lambda: torch.cuda.Event(enable_timing=True)   # noqa: E731
+    ev_s = [(mk(), mk()) for _ in range(K)]
+    ev_c = [(mk(), mk()) for _ in range(K)]
+    for a, b in ev_s + ev_c:        # materialise the events before handing them to the library
+        a.record()
+        b.record()
+    start, end = mk(), mk()
+    torch.cuda.synchronize()
+    log(f"[bench] timing {K} steps")
+    t0 = time.perf_counter()
+    start.record()
+    for i in range(K):
+        htam.lib.htam_set_kernel_events(htam.HTAM_KERNEL_STREAM, ev_s[i][0].cuda_event,
+                                        ev_s[i][1].cuda_event)
+        htam.lib.htam_set_kernel_events(htam.HTAM_KERNEL_COARSE, ev_c[i][0].cuda_event,
+                                        ev_c[i][1].cuda_event)
+        r.run(q)
+    end.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    htam.lib.htam_set_kernel_events(htam.HTAM_KERNEL_STREAM, None, None)
+    htam.lib.htam_set_kernel_events(htam.HTAM_KERNEL_COARSE, None, None)
+    ms_step = start.elapsed_time(end) / K
+    t_stream = sum(a.elapsed_time(b) for a, b in ev_s) / K * 1e-3
+    t_coarse = sum(a.elapsed_time(b) for a, b in ev_c) / K * 1e-3
+
+    # algorithmic bytes of one bank-stream launch: every row of every selected
+    # segment read once, plus the queries
+    sel = r.sel[0].cpu().numpy()
+    off = bank.seg_offsets.cpu().numpy()
+    kb = bank.fine_keys.element_size()
+    touched = np.unique(sel)
+    rows_touched = int((off[touched + 1] - off[touched]).sum())
+    alg_bytes = rows_touched * spec.d * kb + spec.B * spec.d * q.element_size()
+    achieved = alg_bytes / t_stream / 1e9
+    coarse_flops = 2.0 * spec.B * spec.G * spec.d
+    pairs = int((off[sel + 1] - off[sel]).sum())
+
+    res = {
+        "metric": METRIC,
+        "value": spec.B * K / wall,
+        "unit": "queries/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if spec.compute == "bf16" else "f32",
+        "data": "synthetic",
+        "config": {"workload": spec.name, "queries": spec.B, "d": spec.d, "clusters": spec.G,
+                   "transitions": spec.N, "top_c": spec.top_c, "top_k": spec.top_k,
+                   "tau": spec.tau, "key_storage": spec.storage,
+                   "bank_bytes": int(spec.N * spec.d * kb)},
+        "roofline": {"bound": "hbm", "kernel": "fine_stream", "achieved": achieved,
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": stream_kernel_traffic(spec.name),
+                     "alg_bytes_per_launch": alg_bytes, "launch_ms": t_stream * 1e3},
+        "stages": {"coarse_scores_ms": t_coarse * 1e3,
+                   "coarse_tflops": coarse_flops / t_coarse / 1e12,
+                   "coarse_mfma_frac": coarse_flops / t_coarse / 1e12 / MFMA_BF16_PEAK_TFLOPS,
+                   "fine_stream_ms": t_stream * 1e3,
+                   "scored_pairs_per_step": pairs,
+                   "step_ms_event": ms_step, "step_ms_wall": wall / K * 1e3},
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] CPU oracle baseline")
+        res["cpu_baseline"] = cpu_baseline(spec, w, bank, args.cpu_seconds)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

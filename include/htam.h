@@ -223,6 +223,20 @@ htam_status htam_topk(int32_t n_rows, int32_t n_lists, int32_t k_in, const float
                       float *out_weight, float *row_max, float *row_sum, int32_t *out_count,
                       hipStream_t stream);
 
+/*
+ * Diagnostics: kernel timing hooks. After htam_set_kernel_events(which, before,
+ * after) with two hipEvent_t handles (passed as void *), every later call on
+ * the calling thread that launches kernel `which` records `before` on the
+ * call's stream just before that kernel and `after` just after it, so that
+ * hipEventElapsedTime gives the kernel's own duration. NULL handles switch the
+ * hook off. The events are owned by the caller.
+ *   HTAM_KERNEL_COARSE  the coarse scoring kernel (htam_retrieve_coarse);
+ *   HTAM_KERNEL_STREAM  the bank-streaming kernel (htam_attend_transitions).
+ */
+#define HTAM_KERNEL_COARSE 0
+#define HTAM_KERNEL_STREAM 1
+htam_status htam_set_kernel_events(int32_t which, void *before, void *after);
+
 /* Human-readable name of a status, and the last error message of the calling thread. */
 const char *htam_status_string(htam_status status);
 const char *htam_last_error(void);

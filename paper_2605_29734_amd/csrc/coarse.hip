@@ -91,8 +91,10 @@ CoarseWs coarse_layout(void *ws, int32_t B, int32_t G, size_t *bytes) {
 
 hipError_t launch_coarse(int32_t key_dtype, int32_t compute_dtype, int32_t d, int32_t G,
                          const void *coarse_keys, const void *q, int32_t B, int32_t top_c,
-                         int32_t *sel, float *sel_score, const CoarseWs &w, hipStream_t s) {
+                         int32_t *sel, float *sel_score, const CoarseWs &w, KernelEvents ev,
+                         hipStream_t s) {
     const dim3 grid((G + 63) / 64, (B + 63) / 64);
+    if (ev.before) hipEventRecord(ev.before, s);
     if (compute_dtype == kF32)
         hipLaunchKernelGGL((coarse_scores<float, false>), grid, dim3(256), 0, s,
                            static_cast<const float *>(q), static_cast<const float *>(coarse_keys),
@@ -105,6 +107,7 @@ hipError_t launch_coarse(int32_t key_dtype, int32_t compute_dtype, int32_t d, in
         hipLaunchKernelGGL((coarse_scores<__bf16, true>), grid, dim3(256), 0, s,
                            static_cast<const __bf16 *>(q), static_cast<const __bf16 *>(coarse_keys),
                            B, G, d, w.scores);
+    if (ev.after) hipEventRecord(ev.after, s);
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
     return launch_topk(B, 1, G, w.scores, nullptr, nullptr, nullptr, 1.0f, top_c, sel, sel_score,

@@ -499,12 +499,16 @@ AttendWs attend_layout(void *ws, int32_t d, int32_t G, int64_t N, int32_t key_by
 }
 
 template <typename T, bool BF16>
-static hipError_t launch_fine_stream(const FineArgs &fa, int grid, size_t smem, hipStream_t s) {
+static hipError_t launch_fine_stream(const FineArgs &fa, int grid, size_t smem, KernelEvents ev,
+                                     hipStream_t s) {
     auto kern = fine_stream<T, BF16>;
+    // allow more than 64 KiB of dynamic LDS (a function attribute, not a stream operation)
     hipError_t err = hipFuncSetAttribute((const void *)kern,
-                                         hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+                                         hipFuncAttributeMaxDynamicSharedMemorySize, 96 * 1024);
     if (err != hipSuccess) return err;
+    if (ev.before) hipEventRecord(ev.before, s);
     hipLaunchKernelGGL(kern, dim3(grid), dim3(kFineThreads), smem, s, fa);
+    if (ev.after) hipEventRecord(ev.after, s);
     return hipGetLastError();
 }
 
@@ -513,7 +517,7 @@ hipError_t launch_attend(int32_t key_dtype, int32_t compute_dtype, int32_t d, in
                          const int32_t *transition_id, const void *q, int32_t B,
                          const int32_t *sel, int32_t c, float tau, int32_t k, float *slot_max,
                          float *slot_sum, float *cand_score, int32_t *cand_id, const AttendWs &w,
-                         int n_cu, hipStream_t s) {
+                         int n_cu, KernelEvents ev, hipStream_t s) {
     const int64_t bc = (int64_t)B * c;
     const float cexp = 1.4426950408889634f / tau;
     const int gblocks = (int)((bc + 255) / 256 < 4096 ? (bc + 255) / 256 : 4096);
@@ -553,11 +557,11 @@ hipError_t launch_attend(int32_t key_dtype, int32_t compute_dtype, int32_t d, in
     if (grid > w.w_max) grid = w.w_max;
     if (grid < 1) grid = 1;
     if (compute_dtype == kF32)
-        err = launch_fine_stream<float, false>(fa, (int)grid, smem, s);
+        err = launch_fine_stream<float, false>(fa, (int)grid, smem, ev, s);
     else if (key_dtype == kF32)
-        err = launch_fine_stream<float, true>(fa, (int)grid, smem, s);
+        err = launch_fine_stream<float, true>(fa, (int)grid, smem, ev, s);
     else
-        err = launch_fine_stream<__bf16, true>(fa, (int)grid, smem, s);
+        err = launch_fine_stream<__bf16, true>(fa, (int)grid, smem, ev, s);
     if (err != hipSuccess) return err;
 
     MergeArgs ma{};

@@ -15,6 +15,7 @@
 namespace {
 
 thread_local std::string g_last_error;
+thread_local htam::KernelEvents g_events[2];
 
 htam_status fail(htam_status st, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
 htam_status fail(htam_status st, const char *fmt, ...) {
@@ -179,7 +180,8 @@ HTAM_API htam_status htam_retrieve_coarse(const htam_bank *bank, const void *q, 
     const htam::CoarseWs w = htam::coarse_layout(ws, n_queries, bank->n_clusters, nullptr);
     return device_status(htam::launch_coarse(bank->key_dtype, bank->compute_dtype, bank->d,
                                              bank->n_clusters, bank->coarse_keys, q, n_queries,
-                                             top_c, sel_cluster, sel_score, w, stream),
+                                             top_c, sel_cluster, sel_score, w,
+                                             g_events[HTAM_KERNEL_COARSE], stream),
                          "htam_retrieve_coarse");
 }
 
@@ -224,7 +226,8 @@ HTAM_API htam_status htam_attend_transitions(const htam_bank *bank, const void *
         htam::launch_attend(bank->key_dtype, bank->compute_dtype, bank->d, bank->n_clusters,
                             bank->n_transitions, bank->fine_keys, bank->seg_offsets,
                             bank->transition_id, q, n_queries, sel_cluster, top_c, tau, top_k,
-                            slot_max, slot_sum, cand_score, cand_id, w, n_cu, stream),
+                            slot_max, slot_sum, cand_score, cand_id, w, n_cu,
+                            g_events[HTAM_KERNEL_STREAM], stream),
         "htam_attend_transitions");
 }
 
@@ -272,3 +275,13 @@ HTAM_API const char *htam_status_string(htam_status st) {
 }
 
 HTAM_API const char *htam_last_error(void) { return g_last_error.c_str(); }
+
+HTAM_API htam_status htam_set_kernel_events(int32_t which, void *before, void *after) {
+    if (which != HTAM_KERNEL_COARSE && which != HTAM_KERNEL_STREAM)
+        return fail(HTAM_ERR_VALUE, "unknown kernel %d", which);
+    if ((before == nullptr) != (after == nullptr))
+        return fail(HTAM_ERR_NULL, "give both events or neither");
+    g_events[which].before = static_cast<hipEvent_t>(before);
+    g_events[which].after = static_cast<hipEvent_t>(after);
+    return ok();
+}

@@ -9,6 +9,11 @@ namespace htam {
 
 enum DType : int32_t { kF32 = 0, kBF16 = 1 };
 
+// Optional events recorded around one kernel (timing hooks of the C ABI).
+struct KernelEvents {
+    hipEvent_t before = nullptr, after = nullptr;
+};
+
 // Routing plan written on the device by the planning kernel of the fine stage.
 struct Plan {
     int64_t chunk;     // rows per work item (chunk of a segment)
@@ -52,7 +57,8 @@ struct CoarseWs {
 CoarseWs coarse_layout(void *ws, int32_t B, int32_t G, size_t *bytes);
 hipError_t launch_coarse(int32_t key_dtype, int32_t compute_dtype, int32_t d, int32_t G,
                          const void *coarse_keys, const void *q, int32_t B, int32_t top_c,
-                         int32_t *sel, float *sel_score, const CoarseWs &w, hipStream_t s);
+                         int32_t *sel, float *sel_score, const CoarseWs &w, KernelEvents ev,
+                         hipStream_t s);
 
 // ---- fine stage (routing + bank stream + per-slot merge) ----------------------
 struct AttendWs {
@@ -79,7 +85,7 @@ hipError_t launch_attend(int32_t key_dtype, int32_t compute_dtype, int32_t d, in
                          const int32_t *transition_id, const void *q, int32_t B,
                          const int32_t *sel, int32_t c, float tau, int32_t k, float *slot_max,
                          float *slot_sum, float *cand_score, int32_t *cand_id, const AttendWs &w,
-                         int n_cu, hipStream_t s);
+                         int n_cu, KernelEvents ev, hipStream_t s);
 
 // ---- top-k merge -----------------------------------------------------------
 hipError_t launch_topk(int32_t rows, int32_t lists, int32_t k_in, const float *score,

@@ -22,6 +22,9 @@ HTAM_MAX_TOP_K = 256
 HTAM_MAX_TOP_C = 256
 HTAM_MAX_DIM = 8192
 
+HTAM_KERNEL_COARSE = 0
+HTAM_KERNEL_STREAM = 1
+
 STATUS = {0: "HTAM_OK", -1: "HTAM_ERR_NULL", -2: "HTAM_ERR_SHAPE", -3: "HTAM_ERR_DTYPE",
           -4: "HTAM_ERR_VALUE", -5: "HTAM_ERR_WORKSPACE", -6: "HTAM_ERR_ALIGN",
           -7: "HTAM_ERR_DEVICE"}
@@ -58,6 +61,7 @@ def _load():
         "htam_attend_transitions": ([BP, P, i32, i32, P, i32, f32, i32, P, P, P, P, P, sz, P], i32),
         "htam_attend_transitions_workspace_size": ([BP, i32, i32, i32], sz),
         "htam_topk": ([i32, i32, i32, P, P, P, P, f32, i32, P, P, P, P, P, P, P], i32),
+        "htam_set_kernel_events": ([i32, P, P], i32),
         "htam_status_string": ([i32], ctypes.c_char_p),
         "htam_last_error": ([], ctypes.c_char_p),
     }
