@@ -1,5 +1,6 @@
 // Device helpers shared by the gfx950 kernels: MFMA fragment loads, ordered
-// 64-bit ranking keys, softmax-statistic merges and wave-level LDS sorting.
+// 64-bit ranking keys, softmax-statistic merges, and wave-level sorting and
+// top-k compaction in registers.
 #pragma once
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -75,60 +76,204 @@ __device__ __forceinline__ void wave_lds_sync() {
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
 }
 
-// Descending bitonic sort of n = 2^j (2 <= n) 64-bit keys in LDS by one wave.
-__device__ __forceinline__ void wave_sort_desc(uint64_t *a, int n, int lane) {
-    for (int size = 2; size <= n; size <<= 1) {
-        for (int stride = size >> 1; stride > 0; stride >>= 1) {
-            for (int i = lane; i < (n >> 1); i += kWave) {
-                const int lo = 2 * i - (i & (stride - 1));
-                const int hi = lo + stride;
-                const uint64_t x = a[lo], y = a[hi];
-                const bool desc = (lo & size) == 0;
-                if (desc ? (x < y) : (x > y)) { a[lo] = y; a[hi] = x; }
+
+// ---------------------------------------------------------------------------
+// Register-resident sorting networks over one wave. A list of 64*NPL keys is
+// held as v[j] on every lane, element index i = j*64 + lane. Every stage's
+// stride is a compile-time constant: strides >= 64 exchange registers within a
+// lane; strides 1..32 exchange across lanes without going through LDS:
+//   1, 2   quad permutations (DPP);
+//   4      two row rotations by 4 and 12 (DPP), one of them selected per lane;
+//   8      row rotation by 8 (DPP);
+//   16, 32 v_permlane16_swap / v_permlane32_swap (gfx950).
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ uint64_t shfl64(uint64_t v, int src) {
+    const uint32_t lo = __shfl((uint32_t)v, src);
+    const uint32_t hi = __shfl((uint32_t)(v >> 32), src);
+    return ((uint64_t)hi << 32) | lo;
+}
+
+// The value held by lane (lane ^ M).
+template <int M>
+__device__ __forceinline__ uint32_t lane_xor32(uint32_t x, int lane) {
+    if constexpr (M == 1) {
+        return (uint32_t)__builtin_amdgcn_mov_dpp((int)x, 0xB1, 0xF, 0xF, false);   // [1,0,3,2]
+    } else if constexpr (M == 2) {
+        return (uint32_t)__builtin_amdgcn_mov_dpp((int)x, 0x4E, 0xF, 0xF, false);   // [2,3,0,1]
+    } else if constexpr (M == 4) {
+        const uint32_t a = (uint32_t)__builtin_amdgcn_mov_dpp((int)x, 0x124, 0xF, 0xF, false);
+        const uint32_t b = (uint32_t)__builtin_amdgcn_mov_dpp((int)x, 0x12C, 0xF, 0xF, false);
+        return (lane & 4) ? a : b;
+    } else if constexpr (M == 8) {
+        return (uint32_t)__builtin_amdgcn_mov_dpp((int)x, 0x128, 0xF, 0xF, false);
+    } else if constexpr (M == 16) {
+        const auto r = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+        return (lane & 16) ? r[0] : r[1];
+    } else {
+        static_assert(M == 32, "lane_xor32: mask must be a power of two below 64");
+        const auto r = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+        return (lane & 32) ? r[0] : r[1];
+    }
+}
+template <int M>
+__device__ __forceinline__ uint64_t lane_xor64(uint64_t v, int lane) {
+    const uint32_t lo = lane_xor32<M>((uint32_t)v, lane);
+    const uint32_t hi = lane_xor32<M>((uint32_t)(v >> 32), lane);
+    return ((uint64_t)hi << 32) | lo;
+}
+
+template <int NPL>
+struct Log2Npl {
+    static constexpr int value = NPL == 1 ? 6 : NPL == 2 ? 7 : NPL == 4 ? 8 : NPL == 8 ? 9 : -1;
+};
+
+// One compare-exchange stage: elements i and i ^ STRIDE, the pair ordered
+// descending when desc_all, else by the bitonic-sort rule for block `size`.
+template <int NPL, int STRIDE>
+__device__ __forceinline__ void wave_cx(uint64_t (&v)[NPL], int lane, int size, bool desc_all) {
+    if constexpr (STRIDE >= kWave) {
+        constexpr int js = STRIDE / kWave;
+#pragma unroll
+        for (int j = 0; j < NPL; ++j) {
+            if ((j & js) == 0) {
+                const int j2 = j | js;
+                const bool desc = desc_all || ((j * kWave) & size) == 0;
+                const uint64_t x = v[j], y = v[j2];
+                const bool sw = desc ? (x < y) : (x > y);
+                v[j] = sw ? y : x;
+                v[j2] = sw ? x : y;
             }
-            wave_lds_sync();
+        }
+    } else {
+        const bool lo = (lane & STRIDE) == 0;
+#pragma unroll
+        for (int j = 0; j < NPL; ++j) {
+            const uint64_t y = lane_xor64<STRIDE>(v[j], lane);
+            const bool desc = desc_all || ((j * kWave + lane) & size) == 0;
+            const uint64_t mx = v[j] > y ? v[j] : y, mn = v[j] > y ? y : v[j];
+            v[j] = (lo == desc) ? mx : mn;
         }
     }
+}
+
+// Stages of block size 2^LS with strides 2^LT, 2^(LT-1), ..., 1, on NB lists
+// side by side (independent exchanges overlap).
+template <int NB, int NPL, int LS, int LT>
+struct BitonicStages {
+    __device__ static __forceinline__ void run(uint64_t (&v)[NB][NPL], int lane) {
+#pragma unroll
+        for (int b = 0; b < NB; ++b) wave_cx<NPL, (1 << LT)>(v[b], lane, 1 << LS, false);
+        if constexpr (LT > 0) BitonicStages<NB, NPL, LS, LT - 1>::run(v, lane);
+    }
+};
+template <int NB, int NPL, int LS>
+struct BitonicSort {
+    __device__ static __forceinline__ void run(uint64_t (&v)[NB][NPL], int lane) {
+        if constexpr (LS > 1) BitonicSort<NB, NPL, LS - 1>::run(v, lane);
+        BitonicStages<NB, NPL, LS, LS - 1>::run(v, lane);
+    }
+};
+template <int NPL, int LT>
+struct MergeStages {
+    __device__ static __forceinline__ void run(uint64_t (&v)[NPL], int lane) {
+        wave_cx<NPL, (1 << LT)>(v, lane, 0, true);
+        if constexpr (LT > 0) MergeStages<NPL, LT - 1>::run(v, lane);
+    }
+};
+
+// Sort NB lists of 64*NPL keys each, descending, side by side.
+template <int NB, int NPL>
+__device__ __forceinline__ void wave_sort_multi(uint64_t (&v)[NB][NPL], int lane) {
+    BitonicSort<NB, NPL, Log2Npl<NPL>::value>::run(v, lane);
+}
+
+// Sort 64*NPL keys descending.
+template <int NPL>
+__device__ __forceinline__ void wave_sort_regs(uint64_t (&v)[NPL], int lane) {
+    uint64_t(&w)[1][NPL] = *reinterpret_cast<uint64_t(*)[1][NPL]>(&v);
+    BitonicSort<1, NPL, Log2Npl<NPL>::value>::run(w, lane);
+}
+
+// a, b: sorted descending. Leaves in a the 64*NPL largest of a and b, sorted.
+template <int NPL>
+__device__ __forceinline__ void wave_merge_top(uint64_t (&a)[NPL], const uint64_t (&b)[NPL],
+                                               int lane) {
+#pragma unroll
+    for (int j = 0; j < NPL; ++j) {
+        const uint64_t rb = shfl64(b[NPL - 1 - j], kWave - 1 - lane);
+        a[j] = a[j] > rb ? a[j] : rb;      // bitonic: the top half of a u b
+    }
+    MergeStages<NPL, Log2Npl<NPL>::value - 1>::run(a, lane);
+}
+
+// Element i (held by lane i % 64 as v[i / 64]) broadcast to the whole wave.
+template <int NPL>
+__device__ __forceinline__ uint64_t wave_element(const uint64_t (&v)[NPL], int i) {
+    uint64_t x = 0;
+#pragma unroll
+    for (int j = 0; j < NPL; ++j)
+        if (j == i / kWave) x = v[j];
+    return shfl64(x, i % kWave);
+}
+
+// Compaction of a top-k buffer of n keys (n > k, capacity 64*NPL) by one wave.
+// A radix select over the keys' high halves (the ordered scores) finds T, the
+// k-th largest score in the buffer; every key scoring >= T is kept (so all
+// exact ties at T stay) and the threshold becomes T: later keys must score
+// above it, or tie it with a valid id. If the ties at T leave fewer than
+// `room` free slots, the buffer is sorted instead and cut to exactly k keys
+// (threshold = the k-th key). Returns the new count.
+template <int NPL>
+__device__ __forceinline__ int compact_select(uint64_t *buf, int n, int k, int room, int lane,
+                                              uint64_t &theta) {
+    constexpr int cap = NPL * kWave;
+    uint64_t v[NPL];
+    uint32_t hi[NPL];
+#pragma unroll
+    for (int q = 0; q < NPL; ++q) {
+        v[q] = (q * kWave + lane < n) ? buf[q * kWave + lane] : 0;
+        hi[q] = (uint32_t)(v[q] >> 32);
+    }
+    uint32_t T = 0;
+#pragma unroll
+    for (int bit = 31; bit >= 0; --bit) {
+        const uint32_t cand = T | (1u << bit);
+        int c = 0;
+#pragma unroll
+        for (int q = 0; q < NPL; ++q) c += __popcll(__ballot(hi[q] >= cand));
+        if (c >= k) T = cand;
+    }
+    const uint64_t lt_mask = (1ull << lane) - 1;
+    int keep = 0;
+#pragma unroll
+    for (int q = 0; q < NPL; ++q) keep += __popcll(__ballot(hi[q] >= T && v[q] != 0));
+    wave_lds_sync();
+    if (keep <= cap - room) {
+        int base = 0;
+#pragma unroll
+        for (int q = 0; q < NPL; ++q) {
+            const bool pass = hi[q] >= T && v[q] != 0;
+            const uint64_t mask = __ballot(pass);
+            if (pass) buf[base + __popcll(mask & lt_mask)] = v[q];
+            base += __popcll(mask);
+        }
+        theta = (uint64_t)T << 32;
+        wave_lds_sync();
+        return keep;
+    }
+    wave_sort_regs<NPL>(v, lane);
+#pragma unroll
+    for (int q = 0; q < NPL; ++q)
+        if (q * kWave + lane < k) buf[q * kWave + lane] = v[q];
+    theta = wave_element<NPL>(v, k - 1);
+    wave_lds_sync();
+    return k;
 }
 
 __host__ __device__ constexpr int next_pow2(int x) {
     int p = 1;
     while (p < x) p <<= 1;
     return p;
-}
-
-// ---------------------------------------------------------------------------
-// Top-k accumulator of one row in LDS: a buffer of `cap` (a power of two)
-// keys, a fill count and a threshold (the k-th best key seen once at least k
-// keys were kept; 0 before). Keys above the threshold are appended with an LDS
-// atomic; a compaction sorts the buffer and keeps the k best. The caller
-// compacts whenever fewer free slots remain than it may append before the
-// next compaction point, so an append never overflows.
-// ---------------------------------------------------------------------------
-struct TopkRow {
-    uint64_t *buf;
-    uint32_t *cnt;
-    uint64_t *theta;
-};
-
-__device__ __forceinline__ void topk_offer(const TopkRow &r, uint64_t key) {
-    if (key > *r.theta) {
-        const uint32_t p = atomicAdd(r.cnt, 1u);
-        r.buf[p] = key;
-    }
-}
-
-// Compact (one wave): sort the kept keys and keep the best k.
-__device__ __forceinline__ void topk_compact(const TopkRow &r, int k, int lane) {
-    const int n = (int)*r.cnt;
-    const int np = next_pow2(n < 2 ? 2 : n);
-    for (int i = n + lane; i < np; i += kWave) r.buf[i] = 0;
-    wave_lds_sync();
-    wave_sort_desc(r.buf, np, lane);
-    if (lane == 0) {
-        if (n >= k) { *r.cnt = (uint32_t)k; *r.theta = r.buf[k - 1]; }
-    }
-    wave_lds_sync();
 }
 
 }  // namespace htam

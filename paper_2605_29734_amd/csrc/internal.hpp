@@ -74,9 +74,8 @@ struct AttendWs {
     float *pz;         // [P] partial sum
     int32_t *pc;       // [P] partial kept count
     uint64_t *pk;      // [P][k] partial keys, descending
-    int64_t p_cap;
-    int64_t chunk_min;
-    int64_t w_max;
+    int64_t p_cap;     // partial results the workspace holds (>= B*c)
+    int64_t w_max;     // bound on work items (grid sizing)
 };
 AttendWs attend_layout(void *ws, int32_t d, int32_t G, int64_t N, int32_t key_bytes, int32_t B,
                        int32_t c, int32_t k, size_t *bytes);

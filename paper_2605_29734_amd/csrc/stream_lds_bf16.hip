@@ -1,0 +1,8 @@
+// Bank-streaming kernel, LDS-staged queries, bf16 key storage (see stream.hpp).
+#include "stream.hpp"
+
+namespace htam {
+hipError_t launch_stream_lds_bf16(int npl, bool has_tid, const StreamLaunch &l) {
+    return launch_stream_lds_t<__bf16>(npl, has_tid, l);
+}
+}  // namespace htam

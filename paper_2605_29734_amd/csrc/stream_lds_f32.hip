@@ -1,0 +1,9 @@
+// Bank-streaming kernel, LDS-staged queries, fp32 key storage rounded to bf16
+// for the MFMA (see stream.hpp).
+#include "stream.hpp"
+
+namespace htam {
+hipError_t launch_stream_lds_f32(int npl, bool has_tid, const StreamLaunch &l) {
+    return launch_stream_lds_t<float>(npl, has_tid, l);
+}
+}  // namespace htam

@@ -3,9 +3,11 @@
 // union of a query's candidate lists, with the temperature-softmax statistics
 // of the lists merged into the row's (max, sum) and per-candidate weights.
 //
-// One block of 256 threads per row. Candidates stream through a threshold
-// filter into an LDS buffer (see TopkRow); the buffer is compacted by one wave
-// whenever the next round of 256 offers might not fit.
+// One wave per row. Candidates are read 8 x 64 at a time; those above the
+// row's threshold are appended to the wave's LDS buffer (positions from a
+// ballot prefix count, no atomics). When fewer than 64 free slots remain the
+// buffer is cut down by a radix select (compact_select), which raises the
+// threshold to the k-th best score.
 #include "dev.hpp"
 #include "internal.hpp"
 
@@ -13,12 +15,12 @@ namespace htam {
 
 namespace {
 
-constexpr int kTopkThreads = 256;
-constexpr int kTopkWaves = kTopkThreads / kWave;
+constexpr int kTopkWaves = 4;
+constexpr int kTopkBatch = 8;          // 64-entry groups loaded before they are offered
 
 struct TopkArgs {
-    int64_t n;                    // entries per row = lists * k_in
-    int32_t lists, top_k, cap;
+    int64_t rows, n;              // entries per row = lists * k_in
+    int32_t lists, top_k;
     float cexp;                   // log2(e) / tau
     const float *score;
     const int32_t *id;            // nullable: id = position in the row
@@ -28,80 +30,80 @@ struct TopkArgs {
     int32_t *out_count;
 };
 
-__global__ __launch_bounds__(kTopkThreads) void topk_rows(TopkArgs a) {
+// cap = 64 * NPL >= top_k + 64 keys of LDS per wave.
+template <int NPL>
+__global__ __launch_bounds__(kWave * kTopkWaves) void topk_rows(TopkArgs a) {
     extern __shared__ __align__(16) uint64_t tbuf[];
-    __shared__ uint32_t s_cnt, s_total;
-    __shared__ uint64_t s_theta;
-    __shared__ float s_m[kTopkWaves], s_z[kTopkWaves];
-    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-    const int64_t row = blockIdx.x;
+    constexpr int cap = NPL * kWave;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int64_t row = (int64_t)blockIdx.x * kTopkWaves + wave;
+    if (row >= a.rows) return;              // no block-wide synchronisation below
+    uint64_t *buf = tbuf + wave * cap;
     const float *sc = a.score + row * a.n;
     const int32_t *ids = a.id ? a.id + row * a.n : nullptr;
-    if (t == 0) { s_cnt = 0; s_total = 0; s_theta = 0; }
-    __syncthreads();
-    TopkRow acc{tbuf, &s_cnt, &s_theta};
+    const uint64_t lt_mask = (1ull << lane) - 1;
 
-    uint32_t mine = 0;
-    for (int64_t base = 0; base < a.n; base += kTopkThreads) {
-        const int64_t i = base + t;
-        if (i < a.n) {
-            const int32_t cid = ids ? ids[i] : (int32_t)i;
-            if (cid >= 0) {
-                ++mine;
-                const float s = sc[i];
-                if (ord_of(s) >= (uint32_t)(s_theta >> 32)) topk_offer(acc, make_key(s, cid));
+    int cnt = 0, total = 0;
+    uint64_t theta = 0;
+    for (int64_t base = 0; base < a.n; base += kWave * kTopkBatch) {
+        float s[kTopkBatch];
+        int32_t cid[kTopkBatch];
+#pragma unroll
+        for (int u = 0; u < kTopkBatch; ++u) {
+            const int64_t i = base + u * kWave + lane;
+            const int64_t ic = i < a.n ? i : a.n - 1;
+            s[u] = sc[ic];
+            cid[u] = i < a.n ? (ids ? ids[ic] : (int32_t)i) : -1;
+        }
+#pragma unroll
+        for (int u = 0; u < kTopkBatch; ++u) {
+            const bool ok = cid[u] >= 0;
+            total += __popcll(__ballot(ok));
+            const uint64_t key = ok ? make_key(s[u], cid[u]) : 0;
+            const bool pass = ok && key > theta;
+            const uint64_t mask = __ballot(pass);
+            if (pass) buf[cnt + __popcll(mask & lt_mask)] = key;
+            cnt += __popcll(mask);
+            if (cnt > cap - kWave) {
+                wave_lds_sync();
+                cnt = compact_select<NPL>(buf, cnt, a.top_k, kWave, lane, theta);
             }
         }
-        __syncthreads();
-        if ((int)s_cnt > a.cap - kTopkThreads) {
-            if (wave == 0) topk_compact(acc, a.top_k, lane);
-        }
-        __syncthreads();
     }
-    atomicAdd(&s_total, mine);
 
     // merged softmax statistics of the row's lists
     float M = -INFINITY, Z = 0.0f;
     if (a.slot_max) {
-        for (int l = t; l < a.lists; l += kTopkThreads)
+        for (int l = lane; l < a.lists; l += kWave)
             mz_merge(M, Z, a.slot_max[row * a.lists + l], a.slot_sum[row * a.lists + l], a.cexp);
         for (int sh = 32; sh >= 1; sh >>= 1) {
             const float m2 = __shfl_xor(M, sh), z2 = __shfl_xor(Z, sh);
             mz_merge(M, Z, m2, z2, a.cexp);
         }
-        if (lane == 0) { s_m[wave] = M; s_z[wave] = Z; }
-    }
-    __syncthreads();
-    if (a.slot_max) {
-        M = -INFINITY;
-        Z = 0.0f;
-        for (int w = 0; w < kTopkWaves; ++w) mz_merge(M, Z, s_m[w], s_z[w], a.cexp);
     }
 
-    if (wave == 0) {
-        const int cn = (int)s_cnt;
-        const int np = next_pow2(cn < 2 ? 2 : cn);
-        for (int i = cn + lane; i < np; i += kWave) tbuf[i] = 0;
-        wave_lds_sync();
-        wave_sort_desc(tbuf, np, lane);
-        const int kept = cn < a.top_k ? cn : a.top_k;
-        for (int r = lane; r < a.top_k; r += kWave) {
-            const uint64_t key = tbuf[r];
+    wave_lds_sync();
+    uint64_t v[NPL];
+#pragma unroll
+    for (int q = 0; q < NPL; ++q) v[q] = (q * kWave + lane < cnt) ? buf[q * kWave + lane] : 0;
+    wave_sort_regs<NPL>(v, lane);
+    const int kept = cnt < a.top_k ? cnt : a.top_k;
+#pragma unroll
+    for (int q = 0; q < NPL; ++q) {
+        const int r = q * kWave + lane;
+        if (r < a.top_k) {
             const bool ok = r < kept;
-            const float s = ok ? key_score(key) : -INFINITY;
-            a.out_id[row * a.top_k + r] = ok ? key_id(key) : -1;
-            if (a.out_score) a.out_score[row * a.top_k + r] = s;
+            const float sv = ok ? key_score(v[q]) : -INFINITY;
+            a.out_id[row * a.top_k + r] = ok ? key_id(v[q]) : -1;
+            if (a.out_score) a.out_score[row * a.top_k + r] = sv;
             if (a.out_weight)
-                a.out_weight[row * a.top_k + r] = ok ? exp2f((s - M) * a.cexp) / Z : 0.0f;
+                a.out_weight[row * a.top_k + r] = ok ? exp2f((sv - M) * a.cexp) / Z : 0.0f;
         }
-        if (lane == 0) {
-            if (a.row_max) a.row_max[row] = M;
-            if (a.row_sum) a.row_sum[row] = Z;
-            if (a.out_count) {
-                const uint32_t tot = s_total;
-                a.out_count[row] = (int32_t)(tot < (uint32_t)a.top_k ? tot : (uint32_t)a.top_k);
-            }
-        }
+    }
+    if (lane == 0) {
+        if (a.row_max) a.row_max[row] = M;
+        if (a.row_sum) a.row_sum[row] = Z;
+        if (a.out_count) a.out_count[row] = total < a.top_k ? total : a.top_k;
     }
 }
 
@@ -113,10 +115,10 @@ hipError_t launch_topk(int32_t rows, int32_t lists, int32_t k_in, const float *s
                        float *row_max, float *row_sum, int32_t *out_count, hipStream_t s) {
     if (rows == 0) return hipSuccess;
     TopkArgs a{};
+    a.rows = rows;
     a.n = (int64_t)lists * k_in;
     a.lists = lists;
     a.top_k = top_k;
-    a.cap = next_pow2(top_k + kTopkThreads);
     a.cexp = 1.4426950408889634f / tau;
     a.score = score;
     a.id = id;
@@ -128,7 +130,15 @@ hipError_t launch_topk(int32_t rows, int32_t lists, int32_t k_in, const float *s
     a.row_max = row_max;
     a.row_sum = row_sum;
     a.out_count = out_count;
-    hipLaunchKernelGGL(topk_rows, dim3(rows), dim3(kTopkThreads), (size_t)a.cap * 8, s, a);
+    const int npl = next_pow2(top_k + kWave) / kWave;
+    const dim3 grid((unsigned)((rows + kTopkWaves - 1) / kTopkWaves)), block(kWave * kTopkWaves);
+    const size_t smem = (size_t)kTopkWaves * npl * kWave * 8;
+    switch (npl) {
+        case 2: hipLaunchKernelGGL(topk_rows<2>, grid, block, smem, s, a); break;
+        case 4: hipLaunchKernelGGL(topk_rows<4>, grid, block, smem, s, a); break;
+        case 8: hipLaunchKernelGGL(topk_rows<8>, grid, block, smem, s, a); break;
+        default: return hipErrorInvalidValue;
+    }
     return hipGetLastError();
 }
 

@@ -67,9 +67,19 @@ def test_short_and_empty_segments():
     run_case(spec)
 
 
-def test_large_k():
-    run_case(synth.Spec("bigk", B=20, d=256, G=8, N=20000, top_c=3, top_k=256, tau=1.0,
+@pytest.mark.parametrize("d", [256, 512])
+def test_large_k(d):
+    """k = 256 (the largest top-k buffers); d = 512 runs the LDS-staged kernel, d = 256 the generic one."""
+    run_case(synth.Spec("bigk", B=20, d=d, G=8, N=20000, top_c=3, top_k=256, tau=1.0,
                         storage="bf16", compute="bf16", sizes="uniform"))
+
+
+@pytest.mark.parametrize("storage", ["bf16", "f32"])
+def test_many_queries_per_cluster_lds_kernel(storage):
+    """More queries per cluster than one pass of the LDS-staged kernel holds (several passes)."""
+    run_case(synth.Spec("crowded_lds", B=400, d=512, G=4, N=6000, top_c=2, top_k=32, tau=0.3,
+                        storage=storage, compute="bf16", sizes="zipf", zipf_s=0.5, min_size=100),
+             determinism=True)
 
 
 def test_topk_merge_standalone():
