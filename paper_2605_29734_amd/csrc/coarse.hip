@@ -1,12 +1,21 @@
 // Coarse stage on gfx950: the global-direction score of every cluster for
 // every query (Alg. 1 Step 2; Eq. score with a one-term prefix and the linear
-// scorer of App. B.6: an inner product), S = Q C^T on MFMA, then the top_c
-// clusters of each row (greedy limit of Eq. global direction).
+// scorer of App. B.6: an inner product), S = Q C^T, then the top_c clusters
+// of each row (the greedy limit of Eq. global direction).
 //
-// Block tile 64 queries x 64 clusters (4 waves, each 32 x 32 = 2 x 2 MFMA
-// 16x16 tiles), operands loaded straight from global memory in MFMA fragment
-// layout; scores go to a [B][G] fp32 workspace and the top-c selection runs
-// the row-wise top-k kernel over it with implicit ids.
+// bf16 arithmetic: an LDS-tiled MFMA GEMM (v_mfma_f32_16x16x32_bf16).
+//   block tile 256 queries x 256 clusters, 8 waves (2 x 4), each wave
+//   128 x 64 = 8 x 4 MFMA tiles; K staged 64 at a time through two LDS
+//   buffers (rows padded to 144 bytes so that fragment reads are free of bank
+//   conflicts); global loads for the next stage are in flight during the
+//   current stage's MFMAs; tiles ordered so that the blocks of one XCD share
+//   query rows in their L2. fp32 inputs are rounded to bf16 once per call.
+// Too few 256 x 256 tiles to fill the GPU: 64 x 64 tiles read directly from
+//   global memory in MFMA fragment layout.
+// fp32 arithmetic (small configurations): a direct MFMA kernel on
+//   v_mfma_f32_16x16x4f32.
+// The scores go to a [B][G] fp32 workspace; the top-c selection is the
+// row-wise top-k kernel with implicit ids.
 #include "dev.hpp"
 #include "internal.hpp"
 
@@ -14,10 +23,136 @@ namespace htam {
 
 namespace {
 
-template <typename T, bool BF16>
-__global__ __launch_bounds__(256) void coarse_scores(const T *__restrict__ q,
-                                                     const T *__restrict__ ck, int32_t B,
-                                                     int32_t G, int32_t d, float *__restrict__ S) {
+constexpr int BM = 256, BN = 256, BK = 64;
+constexpr int kGemmThreads = 512;
+constexpr int kLdsRow = BK + 8;                  // bf16 elements per padded LDS row
+constexpr int kStageElems = (BM + BN) * kLdsRow;
+constexpr int kChunksPerStage = (BM + BN) * BK / 8;       // 16-byte chunks
+constexpr int kChunksPerThread = kChunksPerStage / kGemmThreads;
+constexpr size_t kGemmLds = (size_t)2 * kStageElems * 2;  // bytes, two stages
+
+// fp32 -> bf16 (round to nearest even), 8 elements per thread.
+__global__ void to_bf16(const float *__restrict__ x, __bf16 *__restrict__ y, int64_t n8) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n8;
+         i += (int64_t)gridDim.x * blockDim.x)
+        reinterpret_cast<bf16x8_t *>(y)[i] = load8(x + i * 8);
+}
+
+// Tile of block b: the blocks that run on one XCD (b % 8) take consecutive
+// tiles, and within that range tiles go column-major in groups of 8 row tiles.
+__device__ __forceinline__ void gemm_tile(int b, int nb, int tm, int tn, int &mt, int &nt) {
+    const int xcd = b % 8, per = (nb + 7) / 8;
+    int lin = xcd * per + b / 8;
+    if (lin >= nb) lin = b;                       // nb not a multiple of 8: keep a bijection
+    const int group = 8 * tn;
+    const int g = lin / group, first_m = g * 8;
+    const int gm = min(tm - first_m, 8);
+    const int in = lin - g * group;
+    mt = first_m + in % gm;
+    nt = in / gm;
+}
+
+__device__ __forceinline__ void gemm_load_stage(uint4 (&stage)[kChunksPerThread],
+                                                const __bf16 *const (&src)[kChunksPerThread],
+                                                const int (&col)[kChunksPerThread], int k0, int d) {
+#pragma unroll
+    for (int i = 0; i < kChunksPerThread; ++i)
+        stage[i] = (k0 + col[i] < d) ? *reinterpret_cast<const uint4 *>(src[i] + k0)
+                                     : make_uint4(0, 0, 0, 0);
+}
+
+__device__ __forceinline__ void gemm_store_stage(const uint4 (&stage)[kChunksPerThread],
+                                                 const int (&dst)[kChunksPerThread], __bf16 *base) {
+#pragma unroll
+    for (int i = 0; i < kChunksPerThread; ++i) *reinterpret_cast<uint4 *>(base + dst[i]) = stage[i];
+}
+
+__global__ __launch_bounds__(kGemmThreads) void coarse_gemm(const __bf16 *__restrict__ q,
+                                                            const __bf16 *__restrict__ ck,
+                                                            int32_t B, int32_t G, int32_t d,
+                                                            float *__restrict__ S) {
+    extern __shared__ __align__(16) __bf16 lds[];
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    const int r16 = lane & 15, kg = lane >> 4;
+    const int wm = wave >> 2, wn = wave & 3;
+    const int tm = (B + BM - 1) / BM, tn = (G + BN - 1) / BN;
+    int mt, nt;
+    if (tm * tn % 8 == 0) gemm_tile(blockIdx.x, tm * tn, tm, tn, mt, nt);
+    else { mt = blockIdx.x / tn; nt = blockIdx.x % tn; }
+    const int64_t m0 = (int64_t)mt * BM, n0 = (int64_t)nt * BN;
+
+    // this thread's chunks of a stage: rows 0..255 of Q's tile, then of C's tile
+    const __bf16 *src[kChunksPerThread];
+    int dst[kChunksPerThread], col[kChunksPerThread];
+#pragma unroll
+    for (int i = 0; i < kChunksPerThread; ++i) {
+        const int c = t + i * kGemmThreads;
+        const int row = c / (BK / 8), cc = c % (BK / 8);
+        col[i] = cc * 8;
+        dst[i] = row * kLdsRow + cc * 8;
+        if (row < BM) {
+            const int64_t r = min(m0 + row, (int64_t)B - 1);
+            src[i] = q + r * d + cc * 8;
+        } else {
+            const int64_t r = min(n0 + row - BM, (int64_t)G - 1);
+            src[i] = ck + r * d + cc * 8;
+        }
+    }
+    uint4 stage[kChunksPerThread];
+    const int nk = (d + BK - 1) / BK;
+    f32x4_t acc[8][4];
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+    gemm_load_stage(stage, src, col, 0, d);
+    gemm_store_stage(stage, dst, lds);
+    __syncthreads();
+    for (int ks = 0; ks < nk; ++ks) {
+        const int cur = ks & 1;
+        if (ks + 1 < nk) gemm_load_stage(stage, src, col, (ks + 1) * BK, d);
+        const __bf16 *As = lds + cur * kStageElems + (wm * 128 + r16) * kLdsRow + kg * 8;
+        const __bf16 *Bs = lds + cur * kStageElems + (BM + wn * 64 + r16) * kLdsRow + kg * 8;
+#pragma unroll
+        for (int kk = 0; kk < BK; kk += 32) {
+            bf16x8_t a[8], b[4];
+#pragma unroll
+            for (int i = 0; i < 8; ++i)
+                a[i] = *reinterpret_cast<const bf16x8_t *>(As + i * 16 * kLdsRow + kk);
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                b[j] = *reinterpret_cast<const bf16x8_t *>(Bs + j * 16 * kLdsRow + kk);
+#pragma unroll
+            for (int i = 0; i < 8; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+        }
+        if (ks + 1 < nk) gemm_store_stage(stage, dst, lds + (cur ^ 1) * kStageElems);
+        __syncthreads();
+    }
+
+    // D[m][n]: this lane holds rows 4*kg + e of each 16x16 tile, column r16.
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int64_t r = m0 + wm * 128 + i * 16 + 4 * kg + e;
+                const int64_t c = n0 + wn * 64 + j * 16 + r16;
+                if (r < B && c < G) S[r * G + c] = acc[i][j][e];
+            }
+}
+
+// Small problems (fewer 256 x 256 tiles than compute units): 64 x 64 block
+// tiles, 4 waves of 32 x 32, operands read directly in MFMA fragment layout.
+template <typename T>
+__global__ __launch_bounds__(256) void coarse_small_bf16(const T *__restrict__ q,
+                                                         const T *__restrict__ ck, int32_t B,
+                                                         int32_t G, int32_t d,
+                                                         float *__restrict__ S) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int r16 = lane & 15, kg = lane >> 4;
     const int64_t row0 = (int64_t)blockIdx.y * 64 + (wave >> 1) * 32;
@@ -34,40 +169,66 @@ __global__ __launch_bounds__(256) void coarse_scores(const T *__restrict__ q,
     for (int i = 0; i < 2; ++i)
 #pragma unroll
         for (int j = 0; j < 2; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-
-    if constexpr (BF16) {
-        for (int k0 = 0; k0 < d; k0 += 32) {
-            const int k = k0 + kg * 8;
-            const bool ok = k < d;
-            bf16x8_t a[2], b[2];
+    for (int k0 = 0; k0 < d; k0 += 32) {
+        const int k = k0 + kg * 8;
+        const bool ok = k < d;
+        bf16x8_t a[2], b[2];
 #pragma unroll
-            for (int i = 0; i < 2; ++i) {
-                a[i] = ok ? load8(qp[i] + k) : zero8();
-                b[i] = ok ? load8(cp[i] + k) : zero8();
-            }
-#pragma unroll
-            for (int i = 0; i < 2; ++i)
-#pragma unroll
-                for (int j = 0; j < 2; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+        for (int i = 0; i < 2; ++i) {
+            a[i] = ok ? load8(qp[i] + k) : zero8();
+            b[i] = ok ? load8(cp[i] + k) : zero8();
         }
-    } else {
-        for (int k0 = 0; k0 < d; k0 += 4) {
-            const int k = k0 + kg;
-            float a[2], b[2];
 #pragma unroll
-            for (int i = 0; i < 2; ++i) {
-                a[i] = (float)qp[i][k];
-                b[i] = (float)cp[i][k];
-            }
+        for (int i = 0; i < 2; ++i)
 #pragma unroll
-            for (int i = 0; i < 2; ++i)
-#pragma unroll
-                for (int j = 0; j < 2; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i], b[j], acc[i][j], 0, 0, 0);
-        }
+            for (int j = 0; j < 2; ++j)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
     }
-    // D[m][n]: this lane holds rows 4*kg + e of the 16x16 tile, column r16.
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int64_t r = row0 + 16 * i + 4 * kg + e, c = col0 + 16 * j + r16;
+                if (r < B && c < G) S[r * G + c] = acc[i][j][e];
+            }
+}
+
+// fp32 arithmetic: 64 x 64 block tiles, operands read directly in MFMA layout.
+__global__ __launch_bounds__(256) void coarse_f32(const float *__restrict__ q,
+                                                  const float *__restrict__ ck, int32_t B,
+                                                  int32_t G, int32_t d, float *__restrict__ S) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int r16 = lane & 15, kg = lane >> 4;
+    const int64_t row0 = (int64_t)blockIdx.y * 64 + (wave >> 1) * 32;
+    const int64_t col0 = (int64_t)blockIdx.x * 64 + (wave & 1) * 32;
+    const float *qp[2], *cp[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const int64_t r = row0 + 16 * i + r16, c = col0 + 16 * i + r16;
+        qp[i] = q + (r < B ? r : B - 1) * d;
+        cp[i] = ck + (c < G ? c : G - 1) * d;
+    }
+    f32x4_t acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int k0 = 0; k0 < d; k0 += 4) {
+        const int k = k0 + kg;
+        float a[2], b[2];
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            a[i] = qp[i][k];
+            b[i] = cp[i][k];
+        }
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int j = 0; j < 2; ++j)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i], b[j], acc[i][j], 0, 0, 0);
+    }
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll
@@ -81,33 +242,62 @@ __global__ __launch_bounds__(256) void coarse_scores(const T *__restrict__ q,
 
 }  // namespace
 
-CoarseWs coarse_layout(void *ws, int32_t B, int32_t G, size_t *bytes) {
+CoarseWs coarse_layout(void *ws, int32_t B, int32_t G, int32_t d, int32_t key_dtype,
+                       int32_t compute_dtype, size_t *bytes) {
     Carve cv(ws);
     CoarseWs w{};
     w.scores = cv.take<float>((size_t)B * G);
+    const bool convert = compute_dtype == kBF16 && key_dtype == kF32;
+    w.q16 = convert ? cv.take<__bf16>((size_t)B * d) : nullptr;
+    w.c16 = convert ? cv.take<__bf16>((size_t)G * d) : nullptr;
     if (bytes) *bytes = cv.off + 256;
     return w;
 }
 
 hipError_t launch_coarse(int32_t key_dtype, int32_t compute_dtype, int32_t d, int32_t G,
                          const void *coarse_keys, const void *q, int32_t B, int32_t top_c,
-                         int32_t *sel, float *sel_score, const CoarseWs &w, KernelEvents ev,
-                         hipStream_t s) {
-    const dim3 grid((G + 63) / 64, (B + 63) / 64);
-    if (ev.before) hipEventRecord(ev.before, s);
-    if (compute_dtype == kF32)
-        hipLaunchKernelGGL((coarse_scores<float, false>), grid, dim3(256), 0, s,
+                         int32_t *sel, float *sel_score, const CoarseWs &w, int n_cu,
+                         KernelEvents ev, hipStream_t s) {
+    if (compute_dtype == kF32) {
+        if (ev.before) hipEventRecord(ev.before, s);
+        hipLaunchKernelGGL(coarse_f32, dim3((G + 63) / 64, (B + 63) / 64), dim3(256), 0, s,
                            static_cast<const float *>(q), static_cast<const float *>(coarse_keys),
                            B, G, d, w.scores);
-    else if (key_dtype == kF32)
-        hipLaunchKernelGGL((coarse_scores<float, true>), grid, dim3(256), 0, s,
-                           static_cast<const float *>(q), static_cast<const float *>(coarse_keys),
-                           B, G, d, w.scores);
-    else
-        hipLaunchKernelGGL((coarse_scores<__bf16, true>), grid, dim3(256), 0, s,
-                           static_cast<const __bf16 *>(q), static_cast<const __bf16 *>(coarse_keys),
-                           B, G, d, w.scores);
-    if (ev.after) hipEventRecord(ev.after, s);
+        if (ev.after) hipEventRecord(ev.after, s);
+    } else if ((int64_t)((B + BM - 1) / BM) * ((G + BN - 1) / BN) < n_cu) {
+        const dim3 grid((G + 63) / 64, (B + 63) / 64);
+        if (ev.before) hipEventRecord(ev.before, s);
+        if (key_dtype == kF32)
+            hipLaunchKernelGGL(coarse_small_bf16<float>, grid, dim3(256), 0, s,
+                               static_cast<const float *>(q),
+                               static_cast<const float *>(coarse_keys), B, G, d, w.scores);
+        else
+            hipLaunchKernelGGL(coarse_small_bf16<__bf16>, grid, dim3(256), 0, s,
+                               static_cast<const __bf16 *>(q),
+                               static_cast<const __bf16 *>(coarse_keys), B, G, d, w.scores);
+        if (ev.after) hipEventRecord(ev.after, s);
+    } else {
+        const __bf16 *q16 = static_cast<const __bf16 *>(q);
+        const __bf16 *c16 = static_cast<const __bf16 *>(coarse_keys);
+        if (key_dtype == kF32) {
+            const int64_t nq = (int64_t)B * d / 8, nc = (int64_t)G * d / 8;
+            hipLaunchKernelGGL(to_bf16, dim3((unsigned)((nq + 255) / 256 < 4096 ? (nq + 255) / 256 : 4096)),
+                               dim3(256), 0, s, static_cast<const float *>(q), w.q16, nq);
+            hipLaunchKernelGGL(to_bf16, dim3((unsigned)((nc + 255) / 256 < 4096 ? (nc + 255) / 256 : 4096)),
+                               dim3(256), 0, s, static_cast<const float *>(coarse_keys), w.c16, nc);
+            q16 = w.q16;
+            c16 = w.c16;
+        }
+        hipError_t err = hipFuncSetAttribute((const void *)coarse_gemm,
+                                             hipFuncAttributeMaxDynamicSharedMemorySize,
+                                             (int)kGemmLds);
+        if (err != hipSuccess) return err;
+        const int tiles = ((B + BM - 1) / BM) * ((G + BN - 1) / BN);
+        if (ev.before) hipEventRecord(ev.before, s);
+        hipLaunchKernelGGL(coarse_gemm, dim3(tiles), dim3(kGemmThreads), kGemmLds, s, q16, c16, B, G,
+                           d, w.scores);
+        if (ev.after) hipEventRecord(ev.after, s);
+    }
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
     return launch_topk(B, 1, G, w.scores, nullptr, nullptr, nullptr, 1.0f, top_c, sel, sel_score,

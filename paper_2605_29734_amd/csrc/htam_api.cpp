@@ -161,7 +161,8 @@ HTAM_API size_t htam_retrieve_coarse_workspace_size(const htam_bank *bank, int32
     (void)top_c;
     if (!bank || n_queries < 0 || bank->n_clusters < 1) return 0;
     size_t bytes = 0;
-    htam::coarse_layout(nullptr, n_queries, bank->n_clusters, &bytes);
+    htam::coarse_layout(nullptr, n_queries, bank->n_clusters, bank->d, bank->key_dtype,
+                        bank->compute_dtype, &bytes);
     return bytes;
 }
 
@@ -177,10 +178,13 @@ HTAM_API htam_status htam_retrieve_coarse(const htam_bank *bank, const void *q, 
     if (n_queries > 0 && !sel_cluster) return fail(HTAM_ERR_NULL, "sel_cluster is NULL");
     if (n_queries == 0) return ok();
     HTAM_TRY(check_ws(ws, ws_bytes, htam_retrieve_coarse_workspace_size(bank, n_queries, top_c)));
-    const htam::CoarseWs w = htam::coarse_layout(ws, n_queries, bank->n_clusters, nullptr);
+    const int n_cu = device_cus(nullptr);
+    if (n_cu <= 0) return fail(HTAM_ERR_DEVICE, "no HIP device");
+    const htam::CoarseWs w = htam::coarse_layout(ws, n_queries, bank->n_clusters, bank->d,
+                                                 bank->key_dtype, bank->compute_dtype, nullptr);
     return device_status(htam::launch_coarse(bank->key_dtype, bank->compute_dtype, bank->d,
                                              bank->n_clusters, bank->coarse_keys, q, n_queries,
-                                             top_c, sel_cluster, sel_score, w,
+                                             top_c, sel_cluster, sel_score, w, n_cu,
                                              g_events[HTAM_KERNEL_COARSE], stream),
                          "htam_retrieve_coarse");
 }

@@ -53,12 +53,15 @@ hipError_t launch_build(int64_t n, int32_t G, int32_t row_bytes, const int32_t *
 // ---- coarse scoring --------------------------------------------------------
 struct CoarseWs {
     float *scores;     // [B][G]
+    __bf16 *q16;       // [B][d] bf16 copy of fp32 queries (bf16 arithmetic on fp32 storage)
+    __bf16 *c16;       // [G][d] bf16 copy of fp32 coarse keys
 };
-CoarseWs coarse_layout(void *ws, int32_t B, int32_t G, size_t *bytes);
+CoarseWs coarse_layout(void *ws, int32_t B, int32_t G, int32_t d, int32_t key_dtype,
+                       int32_t compute_dtype, size_t *bytes);
 hipError_t launch_coarse(int32_t key_dtype, int32_t compute_dtype, int32_t d, int32_t G,
                          const void *coarse_keys, const void *q, int32_t B, int32_t top_c,
-                         int32_t *sel, float *sel_score, const CoarseWs &w, KernelEvents ev,
-                         hipStream_t s);
+                         int32_t *sel, float *sel_score, const CoarseWs &w, int n_cu,
+                         KernelEvents ev, hipStream_t s);
 
 // ---- fine stage (routing + bank stream + per-slot merge) ----------------------
 struct AttendWs {
@@ -73,7 +76,7 @@ struct AttendWs {
     float *pm;         // [P] partial max
     float *pz;         // [P] partial sum
     int32_t *pc;       // [P] partial kept count
-    uint64_t *pk;      // [P][k] partial keys, descending
+    uint64_t *pk;      // [P][k] partial keys (a chunk's top-k, unsorted, zero-padded)
     int64_t p_cap;     // partial results the workspace holds (>= B*c)
     int64_t w_max;     // bound on work items (grid sizing)
 };

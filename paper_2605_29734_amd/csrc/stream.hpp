@@ -9,12 +9,12 @@
 // Eq. local policy). Per query it keeps the online softmax statistics
 // (max, sum of exp((s - max)/tau)) and a top-k of (score, caller id) keys in
 // an LDS buffer behind a threshold filter. At the end of a pass it writes one
-// partial (m, Z, sorted top-k) per (query, chunk).
+// partial (m, Z, the chunk's top-k keys unsorted) per (query, chunk).
 //
 // Two variants:
 //   stream_lds      queries staged once per pass in LDS as B fragments; key
-//                   fragments prefetched two load units ahead with branch-free
-//                   loads (needs d % (32 * U) == 0);
+//                   fragments prefetched through a ring of three load units with
+//                   branch-free loads (needs d % (32 * U) == 0);
 //   stream_generic  query fragments read from global memory (any d, and the
 //                   fp32-arithmetic path).
 #pragma once
@@ -105,24 +105,31 @@ __device__ __forceinline__ void pass_begin(const FineArgs &a, const FineSmem &sm
 
 // Compact the top-k buffers of this wave's queries (n = wave, wave + 4, ...)
 // that cannot take their pending candidates (cnt[n] + pend[n] > cap), and
-// reset pend[n] for every query of the wave.
+// reset pend[n] for every query of the wave. The queries are checked
+// lane-parallel (lane i looks at query wave + 4 i); only the full ones are
+// compacted, one after the other.
 template <int NPL>
 __device__ __forceinline__ void compact_wave_queries(const FineArgs &a, const FineSmem &sm, int nqg) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    for (int n = wave; n < nqg; n += kFineWaves) {
-        const int c = (int)sm.cnt[n];
-        const bool full = c + (int)sm.pend[n] > a.cap;
-        wave_lds_sync();
-        if (lane == 0) sm.pend[n] = 0;
-        if (full) {
-            uint64_t th = 0;
-            const int kept = compact_select<NPL>(sm.buf + (size_t)n * a.cap, c, a.k, kRowsPerStep,
-                                                 lane, th);
-            if (lane == 0) {
-                sm.cnt[n] = (uint32_t)kept;
-                sm.theta[n] = th;
-            }
+    const int n_mine = lane * kFineWaves + wave;
+    bool full = false;
+    if (n_mine < nqg) {
+        full = (int)sm.cnt[n_mine] + (int)sm.pend[n_mine] > a.cap;
+        sm.pend[n_mine] = 0;
+    }
+    uint64_t mask = __ballot(full);
+    while (mask) {
+        const int i = __builtin_ctzll(mask);
+        mask &= mask - 1;
+        const int n = i * kFineWaves + wave;
+        uint64_t th = 0;
+        const int kept = compact_select<NPL>(sm.buf + (size_t)n * a.cap, (int)sm.cnt[n], a.k,
+                                             kRowsPerStep, lane, th);
+        if (lane == 0) {
+            sm.cnt[n] = (uint32_t)kept;
+            sm.theta[n] = th;
         }
+        wave_lds_sync();
     }
 }
 
@@ -131,9 +138,9 @@ __device__ __forceinline__ void compact_wave_queries(const FineArgs &a, const Fi
 // into the online (max, sum), then offers them to the queries' top-k buffers
 // in three phases: count the candidates above each threshold; compact the
 // buffers that could not take them (the threshold rises); append the
-// candidates still above the threshold. A buffer is compacted only when it
-// would otherwise overflow (at most 64 candidates per step, and a compaction
-// leaves at least 64 free slots).
+// candidates still above the threshold (one LDS atomic per lane and query
+// tile). A buffer is compacted only when it would otherwise overflow (at most
+// 64 candidates per step, and a compaction leaves at least 64 free slots).
 template <int NQT, int NPL>
 __device__ __forceinline__ void tile_epilogue(const FineArgs &a, const FineSmem &sm,
                                               const f32x4_t (&acc)[NQT], int64_t rt, int64_t r1,
@@ -184,12 +191,14 @@ __device__ __forceinline__ void tile_epilogue(const FineArgs &a, const FineSmem 
         const int n = qt * 16 + r16;
         if (n < nqg && (key[qt][0] | key[qt][1] | key[qt][2] | key[qt][3])) {
             const uint64_t th = sm.theta[n];
+            int c = 0;
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                if (key[qt][e] > th) {
-                    const uint32_t p = atomicAdd(&sm.cnt[n], 1u);
-                    sm.buf[(size_t)n * cap + p] = key[qt][e];
-                }
+            for (int e = 0; e < 4; ++e) c += key[qt][e] > th;
+            if (c) {
+                uint64_t *dst = sm.buf + (size_t)n * cap + atomicAdd(&sm.cnt[n], (uint32_t)c);
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    if (key[qt][e] > th) *dst++ = key[qt][e];
             }
         }
     }
@@ -202,21 +211,18 @@ __device__ __forceinline__ void pass_end(const FineArgs &a, const FineSmem &sm, 
                                          float (&m)[NQT], float (&z)[NQT]) {
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6, r16 = lane & 15, kg = lane >> 4;
     __syncthreads();           // the last step's appends are complete
+    // Each query's partial: its chunk's best k keys, in no particular order
+    // (the merge that reads them selects again), zero-padded to k.
     for (int n = wave; n < nqg; n += kFineWaves) {
-        const uint64_t *b = sm.buf + (size_t)n * a.cap;
-        const int cn = (int)sm.cnt[n];
-        uint64_t v[NPL];
-#pragma unroll
-        for (int q = 0; q < NPL; ++q) v[q] = (q * kWave + lane < cn) ? b[q * kWave + lane] : 0;
-        wave_sort_regs<NPL>(v, lane);
-        const int kept = cn < a.k ? cn : a.k;
-        const int64_t p = a.pbase[g] + j * nq + qg0 + n;
-#pragma unroll
-        for (int q = 0; q < NPL; ++q) {
-            const int i = q * kWave + lane;
-            if (i < a.k) a.pk[p * a.k + i] = i < kept ? v[q] : 0;
+        uint64_t *b = sm.buf + (size_t)n * a.cap;
+        int cn = (int)sm.cnt[n];
+        if (cn > a.k) {
+            uint64_t th = 0;
+            cn = compact_select<NPL>(b, cn, a.k, a.cap - a.k, lane, th);
         }
-        if (lane == 0) a.pc[p] = kept;
+        const int64_t p = a.pbase[g] + j * nq + qg0 + n;
+        for (int i = lane; i < a.k; i += kWave) a.pk[p * a.k + i] = i < cn ? b[i] : 0;
+        if (lane == 0) a.pc[p] = cn;
     }
 #pragma unroll
     for (int qt = 0; qt < NQT; ++qt) {
@@ -420,16 +426,20 @@ __device__ __forceinline__ void pass_lds(const FineArgs &a, const FineSmem &sm, 
         acc[qt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     }
 
-    // Two load units in flight: the next unit's loads are issued before the
-    // current unit's MFMAs and epilogue. Past the end, the last unit is loaded
-    // again (an L2 hit) so that every load stays unconditional.
-    LoadUnit<KT> s0, s1;
+    // A ring of three load units: while unit u is multiplied (and its step's
+    // epilogue runs) the loads of units u+1 and u+2 are in flight. Past the
+    // end, the last unit is loaded again (an L2 hit) so that every load stays
+    // unconditional and the compiler can wait for exactly one unit at a time.
+    LoadUnit<KT> s0, s1, s2;
     lds_load_unit<KT, HAS_TID>(s0, K, a.tid, d, NG, 0, r0, r1);
-    for (int u = 0; u < total; u += 2) {
-        lds_load_unit<KT, HAS_TID>(s1, K, a.tid, d, NG, min(u + 1, total - 1), r0, r1);
+    lds_load_unit<KT, HAS_TID>(s1, K, a.tid, d, NG, min(1, total - 1), r0, r1);
+    for (int u = 0; u < total; u += 3) {
+        lds_load_unit<KT, HAS_TID>(s2, K, a.tid, d, NG, min(u + 2, total - 1), r0, r1);
         lds_compute_unit<KT, NQT, NPL>(a, sm, s0, NG, u, r0, r1, nqg, acc, m, z);
-        lds_load_unit<KT, HAS_TID>(s0, K, a.tid, d, NG, min(u + 2, total - 1), r0, r1);
+        lds_load_unit<KT, HAS_TID>(s0, K, a.tid, d, NG, min(u + 3, total - 1), r0, r1);
         if (u + 1 < total) lds_compute_unit<KT, NQT, NPL>(a, sm, s1, NG, u + 1, r0, r1, nqg, acc, m, z);
+        lds_load_unit<KT, HAS_TID>(s1, K, a.tid, d, NG, min(u + 4, total - 1), r0, r1);
+        if (u + 2 < total) lds_compute_unit<KT, NQT, NPL>(a, sm, s2, NG, u + 2, r0, r1, nqg, acc, m, z);
     }
     pass_end<NQT, NPL>(a, sm, g, j, nq, qg0, nqg, m, z);
 }
