@@ -38,20 +38,49 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
+def kernel_source_sha256() -> str:
+    """Hash of every device and host source of the library (a changed kernel
+    invalidates counter figures taken from an older build)."""
+    csrc = os.path.join(ROOT, "paper_2605_29734_amd", "csrc")
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(csrc)):
+        if name.endswith((".hip", ".hpp", ".cpp", ".h")):
+            h.update(name.encode())
+            h.update(open(os.path.join(csrc, name), "rb").read())
+    return h.hexdigest()
+
+
 def stream_kernel_traffic(workload: str):
-    """Measured HBM bytes per launch of the bank-stream kernel from a committed
-    rocprofv3 counter summary, valid only while the kernel source is unchanged."""
+    """Measured HBM bytes per launch of the bank-stream kernel (FETCH_SIZE +
+    WRITE_SIZE, scaled by the same counters' reading for a plain copy of known
+    size) from the committed rocprofv3 counter summary; None unless that
+    summary was taken from the current kernel sources."""
     path = os.path.join(ROOT, "profiles", "fine_stream_traffic.json")
     if not os.path.exists(path):
         return None
     try:
         rec = json.load(open(path))
-        src = open(os.path.join(ROOT, "paper_2605_29734_amd", "csrc", "fine.hip"), "rb").read()
-        if rec.get("source_sha256") != hashlib.sha256(src).hexdigest():
+        if rec.get("source_sha256") != kernel_source_sha256():
             return None
         return rec.get("workloads", {}).get(workload, {}).get("bytes_per_launch")
-    except Exception:
+    except (OSError, ValueError, AttributeError):
         return None
+
+
+def copy_calibration(mib: int, launches: int = 5):
+    """Plain streaming copies of known size, the reference reading for the
+    FETCH_SIZE / WRITE_SIZE counters: each launch of the elementwise kernel
+    reads ``mib`` MiB once and writes ``mib`` MiB once (a kernel, not a DMA
+    transfer, so that the counters see it)."""
+    import torch
+    n = mib << 20
+    src = torch.full((n // 4,), 1.0, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(launches):
+        torch.mul(src, 1.0, out=dst)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_per_launch": n, "launches": launches}), flush=True)
 
 
 def cpu_baseline(spec, w, bank, target_s: float):
@@ -106,12 +135,18 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run plain copies of MIB MiB (counter calibration) and exit")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py runs on exactly one GPU: multi-GPU runs are not part of this build "
               "(how the path would shard is described in DESIGN.md)", file=sys.stderr)
         sys.exit(2)
+
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration)
+        return
 
     import torch
 
