@@ -19,8 +19,33 @@ struct Plan {
     int64_t chunk;     // rows per work item (chunk of a segment)
     int64_t n_items;   // work items (cluster, chunk) with at least one query
     int64_t n_parts;   // partial results (query, chunk)
+    int64_t n_groups;  // level-one merge groups (clusters with more chunks than one group)
+    int64_t n_l1;      // level-one merge results (query, group)
+    int64_t n_merge;   // (query, slot) pairs whose cluster spans more than one chunk
     int32_t next;      // dynamic work counter of the streaming kernel
     int32_t bad_sel;   // count of selected cluster ids out of range
+};
+
+// One work item of the bank stream: a chunk of one selected cluster's segment,
+// scored against every query that selected the cluster.
+struct WorkItem {
+    int64_t r0;        // first bank row
+    int64_t p0;        // partial result of the item's first query (query i: p0 + i)
+    int32_t len;       // rows
+    int32_t g;         // cluster
+    int32_t qbeg;      // first entry of the cluster's query list
+    int32_t nq;        // queries that selected the cluster
+    int32_t single;    // 1 if this chunk is the cluster's whole segment
+    int32_t pad;
+};
+
+// Level-one merge group: up to `group` consecutive chunk partials of one
+// cluster, merged for each of its queries into one result.
+struct MergeGroup {
+    int64_t p0;        // partial of the group's first chunk for query 0 (query i, chunk j: p0 + j*nq + i)
+    int64_t u0;        // level-one result for query 0 (query i: u0 + i)
+    int32_t npart;     // chunks in the group
+    int32_t nq;        // queries of the cluster
 };
 
 // Carves a workspace into 256-byte aligned pieces; with base == nullptr it
@@ -69,16 +94,29 @@ struct AttendWs {
     int32_t *cursor;   // [G]
     int32_t *qoff;     // [G+1]
     int32_t *wstart;   // [G+1] first work item of each cluster
+    int32_t *gstart;   // [G+1] first level-one merge group of each cluster
     int64_t *pbase;    // [G]   first partial of each cluster
+    int64_t *ubase;    // [G]   first level-one merge result of each cluster
+    int32_t *mstart;   // [G+1] first entry of each cluster in mlist
+    int32_t *mlist;    // [B*c] pairs to merge (their cluster has several chunks)
+    int2 *units;       // [u_cap] level-one work: (group, query position)
     int32_t *qlist;    // [B*c] (query, slot) entries grouped by cluster
     int32_t *pos;      // [B*c] position of each entry inside its cluster's list
     Plan *plan;
-    float *pm;         // [P] partial max
-    float *pz;         // [P] partial sum
-    int32_t *pc;       // [P] partial kept count
-    uint64_t *pk;      // [P][k] partial keys (a chunk's top-k, unsorted, zero-padded)
+    WorkItem *items;   // [w_max]
+    MergeGroup *groups;// [g_max]
+    float *pm;         // [p_cap] partial max
+    float *pz;         // [p_cap] partial sum
+    int32_t *pc;       // [p_cap] partial kept count
+    uint64_t *pk;      // [p_cap][k] partial keys (a chunk's top-k, unsorted, zero-padded)
+    float *um, *uz;    // [u_cap] level-one merge results, same form as the partials
+    int32_t *uc;
+    uint64_t *uk;      // [u_cap][k]
     int64_t p_cap;     // partial results the workspace holds (>= B*c)
-    int64_t w_max;     // bound on work items (grid sizing)
+    int64_t w_max;     // bound on work items
+    int64_t g_max;     // bound on level-one groups
+    int64_t u_cap;     // bound on level-one results
+    int32_t group;     // chunk partials per level-one group
 };
 AttendWs attend_layout(void *ws, int32_t d, int32_t G, int64_t N, int32_t key_bytes, int32_t B,
                        int32_t c, int32_t k, size_t *bytes);

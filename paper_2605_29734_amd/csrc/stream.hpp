@@ -31,17 +31,18 @@ constexpr int kMaxQueryTiles = 4;      // at most 64 queries per pass over a chu
 
 struct FineArgs {
     const void *keys;
-    const int64_t *off;
     const int32_t *tid;
     const void *q;
     int32_t d, c, G, k, cap, qmax;
     float cexp;                   // log2(e) / tau
-    const int32_t *qoff, *qlist, *wstart;
-    const int64_t *pbase;
+    const int32_t *qlist;
+    const WorkItem *items;
     Plan *plan;
     float *pm, *pz;
     int32_t *pc;
     uint64_t *pk;
+    float *slot_max, *slot_sum, *cand_score;   // final per-slot outputs (single-chunk clusters)
+    int32_t *cand_id;
 };
 
 __host__ __device__ inline size_t fine_state_bytes(int qmax, int cap) {
@@ -204,23 +205,42 @@ __device__ __forceinline__ void tile_epilogue(const FineArgs &a, const FineSmem 
     }
 }
 
-// End of a pass: each query's partial top-k (sorted, at most k) and (max, sum).
+// End of a pass. For a chunk that is its cluster's whole segment, each query's
+// (query, slot) result is final: the top-k sorted into the slot's outputs and
+// the (max, sum) into slot_max / slot_sum. Otherwise each query writes one
+// partial: its chunk's best k keys, in no particular order (the merge that
+// reads them selects again), zero-padded to k, and the chunk's (max, sum).
 template <int NQT, int NPL>
-__device__ __forceinline__ void pass_end(const FineArgs &a, const FineSmem &sm, int32_t g,
-                                         int64_t j, int32_t nq, int32_t qg0, int32_t nqg,
+__device__ __forceinline__ void pass_end(const FineArgs &a, const FineSmem &sm, int64_t p0,
+                                         int32_t qbeg, bool single, int32_t qg0, int32_t nqg,
                                          float (&m)[NQT], float (&z)[NQT]) {
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6, r16 = lane & 15, kg = lane >> 4;
     __syncthreads();           // the last step's appends are complete
-    // Each query's partial: its chunk's best k keys, in no particular order
-    // (the merge that reads them selects again), zero-padded to k.
     for (int n = wave; n < nqg; n += kFineWaves) {
         uint64_t *b = sm.buf + (size_t)n * a.cap;
         int cn = (int)sm.cnt[n];
+        if (single) {
+            const int64_t e = a.qlist[qbeg + qg0 + n];
+            uint64_t v[NPL];
+#pragma unroll
+            for (int q = 0; q < NPL; ++q) v[q] = (q * kWave + lane < cn) ? b[q * kWave + lane] : 0;
+            wave_sort_regs<NPL>(v, lane);
+#pragma unroll
+            for (int q = 0; q < NPL; ++q) {
+                const int r = q * kWave + lane;
+                if (r < a.k) {
+                    const uint64_t key = r < cn ? v[q] : 0;
+                    a.cand_score[e * a.k + r] = key ? key_score(key) : -INFINITY;
+                    a.cand_id[e * a.k + r] = key ? key_id(key) : -1;
+                }
+            }
+            continue;
+        }
         if (cn > a.k) {
             uint64_t th = 0;
             cn = compact_select<NPL>(b, cn, a.k, a.cap - a.k, lane, th);
         }
-        const int64_t p = a.pbase[g] + j * nq + qg0 + n;
+        const int64_t p = p0 + qg0 + n;
         for (int i = lane; i < a.k; i += kWave) a.pk[p * a.k + i] = i < cn ? b[i] : 0;
         if (lane == 0) a.pc[p] = cn;
     }
@@ -243,18 +263,24 @@ __device__ __forceinline__ void pass_end(const FineArgs &a, const FineSmem &sm, 
         float M = -INFINITY, Z = 0.0f;
         for (int w = 0; w < kFineWaves; ++w)
             mz_merge(M, Z, sm.wm[w * a.qmax + n], sm.wz[w * a.qmax + n], a.cexp);
-        const int64_t p = a.pbase[g] + j * nq + qg0 + n;
-        a.pm[p] = M;
-        a.pz[p] = Z;
+        if (single) {
+            const int64_t e = a.qlist[qbeg + qg0 + n];
+            a.slot_max[e] = M;
+            a.slot_sum[e] = Z;
+        } else {
+            const int64_t p = p0 + qg0 + n;
+            a.pm[p] = M;
+            a.pz[p] = Z;
+        }
     }
     __syncthreads();
 }
 
 // ---- generic pass: query fragments read from global memory ------------------
 template <typename T, bool BF16, int NQT, int NPL>
-__device__ __forceinline__ void pass_generic(const FineArgs &a, const FineSmem &sm, int32_t g,
-                                             int64_t j, int64_t r0, int64_t r1, int32_t qbeg,
-                                             int32_t nq, int32_t qg0, int32_t nqg) {
+__device__ __forceinline__ void pass_generic(const FineArgs &a, const FineSmem &sm, int64_t p0,
+                                             bool single, int64_t r0, int64_t r1, int32_t qbeg,
+                                             int32_t qg0, int32_t nqg) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, r16 = lane & 15, kg = lane >> 4;
     const int d = a.d;
     const T *K = static_cast<const T *>(a.keys);
@@ -307,7 +333,7 @@ __device__ __forceinline__ void pass_generic(const FineArgs &a, const FineSmem &
         }
         tile_epilogue<NQT, NPL>(a, sm, acc, rt, r1, nqg, tidv, m, z);
     }
-    pass_end<NQT, NPL>(a, sm, g, j, nq, qg0, nqg, m, z);
+    pass_end<NQT, NPL>(a, sm, p0, qbeg, single, qg0, nqg, m, z);
 }
 
 // ---- LDS pass: query fragments staged in LDS, key fragments prefetched -------
@@ -394,9 +420,9 @@ __device__ __forceinline__ void lds_compute_unit(const FineArgs &a, const FineSm
 }
 
 template <typename KT, bool HAS_TID, int NQT, int NPL>
-__device__ __forceinline__ void pass_lds(const FineArgs &a, const FineSmem &sm, int32_t g,
-                                         int64_t j, int64_t r0, int64_t r1, int32_t qbeg,
-                                         int32_t nq, int32_t qg0, int32_t nqg) {
+__device__ __forceinline__ void pass_lds(const FineArgs &a, const FineSmem &sm, int64_t p0,
+                                         bool single, int64_t r0, int64_t r1, int32_t qbeg,
+                                         int32_t qg0, int32_t nqg) {
     constexpr int U = AFrag<KT>::U;
     const int t = threadIdx.x;
     const int d = a.d;
@@ -441,35 +467,34 @@ __device__ __forceinline__ void pass_lds(const FineArgs &a, const FineSmem &sm, 
         lds_load_unit<KT, HAS_TID>(s1, K, a.tid, d, NG, min(u + 4, total - 1), r0, r1);
         if (u + 2 < total) lds_compute_unit<KT, NQT, NPL>(a, sm, s2, NG, u + 2, r0, r1, nqg, acc, m, z);
     }
-    pass_end<NQT, NPL>(a, sm, g, j, nq, qg0, nqg, m, z);
+    pass_end<NQT, NPL>(a, sm, p0, qbeg, single, qg0, nqg, m, z);
 }
 
-// Work loop shared by both kernels: items (cluster, chunk) from a dynamic
+// Work loop shared by both kernels: items (cluster, chunk) from the planned
+// item table, the first one by block index and the rest from a dynamic
 // counter; the queries of an item in passes of at most qmax.
 struct ItemPass {
-    int32_t g;
-    int64_t j, r0, r1;
+    int64_t p0, r0, r1;
     int32_t qbeg, nq;
+    bool single;
 };
 
-__device__ __forceinline__ bool next_item(const FineArgs &a, int32_t *s_item, ItemPass &it) {
-    if (threadIdx.x == 0) *s_item = atomicAdd(&a.plan->next, 1);
+__device__ __forceinline__ bool next_item(const FineArgs &a, int32_t *s_item, bool first,
+                                          ItemPass &it) {
+    if (threadIdx.x == 0)
+        *s_item = first ? (int32_t)blockIdx.x : (int32_t)gridDim.x + atomicAdd(&a.plan->next, 1);
     __syncthreads();
     const int64_t w = *s_item;
     __syncthreads();
     if (w >= a.plan->n_items) return false;
-    int32_t lo = 0, hi = a.G;          // wstart[lo] <= w < wstart[hi]
-    while (hi - lo > 1) {
-        const int32_t mid = (lo + hi) >> 1;
-        if (a.wstart[mid] <= w) lo = mid; else hi = mid;
-    }
-    const int64_t CH = a.plan->chunk;
-    it.g = lo;
-    it.j = w - a.wstart[lo];
-    it.r0 = a.off[lo] + it.j * CH;
-    it.r1 = min(a.off[lo + 1], it.r0 + CH);
-    it.qbeg = a.qoff[lo];
-    it.nq = a.qoff[lo + 1] - it.qbeg;
+    const WorkItem wi = a.items[w];
+    it.p0 = wi.p0;
+    it.r0 = wi.r0;
+    it.r1 = wi.r0 + wi.len;
+    it.qbeg = wi.qbeg;
+    it.nq = wi.nq;
+    // passes over one item cover disjoint queries, so a single-chunk item's results are final
+    it.single = wi.single != 0;
     return true;
 }
 
@@ -479,14 +504,14 @@ __global__ __launch_bounds__(kFineThreads) void stream_lds(FineArgs a, int32_t q
     __shared__ int32_t s_item;
     const FineSmem sm = fine_carve(smem_raw, qs_bytes, a.qmax, a.cap);
     ItemPass it;
-    while (next_item(a, &s_item, it)) {
+    for (bool first = true; next_item(a, &s_item, first, it); first = false) {
         for (int32_t qg0 = 0; qg0 < it.nq; qg0 += a.qmax) {
             const int32_t nqg = min(a.qmax, it.nq - qg0);
             switch ((nqg + 15) >> 4) {
-                case 1: pass_lds<KT, HAS_TID, 1, NPL>(a, sm, it.g, it.j, it.r0, it.r1, it.qbeg, it.nq, qg0, nqg); break;
-                case 2: pass_lds<KT, HAS_TID, 2, NPL>(a, sm, it.g, it.j, it.r0, it.r1, it.qbeg, it.nq, qg0, nqg); break;
-                case 3: pass_lds<KT, HAS_TID, 3, NPL>(a, sm, it.g, it.j, it.r0, it.r1, it.qbeg, it.nq, qg0, nqg); break;
-                default: pass_lds<KT, HAS_TID, 4, NPL>(a, sm, it.g, it.j, it.r0, it.r1, it.qbeg, it.nq, qg0, nqg); break;
+                case 1: pass_lds<KT, HAS_TID, 1, NPL>(a, sm, it.p0, it.single, it.r0, it.r1, it.qbeg, qg0, nqg); break;
+                case 2: pass_lds<KT, HAS_TID, 2, NPL>(a, sm, it.p0, it.single, it.r0, it.r1, it.qbeg, qg0, nqg); break;
+                case 3: pass_lds<KT, HAS_TID, 3, NPL>(a, sm, it.p0, it.single, it.r0, it.r1, it.qbeg, qg0, nqg); break;
+                default: pass_lds<KT, HAS_TID, 4, NPL>(a, sm, it.p0, it.single, it.r0, it.r1, it.qbeg, qg0, nqg); break;
             }
         }
     }
@@ -498,14 +523,14 @@ __global__ __launch_bounds__(kFineThreads) void stream_generic(FineArgs a) {
     __shared__ int32_t s_item;
     const FineSmem sm = fine_carve(smem_raw, 0, a.qmax, a.cap);
     ItemPass it;
-    while (next_item(a, &s_item, it)) {
+    for (bool first = true; next_item(a, &s_item, first, it); first = false) {
         for (int32_t qg0 = 0; qg0 < it.nq; qg0 += a.qmax) {
             const int32_t nqg = min(a.qmax, it.nq - qg0);
             switch ((nqg + 15) >> 4) {
-                case 1: pass_generic<T, BF16, 1, NPL>(a, sm, it.g, it.j, it.r0, it.r1, it.qbeg, it.nq, qg0, nqg); break;
-                case 2: pass_generic<T, BF16, 2, NPL>(a, sm, it.g, it.j, it.r0, it.r1, it.qbeg, it.nq, qg0, nqg); break;
-                case 3: pass_generic<T, BF16, 3, NPL>(a, sm, it.g, it.j, it.r0, it.r1, it.qbeg, it.nq, qg0, nqg); break;
-                default: pass_generic<T, BF16, 4, NPL>(a, sm, it.g, it.j, it.r0, it.r1, it.qbeg, it.nq, qg0, nqg); break;
+                case 1: pass_generic<T, BF16, 1, NPL>(a, sm, it.p0, it.single, it.r0, it.r1, it.qbeg, qg0, nqg); break;
+                case 2: pass_generic<T, BF16, 2, NPL>(a, sm, it.p0, it.single, it.r0, it.r1, it.qbeg, qg0, nqg); break;
+                case 3: pass_generic<T, BF16, 3, NPL>(a, sm, it.p0, it.single, it.r0, it.r1, it.qbeg, qg0, nqg); break;
+                default: pass_generic<T, BF16, 4, NPL>(a, sm, it.p0, it.single, it.r0, it.r1, it.qbeg, qg0, nqg); break;
             }
         }
     }

@@ -121,3 +121,29 @@ def test_topk_merge_standalone():
     for r in range(17):
         order = np.lexsort((np.arange(1000), -dense[r].astype(np.float64)))[:50]
         np.testing.assert_array_equal(to_np(o2[0])[r], order)
+
+
+def test_attend_out_of_range_selection_is_empty():
+    """Selected cluster ids outside [0, G) give empty slots; the other slots are unaffected."""
+    from paper_2605_29734_amd import htam
+    spec = synth.scaled(synth.SPECS["tiny_f32"], B=8)
+    say("[case] attend with out-of-range selections")
+    w = synth.make(spec, device="cpu", seed=3)
+    dev = torch.device("cuda:0")
+    bank = htam.build_bank(w.cluster_of.to(dev), w.keys_in.to(dev), w.coarse_keys.to(dev),
+                           spec.compute)
+    q = w.queries.to(dev)
+    sel = torch.tensor([[0, 5, -1, 7]] * 4 + [[spec.G, 1, 2, 3]] * 4, dtype=torch.int32,
+                       device=dev)
+    good = torch.tensor([[0, 5, 6, 7]] * 4 + [[4, 1, 2, 3]] * 4, dtype=torch.int32, device=dev)
+    out = htam.htam_attend_transitions(bank, q, sel, spec.tau, spec.top_k)
+    ref = htam.htam_attend_transitions(bank, q, good, spec.tau, spec.top_k)
+    torch.cuda.synchronize()
+    out = [to_np(x) for x in out]
+    ref = [to_np(x) for x in ref]
+    bad = (to_np(sel) < 0) | (to_np(sel) >= spec.G)
+    smax, ssum, cscore, cid = out
+    assert np.all(smax[bad] == -np.inf) and np.all(ssum[bad] == 0)
+    assert np.all(cscore[bad] == -np.inf) and np.all(cid[bad] == -1)
+    for a, b in zip(out, ref):
+        np.testing.assert_array_equal(a[~bad], b[~bad])
