@@ -47,6 +47,12 @@ __device__ __forceinline__ void mz_merge(float &m, float &z, float m2, float z2,
     m = M;
 }
 
+// 2^x by the hardware instruction (v_exp_f32, about 1 ulp), without the
+// denormal-range handling of exp2f: results below the smallest normal float
+// may come out as zero. Used for softmax terms exp((s - m)/tau) <= 1 summed
+// next to the maximum's own term 1, where such terms do not change the sum.
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
 // ---------------------------------------------------------------------------
 // Fragment loads for v_mfma_f32_16x16x32_bf16: 8 consecutive elements of one
 // row starting at p, as bf16 (fp32 storage is rounded to nearest even by the
@@ -220,23 +226,44 @@ __device__ __forceinline__ uint64_t wave_element(const uint64_t (&v)[NPL], int i
 // A radix select over the keys' high halves (the ordered scores) finds T, the
 // k-th largest score in the buffer; every key scoring >= T is kept (so all
 // exact ties at T stay) and the threshold becomes T: later keys must score
-// above it, or tie it with a valid id. If the ties at T leave fewer than
-// `room` free slots, the buffer is sorted instead and cut to exactly k keys
-// (threshold = the k-th key). Returns the new count.
+// above it, or tie it with a valid id. The select starts below the highest
+// bit in which the buffer's scores differ (the bits above are the same in all
+// of them and so in T). If the ties at T leave fewer than `room` free slots,
+// the buffer is sorted instead and cut to exactly k keys (threshold = the
+// k-th key). Returns the new count.
 template <int NPL>
 __device__ __forceinline__ int compact_select(uint64_t *buf, int n, int k, int room, int lane,
                                               uint64_t &theta) {
     constexpr int cap = NPL * kWave;
     uint64_t v[NPL];
     uint32_t hi[NPL];
+    uint32_t hand = 0xffffffffu, hor = 0;
 #pragma unroll
     for (int q = 0; q < NPL; ++q) {
-        v[q] = (q * kWave + lane < n) ? buf[q * kWave + lane] : 0;
+        const bool ok = q * kWave + lane < n;
+        v[q] = ok ? buf[q * kWave + lane] : 0;
         hi[q] = (uint32_t)(v[q] >> 32);
+        if (ok) {
+            hand &= hi[q];
+            hor |= hi[q];
+        }
     }
-    uint32_t T = 0;
-#pragma unroll
-    for (int bit = 31; bit >= 0; --bit) {
+    hand &= lane_xor32<1>(hand, lane);
+    hor |= lane_xor32<1>(hor, lane);
+    hand &= lane_xor32<2>(hand, lane);
+    hor |= lane_xor32<2>(hor, lane);
+    hand &= lane_xor32<4>(hand, lane);
+    hor |= lane_xor32<4>(hor, lane);
+    hand &= lane_xor32<8>(hand, lane);
+    hor |= lane_xor32<8>(hor, lane);
+    hand &= lane_xor32<16>(hand, lane);
+    hor |= lane_xor32<16>(hor, lane);
+    hand &= lane_xor32<32>(hand, lane);
+    hor |= lane_xor32<32>(hor, lane);
+    const uint32_t diff = hand ^ hor;
+    const int top = diff ? 31 - __builtin_clz(diff) : -1;
+    uint32_t T = top < 0 ? hand : (top == 31 ? 0u : hand & ~((2u << top) - 1u));
+    for (int bit = top; bit >= 0; --bit) {
         const uint32_t cand = T | (1u << bit);
         int c = 0;
 #pragma unroll

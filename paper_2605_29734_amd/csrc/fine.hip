@@ -529,19 +529,20 @@ static int64_t chunk_floor_rows(int64_t N, int n_cu) {
     return ch;
 }
 
-// Queries per pass of the generic kernel (its LDS holds only the top-k state).
+// Queries per pass of the generic kernel (its LDS holds only the top-k
+// buffers and the score tiles).
 static int qmax_generic(int cap) {
-    int q = (72 * 1024) / (cap * 8);
-    q = (q / 16) * 16;
-    if (q > 16 * kMaxQueryTiles) q = 16 * kMaxQueryTiles;
-    return q < 16 ? 16 : q;
+    int q = 16 * kMaxQueryTiles;
+    while (q > 16 && fine_state_bytes(q, cap, 2) > 72 * 1024) q -= 16;
+    return q;
 }
 
 // Queries per pass of the LDS kernel: the most (a multiple of 16, at most 64)
-// whose B fragments and top-k state fit in the LDS budget; 0 if 16 do not.
+// whose B fragments, top-k buffers and one score tile fit in the LDS budget;
+// 0 if 16 do not.
 static int qmax_lds(int d, int cap, size_t budget) {
     for (int q = 16 * kMaxQueryTiles; q >= 16; q -= 16)
-        if (fine_qs_bytes(d, q) + fine_state_bytes(q, cap) <= budget) return q;
+        if (fine_qs_bytes(d, q) + fine_state_bytes(q, cap, 1) <= budget) return q;
     return 0;
 }
 
@@ -554,7 +555,7 @@ static size_t lds_budget() {
     if (hipDeviceGetAttribute(&bytes, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess ||
         bytes <= 0)
         bytes = 64 * 1024;
-    bytes -= 1024;      // static LDS of the kernels
+    bytes -= 256;       // static LDS of the kernels (a few words)
     if (dev >= 0 && dev < 64) cached[dev] = bytes;
     return (size_t)bytes;
 }
@@ -647,14 +648,16 @@ static hipError_t launch_stream(int32_t key_dtype, int32_t compute_dtype, const 
         ql = qmax_for_load(ql, bc, fa0.G);
         l.fa.qmax = ql;
         l.qs_bytes = (int32_t)fine_qs_bytes(fa0.d, ql);
-        l.smem = l.qs_bytes + fine_state_bytes(ql, fa0.cap);
+        // two score tiles (one barrier per step) when they fit
+        l.fa.ntile = l.qs_bytes + fine_state_bytes(ql, fa0.cap, 2) <= budget ? 2 : 1;
+        l.smem = l.qs_bytes + fine_state_bytes(ql, fa0.cap, l.fa.ntile);
         l.grid = grid_for(l.smem);
-        return key_dtype == kF32 ? launch_stream_lds_f32(npl, fa0.tid != nullptr, l)
-                                 : launch_stream_lds_bf16(npl, fa0.tid != nullptr, l);
+        return key_dtype == kF32 ? launch_stream_lds_f32(npl, l) : launch_stream_lds_bf16(npl, l);
     }
     l.fa.qmax = qmax_generic(fa0.cap);
+    l.fa.ntile = 2;
     l.qs_bytes = 0;
-    l.smem = fine_state_bytes(l.fa.qmax, fa0.cap);
+    l.smem = fine_state_bytes(l.fa.qmax, fa0.cap, 2);
     l.grid = grid_for(l.smem);
     return launch_stream_generic(key_dtype, compute_dtype, npl, l);
 }
@@ -720,6 +723,8 @@ hipError_t launch_attend(int32_t key_dtype, int32_t compute_dtype, int32_t d, in
     FineArgs fa{};
     fa.keys = fine_keys;
     fa.tid = transition_id;
+    // without ids the id loads read the key array (at least N ints) and are ignored
+    fa.tid_src = transition_id ? transition_id : static_cast<const int32_t *>(fine_keys);
     fa.q = q;
     fa.d = d;
     fa.c = c;

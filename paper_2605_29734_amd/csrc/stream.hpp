@@ -1,15 +1,29 @@
 // Bank-streaming kernels of the fine stage (shared by the translation units
 // that instantiate them).
 //
-// Work item = (selected cluster g, chunk j of g's segment). One block takes an
-// item from a dynamic counter and streams the chunk's key rows from HBM
-// exactly once per pass, scoring them on MFMA (v_mfma_f32_16x16x32_bf16,
-// keys as the 16-row A operand, queries as the 16-column B operand) against
-// every query that selected g (the children of Eq. local nodes, scored as in
-// Eq. local policy). Per query it keeps the online softmax statistics
-// (max, sum of exp((s - max)/tau)) and a top-k of (score, caller id) keys in
-// an LDS buffer behind a threshold filter. At the end of a pass it writes one
-// partial (m, Z, the chunk's top-k keys unsorted) per (query, chunk).
+// Work item = (selected cluster g, chunk j of g's segment). A block of four
+// waves streams the chunk's key rows from HBM exactly once per pass, scoring
+// them on MFMA (v_mfma_f32_16x16x32_bf16, keys as the 16-row A operand,
+// queries as the 16-column B operand) against every query that selected g
+// (the children of Eq. local nodes, scored as in Eq. local policy).
+//
+// A step covers 64 rows: each wave multiplies 16 of them against all the
+// pass's queries and writes the scores to an LDS tile (query-major). After one
+// barrier each wave reads the whole step for the queries it owns (n = wave,
+// wave + 4, ...), one row per lane, and keeps for them
+//   - online softmax statistics per lane (max, sum of exp((s - max)/tau)),
+//     reduced across the lanes when the pass ends;
+//   - a top-k of (score, caller id) keys in an LDS buffer private to the
+//     wave, behind a threshold filter; candidates are appended at ballot
+//     prefix positions and the buffer is cut down by a radix select when it
+//     could not take another step.
+// No LDS atomics and no other barrier are involved. With room for two score
+// tiles the steps alternate between them; with one, a second barrier per step
+// keeps a step's writes behind the previous step's reads.
+//
+// At the end of a pass each query writes its result: the final sorted top-k
+// and statistics of its (query, slot) pair when the chunk is the cluster's
+// whole segment, else one partial (m, Z, the chunk's top-k keys unsorted).
 //
 // Two variants:
 //   stream_lds      queries staged once per pass in LDS as B fragments; key
@@ -28,12 +42,15 @@ constexpr int kFineWaves = kFineThreads / kWave;
 constexpr int kRowsPerWave = 16;       // one MFMA tile of key rows per wave per step
 constexpr int kRowsPerStep = kRowsPerWave * kFineWaves;   // rows per block per step
 constexpr int kMaxQueryTiles = 4;      // at most 64 queries per pass over a chunk
+constexpr int kRing = 3;               // key load units in the LDS kernel's prefetch ring
 
 struct FineArgs {
     const void *keys;
-    const int32_t *tid;
+    const int32_t *tid;           // caller ids, or NULL: ids are bank rows
+    const int32_t *tid_src;       // tid, or (when NULL) any readable array of >= N ints
     const void *q;
     int32_t d, c, G, k, cap, qmax;
+    int32_t ntile;                // score tiles in LDS (1 or 2)
     float cexp;                   // log2(e) / tau
     const int32_t *qlist;
     const WorkItem *items;
@@ -45,8 +62,32 @@ struct FineArgs {
     int32_t *cand_id;
 };
 
-__host__ __device__ inline size_t fine_state_bytes(int qmax, int cap) {
-    return (size_t)qmax * cap * 8 + (size_t)qmax * (8 + 4 + 4 + 4) + (size_t)2 * kFineWaves * qmax * 4;
+// Epilogue lane map. A wave owns a contiguous run of qw = ceil(nqg / 4)
+// queries (n = wave * qw + jq). Each owned query gets a group of RG lanes
+// (jq = lane / RG, rg = lane % RG), and lane rg of the group takes the QP
+// consecutive rows rg*QP .. rg*QP + QP-1 of the step (QP = 64 / RG,
+// QP >= 4 * NQT >= qw), read four at a time. A query's row of the score tile
+// holds kTileRow = 68 floats, which spreads every 16-lane phase of those
+// 16-byte reads over all 64 banks.
+constexpr int kTileRow = kRowsPerStep + 4;
+template <int NQT>
+struct OwnerMap {
+    static constexpr int QP = NQT == 1 ? 4 : NQT == 2 ? 8 : 16;
+    static constexpr int RG = kWave / QP;
+};
+
+// Floats of one score tile for passes of up to qmax queries: the step's 64
+// caller ids, then one row per query.
+__host__ __device__ inline size_t fine_tile_floats(int qmax) {
+    return (size_t)kWave + (size_t)qmax * kTileRow;
+}
+
+// LDS of one block besides the staged queries: top-k buffers, score tiles,
+// per-query hand-over slots (threshold, count) and the query rows. The
+// end-of-pass softmax statistics reuse the first score tile.
+__host__ __device__ inline size_t fine_state_bytes(int qmax, int cap, int ntile) {
+    return (size_t)qmax * cap * 8 + (size_t)ntile * fine_tile_floats(qmax) * 4 +
+           (size_t)qmax * (8 + 4 + 4);
 }
 __host__ __device__ inline size_t fine_qs_bytes(int d, int qmax) {
     return (size_t)((d + 31) / 32) * (qmax / 16) * kWave * 16;
@@ -62,218 +103,311 @@ struct StreamLaunch {
     KernelEvents ev;
     hipStream_t stream;
 };
-hipError_t launch_stream_lds_bf16(int npl, bool has_tid, const StreamLaunch &l);
-hipError_t launch_stream_lds_f32(int npl, bool has_tid, const StreamLaunch &l);
+hipError_t launch_stream_lds_bf16(int npl, const StreamLaunch &l);
+hipError_t launch_stream_lds_f32(int npl, const StreamLaunch &l);
 hipError_t launch_stream_generic(int key_dtype, int compute_dtype, int npl, const StreamLaunch &l);
 
 namespace {
 
 struct FineSmem {
     bf16x8_t *qs;      // [d/32][16-query tiles][64 lanes] query B fragments (LDS kernel)
-    uint64_t *buf;     // [qmax][cap]
-    uint64_t *theta;   // [qmax]
-    uint32_t *cnt;     // [qmax]
-    uint32_t *pend;    // [qmax] candidates counted in the current step
+    uint64_t *buf;     // [qmax][cap] top-k buffers
+    float *st;         // [ntile][fine_tile_floats(qmax)] a step's caller ids, then its scores
+    uint64_t *otheta;  // [qmax] owner-wave hand-over of a query's threshold
+    int32_t *ocnt;     //        and buffer count
+    float *wm, *wz;    // [waves][qmax] per-wave softmax statistics at the end of a pass,
+    float *om, *oz;    // [qmax] and merged (both in the first score tile, then free)
     int32_t *qrow;     // [qmax]
-    float *wm, *wz;    // [waves][qmax]
 };
 
 __device__ __forceinline__ FineSmem fine_carve(unsigned char *raw, size_t qs_bytes, int qmax,
-                                               int cap) {
+                                               int cap, int ntile) {
     FineSmem sm;
     sm.qs = reinterpret_cast<bf16x8_t *>(raw);
     sm.buf = reinterpret_cast<uint64_t *>(raw + qs_bytes);
-    sm.theta = sm.buf + (size_t)qmax * cap;
-    sm.cnt = reinterpret_cast<uint32_t *>(sm.theta + qmax);
-    sm.pend = sm.cnt + qmax;
-    sm.qrow = reinterpret_cast<int32_t *>(sm.pend + qmax);
-    sm.wm = reinterpret_cast<float *>(sm.qrow + qmax);
+    sm.st = reinterpret_cast<float *>(sm.buf + (size_t)qmax * cap);
+    sm.otheta = reinterpret_cast<uint64_t *>(sm.st + (size_t)ntile * fine_tile_floats(qmax));
+    sm.ocnt = reinterpret_cast<int32_t *>(sm.otheta + qmax);
+    sm.qrow = sm.ocnt + qmax;
+    // 2 * 4 * qmax + 2 * qmax floats <= 64 + 68 * qmax: they fit in one tile
+    sm.wm = sm.st;
     sm.wz = sm.wm + kFineWaves * qmax;
+    sm.om = sm.wz + kFineWaves * qmax;
+    sm.oz = sm.om + qmax;
     return sm;
 }
 
-// Per-pass state: the rows of the pass's queries, empty top-k buffers.
-__device__ __forceinline__ void pass_begin(const FineArgs &a, const FineSmem &sm, int32_t qbeg,
-                                           int32_t qg0, int32_t nqg) {
-    for (int n = threadIdx.x; n < nqg; n += kFineThreads) {
-        sm.qrow[n] = a.qlist[qbeg + qg0 + n] / a.c;
-        sm.cnt[n] = 0;
-        sm.pend[n] = 0;
-        sm.theta[n] = 0;
-    }
-    __syncthreads();
+// Per-lane state of the owned query of the lane's group during a pass: the
+// query's top-k buffer count and threshold (the same in every lane of the
+// group).
+struct OwnedLane {
+    int cnt;
+    uint64_t theta;
+};
+
+__device__ __forceinline__ void owned_reset(OwnedLane &o) {
+    o.cnt = 0;
+    o.theta = 0;
 }
 
-// Compact the top-k buffers of this wave's queries (n = wave, wave + 4, ...)
-// that cannot take their pending candidates (cnt[n] + pend[n] > cap), and
-// reset pend[n] for every query of the wave. The queries are checked
-// lane-parallel (lane i looks at query wave + 4 i); only the full ones are
-// compacted, one after the other.
-template <int NPL>
-__device__ __forceinline__ void compact_wave_queries(const FineArgs &a, const FineSmem &sm, int nqg) {
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int n_mine = lane * kFineWaves + wave;
-    bool full = false;
-    if (n_mine < nqg) {
-        full = (int)sm.cnt[n_mine] + (int)sm.pend[n_mine] > a.cap;
-        sm.pend[n_mine] = 0;
-    }
-    uint64_t mask = __ballot(full);
-    while (mask) {
-        const int i = __builtin_ctzll(mask);
-        mask &= mask - 1;
-        const int n = i * kFineWaves + wave;
-        uint64_t th = 0;
-        const int kept = compact_select<NPL>(sm.buf + (size_t)n * a.cap, (int)sm.cnt[n], a.k,
-                                             kRowsPerStep, lane, th);
-        if (lane == 0) {
-            sm.cnt[n] = (uint32_t)kept;
-            sm.theta[n] = th;
-        }
-        wave_lds_sync();
-    }
-}
+// Softmax statistics in the MFMA result layout: lane (r16, kg) keeps, for
+// query column qt*16 + r16, the running max and sum of exp((s - max)/tau)
+// over its rows (4 kg + e of each of the wave's 16-row tiles). The rows a
+// lane sees do not depend on how many queries share the pass, and the lanes
+// and waves are merged in a fixed order, so a query's statistics are the same
+// bits whichever pass it falls in.
+template <int NQT>
+struct Stats {
+    float m[NQT], z[NQT];
+};
 
-// Scores of one 64-row step are in acc: this lane holds rows rt + 4*kg + e
-// (e = 0..3) for query column qt*16 + r16, with caller ids tidv[e]. Folds them
-// into the online (max, sum), then offers them to the queries' top-k buffers
-// in three phases: count the candidates above each threshold; compact the
-// buffers that could not take them (the threshold rises); append the
-// candidates still above the threshold (one LDS atomic per lane and query
-// tile). A buffer is compacted only when it would otherwise overflow (at most
-// 64 candidates per step, and a compaction leaves at least 64 free slots).
-template <int NQT, int NPL>
-__device__ __forceinline__ void tile_epilogue(const FineArgs &a, const FineSmem &sm,
-                                              const f32x4_t (&acc)[NQT], int64_t rt, int64_t r1,
-                                              int nqg, const int32_t (&tidv)[4], float (&m)[NQT],
-                                              float (&z)[NQT]) {
-    const int lane = threadIdx.x & 63, r16 = lane & 15, kg = lane >> 4;
-    const int cap = a.cap;
-    uint64_t key[NQT][4];
+template <int NQT>
+__device__ __forceinline__ void stats_reset(Stats<NQT> &st) {
 #pragma unroll
     for (int qt = 0; qt < NQT; ++qt) {
-        const int n = qt * 16 + r16;
-        const bool vq = n < nqg;
+        st.m[qt] = -INFINITY;
+        st.z[qt] = 0.0f;
+    }
+}
+
+// Folds one step's scores (this wave's 16 rows starting at rt) into the stats.
+template <int NQT>
+__device__ __forceinline__ void stats_update(Stats<NQT> &st, const f32x4_t (&acc)[NQT],
+                                             int64_t rt, int64_t r1, float cexp) {
+    const int kg = (threadIdx.x & 63) >> 4;
+    const int64_t nvalid = r1 - (rt + 4 * kg);    // rows of this lane's four that exist
+#pragma unroll
+    for (int qt = 0; qt < NQT; ++qt) {
         float tm = -INFINITY;
 #pragma unroll
         for (int e = 0; e < 4; ++e)
-            if (vq && rt + 4 * kg + e < r1) tm = fmaxf(tm, acc[qt][e]);
-        int pending = 0;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) key[qt][e] = 0;
+            if (e < nvalid) tm = fmaxf(tm, acc[qt][e]);
         if (tm != -INFINITY) {
-            const float M = fmaxf(m[qt], tm);
-            float zz = m[qt] == -INFINITY ? 0.0f : z[qt] * exp2f((m[qt] - M) * a.cexp);
+            const float M = fmaxf(st.m[qt], tm);
+            float zz = st.m[qt] == -INFINITY ? 0.0f : st.z[qt] * fast_exp2((st.m[qt] - M) * cexp);
 #pragma unroll
             for (int e = 0; e < 4; ++e)
-                if (rt + 4 * kg + e < r1) zz += exp2f((acc[qt][e] - M) * a.cexp);
-            m[qt] = M;
-            z[qt] = zz;
-            const uint64_t th = sm.theta[n];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                if (rt + 4 * kg + e < r1) {
-                    const uint64_t kk = ((uint64_t)ord_of(acc[qt][e]) << 32) |
-                                        (uint64_t)(~(uint32_t)tidv[e]);
-                    if (kk > th) {
-                        key[qt][e] = kk;
-                        ++pending;
-                    }
-                }
-            }
-        }
-        if (pending) atomicAdd(&sm.pend[n], (uint32_t)pending);
-    }
-    __syncthreads();
-    compact_wave_queries<NPL>(a, sm, nqg);
-    __syncthreads();
-#pragma unroll
-    for (int qt = 0; qt < NQT; ++qt) {
-        const int n = qt * 16 + r16;
-        if (n < nqg && (key[qt][0] | key[qt][1] | key[qt][2] | key[qt][3])) {
-            const uint64_t th = sm.theta[n];
-            int c = 0;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) c += key[qt][e] > th;
-            if (c) {
-                uint64_t *dst = sm.buf + (size_t)n * cap + atomicAdd(&sm.cnt[n], (uint32_t)c);
-#pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    if (key[qt][e] > th) *dst++ = key[qt][e];
-            }
+                if (e < nvalid) zz += fast_exp2((acc[qt][e] - M) * cexp);
+            st.m[qt] = M;
+            st.z[qt] = zz;
         }
     }
 }
 
-// End of a pass. For a chunk that is its cluster's whole segment, each query's
-// (query, slot) result is final: the top-k sorted into the slot's outputs and
-// the (max, sum) into slot_max / slot_sum. Otherwise each query writes one
-// partial: its chunk's best k keys, in no particular order (the merge that
-// reads them selects again), zero-padded to k, and the chunk's (max, sum).
+// Per-pass set-up: the rows of the pass's queries.
+__device__ __forceinline__ void pass_begin(const FineArgs &a, const FineSmem &sm, int32_t qbeg,
+                                           int32_t qg0, int32_t nqg) {
+    for (int n = threadIdx.x; n < nqg; n += kFineThreads) sm.qrow[n] = a.qlist[qbeg + qg0 + n] / a.c;
+    __syncthreads();
+}
+
+// This wave's MFMA results for one step into the score tile: the lane holds
+// rows 4 kg + e (e = 0..3) of the wave's 16 for query column qt*16 + r16.
+// Wave 0 also stores the step's caller ids (lane = row) ahead of the scores.
+template <int NQT>
+__device__ __forceinline__ void tile_write(float *tile, const f32x4_t (&acc)[NQT], int32_t tid) {
+    constexpr int ROW = kTileRow;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, r16 = lane & 15, kg = lane >> 4;
+#pragma unroll
+    for (int qt = 0; qt < NQT; ++qt)
+        *reinterpret_cast<f32x4_t *>(tile + kWave + (qt * 16 + r16) * ROW + wave * kRowsPerWave +
+                                     4 * kg) = acc[qt];
+    if (wave == 0) reinterpret_cast<int32_t *>(tile)[lane] = tid;
+}
+
+// Sum over the RG lanes of this lane's group (the same in all of them).
+template <int RG>
+__device__ __forceinline__ int group_sum(int x, int lane) {
+    if constexpr (RG > 1) x += (int)lane_xor32<1>((uint32_t)x, lane);
+    if constexpr (RG > 2) x += (int)lane_xor32<2>((uint32_t)x, lane);
+    if constexpr (RG > 4) x += (int)lane_xor32<4>((uint32_t)x, lane);
+    if constexpr (RG > 8) x += (int)lane_xor32<8>((uint32_t)x, lane);
+    return x;
+}
+
+// The owned queries' share of one step (see OwnerMap). Rows at or beyond r1
+// are not candidates. Each lane counts its candidates above the threshold;
+// a buffer that cannot take its group's candidates is compacted (one query at
+// a time by the whole wave, raising its threshold); then each lane appends
+// the candidates still above the threshold at its place in the group (an
+// exclusive scan of the counts over the group's lanes).
+template <int NQT, int NPL>
+__device__ __forceinline__ void owner_epilogue(const FineArgs &a, const FineSmem &sm,
+                                               const float *tile, int64_t base, int64_t r1,
+                                               int nqg, OwnedLane &o) {
+    constexpr int QP = OwnerMap<NQT>::QP, RG = OwnerMap<NQT>::RG;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int jq = lane / RG, rg = lane % RG;
+    const int qw = (nqg + kFineWaves - 1) / kFineWaves;
+    const int n = wave * qw + jq;
+    const bool active = jq < qw && n < nqg;
+    const int nn = active ? n : 0;
+    const float *trow = tile + kWave + nn * kTileRow + rg * QP;
+    const int32_t *tids = reinterpret_cast<const int32_t *>(tile) + rg * QP;
+    const int64_t valid = active ? r1 - base - rg * QP : 0;   // of this lane's rows, those that exist
+    uint64_t key[QP];
+    int mine = 0;
+#pragma unroll
+    for (int i4 = 0; i4 < QP; i4 += 4) {
+        const f32x4_t s4 = *reinterpret_cast<const f32x4_t *>(trow + i4);
+        const int4 t4 = *reinterpret_cast<const int4 *>(tids + i4);
+        const int32_t tv[4] = {t4.x, t4.y, t4.z, t4.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int i = i4 + e;
+            const uint64_t kk = ((uint64_t)ord_of(s4[e]) << 32) | (uint64_t)(~(uint32_t)tv[e]);
+            key[i] = i < valid ? kk : 0;
+            mine += key[i] > o.theta;
+        }
+    }
+    if (!__ballot(mine > 0)) return;
+    const int count = group_sum<RG>(mine, lane);
+    uint64_t full = __ballot(active && rg == 0 && o.cnt + count > a.cap);
+    if (full) {
+        wave_lds_sync();
+        for (; full; full &= full - 1) {
+            const int l0 = __builtin_ctzll(full);
+            const int n0 = wave * qw + l0 / RG;
+            const int c0 = __shfl(o.cnt, l0);
+            uint64_t th = 0;
+            const int c1 = compact_select<NPL>(sm.buf + (size_t)n0 * a.cap, c0, a.k, kWave, lane, th);
+            if (jq == l0 / RG) {
+                o.cnt = c1;
+                o.theta = th;
+            }
+        }
+        mine = 0;
+#pragma unroll
+        for (int i = 0; i < QP; ++i) mine += key[i] > o.theta;
+    }
+    // exclusive scan of the lanes' counts within the group
+    int incl = mine;
+#pragma unroll
+    for (int off = 1; off < RG; off <<= 1) {
+        const int y = __shfl_up(incl, off, RG);
+        if (rg >= off) incl += y;
+    }
+    const int total = __shfl(incl, jq * RG + RG - 1);
+    uint64_t *b = sm.buf + (size_t)nn * a.cap + o.cnt + (incl - mine);
+    int w = 0;
+#pragma unroll
+    for (int i = 0; i < QP; ++i) {
+        if (key[i] > o.theta) b[w++] = key[i];
+    }
+    o.cnt += total;
+}
+
+// One step's end, common to both kernels: scores to the tile, barrier(s),
+// then the owned queries' epilogue. Every wave of the block calls it the same
+// number of times. tid: caller id of row base + lane (loaded with the step's
+// keys, so that no load is waited for here).
+template <int NQT, int NPL>
+__device__ __forceinline__ void step_end(const FineArgs &a, const FineSmem &sm,
+                                         const f32x4_t (&acc)[NQT], int step, int64_t base,
+                                         int64_t r1, int nqg, int32_t tid, OwnedLane &o,
+                                         Stats<NQT> &st) {
+    stats_update<NQT>(st, acc, base + (threadIdx.x >> 6) * kRowsPerWave, r1, a.cexp);
+    float *tile = sm.st + (size_t)(a.ntile == 2 ? step & 1 : 0) * fine_tile_floats(a.qmax);
+    if (a.ntile == 1) __syncthreads();      // the previous step's reads are done
+    tile_write<NQT>(tile, acc, tid);
+    __syncthreads();
+    owner_epilogue<NQT, NPL>(a, sm, tile, base, r1, nqg, o);
+}
+
+// Caller id of row base + lane of a step (rows past the chunk clamped). The
+// load is unconditional, so that the compiler can count outstanding loads
+// exactly: a bank without an id array (ids = bank rows) passes any readable
+// array of at least N ints as `src`, and tid_value() replaces the loaded
+// value by the row where the step uses it (a select on the loaded value at
+// load time would make the compiler wait for every load in flight).
+__device__ __forceinline__ int32_t step_tid_load(const int32_t *__restrict__ src, int64_t base,
+                                                 int64_t r1) {
+    return src[min(base + (int64_t)(threadIdx.x & 63), r1 - 1)];
+}
+__device__ __forceinline__ int32_t tid_value(int32_t loaded, bool identity, int64_t base,
+                                             int64_t r1) {
+    return identity ? (int32_t)min(base + (int64_t)(threadIdx.x & 63), r1 - 1) : loaded;
+}
+
+// End of a pass: for each owned query, the final sorted top-k and statistics
+// of its (query, slot) pair when the chunk is the cluster's whole segment
+// (passes over an item cover disjoint queries), else one partial: the
+// chunk's best k keys unsorted and zero-padded, and (max, sum). The lanes'
+// statistics are merged within each group and handed over through LDS with
+// the counts, then the buffers are written out query by query.
 template <int NQT, int NPL>
 __device__ __forceinline__ void pass_end(const FineArgs &a, const FineSmem &sm, int64_t p0,
                                          int32_t qbeg, bool single, int32_t qg0, int32_t nqg,
-                                         float (&m)[NQT], float (&z)[NQT]) {
+                                         OwnedLane &o, Stats<NQT> &st) {
+    constexpr int RG = OwnerMap<NQT>::RG;
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6, r16 = lane & 15, kg = lane >> 4;
-    __syncthreads();           // the last step's appends are complete
-    for (int n = wave; n < nqg; n += kFineWaves) {
-        uint64_t *b = sm.buf + (size_t)n * a.cap;
-        int cn = (int)sm.cnt[n];
-        if (single) {
-            const int64_t e = a.qlist[qbeg + qg0 + n];
-            uint64_t v[NPL];
-#pragma unroll
-            for (int q = 0; q < NPL; ++q) v[q] = (q * kWave + lane < cn) ? b[q * kWave + lane] : 0;
-            wave_sort_regs<NPL>(v, lane);
-#pragma unroll
-            for (int q = 0; q < NPL; ++q) {
-                const int r = q * kWave + lane;
-                if (r < a.k) {
-                    const uint64_t key = r < cn ? v[q] : 0;
-                    a.cand_score[e * a.k + r] = key ? key_score(key) : -INFINITY;
-                    a.cand_id[e * a.k + r] = key ? key_id(key) : -1;
-                }
-            }
-            continue;
-        }
-        if (cn > a.k) {
-            uint64_t th = 0;
-            cn = compact_select<NPL>(b, cn, a.k, a.cap - a.k, lane, th);
-        }
-        const int64_t p = p0 + qg0 + n;
-        for (int i = lane; i < a.k; i += kWave) a.pk[p * a.k + i] = i < cn ? b[i] : 0;
-        if (lane == 0) a.pc[p] = cn;
-    }
+    const int jq = lane / RG, rg = lane % RG;
+    const int qw = (nqg + kFineWaves - 1) / kFineWaves;
+    const int n = wave * qw + jq;
+    if (jq < qw && n < nqg && rg == 0) sm.ocnt[n] = o.cnt;
+    __syncthreads();           // every wave is done with the score tile, which the statistics reuse
+    // statistics: the four row groups of a lane column, then the waves in order
 #pragma unroll
     for (int qt = 0; qt < NQT; ++qt) {
 #pragma unroll
         for (int sh = 16; sh <= 32; sh <<= 1) {
-            const float m2 = __shfl_xor(m[qt], sh);
-            const float z2 = __shfl_xor(z[qt], sh);
-            mz_merge(m[qt], z[qt], m2, z2, a.cexp);
+            const float m2 = __shfl_xor(st.m[qt], sh), z2 = __shfl_xor(st.z[qt], sh);
+            mz_merge(st.m[qt], st.z[qt], m2, z2, a.cexp);
         }
-        const int n = qt * 16 + r16;
-        if (kg == 0 && n < nqg) {
-            sm.wm[wave * a.qmax + n] = m[qt];
-            sm.wz[wave * a.qmax + n] = z[qt];
+        const int q = qt * 16 + r16;
+        if (kg == 0 && q < nqg) {
+            sm.wm[wave * a.qmax + q] = st.m[qt];
+            sm.wz[wave * a.qmax + q] = st.z[qt];
         }
     }
     __syncthreads();
-    for (int n = t; n < nqg; n += kFineThreads) {
+    for (int q = t; q < nqg; q += kFineThreads) {
         float M = -INFINITY, Z = 0.0f;
         for (int w = 0; w < kFineWaves; ++w)
-            mz_merge(M, Z, sm.wm[w * a.qmax + n], sm.wz[w * a.qmax + n], a.cexp);
-        if (single) {
-            const int64_t e = a.qlist[qbeg + qg0 + n];
-            a.slot_max[e] = M;
-            a.slot_sum[e] = Z;
-        } else {
-            const int64_t p = p0 + qg0 + n;
-            a.pm[p] = M;
-            a.pz[p] = Z;
-        }
+            mz_merge(M, Z, sm.wm[w * a.qmax + q], sm.wz[w * a.qmax + q], a.cexp);
+        sm.om[q] = M;
+        sm.oz[q] = Z;
     }
     __syncthreads();
+    const int n1 = min(nqg, (wave + 1) * qw);
+    for (int q = wave * qw; q < n1; ++q) {
+        uint64_t *b = sm.buf + (size_t)q * a.cap;
+        int cn = sm.ocnt[q];
+        const float Mq = sm.om[q], Zq = sm.oz[q];
+        if (single) {
+            const int64_t e = a.qlist[qbeg + qg0 + q];
+            uint64_t v[NPL];
+#pragma unroll
+            for (int j = 0; j < NPL; ++j) v[j] = (j * kWave + lane < cn) ? b[j * kWave + lane] : 0;
+            wave_sort_regs<NPL>(v, lane);
+#pragma unroll
+            for (int j = 0; j < NPL; ++j) {
+                const int r = j * kWave + lane;
+                if (r < a.k) {
+                    const uint64_t key = r < cn ? v[j] : 0;
+                    a.cand_score[e * a.k + r] = key ? key_score(key) : -INFINITY;
+                    a.cand_id[e * a.k + r] = key ? key_id(key) : -1;
+                }
+            }
+            if (lane == 0) {
+                a.slot_max[e] = Mq;
+                a.slot_sum[e] = Zq;
+            }
+        } else {
+            if (cn > a.k) {
+                uint64_t th = 0;
+                cn = compact_select<NPL>(b, cn, a.k, a.cap - a.k, lane, th);
+            }
+            const int64_t p = p0 + qg0 + q;
+            for (int i = lane; i < a.k; i += kWave) a.pk[p * a.k + i] = i < cn ? b[i] : 0;
+            if (lane == 0) {
+                a.pc[p] = cn;
+                a.pm[p] = Mq;
+                a.pz[p] = Zq;
+            }
+        }
+        wave_lds_sync();
+    }
 }
 
 // ---- generic pass: query fragments read from global memory ------------------
@@ -287,16 +421,19 @@ __device__ __forceinline__ void pass_generic(const FineArgs &a, const FineSmem &
     const T *Q = static_cast<const T *>(a.q);
     pass_begin(a, sm, qbeg, qg0, nqg);
     const T *qp[NQT];
-    float m[NQT], z[NQT];
 #pragma unroll
     for (int qt = 0; qt < NQT; ++qt) {
         const int n = qt * 16 + r16;
         qp[qt] = Q + (int64_t)sm.qrow[n < nqg ? n : 0] * d;
-        m[qt] = -INFINITY;
-        z[qt] = 0.0f;
     }
-    for (int64_t base = r0; base < r1; base += kRowsPerStep) {
+    OwnedLane o;
+    owned_reset(o);
+    Stats<NQT> st;
+    stats_reset<NQT>(st);
+    int step = 0;
+    for (int64_t base = r0; base < r1; base += kRowsPerStep, ++step) {
         const int64_t rt = base + wave * kRowsPerWave;
+        const int32_t tid = tid_value(step_tid_load(a.tid_src, base, r1), a.tid == nullptr, base, r1);
         f32x4_t acc[NQT];
 #pragma unroll
         for (int qt = 0; qt < NQT; ++qt) acc[qt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
@@ -325,15 +462,9 @@ __device__ __forceinline__ void pass_generic(const FineArgs &a, const FineSmem &
                 }
             }
         }
-        int32_t tidv[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const int64_t row = rt + 4 * kg + e;
-            tidv[e] = row < r1 ? (a.tid ? a.tid[row] : (int32_t)row) : -1;
-        }
-        tile_epilogue<NQT, NPL>(a, sm, acc, rt, r1, nqg, tidv, m, z);
+        step_end<NQT, NPL>(a, sm, acc, step, base, r1, nqg, tid, o, st);
     }
-    pass_end<NQT, NPL>(a, sm, p0, qbeg, single, qg0, nqg, m, z);
+    pass_end<NQT, NPL>(a, sm, p0, qbeg, single, qg0, nqg, o, st);
 }
 
 // ---- LDS pass: query fragments staged in LDS, key fragments prefetched -------
@@ -365,39 +496,35 @@ struct AFrag<float> {
 };
 
 // One load unit: U k-steps of one 16-row tile for this lane, and the caller
-// ids of the lane's 4 output rows of that tile.
+// id of row lane of the unit's step (used by the step's epilogue).
 template <typename KT>
 struct LoadUnit {
     AFrag<KT> f[AFrag<KT>::U];
-    int32_t tid[4];
+    int32_t tid;
 };
 
 // Unconditional loads only (rows clamped into the chunk), so that the compiler
 // can count outstanding loads exactly and wait for one unit at a time.
-template <typename KT, bool HAS_TID>
+template <typename KT>
 __device__ __forceinline__ void lds_load_unit(LoadUnit<KT> &lu, const KT *__restrict__ K,
-                                              const int32_t *__restrict__ tid, int d, int NG, int u,
-                                              int64_t r0, int64_t r1) {
+                                              const int32_t *__restrict__ tid_src, int d, int NG,
+                                              int u, int64_t r0, int64_t r1) {
     constexpr int U = AFrag<KT>::U;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, r16 = lane & 15, kg = lane >> 4;
     const int tt = u / NG, gi = u - tt * NG;
-    const int64_t rt = r0 + (int64_t)tt * kRowsPerStep + wave * kRowsPerWave;
-    const int64_t row = min(rt + r16, r1 - 1);
+    const int64_t base = r0 + (int64_t)tt * kRowsPerStep;
+    const int64_t row = min(base + wave * kRowsPerWave + r16, r1 - 1);
     const KT *kp = K + row * d + 32 * U * gi + 8 * kg;
 #pragma unroll
     for (int uu = 0; uu < U; ++uu) lu.f[uu].load(kp + 32 * uu);
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-        const int64_t rr = min(rt + 4 * kg + e, r1 - 1);
-        lu.tid[e] = HAS_TID ? tid[rr] : (int32_t)rr;
-    }
+    lu.tid = step_tid_load(tid_src, base, r1);
 }
 
 template <typename KT, int NQT, int NPL>
 __device__ __forceinline__ void lds_compute_unit(const FineArgs &a, const FineSmem &sm,
                                                  const LoadUnit<KT> &lu, int NG, int u, int64_t r0,
                                                  int64_t r1, int nqg, f32x4_t (&acc)[NQT],
-                                                 float (&m)[NQT], float (&z)[NQT]) {
+                                                 OwnedLane &o, Stats<NQT> &st) {
     constexpr int U = AFrag<KT>::U;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int tt = u / NG, gi = u - tt * NG;
@@ -405,6 +532,9 @@ __device__ __forceinline__ void lds_compute_unit(const FineArgs &a, const FineSm
 #pragma unroll
     for (int qt = 0; qt < NQT; ++qt) acc[qt] *= keep;
     const bf16x8_t *qs = sm.qs + (size_t)gi * U * NQT * kWave + lane;
+    // Query fragments are read from LDS a few k-steps ahead of their MFMAs;
+    // the scheduling barriers keep the compiler from hoisting all of them
+    // (4 registers each) to the top of the unit.
 #pragma unroll
     for (int uu = 0; uu < U; ++uu) {
         const bf16x8_t A = lu.f[uu].bf16();
@@ -412,14 +542,16 @@ __device__ __forceinline__ void lds_compute_unit(const FineArgs &a, const FineSm
         for (int qt = 0; qt < NQT; ++qt)
             acc[qt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, qs[(uu * NQT + qt) * kWave],
                                                               acc[qt], 0, 0, 0);
+        if ((uu & 3) == 3) __builtin_amdgcn_sched_barrier(0);
     }
     if (gi == NG - 1) {
-        const int64_t rt = r0 + (int64_t)tt * kRowsPerStep + wave * kRowsPerWave;
-        tile_epilogue<NQT, NPL>(a, sm, acc, rt, r1, nqg, lu.tid, m, z);
+        const int64_t base = r0 + (int64_t)tt * kRowsPerStep;
+        step_end<NQT, NPL>(a, sm, acc, tt, base, r1, nqg,
+                           tid_value(lu.tid, a.tid == nullptr, base, r1), o, st);
     }
 }
 
-template <typename KT, bool HAS_TID, int NQT, int NPL>
+template <typename KT, int NQT, int NPL>
 __device__ __forceinline__ void pass_lds(const FineArgs &a, const FineSmem &sm, int64_t p0,
                                          bool single, int64_t r0, int64_t r1, int32_t qbeg,
                                          int32_t qg0, int32_t nqg) {
@@ -428,46 +560,65 @@ __device__ __forceinline__ void pass_lds(const FineArgs &a, const FineSmem &sm, 
     const int d = a.d;
     const KT *__restrict__ K = static_cast<const KT *>(a.keys);
     const KT *__restrict__ Q = static_cast<const KT *>(a.q);
-    pass_begin(a, sm, qbeg, qg0, nqg);
-
-    // stage the queries as MFMA B fragments: [k-step][query tile][lane]
     const int KS = d >> 5;
-    for (int idx = t; idx < KS * NQT * kWave; idx += kFineThreads) {
-        const int s = idx / (NQT * kWave), rem = idx - s * NQT * kWave;
-        const int qt = rem >> 6, ln = rem & 63;
-        const int n = qt * 16 + (ln & 15), k = 32 * s + 8 * (ln >> 4);
-        sm.qs[idx] = n < nqg ? load8(Q + (int64_t)sm.qrow[n] * d + k) : zero8();
-    }
-    __syncthreads();
-
     const int NG = KS / U;
     const int T = (int)((r1 - r0 + kRowsPerStep - 1) / kRowsPerStep);
     const int total = T * NG;
-    float m[NQT], z[NQT];
+
+    // A ring of kRing load units: while unit u is multiplied (and its step's
+    // epilogue runs) the loads of the next kRing - 1 units are in flight. Past
+    // the end, the last unit is loaded again (an L2 hit) so that every load
+    // stays unconditional and the compiler can wait for exactly one unit at a
+    // time. The first units are requested before the queries are staged.
+    // the largest top-k buffers leave fewer registers for the ring
+    constexpr int R = NPL < 8 ? kRing : (sizeof(KT) == 4 ? 2 : 3);
+    LoadUnit<KT> ring[R];
+#pragma unroll
+    for (int j = 0; j < R - 1; ++j)
+        lds_load_unit<KT>(ring[j], K, a.tid_src, d, NG, min(j, total - 1), r0, r1);
+
+    pass_begin(a, sm, qbeg, qg0, nqg);
+    // stage the queries as MFMA B fragments: [k-step][query tile][lane], eight
+    // fragments per thread loaded before any is stored (indices past the end
+    // load the last fragment again and store nothing)
+    {
+        constexpr int kBatch = 8;
+        const int nfrag = KS * NQT * kWave;
+        for (int i0 = t; i0 < nfrag; i0 += kFineThreads * kBatch) {
+            bf16x8_t f[kBatch];
+#pragma unroll
+            for (int b = 0; b < kBatch; ++b) {
+                const int idx = min(i0 + b * kFineThreads, nfrag - 1);
+                const int s = idx / (NQT * kWave), rem = idx - s * NQT * kWave;
+                const int qt = rem >> 6, ln = rem & 63;
+                const int n = qt * 16 + (ln & 15), k = 32 * s + 8 * (ln >> 4);
+                f[b] = load8(Q + (int64_t)sm.qrow[n < nqg ? n : 0] * d + k);
+                if (n >= nqg) f[b] = zero8();
+            }
+#pragma unroll
+            for (int b = 0; b < kBatch; ++b)
+                if (i0 + b * kFineThreads < nfrag) sm.qs[i0 + b * kFineThreads] = f[b];
+        }
+    }
+    __syncthreads();
+
+    OwnedLane o;
+    owned_reset(o);
+    Stats<NQT> st;
+    stats_reset<NQT>(st);
     f32x4_t acc[NQT];
 #pragma unroll
-    for (int qt = 0; qt < NQT; ++qt) {
-        m[qt] = -INFINITY;
-        z[qt] = 0.0f;
-        acc[qt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int qt = 0; qt < NQT; ++qt) acc[qt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int u = 0; u < total; u += R) {
+#pragma unroll
+        for (int j = 0; j < R; ++j) {
+            lds_load_unit<KT>(ring[(j + R - 1) % R], K, a.tid_src, d, NG,
+                              min(u + j + R - 1, total - 1), r0, r1);
+            if (u + j < total)
+                lds_compute_unit<KT, NQT, NPL>(a, sm, ring[j], NG, u + j, r0, r1, nqg, acc, o, st);
+        }
     }
-
-    // A ring of three load units: while unit u is multiplied (and its step's
-    // epilogue runs) the loads of units u+1 and u+2 are in flight. Past the
-    // end, the last unit is loaded again (an L2 hit) so that every load stays
-    // unconditional and the compiler can wait for exactly one unit at a time.
-    LoadUnit<KT> s0, s1, s2;
-    lds_load_unit<KT, HAS_TID>(s0, K, a.tid, d, NG, 0, r0, r1);
-    lds_load_unit<KT, HAS_TID>(s1, K, a.tid, d, NG, min(1, total - 1), r0, r1);
-    for (int u = 0; u < total; u += 3) {
-        lds_load_unit<KT, HAS_TID>(s2, K, a.tid, d, NG, min(u + 2, total - 1), r0, r1);
-        lds_compute_unit<KT, NQT, NPL>(a, sm, s0, NG, u, r0, r1, nqg, acc, m, z);
-        lds_load_unit<KT, HAS_TID>(s0, K, a.tid, d, NG, min(u + 3, total - 1), r0, r1);
-        if (u + 1 < total) lds_compute_unit<KT, NQT, NPL>(a, sm, s1, NG, u + 1, r0, r1, nqg, acc, m, z);
-        lds_load_unit<KT, HAS_TID>(s1, K, a.tid, d, NG, min(u + 4, total - 1), r0, r1);
-        if (u + 2 < total) lds_compute_unit<KT, NQT, NPL>(a, sm, s2, NG, u + 2, r0, r1, nqg, acc, m, z);
-    }
-    pass_end<NQT, NPL>(a, sm, p0, qbeg, single, qg0, nqg, m, z);
+    pass_end<NQT, NPL>(a, sm, p0, qbeg, single, qg0, nqg, o, st);
 }
 
 // Work loop shared by both kernels: items (cluster, chunk) from the planned
@@ -498,20 +649,20 @@ __device__ __forceinline__ bool next_item(const FineArgs &a, int32_t *s_item, bo
     return true;
 }
 
-template <typename KT, bool HAS_TID, int NPL>
+template <typename KT, int NPL>
 __global__ __launch_bounds__(kFineThreads) void stream_lds(FineArgs a, int32_t qs_bytes) {
     extern __shared__ __align__(16) unsigned char smem_raw[];
     __shared__ int32_t s_item;
-    const FineSmem sm = fine_carve(smem_raw, qs_bytes, a.qmax, a.cap);
+    const FineSmem sm = fine_carve(smem_raw, qs_bytes, a.qmax, a.cap, a.ntile);
     ItemPass it;
     for (bool first = true; next_item(a, &s_item, first, it); first = false) {
         for (int32_t qg0 = 0; qg0 < it.nq; qg0 += a.qmax) {
             const int32_t nqg = min(a.qmax, it.nq - qg0);
             switch ((nqg + 15) >> 4) {
-                case 1: pass_lds<KT, HAS_TID, 1, NPL>(a, sm, it.p0, it.single, it.r0, it.r1, it.qbeg, qg0, nqg); break;
-                case 2: pass_lds<KT, HAS_TID, 2, NPL>(a, sm, it.p0, it.single, it.r0, it.r1, it.qbeg, qg0, nqg); break;
-                case 3: pass_lds<KT, HAS_TID, 3, NPL>(a, sm, it.p0, it.single, it.r0, it.r1, it.qbeg, qg0, nqg); break;
-                default: pass_lds<KT, HAS_TID, 4, NPL>(a, sm, it.p0, it.single, it.r0, it.r1, it.qbeg, qg0, nqg); break;
+                case 1: pass_lds<KT, 1, NPL>(a, sm, it.p0, it.single, it.r0, it.r1, it.qbeg, qg0, nqg); break;
+                case 2: pass_lds<KT, 2, NPL>(a, sm, it.p0, it.single, it.r0, it.r1, it.qbeg, qg0, nqg); break;
+                case 3: pass_lds<KT, 3, NPL>(a, sm, it.p0, it.single, it.r0, it.r1, it.qbeg, qg0, nqg); break;
+                default: pass_lds<KT, 4, NPL>(a, sm, it.p0, it.single, it.r0, it.r1, it.qbeg, qg0, nqg); break;
             }
         }
     }
@@ -521,7 +672,7 @@ template <typename T, bool BF16, int NPL>
 __global__ __launch_bounds__(kFineThreads) void stream_generic(FineArgs a) {
     extern __shared__ __align__(16) unsigned char smem_raw[];
     __shared__ int32_t s_item;
-    const FineSmem sm = fine_carve(smem_raw, 0, a.qmax, a.cap);
+    const FineSmem sm = fine_carve(smem_raw, 0, a.qmax, a.cap, a.ntile);
     ItemPass it;
     for (bool first = true; next_item(a, &s_item, first, it); first = false) {
         for (int32_t qg0 = 0; qg0 < it.nq; qg0 += a.qmax) {
@@ -549,14 +700,11 @@ hipError_t launch_stream_kernel(Kern kern, const StreamLaunch &l, Args... args) 
 }
 
 template <typename KT>
-hipError_t launch_stream_lds_t(int npl, bool has_tid, const StreamLaunch &l) {
-    switch (npl * 2 + (has_tid ? 1 : 0)) {
-        case 4: return launch_stream_kernel(stream_lds<KT, false, 2>, l, l.fa, l.qs_bytes);
-        case 5: return launch_stream_kernel(stream_lds<KT, true, 2>, l, l.fa, l.qs_bytes);
-        case 8: return launch_stream_kernel(stream_lds<KT, false, 4>, l, l.fa, l.qs_bytes);
-        case 9: return launch_stream_kernel(stream_lds<KT, true, 4>, l, l.fa, l.qs_bytes);
-        case 16: return launch_stream_kernel(stream_lds<KT, false, 8>, l, l.fa, l.qs_bytes);
-        case 17: return launch_stream_kernel(stream_lds<KT, true, 8>, l, l.fa, l.qs_bytes);
+hipError_t launch_stream_lds_t(int npl, const StreamLaunch &l) {
+    switch (npl) {
+        case 2: return launch_stream_kernel(stream_lds<KT, 2>, l, l.fa, l.qs_bytes);
+        case 4: return launch_stream_kernel(stream_lds<KT, 4>, l, l.fa, l.qs_bytes);
+        case 8: return launch_stream_kernel(stream_lds<KT, 8>, l, l.fa, l.qs_bytes);
     }
     return hipErrorInvalidValue;
 }

@@ -2,7 +2,7 @@
 #include "stream.hpp"
 
 namespace htam {
-hipError_t launch_stream_lds_bf16(int npl, bool has_tid, const StreamLaunch &l) {
-    return launch_stream_lds_t<__bf16>(npl, has_tid, l);
+hipError_t launch_stream_lds_bf16(int npl, const StreamLaunch &l) {
+    return launch_stream_lds_t<__bf16>(npl, l);
 }
 }  // namespace htam

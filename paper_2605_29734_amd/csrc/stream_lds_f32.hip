@@ -3,7 +3,7 @@
 #include "stream.hpp"
 
 namespace htam {
-hipError_t launch_stream_lds_f32(int npl, bool has_tid, const StreamLaunch &l) {
-    return launch_stream_lds_t<float>(npl, has_tid, l);
+hipError_t launch_stream_lds_f32(int npl, const StreamLaunch &l) {
+    return launch_stream_lds_t<float>(npl, l);
 }
 }  // namespace htam

@@ -24,7 +24,7 @@ def to_np(t: torch.Tensor) -> np.ndarray:
 
 
 def run_case(spec, seed=0, rows=None, tau=None, gen_device="cpu", check_build=True,
-             determinism=False):
+             determinism=False, identity_ids=False):
     from paper_2605_29734_amd import htam
     dev = torch.device("cuda:0")
     tau = spec.tau if tau is None else tau
@@ -48,6 +48,10 @@ def run_case(spec, seed=0, rows=None, tau=None, gen_device="cpu", check_build=Tr
         if spec.N <= (1 << 20):
             assert torch.equal(bank.fine_keys, kin[bank.transition_id.long()]), "key gather"
     del kin
+    if identity_ids:        # the bank without a transition id array: ids are bank rows
+        bank = htam.Bank(coarse_keys=bank.coarse_keys, fine_keys=bank.fine_keys,
+                         seg_offsets=bank.seg_offsets, transition_id=None, compute=bank.compute)
+        tid = None
     say("[step] retrieve (coarse, attend, topk)")
     r = htam.Retriever(bank, spec.B, spec.top_c, spec.top_k, tau)
     out = r.run(q)

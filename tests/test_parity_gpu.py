@@ -82,6 +82,15 @@ def test_many_queries_per_cluster_lds_kernel(storage):
              determinism=True)
 
 
+@pytest.mark.parametrize("storage,compute,d", [("bf16", "bf16", 512), ("f32", "bf16", 512),
+                                               ("f32", "f32", 96)])
+def test_identity_transition_ids(storage, compute, d):
+    """A bank without a transition id array reports bank rows as ids (LDS and generic kernels)."""
+    run_case(synth.Spec("identity", B=96, d=d, G=24, N=12000, top_c=3, top_k=20, tau=0.5,
+                        storage=storage, compute=compute, sizes="zipf", zipf_s=1.0, min_size=4),
+             identity_ids=True)
+
+
 def test_topk_merge_standalone():
     """htam_topk on unsorted lists with padding and exact ties, against the oracle's sort."""
     from paper_2605_29734_amd import htam
