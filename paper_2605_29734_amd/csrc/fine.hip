@@ -606,16 +606,6 @@ AttendWs attend_layout(void *ws, int32_t d, int32_t G, int64_t N, int32_t key_by
     return w;
 }
 
-// Queries per pass of the LDS kernel: the most (a multiple of 16, at most 64)
-// whose B fragments and top-k state fit in the LDS budget; 0 when the LDS
-// kernel does not apply (fp32 arithmetic, d not a multiple of 32 * U, or not
-// even 16 queries fit).
-static int qmax_for_lds(int32_t key_dtype, int32_t compute_dtype, int d, int cap, size_t budget) {
-    const int U = key_dtype == kF32 ? 8 : 16;
-    if (compute_dtype != kBF16 || d % (32 * U) != 0) return 0;
-    return qmax_lds(d, cap, budget);
-}
-
 // Queries per pass actually provisioned: enough for about twice the mean
 // number of queries per selected cluster (a cluster with more takes several
 // passes), so that small query groups leave room for more blocks per CU.
@@ -635,15 +625,11 @@ static hipError_t launch_stream(int32_t key_dtype, int32_t compute_dtype, const 
     l.fa = fa0;
     l.ev = ev;
     l.stream = s;
-    auto grid_for = [&](size_t smem) {
-        int per_cu = (int)((budget + 1024) / (smem + 1024));
-        if (per_cu < 1) per_cu = 1;
-        if (per_cu > 4) per_cu = 4;
-        int64_t g = (int64_t)n_cu * per_cu;
-        if (g > w_max) g = w_max;
-        return (int)(g < 1 ? 1 : g);
-    };
-    int ql = qmax_for_lds(key_dtype, compute_dtype, fa0.d, fa0.cap, budget);
+    l.n_cu = n_cu > 0 ? n_cu : 1;
+    l.max_grid = w_max;
+    // The LDS-staged kernels need bf16 arithmetic and d % 256 == 0 (one block
+    // per CU with bf16 storage reads longer units: d % 512 == 0 there).
+    int ql = (compute_dtype == kBF16 && fa0.d % 256 == 0) ? qmax_lds(fa0.d, fa0.cap, budget) : 0;
     if (ql > 0) {
         ql = qmax_for_load(ql, bc, fa0.G);
         l.fa.qmax = ql;
@@ -651,14 +637,17 @@ static hipError_t launch_stream(int32_t key_dtype, int32_t compute_dtype, const 
         // two score tiles (one barrier per step) when they fit
         l.fa.ntile = l.qs_bytes + fine_state_bytes(ql, fa0.cap, 2) <= budget ? 2 : 1;
         l.smem = l.qs_bytes + fine_state_bytes(ql, fa0.cap, l.fa.ntile);
-        l.grid = grid_for(l.smem);
-        return key_dtype == kF32 ? launch_stream_lds_f32(npl, l) : launch_stream_lds_bf16(npl, l);
+        // two blocks per CU when two blocks' LDS fits (and the buffers leave the registers)
+        const bool two = npl <= 4 && 2 * (l.smem + 256) <= budget + 256;
+        const int unit_k = key_dtype == kF32 ? 8 : 16;
+        if (two || fa0.d % (32 * unit_k) == 0)
+            return key_dtype == kF32 ? launch_stream_lds_f32(npl, two, l)
+                                     : launch_stream_lds_bf16(npl, two, l);
     }
     l.fa.qmax = qmax_generic(fa0.cap);
     l.fa.ntile = 2;
     l.qs_bytes = 0;
     l.smem = fine_state_bytes(l.fa.qmax, fa0.cap, 2);
-    l.grid = grid_for(l.smem);
     return launch_stream_generic(key_dtype, compute_dtype, npl, l);
 }
 

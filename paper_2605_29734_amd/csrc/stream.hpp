@@ -87,7 +87,7 @@ __host__ __device__ inline size_t fine_tile_floats(int qmax) {
 // end-of-pass softmax statistics reuse the first score tile.
 __host__ __device__ inline size_t fine_state_bytes(int qmax, int cap, int ntile) {
     return (size_t)qmax * cap * 8 + (size_t)ntile * fine_tile_floats(qmax) * 4 +
-           (size_t)qmax * (8 + 4 + 4);
+           (size_t)qmax * (8 + 4 + 4 + 4);
 }
 __host__ __device__ inline size_t fine_qs_bytes(int d, int qmax) {
     return (size_t)((d + 31) / 32) * (qmax / 16) * kWave * 16;
@@ -97,14 +97,15 @@ __host__ __device__ inline size_t fine_qs_bytes(int d, int qmax) {
 // translation unit that holds a kernel.
 struct StreamLaunch {
     FineArgs fa;
-    int grid;
+    int n_cu;                     // compute units
+    int64_t max_grid;             // no more blocks than work items
     size_t smem;
     int32_t qs_bytes;
     KernelEvents ev;
     hipStream_t stream;
 };
-hipError_t launch_stream_lds_bf16(int npl, const StreamLaunch &l);
-hipError_t launch_stream_lds_f32(int npl, const StreamLaunch &l);
+hipError_t launch_stream_lds_bf16(int npl, bool two_per_cu, const StreamLaunch &l);
+hipError_t launch_stream_lds_f32(int npl, bool two_per_cu, const StreamLaunch &l);
 hipError_t launch_stream_generic(int key_dtype, int compute_dtype, int npl, const StreamLaunch &l);
 
 namespace {
@@ -117,7 +118,8 @@ struct FineSmem {
     int32_t *ocnt;     //        and buffer count
     float *wm, *wz;    // [waves][qmax] per-wave softmax statistics at the end of a pass,
     float *om, *oz;    // [qmax] and merged (both in the first score tile, then free)
-    int32_t *qrow;     // [qmax]
+    int32_t *qrow;     // [qmax] query row of each of the pass's queries
+    int32_t *qpair;    // [qmax] and its (query, slot) pair index
 };
 
 __device__ __forceinline__ FineSmem fine_carve(unsigned char *raw, size_t qs_bytes, int qmax,
@@ -129,6 +131,7 @@ __device__ __forceinline__ FineSmem fine_carve(unsigned char *raw, size_t qs_byt
     sm.otheta = reinterpret_cast<uint64_t *>(sm.st + (size_t)ntile * fine_tile_floats(qmax));
     sm.ocnt = reinterpret_cast<int32_t *>(sm.otheta + qmax);
     sm.qrow = sm.ocnt + qmax;
+    sm.qpair = sm.qrow + qmax;
     // 2 * 4 * qmax + 2 * qmax floats <= 64 + 68 * qmax: they fit in one tile
     sm.wm = sm.st;
     sm.wz = sm.wm + kFineWaves * qmax;
@@ -194,10 +197,14 @@ __device__ __forceinline__ void stats_update(Stats<NQT> &st, const f32x4_t (&acc
     }
 }
 
-// Per-pass set-up: the rows of the pass's queries.
+// Per-pass set-up: the (query, slot) pairs of the pass and their query rows.
 __device__ __forceinline__ void pass_begin(const FineArgs &a, const FineSmem &sm, int32_t qbeg,
                                            int32_t qg0, int32_t nqg) {
-    for (int n = threadIdx.x; n < nqg; n += kFineThreads) sm.qrow[n] = a.qlist[qbeg + qg0 + n] / a.c;
+    for (int n = threadIdx.x; n < nqg; n += kFineThreads) {
+        const int32_t e = a.qlist[qbeg + qg0 + n];
+        sm.qpair[n] = e;
+        sm.qrow[n] = e / a.c;
+    }
     __syncthreads();
 }
 
@@ -375,7 +382,7 @@ __device__ __forceinline__ void pass_end(const FineArgs &a, const FineSmem &sm, 
         int cn = sm.ocnt[q];
         const float Mq = sm.om[q], Zq = sm.oz[q];
         if (single) {
-            const int64_t e = a.qlist[qbeg + qg0 + q];
+            const int64_t e = sm.qpair[q];
             uint64_t v[NPL];
 #pragma unroll
             for (int j = 0; j < NPL; ++j) v[j] = (j * kWave + lane < cn) ? b[j * kWave + lane] : 0;
@@ -474,14 +481,14 @@ template <typename KT>
 struct AFrag;
 template <>
 struct AFrag<__bf16> {
-    static constexpr int U = 16;   // k-steps per load unit: 16 x 16 B per lane
+    static constexpr int U = 16;   // k-steps per load unit (one-block-per-CU kernels): 16 x 16 B per lane
     uint4 v;
     __device__ __forceinline__ void load(const __bf16 *p) { v = *reinterpret_cast<const uint4 *>(p); }
     __device__ __forceinline__ bf16x8_t bf16() const { return __builtin_bit_cast(bf16x8_t, v); }
 };
 template <>
 struct AFrag<float> {
-    static constexpr int U = 8;    // 8 x 32 B per lane
+    static constexpr int U = 8;    // k-steps per load unit: 8 x 32 B per lane
     float4 lo, hi;
     __device__ __forceinline__ void load(const float *p) {
         lo = reinterpret_cast<const float4 *>(p)[0];
@@ -497,19 +504,18 @@ struct AFrag<float> {
 
 // One load unit: U k-steps of one 16-row tile for this lane, and the caller
 // id of row lane of the unit's step (used by the step's epilogue).
-template <typename KT>
+template <typename KT, int U>
 struct LoadUnit {
-    AFrag<KT> f[AFrag<KT>::U];
+    AFrag<KT> f[U];
     int32_t tid;
 };
 
 // Unconditional loads only (rows clamped into the chunk), so that the compiler
 // can count outstanding loads exactly and wait for one unit at a time.
-template <typename KT>
-__device__ __forceinline__ void lds_load_unit(LoadUnit<KT> &lu, const KT *__restrict__ K,
+template <typename KT, int U>
+__device__ __forceinline__ void lds_load_unit(LoadUnit<KT, U> &lu, const KT *__restrict__ K,
                                               const int32_t *__restrict__ tid_src, int d, int NG,
                                               int u, int64_t r0, int64_t r1) {
-    constexpr int U = AFrag<KT>::U;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, r16 = lane & 15, kg = lane >> 4;
     const int tt = u / NG, gi = u - tt * NG;
     const int64_t base = r0 + (int64_t)tt * kRowsPerStep;
@@ -520,12 +526,11 @@ __device__ __forceinline__ void lds_load_unit(LoadUnit<KT> &lu, const KT *__rest
     lu.tid = step_tid_load(tid_src, base, r1);
 }
 
-template <typename KT, int NQT, int NPL>
+template <typename KT, int U, int NQT, int NPL>
 __device__ __forceinline__ void lds_compute_unit(const FineArgs &a, const FineSmem &sm,
-                                                 const LoadUnit<KT> &lu, int NG, int u, int64_t r0,
+                                                 const LoadUnit<KT, U> &lu, int NG, int u, int64_t r0,
                                                  int64_t r1, int nqg, f32x4_t (&acc)[NQT],
                                                  OwnedLane &o, Stats<NQT> &st) {
-    constexpr int U = AFrag<KT>::U;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int tt = u / NG, gi = u - tt * NG;
     const float keep = gi == 0 ? 0.0f : 1.0f;
@@ -551,11 +556,10 @@ __device__ __forceinline__ void lds_compute_unit(const FineArgs &a, const FineSm
     }
 }
 
-template <typename KT, int NQT, int NPL>
+template <typename KT, int U, int NQT, int NPL>
 __device__ __forceinline__ void pass_lds(const FineArgs &a, const FineSmem &sm, int64_t p0,
                                          bool single, int64_t r0, int64_t r1, int32_t qbeg,
                                          int32_t qg0, int32_t nqg) {
-    constexpr int U = AFrag<KT>::U;
     const int t = threadIdx.x;
     const int d = a.d;
     const KT *__restrict__ K = static_cast<const KT *>(a.keys);
@@ -572,10 +576,10 @@ __device__ __forceinline__ void pass_lds(const FineArgs &a, const FineSmem &sm, 
     // time. The first units are requested before the queries are staged.
     // the largest top-k buffers leave fewer registers for the ring
     constexpr int R = NPL < 8 ? kRing : (sizeof(KT) == 4 ? 2 : 3);
-    LoadUnit<KT> ring[R];
+    LoadUnit<KT, U> ring[R];
 #pragma unroll
     for (int j = 0; j < R - 1; ++j)
-        lds_load_unit<KT>(ring[j], K, a.tid_src, d, NG, min(j, total - 1), r0, r1);
+        lds_load_unit<KT, U>(ring[j], K, a.tid_src, d, NG, min(j, total - 1), r0, r1);
 
     pass_begin(a, sm, qbeg, qg0, nqg);
     // stage the queries as MFMA B fragments: [k-step][query tile][lane], eight
@@ -612,10 +616,10 @@ __device__ __forceinline__ void pass_lds(const FineArgs &a, const FineSmem &sm, 
     for (int u = 0; u < total; u += R) {
 #pragma unroll
         for (int j = 0; j < R; ++j) {
-            lds_load_unit<KT>(ring[(j + R - 1) % R], K, a.tid_src, d, NG,
+            lds_load_unit<KT, U>(ring[(j + R - 1) % R], K, a.tid_src, d, NG,
                               min(u + j + R - 1, total - 1), r0, r1);
             if (u + j < total)
-                lds_compute_unit<KT, NQT, NPL>(a, sm, ring[j], NG, u + j, r0, r1, nqg, acc, o, st);
+                lds_compute_unit<KT, U, NQT, NPL>(a, sm, ring[j], NG, u + j, r0, r1, nqg, acc, o, st);
         }
     }
     pass_end<NQT, NPL>(a, sm, p0, qbeg, single, qg0, nqg, o, st);
@@ -623,22 +627,16 @@ __device__ __forceinline__ void pass_lds(const FineArgs &a, const FineSmem &sm, 
 
 // Work loop shared by both kernels: items (cluster, chunk) from the planned
 // item table, the first one by block index and the rest from a dynamic
-// counter; the queries of an item in passes of at most qmax.
+// counter, whose next value is requested when an item starts and read when it
+// ends; the queries of an item in passes of at most qmax.
 struct ItemPass {
     int64_t p0, r0, r1;
     int32_t qbeg, nq;
     bool single;
 };
 
-__device__ __forceinline__ bool next_item(const FineArgs &a, int32_t *s_item, bool first,
-                                          ItemPass &it) {
-    if (threadIdx.x == 0)
-        *s_item = first ? (int32_t)blockIdx.x : (int32_t)gridDim.x + atomicAdd(&a.plan->next, 1);
-    __syncthreads();
-    const int64_t w = *s_item;
-    __syncthreads();
-    if (w >= a.plan->n_items) return false;
-    const WorkItem wi = a.items[w];
+__device__ __forceinline__ ItemPass item_pass(const WorkItem &wi) {
+    ItemPass it;
     it.p0 = wi.p0;
     it.r0 = wi.r0;
     it.r1 = wi.r0 + wi.len;
@@ -646,35 +644,67 @@ __device__ __forceinline__ bool next_item(const FineArgs &a, int32_t *s_item, bo
     it.nq = wi.nq;
     // passes over one item cover disjoint queries, so a single-chunk item's results are final
     it.single = wi.single != 0;
-    return true;
+    return it;
 }
 
-template <typename KT, int NPL>
-__global__ __launch_bounds__(kFineThreads) void stream_lds(FineArgs a, int32_t qs_bytes) {
-    extern __shared__ __align__(16) unsigned char smem_raw[];
-    __shared__ int32_t s_item;
+// Runs body(item) for every item this block takes. s_next: two LDS words.
+template <typename Body>
+__device__ __forceinline__ void for_each_item(const FineArgs &a, int32_t *s_next, Body &&body) {
+    const int64_t n_items = a.plan->n_items;
+    int64_t w = blockIdx.x;
+    for (int parity = 0; w < n_items; parity ^= 1) {
+        int32_t nxt = 0;
+        if (threadIdx.x == 0) nxt = atomicAdd(&a.plan->next, 1);    // consumed after the item
+        body(item_pass(a.items[w]));
+        if (threadIdx.x == 0) s_next[parity] = (int32_t)gridDim.x + nxt;
+        __syncthreads();
+        w = s_next[parity];
+    }
+}
+
+template <typename KT, int U, int NPL>
+__device__ __forceinline__ void stream_lds_body(const FineArgs &a, int32_t qs_bytes,
+                                                unsigned char *smem_raw, int32_t *s_next) {
     const FineSmem sm = fine_carve(smem_raw, qs_bytes, a.qmax, a.cap, a.ntile);
-    ItemPass it;
-    for (bool first = true; next_item(a, &s_item, first, it); first = false) {
+    for_each_item(a, s_next, [&](const ItemPass &it) {
         for (int32_t qg0 = 0; qg0 < it.nq; qg0 += a.qmax) {
             const int32_t nqg = min(a.qmax, it.nq - qg0);
             switch ((nqg + 15) >> 4) {
-                case 1: pass_lds<KT, 1, NPL>(a, sm, it.p0, it.single, it.r0, it.r1, it.qbeg, qg0, nqg); break;
-                case 2: pass_lds<KT, 2, NPL>(a, sm, it.p0, it.single, it.r0, it.r1, it.qbeg, qg0, nqg); break;
-                case 3: pass_lds<KT, 3, NPL>(a, sm, it.p0, it.single, it.r0, it.r1, it.qbeg, qg0, nqg); break;
-                default: pass_lds<KT, 4, NPL>(a, sm, it.p0, it.single, it.r0, it.r1, it.qbeg, qg0, nqg); break;
+                case 1: pass_lds<KT, U, 1, NPL>(a, sm, it.p0, it.single, it.r0, it.r1, it.qbeg, qg0, nqg); break;
+                case 2: pass_lds<KT, U, 2, NPL>(a, sm, it.p0, it.single, it.r0, it.r1, it.qbeg, qg0, nqg); break;
+                case 3: pass_lds<KT, U, 3, NPL>(a, sm, it.p0, it.single, it.r0, it.r1, it.qbeg, qg0, nqg); break;
+                default: pass_lds<KT, U, 4, NPL>(a, sm, it.p0, it.single, it.r0, it.r1, it.qbeg, qg0, nqg); break;
             }
         }
-    }
+    });
+}
+
+// One block per CU (LDS-bound launches): all registers, long load units.
+template <typename KT, int NPL>
+__global__ __launch_bounds__(kFineThreads) void stream_lds(FineArgs a, int32_t qs_bytes) {
+    extern __shared__ __align__(16) unsigned char smem_raw[];
+    __shared__ int32_t s_next[2];
+    stream_lds_body<KT, AFrag<KT>::U, NPL>(a, qs_bytes, smem_raw, s_next);
+}
+
+// Two blocks per CU when their LDS fits (small query groups): registers
+// capped at two waves per SIMD, so that one block's latency-bound steps
+// (staging, epilogue, pass end) overlap the other's; shorter load units keep
+// the ring within that budget (d must be a multiple of 256).
+template <typename KT, int NPL>
+__global__ __launch_bounds__(kFineThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void stream_lds2(FineArgs a, int32_t qs_bytes) {
+    extern __shared__ __align__(16) unsigned char smem_raw[];
+    __shared__ int32_t s_next[2];
+    stream_lds_body<KT, 8, NPL>(a, qs_bytes, smem_raw, s_next);
 }
 
 template <typename T, bool BF16, int NPL>
 __global__ __launch_bounds__(kFineThreads) void stream_generic(FineArgs a) {
     extern __shared__ __align__(16) unsigned char smem_raw[];
-    __shared__ int32_t s_item;
+    __shared__ int32_t s_next[2];
     const FineSmem sm = fine_carve(smem_raw, 0, a.qmax, a.cap, a.ntile);
-    ItemPass it;
-    for (bool first = true; next_item(a, &s_item, first, it); first = false) {
+    for_each_item(a, s_next, [&](const ItemPass &it) {
         for (int32_t qg0 = 0; qg0 < it.nq; qg0 += a.qmax) {
             const int32_t nqg = min(a.qmax, it.nq - qg0);
             switch ((nqg + 15) >> 4) {
@@ -684,7 +714,7 @@ __global__ __launch_bounds__(kFineThreads) void stream_generic(FineArgs a) {
                 default: pass_generic<T, BF16, 4, NPL>(a, sm, it.p0, it.single, it.r0, it.r1, it.qbeg, qg0, nqg); break;
             }
         }
-    }
+    });
 }
 
 template <typename Kern, typename... Args>
@@ -693,14 +723,29 @@ hipError_t launch_stream_kernel(Kern kern, const StreamLaunch &l, Args... args) 
     hipError_t err = hipFuncSetAttribute((const void *)kern,
                                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)l.smem);
     if (err != hipSuccess) return err;
+    // as many blocks as are resident at once (registers and LDS), no more:
+    // the rest of the work is handed out by the item counter
+    int per_cu = 0;
+    err = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, kFineThreads, l.smem);
+    if (err != hipSuccess) return err;
+    int64_t grid = (int64_t)l.n_cu * (per_cu > 0 ? per_cu : 1);
+    if (grid > l.max_grid) grid = l.max_grid;
+    if (grid < 1) grid = 1;
     if (l.ev.before) hipEventRecord(l.ev.before, l.stream);
-    hipLaunchKernelGGL(kern, dim3(l.grid), dim3(kFineThreads), l.smem, l.stream, args...);
+    hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(kFineThreads), l.smem, l.stream, args...);
     if (l.ev.after) hipEventRecord(l.ev.after, l.stream);
     return hipGetLastError();
 }
 
 template <typename KT>
-hipError_t launch_stream_lds_t(int npl, const StreamLaunch &l) {
+hipError_t launch_stream_lds_t(int npl, bool two_per_cu, const StreamLaunch &l) {
+    if (two_per_cu) {
+        switch (npl) {
+            case 2: return launch_stream_kernel(stream_lds2<KT, 2>, l, l.fa, l.qs_bytes);
+            case 4: return launch_stream_kernel(stream_lds2<KT, 4>, l, l.fa, l.qs_bytes);
+        }
+        return hipErrorInvalidValue;
+    }
     switch (npl) {
         case 2: return launch_stream_kernel(stream_lds<KT, 2>, l, l.fa, l.qs_bytes);
         case 4: return launch_stream_kernel(stream_lds<KT, 4>, l, l.fa, l.qs_bytes);

@@ -3,7 +3,7 @@
 #include "stream.hpp"
 
 namespace htam {
-hipError_t launch_stream_lds_f32(int npl, const StreamLaunch &l) {
-    return launch_stream_lds_t<float>(npl, l);
+hipError_t launch_stream_lds_f32(int npl, bool two_per_cu, const StreamLaunch &l) {
+    return launch_stream_lds_t<float>(npl, two_per_cu, l);
 }
 }  // namespace htam
