@@ -26,7 +26,7 @@ namespace {
 
 constexpr int kPlanThreads = 1024;
 constexpr int64_t kChunkFloor = 64;
-constexpr size_t kRouteLdsBytes = 64 * 1024;   // per-cluster counters of the fused routing kernel
+constexpr size_t kRouteLdsBytes = 128 * 1024;  // per-cluster tables of the fused routing kernel
 constexpr int64_t kFusedRoutePairs = 16384;     // above this many pairs, route with many blocks
 constexpr int64_t kChunkCeil = 4096;
 
@@ -54,58 +54,6 @@ __global__ void route_count(const int32_t *sel, int64_t n, int32_t G, int32_t *c
     }
 }
 
-// Exclusive scan of one int64 value per thread over a 1024-thread block:
-// wave scans through shuffles, then one wave scans the 16 wave totals.
-// `s` holds at least 16 values; every thread must call it.
-__device__ int64_t block_exclusive_scan(int64_t v, int64_t *s, int64_t *total) {
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    constexpr int waves = kPlanThreads / kWave;
-    int64_t x = v;
-#pragma unroll
-    for (int o = 1; o < kWave; o <<= 1) {
-        const int64_t y = __shfl_up(x, o);
-        if (lane >= o) x += y;
-    }
-    if (lane == kWave - 1) s[wave] = x;
-    __syncthreads();
-    if (wave == 0) {
-        int64_t w = lane < waves ? s[lane] : 0;
-#pragma unroll
-        for (int o = 1; o < waves; o <<= 1) {
-            const int64_t y = __shfl_up(w, o);
-            if (lane >= o) w += y;
-        }
-        if (lane < waves) s[lane] = w;
-    }
-    __syncthreads();
-    const int64_t before = wave > 0 ? s[wave - 1] : 0;
-    *total = s[waves - 1];
-    __syncthreads();
-    return before + x - v;
-}
-
-__device__ int64_t block_sum(int64_t v, int64_t *s) {
-    int64_t total;
-    block_exclusive_scan(v, s, &total);
-    return total;
-}
-
-__device__ int64_t block_max(int64_t v, int64_t *s) {
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    constexpr int waves = kPlanThreads / kWave;
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) {
-        const int64_t y = __shfl_xor(v, o);
-        v = v > y ? v : y;
-    }
-    if (lane == 0) s[wave] = v;
-    __syncthreads();
-    int64_t r = s[0];
-    for (int w = 1; w < waves; ++w) r = r > s[w] ? r : s[w];
-    __syncthreads();
-    return r;
-}
-
 // Inputs and outputs of the planning step (device pointers).
 struct PlanArgs {
     int32_t G;
@@ -121,91 +69,164 @@ struct PlanArgs {
     int32_t group;            // chunk partials per level-one merge group
 };
 
+// Exclusive scan and total of N values per thread over the 1024-thread block,
+// in two barriers: each wave scans with shuffles, one lane per value scans the
+// wave totals. s: LDS of at least 16 * N int64. v becomes the exclusive prefix.
+template <int N>
+__device__ void block_scan_n(int64_t (&v)[N], int64_t (&total)[N], int64_t *s) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    constexpr int waves = kPlanThreads / kWave;
+    int64_t x[N];
+#pragma unroll
+    for (int i = 0; i < N; ++i) x[i] = v[i];
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+#pragma unroll
+        for (int i = 0; i < N; ++i) {
+            const int64_t y = __shfl_up(x[i], o);
+            if (lane >= o) x[i] += y;
+        }
+    }
+    if (lane == kWave - 1) {
+#pragma unroll
+        for (int i = 0; i < N; ++i) s[wave * N + i] = x[i];
+    }
+    __syncthreads();
+    if (threadIdx.x < N) {          // one thread per value: prefix over the waves, in place
+        int64_t run = 0;
+        for (int w = 0; w < waves; ++w) {
+            const int64_t c = s[w * N + threadIdx.x];
+            s[w * N + threadIdx.x] = run;
+            run += c;
+        }
+        s[waves * N + threadIdx.x] = run;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+        v[i] = s[wave * N + i] + x[i] - v[i];
+        total[i] = s[waves * N + i];
+    }
+    __syncthreads();
+}
+
+// Sum over the wave of a 64-bit value, in every lane (DPP / permlane).
+__device__ __forceinline__ int64_t wave_sum64(int64_t x) {
+    const int lane = threadIdx.x & 63;
+    x += (int64_t)lane_xor64<1>((uint64_t)x, lane);
+    x += (int64_t)lane_xor64<2>((uint64_t)x, lane);
+    x += (int64_t)lane_xor64<4>((uint64_t)x, lane);
+    x += (int64_t)lane_xor64<8>((uint64_t)x, lane);
+    x += (int64_t)lane_xor64<16>((uint64_t)x, lane);
+    x += (int64_t)lane_xor64<32>((uint64_t)x, lane);
+    return x;
+}
+
+// Block totals of N values per thread (no prefix), in two barriers.
+// s: LDS of at least 17 * N int64.
+template <int N>
+__device__ void block_sum_n(int64_t (&v)[N], int64_t *s) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    constexpr int waves = kPlanThreads / kWave;
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+        const int64_t x = wave_sum64(v[i]);
+        if (lane == 0) s[wave * N + i] = x;
+    }
+    __syncthreads();
+    if (threadIdx.x < N) {
+        int64_t run = 0;
+        for (int w = 0; w < waves; ++w) run += s[w * N + threadIdx.x];
+        s[waves * N + threadIdx.x] = run;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < N; ++i) v[i] = s[waves * N + i];
+    __syncthreads();
+}
+
+// Candidate chunk lengths chunk_min * 2^i, i < kChunkCands: the last is at
+// least 2^31 rows, longer than any segment, so it always fits (each
+// (query, slot) then has one partial and p_cap >= B*c).
+constexpr int kChunkCands = 26;
+
 // Chunk length and work numbering from the per-cluster query counts (read
-// through cnt_of): the chunk is the smallest power-of-two multiple of
-// chunk_min for which the partial results fit in p_cap (it always fits once a
-// chunk spans the longest segment: then each (query, slot) has one partial and
-// p_cap >= B*c). Writes qoff, wstart, gstart, pbase, ubase and the plan; the
-// item and group tables are filled afterwards by route_items. Clusters are
-// split into contiguous ranges, one per thread.
+// through cnt_of): the chunk is the smallest candidate length for which the
+// partial results fit in p_cap. Writes qoff, wstart, gstart, mstart, pbase,
+// ubase and the plan (and the item starts to lds_wstart when given). Clusters
+// are split into contiguous ranges, one per thread.
 template <typename CntOf>
-__device__ void plan_chunks(const PlanArgs &pa, CntOf cnt_of, int64_t *s) {
+__device__ void plan_chunks(const PlanArgs &pa, CntOf cnt_of, int64_t *s, int32_t *lds_wstart) {
     const int t = threadIdx.x;
     const int32_t G = pa.G;
     const int32_t per = (G + kPlanThreads - 1) / kPlanThreads;
     const int32_t g0 = min((int32_t)G, t * per), g1 = min((int32_t)G, g0 + per);
-    int64_t local = 0, lmax = 0;
+    const int lmin = 63 - __builtin_clzll((unsigned long long)pa.chunk_min);   // chunk_min is a power of two
+    int64_t q[1] = {0}, qtot[1];
+    int64_t p[kChunkCands];
+#pragma unroll
+    for (int i = 0; i < kChunkCands; ++i) p[i] = 0;
     for (int32_t g = g0; g < g1; ++g) {
-        local += cnt_of(g);
-        const int64_t len = pa.off[g + 1] - pa.off[g];
-        lmax = len > lmax ? len : lmax;
-    }
-    int64_t total;
-    int64_t run = block_exclusive_scan(local, s, &total);
-    for (int32_t g = g0; g < g1; ++g) {
-        pa.qoff[g] = (int32_t)run;
-        run += cnt_of(g);
-    }
-    if (t == kPlanThreads - 1) pa.qoff[G] = (int32_t)total;
-    const int64_t maxlen = block_max(lmax, s);
-
-    int64_t ch = pa.chunk_min;
-    for (int it = 0; it < 48; ++it) {
-        int64_t p = 0;
-        for (int32_t g = g0; g < g1; ++g) {
-            const int64_t len = pa.off[g + 1] - pa.off[g];
-            const int64_t c = cnt_of(g);
-            if (c > 0 && len > 0) p += c * ((len + ch - 1) / ch);
+        const int64_t c = cnt_of(g), len = pa.off[g + 1] - pa.off[g];
+        q[0] += c;
+        if (c > 0 && len > 0) {
+#pragma unroll
+            for (int i = 0; i < kChunkCands; ++i)
+                p[i] += c * ((len + (int64_t(1) << (lmin + i)) - 1) >> (lmin + i));
         }
-        const int64_t P = block_sum(p, s);
-        if (P <= pa.p_cap || ch >= maxlen) break;
-        ch *= 2;
     }
+    block_scan_n<1>(q, qtot, s);
+    block_sum_n<kChunkCands>(p, s);
+    int cand = kChunkCands - 1;
+    for (int i = kChunkCands - 1; i >= 0; --i)
+        if (p[i] <= pa.p_cap) cand = i;
+    const int lch = lmin + cand;
+    const int64_t ch = int64_t(1) << lch;
 
     const int64_t R = pa.group;
-    auto chunks = [&](int32_t g) -> int64_t {
-        const int64_t len = pa.off[g + 1] - pa.off[g];
-        return (cnt_of(g) > 0 && len > 0) ? (len + ch - 1) / ch : 0;
-    };
-    auto ngroups = [&](int64_t nch) -> int64_t { return nch > R ? (nch + R - 1) / R : 0; };
-    int64_t wl = 0, pl = 0, gl = 0, ul = 0, ml = 0;
+    int64_t w[5] = {0, 0, 0, 0, 0}, wt[5];           // items, partials, groups, level-one, merge list
     for (int32_t g = g0; g < g1; ++g) {
-        const int64_t nch = chunks(g), c = cnt_of(g);
-        wl += nch;
-        pl += nch * c;
-        gl += ngroups(nch);
-        ul += ngroups(nch) * c;
-        ml += nch != 1 ? c : 0;     // empty segments are finished by the merge too
+        const int64_t c = cnt_of(g), len = pa.off[g + 1] - pa.off[g];
+        const int64_t nch = (c > 0 && len > 0) ? (len + ch - 1) >> lch : 0;
+        const int64_t ng = nch > R ? (nch + R - 1) / R : 0;
+        w[0] += nch;
+        w[1] += nch * c;
+        w[2] += ng;
+        w[3] += ng * c;
+        w[4] += nch != 1 ? c : 0;        // empty segments are finished by the merge too
     }
-    int64_t wtot, ptot, gtot, utot, mtot;
-    int64_t wrun = block_exclusive_scan(wl, s, &wtot);
-    int64_t prun = block_exclusive_scan(pl, s, &ptot);
-    int64_t grun = block_exclusive_scan(gl, s, &gtot);
-    int64_t urun = block_exclusive_scan(ul, s, &utot);
-    int64_t mrun = block_exclusive_scan(ml, s, &mtot);
+    block_scan_n<5>(w, wt, s);
+    int64_t qrun = q[0];
     for (int32_t g = g0; g < g1; ++g) {
-        const int64_t nch = chunks(g), c = cnt_of(g), ng = ngroups(nch);
-        pa.wstart[g] = (int32_t)wrun;
-        pa.gstart[g] = (int32_t)grun;
-        pa.mstart[g] = (int32_t)mrun;
-        pa.pbase[g] = prun;
-        pa.ubase[g] = urun;
-        wrun += nch;
-        prun += nch * c;
-        grun += ng;
-        urun += ng * c;
-        mrun += nch != 1 ? c : 0;
+        const int64_t c = cnt_of(g), len = pa.off[g + 1] - pa.off[g];
+        const int64_t nch = (c > 0 && len > 0) ? (len + ch - 1) >> lch : 0;
+        const int64_t ng = nch > R ? (nch + R - 1) / R : 0;
+        pa.qoff[g] = (int32_t)qrun;
+        pa.wstart[g] = (int32_t)w[0];
+        if (lds_wstart) lds_wstart[g] = (int32_t)w[0];
+        pa.pbase[g] = w[1];
+        pa.gstart[g] = (int32_t)w[2];
+        pa.ubase[g] = w[3];
+        pa.mstart[g] = (int32_t)w[4];
+        qrun += c;
+        w[0] += nch;
+        w[1] += nch * c;
+        w[2] += ng;
+        w[3] += ng * c;
+        w[4] += nch != 1 ? c : 0;
     }
     if (t == kPlanThreads - 1) {
-        pa.wstart[G] = (int32_t)wtot;
-        pa.gstart[G] = (int32_t)gtot;
-        pa.mstart[G] = (int32_t)mtot;
-        pa.plan->n_merge = mtot;
+        pa.qoff[G] = (int32_t)qtot[0];
+        pa.wstart[G] = (int32_t)wt[0];
+        if (lds_wstart) lds_wstart[G] = (int32_t)wt[0];
+        pa.gstart[G] = (int32_t)wt[2];
+        pa.mstart[G] = (int32_t)wt[4];
         pa.plan->chunk = ch;
-        pa.plan->n_items = wtot;
-        pa.plan->n_parts = ptot;
-        pa.plan->n_groups = gtot;
-        pa.plan->n_l1 = utot;
+        pa.plan->n_items = wt[0];
+        pa.plan->n_parts = wt[1];
+        pa.plan->n_groups = wt[2];
+        pa.plan->n_l1 = wt[3];
+        pa.plan->n_merge = wt[4];
     }
 }
 
@@ -236,21 +257,26 @@ struct SlotOut {
 
 // Planning step of the multi-kernel routing (counts in global memory).
 __global__ __launch_bounds__(kPlanThreads) void route_plan(PlanArgs pa, const int32_t *cnt) {
-    __shared__ int64_t s[kPlanThreads / kWave];
-    plan_chunks(pa, GlobalCnt{cnt}, s);
+    __shared__ int64_t s[(kPlanThreads / kWave + 1) * kChunkCands];
+    plan_chunks(pa, GlobalCnt{cnt}, s, nullptr);
 }
 
 // The whole routing in one block when the pairs are few and the per-cluster
-// counters fit in LDS: count the (query, slot) pairs per cluster, plan the
-// chunks, then scatter the pairs into per-cluster lists.
+// tables fit in LDS: count the (query, slot) pairs per cluster, plan the
+// chunks, scatter the pairs into per-cluster lists, then fill the work items
+// (each thread finds its items' clusters by binary search over the item starts
+// in LDS), the level-one merge groups and units, and the merge list.
 __global__ __launch_bounds__(kPlanThreads) void route_fused(PlanArgs pa, const int32_t *sel,
                                                             int64_t n, int32_t *qlist,
-                                                            int32_t *pos, SlotOut out) {
-    extern __shared__ int32_t lcnt[];       // [G]
-    __shared__ int64_t s[kPlanThreads / kWave];
+                                                            int32_t *pos, SlotOut out,
+                                                            WorkItem *items, MergeGroup *groups,
+                                                            int2 *units, int32_t *mlist) {
+    extern __shared__ int32_t lds[];        // [G] counts, then fill cursors; [G+1] item starts
+    __shared__ int64_t s[(kPlanThreads / kWave + 1) * kChunkCands];
     __shared__ int32_t s_bad;
     const int t = threadIdx.x;
     const int32_t G = pa.G;
+    int32_t *lcnt = lds, *lwst = lds + G;
     for (int32_t g = t; g < G; g += kPlanThreads) lcnt[g] = 0;
     if (t == 0) s_bad = 0;
     __syncthreads();
@@ -262,7 +288,7 @@ __global__ __launch_bounds__(kPlanThreads) void route_fused(PlanArgs pa, const i
     }
     if (bad) atomicAdd(&s_bad, bad);
     __syncthreads();
-    plan_chunks(pa, LdsCnt{lcnt}, s);
+    plan_chunks(pa, LdsCnt{lcnt}, s, lwst);
     __syncthreads();
     for (int32_t g = t; g < G; g += kPlanThreads) lcnt[g] = pa.qoff[g];   // becomes the fill cursor
     if (t == 0) {
@@ -270,14 +296,61 @@ __global__ __launch_bounds__(kPlanThreads) void route_fused(PlanArgs pa, const i
         pa.plan->bad_sel = s_bad;
     }
     __syncthreads();
+    const int64_t R = pa.group;
     for (int64_t e = t; e < n; e += kPlanThreads) {
         const int32_t g = sel[e];
         if (g >= 0 && g < G) {
+            const int32_t qb = pa.qoff[g];
             const int32_t at = atomicAdd(&lcnt[g], 1);
+            const int32_t i = at - qb;
             qlist[at] = (int32_t)e;
-            pos[e] = at - pa.qoff[g];
+            pos[e] = i;
+            const int32_t nch = lwst[g + 1] - lwst[g];
+            if (nch != 1) mlist[pa.mstart[g] + i] = (int32_t)e;
+            if (nch > R) {                 // this pair's level-one units, one per group
+                const int32_t nq = pa.qoff[g + 1] - qb, gs = pa.gstart[g];
+                const int32_t ng = pa.gstart[g + 1] - gs;
+                for (int32_t jg = 0; jg < ng; ++jg)
+                    units[pa.ubase[g] + (int64_t)jg * nq + i] = make_int2(gs + jg, i);
+            }
         } else {
             out.empty(e);
+        }
+    }
+    const int64_t ch = pa.plan->chunk;
+    const int32_t n_items = lwst[G];
+    for (int32_t w = t; w < n_items; w += kPlanThreads) {
+        int32_t lo = 0, hi = G;                // lwst[lo] <= w < lwst[hi]
+        while (hi - lo > 1) {
+            const int32_t mid = (lo + hi) >> 1;
+            if (lwst[mid] <= w) lo = mid; else hi = mid;
+        }
+        const int32_t g = lo, j = w - lwst[g];
+        const int64_t a0 = pa.off[g], len = pa.off[g + 1] - a0;
+        const int32_t qb = pa.qoff[g], nq = pa.qoff[g + 1] - qb;
+        WorkItem wi;
+        wi.r0 = a0 + j * ch;
+        wi.p0 = pa.pbase[g] + (int64_t)j * nq;
+        wi.len = (int32_t)(len - j * ch < ch ? len - j * ch : ch);
+        wi.g = g;
+        wi.qbeg = qb;
+        wi.nq = nq;
+        wi.single = lwst[g + 1] - lwst[g] == 1;
+        wi.pad = 0;
+        items[w] = wi;
+    }
+    for (int32_t g = t; g < G; g += kPlanThreads) {
+        const int32_t gs = pa.gstart[g], ng = pa.gstart[g + 1] - gs;
+        if (ng == 0) continue;
+        const int32_t nq = pa.qoff[g + 1] - pa.qoff[g], nch = lwst[g + 1] - lwst[g];
+        const int64_t pb = pa.pbase[g], ub = pa.ubase[g];
+        for (int32_t jg = 0; jg < ng; ++jg) {
+            MergeGroup mg;
+            mg.p0 = pb + jg * R * nq;
+            mg.u0 = ub + (int64_t)jg * nq;
+            mg.npart = (int32_t)(nch - jg * R < R ? nch - jg * R : R);
+            mg.nq = nq;
+            groups[gs + jg] = mg;
         }
     }
 }
@@ -560,10 +633,10 @@ static size_t lds_budget() {
     return (size_t)bytes;
 }
 
-// Chunk partials per level-one merge group: about 2048 keys per wave.
+// Chunk partials per level-one merge group: about 4096 keys per wave.
 static int merge_group(int k) {
     int r = 8;
-    while (r * 2 * k <= 2048 && r < 128) r *= 2;
+    while (r * 2 * k <= 4096 && r < 256) r *= 2;
     return r;
 }
 
@@ -693,9 +766,13 @@ hipError_t launch_attend(int32_t key_dtype, int32_t compute_dtype, int32_t d, in
     pa.p_cap = w.p_cap;
     pa.group = w.group;
     const SlotOut so{slot_max, slot_sum, cand_score, cand_id, k};
-    if (bc <= kFusedRoutePairs && (size_t)G * 4 <= kRouteLdsBytes) {
-        hipLaunchKernelGGL(route_fused, dim3(1), dim3(kPlanThreads), (size_t)G * 4, s, pa, sel, bc,
-                           w.qlist, w.pos, so);
+    const size_t route_lds = (size_t)(2 * G + 1) * 4;
+    if (bc <= kFusedRoutePairs && route_lds <= kRouteLdsBytes) {
+        hipError_t e0 = hipFuncSetAttribute((const void *)route_fused,
+                                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)route_lds);
+        if (e0 != hipSuccess) return e0;
+        hipLaunchKernelGGL(route_fused, dim3(1), dim3(kPlanThreads), route_lds, s, pa, sel, bc,
+                           w.qlist, w.pos, so, w.items, w.groups, w.units, w.mlist);
     } else {
         hipLaunchKernelGGL(route_init, dim3((G + 255) / 256 < 1024 ? (G + 255) / 256 : 1024),
                            dim3(256), 0, s, G, w.cnt, w.cursor, w.plan);
@@ -703,9 +780,9 @@ hipError_t launch_attend(int32_t key_dtype, int32_t compute_dtype, int32_t d, in
         hipLaunchKernelGGL(route_plan, dim3(1), dim3(kPlanThreads), 0, s, pa, w.cnt);
         hipLaunchKernelGGL(route_scatter, dim3(gblocks), dim3(256), 0, s, sel, bc, G, w.qoff,
                            w.cursor, w.qlist, w.pos, so);
+        hipLaunchKernelGGL(route_items, dim3((G + 3) / 4 < 2048 ? (G + 3) / 4 : 2048), dim3(256), 0,
+                           s, pa, w.qlist, w.items, w.groups, w.units, w.mlist);
     }
-    hipLaunchKernelGGL(route_items, dim3((G + 3) / 4 < 2048 ? (G + 3) / 4 : 2048), dim3(256), 0, s,
-                       pa, w.qlist, w.items, w.groups, w.units, w.mlist);
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
 
