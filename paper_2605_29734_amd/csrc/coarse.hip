@@ -5,13 +5,13 @@
 //
 // bf16 arithmetic: an LDS-tiled MFMA GEMM (v_mfma_f32_16x16x32_bf16).
 //   block tile 256 queries x 256 clusters, 8 waves (2 x 4), each wave
-//   128 x 64 = 8 x 4 MFMA tiles; K staged 64 at a time through two LDS
-//   buffers (rows padded to 144 bytes so that fragment reads are free of bank
-//   conflicts); global loads for the next stage are in flight during the
-//   current stage's MFMAs; tiles ordered so that the blocks of one XCD share
+//   128 x 64 = 8 x 4 MFMA tiles; K in stages of 32 loaded straight from global
+//   memory into LDS (global_load_lds_dwordx4, no register staging), four
+//   stages in flight, rows swizzled so that fragment reads are free of bank
+//   conflicts (d % 32 == 0); tiles ordered so that the blocks of one XCD share
 //   query rows in their L2. fp32 inputs are rounded to bf16 once per call.
-// Too few 256 x 256 tiles to fill the GPU: 64 x 64 tiles read directly from
-//   global memory in MFMA fragment layout.
+// Too few 256 x 256 tiles to fill the GPU, or d not a multiple of 32: 64 x 64
+//   tiles read directly from global memory in MFMA fragment layout.
 // fp32 arithmetic (small configurations): a direct MFMA kernel on
 //   v_mfma_f32_16x16x4f32.
 // The scores go to a [B][G] fp32 workspace; the top-c selection is the
@@ -23,13 +23,12 @@ namespace htam {
 
 namespace {
 
-constexpr int BM = 256, BN = 256, BK = 64;
+constexpr int BM = 256, BN = 256, BK = 32;
 constexpr int kGemmThreads = 512;
-constexpr int kLdsRow = BK + 8;                  // bf16 elements per padded LDS row
-constexpr int kStageElems = (BM + BN) * kLdsRow;
-constexpr int kChunksPerStage = (BM + BN) * BK / 8;       // 16-byte chunks
-constexpr int kChunksPerThread = kChunksPerStage / kGemmThreads;
-constexpr size_t kGemmLds = (size_t)2 * kStageElems * 2;  // bytes, two stages
+constexpr int kStages = 4;                                // LDS stages in flight
+constexpr int kStageBytes = (BM + BN) * BK * 2;           // 32 KiB: 512 rows x 64 bytes
+constexpr size_t kGemmLds = (size_t)kStages * kStageBytes;
+constexpr int kLoadsPerWave = (BM + BN) * BK / 8 / kWave / (kGemmThreads / kWave);   // 4
 
 // fp32 -> bf16 (round to nearest even), 8 elements per thread.
 __global__ void to_bf16(const float *__restrict__ x, __bf16 *__restrict__ y, int64_t n8) {
@@ -52,26 +51,47 @@ __device__ __forceinline__ void gemm_tile(int b, int nb, int tm, int tn, int &mt
     nt = in / gm;
 }
 
-__device__ __forceinline__ void gemm_load_stage(uint4 (&stage)[kChunksPerThread],
-                                                const __bf16 *const (&src)[kChunksPerThread],
-                                                const int (&col)[kChunksPerThread], int k0, int d) {
-#pragma unroll
-    for (int i = 0; i < kChunksPerThread; ++i)
-        stage[i] = (k0 + col[i] < d) ? *reinterpret_cast<const uint4 *>(src[i] + k0)
-                                     : make_uint4(0, 0, 0, 0);
+// Stage layout in LDS: the stacked [Q tile; C tile] rows (512 of them), 64
+// bytes each = four 16-byte chunks, chunk c of row r stored in slot
+// c ^ ((r >> 2) & 3). A fragment read (16 rows, one chunk each) then touches
+// 16 distinct (row % 4, slot) pairs: all 64 banks once.
+__device__ __forceinline__ int gemm_slot(int row, int c) { return c ^ ((row >> 2) & 3); }
+
+// s_waitcnt with only a vector-memory count (the other counters left free).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
 
-__device__ __forceinline__ void gemm_store_stage(const uint4 (&stage)[kChunksPerThread],
-                                                 const int (&dst)[kChunksPerThread], __bf16 *base) {
+// Requests one stage straight into LDS (global_load_lds_dwordx4: lane i of an
+// instruction writes bytes 16 i .. 16 i + 15 after the instruction's base).
+// Instruction i of wave w covers rows 16 (4 w + i) .. + 15; its lane l loads
+// row + l / 4, slot l % 4, i.e. the chunk gemm_slot(row, l % 4) of global
+// memory. Rows are clamped into the matrices; d % BK == 0.
+__device__ __forceinline__ void gemm_issue_stage(const __bf16 *__restrict__ q,
+                                                 const __bf16 *__restrict__ ck, int64_t m0,
+                                                 int64_t n0, int32_t B, int32_t G, int32_t d,
+                                                 int k0, unsigned char *stage_base) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 #pragma unroll
-    for (int i = 0; i < kChunksPerThread; ++i) *reinterpret_cast<uint4 *>(base + dst[i]) = stage[i];
+    for (int i = 0; i < kLoadsPerWave; ++i) {
+        const int r0 = 16 * (kLoadsPerWave * wave + i);
+        const int row = r0 + (lane >> 2);
+        const int c = gemm_slot(row, lane & 3);
+        const __bf16 *p = row < BM ? q + min(m0 + row, (int64_t)B - 1) * d
+                                   : ck + min(n0 + row - BM, (int64_t)G - 1) * d;
+        __builtin_amdgcn_global_load_lds((const void *)(p + k0 + 8 * c),
+                                         (__attribute__((address_space(3))) void *)(stage_base + r0 * 64),
+                                         16, 0, 0);
+    }
 }
 
 __global__ __launch_bounds__(kGemmThreads) void coarse_gemm(const __bf16 *__restrict__ q,
                                                             const __bf16 *__restrict__ ck,
                                                             int32_t B, int32_t G, int32_t d,
                                                             float *__restrict__ S) {
-    extern __shared__ __align__(16) __bf16 lds[];
+    extern __shared__ __align__(16) unsigned char lds[];
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
     const int r16 = lane & 15, kg = lane >> 4;
     const int wm = wave >> 2, wn = wave & 3;
@@ -80,57 +100,42 @@ __global__ __launch_bounds__(kGemmThreads) void coarse_gemm(const __bf16 *__rest
     if (tm * tn % 8 == 0) gemm_tile(blockIdx.x, tm * tn, tm, tn, mt, nt);
     else { mt = blockIdx.x / tn; nt = blockIdx.x % tn; }
     const int64_t m0 = (int64_t)mt * BM, n0 = (int64_t)nt * BN;
+    const int nk = d / BK;
 
-    // this thread's chunks of a stage: rows 0..255 of Q's tile, then of C's tile
-    const __bf16 *src[kChunksPerThread];
-    int dst[kChunksPerThread], col[kChunksPerThread];
-#pragma unroll
-    for (int i = 0; i < kChunksPerThread; ++i) {
-        const int c = t + i * kGemmThreads;
-        const int row = c / (BK / 8), cc = c % (BK / 8);
-        col[i] = cc * 8;
-        dst[i] = row * kLdsRow + cc * 8;
-        if (row < BM) {
-            const int64_t r = min(m0 + row, (int64_t)B - 1);
-            src[i] = q + r * d + cc * 8;
-        } else {
-            const int64_t r = min(n0 + row - BM, (int64_t)G - 1);
-            src[i] = ck + r * d + cc * 8;
-        }
-    }
-    uint4 stage[kChunksPerThread];
-    const int nk = (d + BK - 1) / BK;
     f32x4_t acc[8][4];
 #pragma unroll
     for (int i = 0; i < 8; ++i)
 #pragma unroll
         for (int j = 0; j < 4; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-    gemm_load_stage(stage, src, col, 0, d);
-    gemm_store_stage(stage, dst, lds);
-    __syncthreads();
+    // kStages - 1 stages in flight ahead of the one being multiplied; past the
+    // end the last stage is requested again into a buffer nobody reads, so that
+    // every wave issues the same loads and the counts below stay exact.
+#pragma unroll
+    for (int s0 = 0; s0 < kStages - 1; ++s0)
+        gemm_issue_stage(q, ck, m0, n0, B, G, d, min(s0, nk - 1) * BK, lds + s0 * kStageBytes);
     for (int ks = 0; ks < nk; ++ks) {
-        const int cur = ks & 1;
-        if (ks + 1 < nk) gemm_load_stage(stage, src, col, (ks + 1) * BK, d);
-        const __bf16 *As = lds + cur * kStageElems + (wm * 128 + r16) * kLdsRow + kg * 8;
-        const __bf16 *Bs = lds + cur * kStageElems + (BM + wn * 64 + r16) * kLdsRow + kg * 8;
+        wait_vmcnt<(kStages - 2) * kLoadsPerWave>();    // this wave's part of stage ks has landed
+        __builtin_amdgcn_s_barrier();                     // everyone's has; stage ks-1 is read
+        gemm_issue_stage(q, ck, m0, n0, B, G, d, min(ks + kStages - 1, nk - 1) * BK,
+                         lds + ((ks + kStages - 1) % kStages) * kStageBytes);
+        const unsigned char *st = lds + (ks % kStages) * kStageBytes;
+        bf16x8_t a[8], b[4];
 #pragma unroll
-        for (int kk = 0; kk < BK; kk += 32) {
-            bf16x8_t a[8], b[4];
+        for (int i = 0; i < 8; ++i) {
+            const int row = wm * 128 + i * 16 + r16;
+            a[i] = *reinterpret_cast<const bf16x8_t *>(st + row * 64 + 16 * gemm_slot(row, kg));
+        }
 #pragma unroll
-            for (int i = 0; i < 8; ++i)
-                a[i] = *reinterpret_cast<const bf16x8_t *>(As + i * 16 * kLdsRow + kk);
+        for (int j = 0; j < 4; ++j) {
+            const int row = BM + wn * 64 + j * 16 + r16;
+            b[j] = *reinterpret_cast<const bf16x8_t *>(st + row * 64 + 16 * gemm_slot(row, kg));
+        }
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
 #pragma unroll
             for (int j = 0; j < 4; ++j)
-                b[j] = *reinterpret_cast<const bf16x8_t *>(Bs + j * 16 * kLdsRow + kk);
-#pragma unroll
-            for (int i = 0; i < 8; ++i)
-#pragma unroll
-                for (int j = 0; j < 4; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
-        }
-        if (ks + 1 < nk) gemm_store_stage(stage, dst, lds + (cur ^ 1) * kStageElems);
-        __syncthreads();
+                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
     }
 
     // D[m][n]: this lane holds rows 4*kg + e of each 16x16 tile, column r16.
@@ -144,6 +149,7 @@ __global__ __launch_bounds__(kGemmThreads) void coarse_gemm(const __bf16 *__rest
                 const int64_t c = n0 + wn * 64 + j * 16 + r16;
                 if (r < B && c < G) S[r * G + c] = acc[i][j][e];
             }
+    wait_vmcnt<0>();      // no load may still be writing LDS when the block ends
 }
 
 // Small problems (fewer 256 x 256 tiles than compute units): 64 x 64 block
@@ -264,7 +270,7 @@ hipError_t launch_coarse(int32_t key_dtype, int32_t compute_dtype, int32_t d, in
                            static_cast<const float *>(q), static_cast<const float *>(coarse_keys),
                            B, G, d, w.scores);
         if (ev.after) hipEventRecord(ev.after, s);
-    } else if ((int64_t)((B + BM - 1) / BM) * ((G + BN - 1) / BN) < n_cu) {
+    } else if ((int64_t)((B + BM - 1) / BM) * ((G + BN - 1) / BN) < n_cu || d % BK != 0) {
         const dim3 grid((G + 63) / 64, (B + 63) / 64);
         if (ev.before) hipEventRecord(ev.before, s);
         if (key_dtype == kF32)
