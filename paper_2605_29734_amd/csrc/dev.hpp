@@ -223,14 +223,17 @@ __device__ __forceinline__ uint64_t wave_element(const uint64_t (&v)[NPL], int i
 }
 
 // Compaction of a top-k buffer of n keys (n > k, capacity 64*NPL) by one wave.
-// A radix select over the keys' high halves (the ordered scores) finds T, the
-// k-th largest score in the buffer; every key scoring >= T is kept (so all
-// exact ties at T stay) and the threshold becomes T: later keys must score
-// above it, or tie it with a valid id. The select starts below the highest
-// bit in which the buffer's scores differ (the bits above are the same in all
-// of them and so in T). If the ties at T leave fewer than `room` free slots,
-// the buffer is sorted instead and cut to exactly k keys (threshold = the
-// k-th key). Returns the new count.
+// A radix select over the keys' high halves (the ordered scores) looks for T,
+// the k-th largest score in the buffer, one bit at a time from the highest bit
+// in which the buffer's scores differ (the bits above are the same in all of
+// them and so in T). Every prefix found on the way is at most T, so keeping
+// all keys scoring >= the current prefix keeps the true top k; the select
+// stops as soon as that keeps few enough keys to leave `room` free slots
+// (most buffers need only the first several bits), and the threshold becomes
+// the prefix: later keys must score at least that much. If even the full T
+// leaves fewer than `room` free slots (ties at T), the buffer is sorted
+// instead and cut to exactly k keys (threshold = the k-th key). Returns the
+// new count.
 template <int NPL>
 __device__ __forceinline__ int compact_select(uint64_t *buf, int n, int k, int room, int lane,
                                               uint64_t &theta) {
@@ -263,17 +266,18 @@ __device__ __forceinline__ int compact_select(uint64_t *buf, int n, int k, int r
     const uint32_t diff = hand ^ hor;
     const int top = diff ? 31 - __builtin_clz(diff) : -1;
     uint32_t T = top < 0 ? hand : (top == 31 ? 0u : hand & ~((2u << top) - 1u));
-    for (int bit = top; bit >= 0; --bit) {
+    int keep = n;                 // keys scoring >= T (all of them at the common prefix)
+    for (int bit = top; bit >= 0 && keep > cap - room; --bit) {
         const uint32_t cand = T | (1u << bit);
         int c = 0;
 #pragma unroll
-        for (int q = 0; q < NPL; ++q) c += __popcll(__ballot(hi[q] >= cand));
-        if (c >= k) T = cand;
+        for (int q = 0; q < NPL; ++q) c += __popcll(__ballot(hi[q] >= cand && v[q] != 0));
+        if (c >= k) {
+            T = cand;
+            keep = c;
+        }
     }
     const uint64_t lt_mask = (1ull << lane) - 1;
-    int keep = 0;
-#pragma unroll
-    for (int q = 0; q < NPL; ++q) keep += __popcll(__ballot(hi[q] >= T && v[q] != 0));
     wave_lds_sync();
     if (keep <= cap - room) {
         int base = 0;
