@@ -59,7 +59,8 @@ struct PlanArgs {
     int32_t G;
     const int64_t *off;
     int32_t *qoff;            // [G+1]
-    int32_t *wstart;          // [G+1] first work item of each cluster
+    int32_t *wstart;          // [G+1] first full-length chunk item of each cluster
+    int32_t *wlast;           // [G]   item of the cluster's shorter last chunk (-1: none)
     int32_t *gstart;          // [G+1] first level-one merge group of each cluster
     int32_t *mstart;          // [G+1] first merge-list entry of each cluster
     int64_t *pbase;           // [G]
@@ -150,13 +151,29 @@ __device__ void block_sum_n(int64_t (&v)[N], int64_t *s) {
 // (query, slot) then has one partial and p_cap >= B*c).
 constexpr int kChunkCands = 26;
 
+// Buckets of the clusters' shorter last chunks by length (item order).
+constexpr int kLenBuckets = 8;
+__device__ __forceinline__ int len_bucket(int64_t len, int lch) {   // 0 < len < 2^lch
+    const int b = lch - 1 - (63 - __builtin_clzll((unsigned long long)len));
+    return b < kLenBuckets - 1 ? b : kLenBuckets - 1;
+}
+
+// LDS copies of the per-cluster tables the planning step writes (fused routing).
+struct PlanMirror {
+    int32_t *qoff, *wstart, *gstart, *mstart;   // [G+1]
+    int32_t *wlast;                             // [G]
+    int64_t *pbase, *ubase;                     // [G]
+};
+
 // Chunk length and work numbering from the per-cluster query counts (read
-// through cnt_of): the chunk is the smallest candidate length for which the
-// partial results fit in p_cap. Writes qoff, wstart, gstart, mstart, pbase,
-// ubase and the plan (and the item starts to lds_wstart when given). Clusters
-// are split into contiguous ranges, one per thread.
-template <typename CntOf>
-__device__ void plan_chunks(const PlanArgs &pa, CntOf cnt_of, int64_t *s, int32_t *lds_wstart) {
+// through cnt_of) and the segment offsets `off` (global or LDS): the chunk is
+// the smallest candidate length for which the partial results fit in p_cap.
+// Writes qoff, wstart, wlast, gstart, mstart, pbase, ubase and the plan, and
+// the same tables to the LDS mirror m when kMirror. Clusters are split into contiguous
+// ranges, one per thread. Returns the chunk length (in every thread).
+template <bool kMirror, typename CntOf>
+__device__ int64_t plan_chunks(const PlanArgs &pa, CntOf cnt_of, const int64_t *off, int64_t *s,
+                               PlanMirror m) {
     const int t = threadIdx.x;
     const int32_t G = pa.G;
     const int32_t per = (G + kPlanThreads - 1) / kPlanThreads;
@@ -167,7 +184,7 @@ __device__ void plan_chunks(const PlanArgs &pa, CntOf cnt_of, int64_t *s, int32_
 #pragma unroll
     for (int i = 0; i < kChunkCands; ++i) p[i] = 0;
     for (int32_t g = g0; g < g1; ++g) {
-        const int64_t c = cnt_of(g), len = pa.off[g + 1] - pa.off[g];
+        const int64_t c = cnt_of(g), len = off[g + 1] - off[g];
         q[0] += c;
         if (c > 0 && len > 0) {
 #pragma unroll
@@ -183,51 +200,100 @@ __device__ void plan_chunks(const PlanArgs &pa, CntOf cnt_of, int64_t *s, int32_
     const int lch = lmin + cand;
     const int64_t ch = int64_t(1) << lch;
 
+    // Items: first every full-length chunk, cluster by cluster; then each
+    // cluster's shorter last chunk, in buckets by length (longest first), so
+    // that the dynamic work counter hands out the longest items first and the
+    // short ones fill the end. Bucket b holds lengths in [ch >> (b+1), ch >> b)
+    // (the last one everything shorter). Counts that fit 32 bits are scanned
+    // two per 64-bit value: (full items, level-one groups), bucket pairs.
     const int64_t R = pa.group;
-    int64_t w[5] = {0, 0, 0, 0, 0}, wt[5];           // items, partials, groups, level-one, merge list
+    constexpr int NW = 4 + kLenBuckets / 2;
+    int64_t w[NW], wt[NW];   // items | groups << 32, partials, level-one, merge list, buckets
+#pragma unroll
+    for (int i = 0; i < NW; ++i) w[i] = 0;
     for (int32_t g = g0; g < g1; ++g) {
-        const int64_t c = cnt_of(g), len = pa.off[g + 1] - pa.off[g];
+        const int64_t c = cnt_of(g), len = off[g + 1] - off[g];
         const int64_t nch = (c > 0 && len > 0) ? (len + ch - 1) >> lch : 0;
+        const int64_t nfull = c > 0 ? len >> lch : 0;
         const int64_t ng = nch > R ? (nch + R - 1) / R : 0;
-        w[0] += nch;
+        w[0] += nfull + (ng << 32);
         w[1] += nch * c;
-        w[2] += ng;
-        w[3] += ng * c;
-        w[4] += nch != 1 ? c : 0;        // empty segments are finished by the merge too
+        w[2] += ng * c;
+        w[3] += nch != 1 ? c : 0;        // empty segments are finished by the merge too
+        if (nch > nfull) {
+            const int b = len_bucket(len - (nfull << lch), lch);
+#pragma unroll
+            for (int i = 0; i < kLenBuckets / 2; ++i)
+                if ((b >> 1) == i) w[4 + i] += int64_t(1) << (32 * (b & 1));
+        }
     }
-    block_scan_n<5>(w, wt, s);
+    block_scan_n<NW>(w, wt, s);
+    const int64_t n_full = wt[0] & 0xffffffff;
+    // next item of each bucket of last chunks, for this thread's clusters
+    int32_t bnext[kLenBuckets];
+    {
+        int64_t at = n_full;
+#pragma unroll
+        for (int b = 0; b < kLenBuckets; ++b) {
+            bnext[b] = (int32_t)(at + ((w[4 + b / 2] >> (32 * (b & 1))) & 0xffffffff));
+            at += (wt[4 + b / 2] >> (32 * (b & 1))) & 0xffffffff;
+        }
+        if (t == kPlanThreads - 1) pa.plan->n_items = at;
+    }
     int64_t qrun = q[0];
     for (int32_t g = g0; g < g1; ++g) {
-        const int64_t c = cnt_of(g), len = pa.off[g + 1] - pa.off[g];
+        const int64_t c = cnt_of(g), len = off[g + 1] - off[g];
         const int64_t nch = (c > 0 && len > 0) ? (len + ch - 1) >> lch : 0;
+        const int64_t nfull = c > 0 ? len >> lch : 0;
         const int64_t ng = nch > R ? (nch + R - 1) / R : 0;
+        int32_t wl = -1;
+        if (nch > nfull) {
+            const int b = len_bucket(len - (nfull << lch), lch);
+#pragma unroll
+            for (int i = 0; i < kLenBuckets; ++i)
+                if (b == i) wl = bnext[i]++;
+        }
+        const int32_t ws = (int32_t)(w[0] & 0xffffffff), gs = (int32_t)(w[0] >> 32);
         pa.qoff[g] = (int32_t)qrun;
-        pa.wstart[g] = (int32_t)w[0];
-        if (lds_wstart) lds_wstart[g] = (int32_t)w[0];
+        pa.wstart[g] = ws;
+        pa.wlast[g] = wl;
         pa.pbase[g] = w[1];
-        pa.gstart[g] = (int32_t)w[2];
-        pa.ubase[g] = w[3];
-        pa.mstart[g] = (int32_t)w[4];
+        pa.gstart[g] = gs;
+        pa.ubase[g] = w[2];
+        pa.mstart[g] = (int32_t)w[3];
+        if (kMirror) {
+            m.qoff[g] = (int32_t)qrun;
+            m.wstart[g] = ws;
+            m.wlast[g] = wl;
+            m.pbase[g] = w[1];
+            m.gstart[g] = gs;
+            m.ubase[g] = w[2];
+            m.mstart[g] = (int32_t)w[3];
+        }
         qrun += c;
-        w[0] += nch;
+        w[0] += nfull + (ng << 32);
         w[1] += nch * c;
-        w[2] += ng;
-        w[3] += ng * c;
-        w[4] += nch != 1 ? c : 0;
+        w[2] += ng * c;
+        w[3] += nch != 1 ? c : 0;
     }
     if (t == kPlanThreads - 1) {
         pa.qoff[G] = (int32_t)qtot[0];
-        pa.wstart[G] = (int32_t)wt[0];
-        if (lds_wstart) lds_wstart[G] = (int32_t)wt[0];
-        pa.gstart[G] = (int32_t)wt[2];
-        pa.mstart[G] = (int32_t)wt[4];
+        pa.wstart[G] = (int32_t)n_full;
+        pa.gstart[G] = (int32_t)(wt[0] >> 32);
+        pa.mstart[G] = (int32_t)wt[3];
+        if (kMirror) {
+            m.qoff[G] = (int32_t)qtot[0];
+            m.wstart[G] = (int32_t)n_full;
+            m.gstart[G] = (int32_t)(wt[0] >> 32);
+            m.mstart[G] = (int32_t)wt[3];
+        }
         pa.plan->chunk = ch;
-        pa.plan->n_items = wt[0];
         pa.plan->n_parts = wt[1];
-        pa.plan->n_groups = wt[2];
-        pa.plan->n_l1 = wt[3];
-        pa.plan->n_merge = wt[4];
+        pa.plan->n_groups = wt[0] >> 32;
+        pa.plan->n_l1 = wt[2];
+        pa.plan->n_merge = wt[3];
     }
+    return ch;
 }
 
 struct GlobalCnt {
@@ -258,92 +324,146 @@ struct SlotOut {
 // Planning step of the multi-kernel routing (counts in global memory).
 __global__ __launch_bounds__(kPlanThreads) void route_plan(PlanArgs pa, const int32_t *cnt) {
     __shared__ int64_t s[(kPlanThreads / kWave + 1) * kChunkCands];
-    plan_chunks(pa, GlobalCnt{cnt}, s, nullptr);
+    plan_chunks<false>(pa, GlobalCnt{cnt}, pa.off, s, PlanMirror{});
 }
+
+// Bytes of the LDS tables of the fused routing kernel for G clusters and n
+// (query, slot) pairs: offsets, partial and level-one bases, counts, four
+// starts tables, the last-chunk items, then the pairs' clusters as 16-bit ids.
+size_t route_fused_lds(int32_t G, int64_t n) {
+    return (size_t)(3 * G + 1) * 8 + (size_t)(6 * G + 4) * 4 + (size_t)n * 2;
+}
+
+// Work item j (a chunk of ch = 2^lch rows) of cluster g, whose segment starts
+// at bank row a0 and has len rows, with nq queries listed from qb and its
+// partials from pb.
+__device__ __forceinline__ WorkItem make_item(int32_t g, int64_t j, int64_t a0, int64_t len,
+                                              int lch, int32_t qb, int32_t nq, int64_t pb) {
+    const int64_t ch = int64_t(1) << lch, r = len - (j << lch);
+    WorkItem wi;
+    wi.r0 = a0 + (j << lch);
+    wi.p0 = pb + j * nq;
+    wi.len = (int32_t)(r < ch ? r : ch);
+    wi.g = g;
+    wi.qbeg = qb;
+    wi.nq = nq;
+    wi.single = len <= ch;          // the chunk is the whole segment
+    wi.pad = 0;
+    return wi;
+}
+constexpr uint16_t kNoCluster = 0xffff;   // selection out of range (G < kNoCluster in LDS)
 
 // The whole routing in one block when the pairs are few and the per-cluster
 // tables fit in LDS: count the (query, slot) pairs per cluster, plan the
 // chunks, scatter the pairs into per-cluster lists, then fill the work items
 // (each thread finds its items' clusters by binary search over the item starts
-// in LDS), the level-one merge groups and units, and the merge list.
+// in LDS), the level-one merge groups and units, and the merge list. The
+// selections and every per-cluster table the later steps read are kept in
+// LDS, so global memory is read once, at the start.
 __global__ __launch_bounds__(kPlanThreads) void route_fused(PlanArgs pa, const int32_t *sel,
                                                             int64_t n, int32_t *qlist,
                                                             int32_t *pos, SlotOut out,
                                                             WorkItem *items, MergeGroup *groups,
                                                             int2 *units, int32_t *mlist) {
-    extern __shared__ int32_t lds[];        // [G] counts, then fill cursors; [G+1] item starts
+    extern __shared__ int64_t lds[];
     __shared__ int64_t s[(kPlanThreads / kWave + 1) * kChunkCands];
     __shared__ int32_t s_bad;
     const int t = threadIdx.x;
     const int32_t G = pa.G;
-    int32_t *lcnt = lds, *lwst = lds + G;
+    int64_t *loff = lds, *lpb = loff + G + 1, *lub = lpb + G;
+    int32_t *lcnt = reinterpret_cast<int32_t *>(lub + G);   // counts, then fill cursors
+    PlanMirror m;
+    m.wstart = lcnt + G;
+    m.qoff = m.wstart + G + 1;
+    m.gstart = m.qoff + G + 1;
+    m.mstart = m.gstart + G + 1;
+    m.wlast = m.mstart + G + 1;
+    m.pbase = lpb;
+    m.ubase = lub;
+    uint16_t *lsel = reinterpret_cast<uint16_t *>(m.wlast + G);
+    for (int64_t e0 = t; e0 < n; e0 += 8 * kPlanThreads) {   // 8 loads in flight per thread
+        int32_t g[8];
+#pragma unroll
+        for (int r = 0; r < 8; ++r) {
+            const int64_t e = e0 + r * kPlanThreads;
+            g[r] = sel[e < n ? e : 0];
+        }
+#pragma unroll
+        for (int r = 0; r < 8; ++r) {
+            const int64_t e = e0 + r * kPlanThreads;
+            if (e < n) lsel[e] = g[r] >= 0 && g[r] < G ? (uint16_t)g[r] : kNoCluster;
+        }
+    }
+    for (int32_t g = t; g <= G; g += kPlanThreads) loff[g] = pa.off[g];
     for (int32_t g = t; g < G; g += kPlanThreads) lcnt[g] = 0;
     if (t == 0) s_bad = 0;
     __syncthreads();
     int32_t bad = 0;
     for (int64_t e = t; e < n; e += kPlanThreads) {
-        const int32_t g = sel[e];
-        if (g >= 0 && g < G) atomicAdd(&lcnt[g], 1);
+        const uint16_t h = lsel[e];
+        if (h != kNoCluster) atomicAdd(&lcnt[h], 1);
         else ++bad;
     }
     if (bad) atomicAdd(&s_bad, bad);
     __syncthreads();
-    plan_chunks(pa, LdsCnt{lcnt}, s, lwst);
+    const int64_t ch = plan_chunks<true>(pa, LdsCnt{lcnt}, loff, s, m);
+    const int lch = 63 - __builtin_clzll((unsigned long long)ch);
     __syncthreads();
-    for (int32_t g = t; g < G; g += kPlanThreads) lcnt[g] = pa.qoff[g];   // becomes the fill cursor
+    for (int32_t g = t; g < G; g += kPlanThreads) lcnt[g] = m.qoff[g];
     if (t == 0) {
         pa.plan->next = 0;
         pa.plan->bad_sel = s_bad;
     }
     __syncthreads();
     const int64_t R = pa.group;
+    const int32_t *lwst = m.wstart;
     for (int64_t e = t; e < n; e += kPlanThreads) {
-        const int32_t g = sel[e];
-        if (g >= 0 && g < G) {
-            const int32_t qb = pa.qoff[g];
+        const uint16_t h = lsel[e];
+        if (h != kNoCluster) {
+            const int32_t g = h;
+            const int32_t qb = m.qoff[g];
             const int32_t at = atomicAdd(&lcnt[g], 1);
             const int32_t i = at - qb;
             qlist[at] = (int32_t)e;
             pos[e] = i;
-            const int32_t nch = lwst[g + 1] - lwst[g];
-            if (nch != 1) mlist[pa.mstart[g] + i] = (int32_t)e;
+            const int64_t len = loff[g + 1] - loff[g];
+            const int64_t nch = (len + ch - 1) >> lch;
+            if (nch != 1) mlist[m.mstart[g] + i] = (int32_t)e;
             if (nch > R) {                 // this pair's level-one units, one per group
-                const int32_t nq = pa.qoff[g + 1] - qb, gs = pa.gstart[g];
-                const int32_t ng = pa.gstart[g + 1] - gs;
+                const int32_t nq = m.qoff[g + 1] - qb, gs = m.gstart[g];
+                const int32_t ng = m.gstart[g + 1] - gs;
+                const int64_t ub = lub[g];
                 for (int32_t jg = 0; jg < ng; ++jg)
-                    units[pa.ubase[g] + (int64_t)jg * nq + i] = make_int2(gs + jg, i);
+                    units[ub + (int64_t)jg * nq + i] = make_int2(gs + jg, i);
             }
         } else {
             out.empty(e);
         }
     }
-    const int64_t ch = pa.plan->chunk;
-    const int32_t n_items = lwst[G];
-    for (int32_t w = t; w < n_items; w += kPlanThreads) {
+    const int32_t n_full = lwst[G];            // full-length chunks, cluster by cluster
+    for (int32_t w = t; w < n_full; w += kPlanThreads) {
         int32_t lo = 0, hi = G;                // lwst[lo] <= w < lwst[hi]
         while (hi - lo > 1) {
             const int32_t mid = (lo + hi) >> 1;
             if (lwst[mid] <= w) lo = mid; else hi = mid;
         }
-        const int32_t g = lo, j = w - lwst[g];
-        const int64_t a0 = pa.off[g], len = pa.off[g + 1] - a0;
-        const int32_t qb = pa.qoff[g], nq = pa.qoff[g + 1] - qb;
-        WorkItem wi;
-        wi.r0 = a0 + j * ch;
-        wi.p0 = pa.pbase[g] + (int64_t)j * nq;
-        wi.len = (int32_t)(len - j * ch < ch ? len - j * ch : ch);
-        wi.g = g;
-        wi.qbeg = qb;
-        wi.nq = nq;
-        wi.single = lwst[g + 1] - lwst[g] == 1;
-        wi.pad = 0;
-        items[w] = wi;
+        const int32_t g = lo, qb = m.qoff[g];
+        items[w] = make_item(g, w - lwst[g], loff[g], loff[g + 1] - loff[g], lch, qb,
+                             m.qoff[g + 1] - qb, lpb[g]);
+    }
+    for (int32_t g = t; g < G; g += kPlanThreads) {   // the shorter last chunks
+        const int32_t wl = m.wlast[g];
+        if (wl < 0) continue;
+        const int64_t len = loff[g + 1] - loff[g];
+        const int32_t qb = m.qoff[g];
+        items[wl] = make_item(g, len >> lch, loff[g], len, lch, qb, m.qoff[g + 1] - qb, lpb[g]);
     }
     for (int32_t g = t; g < G; g += kPlanThreads) {
-        const int32_t gs = pa.gstart[g], ng = pa.gstart[g + 1] - gs;
+        const int32_t gs = m.gstart[g], ng = m.gstart[g + 1] - gs;
         if (ng == 0) continue;
-        const int32_t nq = pa.qoff[g + 1] - pa.qoff[g], nch = lwst[g + 1] - lwst[g];
-        const int64_t pb = pa.pbase[g], ub = pa.ubase[g];
+        const int32_t nq = m.qoff[g + 1] - m.qoff[g];
+        const int64_t nch = (loff[g + 1] - loff[g] + ch - 1) >> lch;
+        const int64_t pb = lpb[g], ub = lub[g];
         for (int32_t jg = 0; jg < ng; ++jg) {
             MergeGroup mg;
             mg.p0 = pb + jg * R * nq;
@@ -364,32 +484,25 @@ __global__ __launch_bounds__(256) void route_items(PlanArgs pa, const int32_t *q
                                                    int2 *units, int32_t *mlist) {
     const int lane = threadIdx.x & 63;
     const int64_t ch = pa.plan->chunk;
+    const int lch = 63 - __builtin_clzll((unsigned long long)ch);
     const int64_t R = pa.group;
     for (int64_t g = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); g < pa.G;
          g += (int64_t)gridDim.x * 4) {
-        const int32_t w0 = pa.wstart[g], nch = pa.wstart[g + 1] - w0;
         const int32_t qb = pa.qoff[g], nq = pa.qoff[g + 1] - qb;
         if (nq == 0) continue;
+        const int64_t a = pa.off[g], len = pa.off[g + 1] - a;
+        const int64_t nch = (len + ch - 1) >> lch;
         if (nch != 1) {
             const int32_t m0 = pa.mstart[g];
             for (int32_t i = lane; i < nq; i += kWave) mlist[m0 + i] = qlist[qb + i];
         }
         if (nch == 0) continue;
+        const int32_t w0 = pa.wstart[g], wl = pa.wlast[g];
         const int32_t gs = pa.gstart[g], ng = pa.gstart[g + 1] - gs;
-        const int64_t a = pa.off[g], len = pa.off[g + 1] - a;
         const int64_t pb = pa.pbase[g], ub = pa.ubase[g];
-        for (int32_t j = lane; j < nch; j += kWave) {
-            WorkItem wi;
-            wi.r0 = a + j * ch;
-            wi.p0 = pb + (int64_t)j * nq;
-            wi.len = (int32_t)(len - j * ch < ch ? len - j * ch : ch);
-            wi.g = (int32_t)g;
-            wi.qbeg = qb;
-            wi.nq = nq;
-            wi.single = nch == 1;
-            wi.pad = 0;
-            items[w0 + j] = wi;
-        }
+        const int64_t nfull = len >> lch;
+        for (int64_t j = lane; j < nch; j += kWave)
+            items[j < nfull ? w0 + j : wl] = make_item((int32_t)g, j, a, len, lch, qb, nq, pb);
         for (int32_t jg = lane; jg < ng; jg += kWave) {
             MergeGroup mg;
             mg.p0 = pb + jg * R * nq;
@@ -656,6 +769,7 @@ AttendWs attend_layout(void *ws, int32_t d, int32_t G, int64_t N, int32_t key_by
     w.cursor = cv.take<int32_t>(G);
     w.qoff = cv.take<int32_t>(G + 1);
     w.wstart = cv.take<int32_t>(G + 1);
+    w.wlast = cv.take<int32_t>(G);
     w.gstart = cv.take<int32_t>(G + 1);
     w.pbase = cv.take<int64_t>(G);
     w.ubase = cv.take<int64_t>(G);
@@ -757,6 +871,7 @@ hipError_t launch_attend(int32_t key_dtype, int32_t compute_dtype, int32_t d, in
     pa.off = seg_offsets;
     pa.qoff = w.qoff;
     pa.wstart = w.wstart;
+    pa.wlast = w.wlast;
     pa.gstart = w.gstart;
     pa.mstart = w.mstart;
     pa.pbase = w.pbase;
@@ -766,7 +881,8 @@ hipError_t launch_attend(int32_t key_dtype, int32_t compute_dtype, int32_t d, in
     pa.p_cap = w.p_cap;
     pa.group = w.group;
     const SlotOut so{slot_max, slot_sum, cand_score, cand_id, k};
-    const size_t route_lds = (size_t)(2 * G + 1) * 4;
+    const size_t route_lds = route_fused_lds(G, bc);
+    static_assert((3 * (size_t)kNoCluster + 1) * 8 > kRouteLdsBytes, "fused routing keeps cluster ids in 16 bits");
     if (bc <= kFusedRoutePairs && route_lds <= kRouteLdsBytes) {
         hipError_t e0 = hipFuncSetAttribute((const void *)route_fused,
                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)route_lds);

@@ -27,7 +27,9 @@ struct Plan {
 };
 
 // One work item of the bank stream: a chunk of one selected cluster's segment,
-// scored against every query that selected the cluster.
+// scored against every query that selected the cluster. The item table holds
+// every full-length chunk first, then the clusters' shorter last chunks,
+// longest first.
 struct WorkItem {
     int64_t r0;        // first bank row
     int64_t p0;        // partial result of the item's first query (query i: p0 + i)
@@ -93,7 +95,8 @@ struct AttendWs {
     int32_t *cnt;      // [G] queries per cluster
     int32_t *cursor;   // [G]
     int32_t *qoff;     // [G+1]
-    int32_t *wstart;   // [G+1] first work item of each cluster
+    int32_t *wstart;   // [G+1] first full-length chunk item of each cluster
+    int32_t *wlast;    // [G]   item of each cluster's shorter last chunk (-1: none)
     int32_t *gstart;   // [G+1] first level-one merge group of each cluster
     int64_t *pbase;    // [G]   first partial of each cluster
     int64_t *ubase;    // [G]   first level-one merge result of each cluster
