@@ -57,13 +57,6 @@ __device__ __forceinline__ void gemm_tile(int b, int nb, int tm, int tn, int &mt
 // 16 distinct (row % 4, slot) pairs: all 64 banks once.
 __device__ __forceinline__ int gemm_slot(int row, int c) { return c ^ ((row >> 2) & 3); }
 
-// s_waitcnt with only a vector-memory count (the other counters left free).
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-    static_assert(N >= 0 && N < 64, "vmcnt range");
-    __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
-}
-
 // Requests one stage straight into LDS (global_load_lds_dwordx4: lane i of an
 // instruction writes bytes 16 i .. 16 i + 15 after the instruction's base).
 // Instruction i of wave w covers rows 16 (4 w + i) .. + 15; its lane l loads

@@ -53,6 +53,14 @@ __device__ __forceinline__ void mz_merge(float &m, float &z, float m2, float z2,
 // next to the maximum's own term 1, where such terms do not change the sum.
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// s_waitcnt with only a vector-memory count (the other counters left free):
+// at most N of this wave's vector memory loads still outstanding.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
 // ---------------------------------------------------------------------------
 // Fragment loads for v_mfma_f32_16x16x32_bf16: 8 consecutive elements of one
 // row starting at p, as bf16 (fp32 storage is rounded to nearest even by the
@@ -235,17 +243,27 @@ __device__ __forceinline__ uint64_t wave_element(const uint64_t (&v)[NPL], int i
 // instead and cut to exactly k keys (threshold = the k-th key). Returns the
 // new count.
 template <int NPL>
-__device__ __forceinline__ int compact_select(uint64_t *buf, int n, int k, int room, int lane,
+__device__ __forceinline__ int compact_select(uint64_t *gbuf, int n, int k, int room, int lane,
                                               uint64_t &theta) {
     constexpr int cap = NPL * kWave;
+    // The buffer is in LDS (every caller's is): addressed as such, its reads
+    // and writes are LDS operations even where address-space inference does
+    // not reach (flat ones would also wait for the wave's global loads).
+    typedef __attribute__((address_space(3))) uint64_t lds_u64;
+    lds_u64 *buf = (lds_u64 *)gbuf;
+    n = __builtin_amdgcn_readfirstlane(n);     // wave-uniform arguments, held as such
+    k = __builtin_amdgcn_readfirstlane(k);
+    room = __builtin_amdgcn_readfirstlane(room);
     uint64_t v[NPL];
     uint32_t hi[NPL];
+    uint64_t vm[NPL];             // lanes holding a key, per register (wave-uniform masks)
     uint32_t hand = 0xffffffffu, hor = 0;
 #pragma unroll
     for (int q = 0; q < NPL; ++q) {
         const bool ok = q * kWave + lane < n;
         v[q] = ok ? buf[q * kWave + lane] : 0;
         hi[q] = (uint32_t)(v[q] >> 32);
+        vm[q] = __ballot(v[q] != 0);
         if (ok) {
             hand &= hi[q];
             hor |= hi[q];
@@ -263,6 +281,10 @@ __device__ __forceinline__ int compact_select(uint64_t *buf, int n, int k, int r
     hor |= lane_xor32<16>(hor, lane);
     hand &= lane_xor32<32>(hand, lane);
     hor |= lane_xor32<32>(hor, lane);
+    // the same in every lane: made explicit, so that the select below is a
+    // scalar loop (ballots and their counts) rather than a lane-masked one
+    hand = __builtin_amdgcn_readfirstlane(hand);
+    hor = __builtin_amdgcn_readfirstlane(hor);
     const uint32_t diff = hand ^ hor;
     const int top = diff ? 31 - __builtin_clz(diff) : -1;
     uint32_t T = top < 0 ? hand : (top == 31 ? 0u : hand & ~((2u << top) - 1u));
@@ -271,7 +293,7 @@ __device__ __forceinline__ int compact_select(uint64_t *buf, int n, int k, int r
         const uint32_t cand = T | (1u << bit);
         int c = 0;
 #pragma unroll
-        for (int q = 0; q < NPL; ++q) c += __popcll(__ballot(hi[q] >= cand && v[q] != 0));
+        for (int q = 0; q < NPL; ++q) c += __popcll(__ballot(hi[q] >= cand) & vm[q]);
         if (c >= k) {
             T = cand;
             keep = c;
@@ -283,9 +305,8 @@ __device__ __forceinline__ int compact_select(uint64_t *buf, int n, int k, int r
         int base = 0;
 #pragma unroll
         for (int q = 0; q < NPL; ++q) {
-            const bool pass = hi[q] >= T && v[q] != 0;
-            const uint64_t mask = __ballot(pass);
-            if (pass) buf[base + __popcll(mask & lt_mask)] = v[q];
+            const uint64_t mask = __ballot(hi[q] >= T) & vm[q];
+            if ((mask >> lane) & 1) buf[base + __popcll(mask & lt_mask)] = v[q];
             base += __popcll(mask);
         }
         theta = (uint64_t)T << 32;

@@ -232,6 +232,21 @@ __device__ __forceinline__ int group_sum(int x, int lane) {
     return x;
 }
 
+// compact_select kept out of line: the stream kernels are far larger than the
+// instruction cache, and a rarely taken path inlined at every step end is
+// fetched from L2 each time it runs; one shared copy stays warmer.
+struct Compacted {
+    int n;
+    uint64_t theta;
+};
+template <int NPL>
+__device__ __noinline__ Compacted compact_cold(uint64_t *buf, int n, int k, int room) {
+    Compacted r;
+    r.theta = 0;
+    r.n = compact_select<NPL>(buf, n, k, room, threadIdx.x & 63, r.theta);
+    return r;
+}
+
 // The owned queries' share of one step (see OwnerMap). Rows at or beyond r1
 // are not candidates. Each lane counts its candidates above the threshold;
 // a buffer that cannot take its group's candidates is compacted (one query at
@@ -276,11 +291,10 @@ __device__ __forceinline__ void owner_epilogue(const FineArgs &a, const FineSmem
             const int l0 = __builtin_ctzll(full);
             const int n0 = wave * qw + l0 / RG;
             const int c0 = __shfl(o.cnt, l0);
-            uint64_t th = 0;
-            const int c1 = compact_select<NPL>(sm.buf + (size_t)n0 * a.cap, c0, a.k, kWave, lane, th);
+            const Compacted c1 = compact_cold<NPL>(sm.buf + (size_t)n0 * a.cap, c0, a.k, kWave);
             if (jq == l0 / RG) {
-                o.cnt = c1;
-                o.theta = th;
+                o.cnt = c1.n;
+                o.theta = c1.theta;
             }
         }
         mine = 0;
@@ -402,8 +416,7 @@ __device__ __forceinline__ void pass_end(const FineArgs &a, const FineSmem &sm, 
             }
         } else {
             if (cn > a.k) {
-                uint64_t th = 0;
-                cn = compact_select<NPL>(b, cn, a.k, a.cap - a.k, lane, th);
+                cn = compact_cold<NPL>(b, cn, a.k, a.cap - a.k).n;
             }
             const int64_t p = p0 + qg0 + q;
             for (int i = lane; i < a.k; i += kWave) a.pk[p * a.k + i] = i < cn ? b[i] : 0;
@@ -513,35 +526,57 @@ struct LoadUnit {
 // Unconditional loads only (rows clamped into the chunk), so that the compiler
 // can count outstanding loads exactly and wait for one unit at a time.
 template <typename KT, int U>
+__device__ __forceinline__ const KT *unit_keys(const KT *__restrict__ K, int d, int NG, int u,
+                                               int64_t r0, int64_t r1, int64_t &base) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, r16 = lane & 15, kg = lane >> 4;
+    const int tt = u / NG, gi = u - tt * NG;
+    base = r0 + (int64_t)tt * kRowsPerStep;
+    const int64_t row = min(base + wave * kRowsPerWave + r16, r1 - 1);
+    return K + row * d + 32 * U * gi + 8 * kg;
+}
+
+template <typename KT, int U>
 __device__ __forceinline__ void lds_load_unit(LoadUnit<KT, U> &lu, const KT *__restrict__ K,
                                               const int32_t *__restrict__ tid_src, int d, int NG,
                                               int u, int64_t r0, int64_t r1) {
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, r16 = lane & 15, kg = lane >> 4;
-    const int tt = u / NG, gi = u - tt * NG;
-    const int64_t base = r0 + (int64_t)tt * kRowsPerStep;
-    const int64_t row = min(base + wave * kRowsPerWave + r16, r1 - 1);
-    const KT *kp = K + row * d + 32 * U * gi + 8 * kg;
+    int64_t base;
+    const KT *kp = unit_keys<KT, U>(K, d, NG, u, r0, r1, base);
 #pragma unroll
     for (int uu = 0; uu < U; ++uu) lu.f[uu].load(kp + 32 * uu);
     lu.tid = step_tid_load(tid_src, base, r1);
 }
 
-template <typename KT, int U, int NQT, int NPL>
+// Multiplies unit u (in lu) and requests unit nu into nx. With SPREAD the
+// loads are spread between the MFMAs, one fragment per k-step, so that a wave
+// that is alone on its SIMD keeps refilling its share of the memory pipeline
+// while it multiplies, instead of issuing a whole unit at once and leaving
+// the pipeline to drain; without it (two blocks per CU, whose waves cover for
+// each other) the unit is requested before the MFMAs.
+template <typename KT, int U, int NQT, int NPL, bool SPREAD>
 __device__ __forceinline__ void lds_compute_unit(const FineArgs &a, const FineSmem &sm,
-                                                 const LoadUnit<KT, U> &lu, int NG, int u, int64_t r0,
-                                                 int64_t r1, int nqg, f32x4_t (&acc)[NQT],
-                                                 OwnedLane &o, Stats<NQT> &st) {
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+                                                 const LoadUnit<KT, U> &lu, LoadUnit<KT, U> &nx,
+                                                 const KT *__restrict__ K, int nu, int NG, int u,
+                                                 bool valid, int64_t r0, int64_t r1, int nqg,
+                                                 f32x4_t (&acc)[NQT], OwnedLane &o, Stats<NQT> &st) {
+    const int lane = threadIdx.x & 63;
     const int tt = u / NG, gi = u - tt * NG;
     const float keep = gi == 0 ? 0.0f : 1.0f;
 #pragma unroll
     for (int qt = 0; qt < NQT; ++qt) acc[qt] *= keep;
+    int64_t nbase;
+    const KT *nkp = unit_keys<KT, U>(K, a.d, NG, nu, r0, r1, nbase);
+    nx.tid = step_tid_load(a.tid_src, nbase, r1);
+    if (!SPREAD) {
+#pragma unroll
+        for (int uu = 0; uu < U; ++uu) nx.f[uu].load(nkp + 32 * uu);
+    }
     const bf16x8_t *qs = sm.qs + (size_t)gi * U * NQT * kWave + lane;
     // Query fragments are read from LDS a few k-steps ahead of their MFMAs;
     // the scheduling barriers keep the compiler from hoisting all of them
-    // (4 registers each) to the top of the unit.
+    // (4 registers each), or the next unit's loads, to the top of the unit.
 #pragma unroll
     for (int uu = 0; uu < U; ++uu) {
+        if (SPREAD) nx.f[uu].load(nkp + 32 * uu);
         const bf16x8_t A = lu.f[uu].bf16();
 #pragma unroll
         for (int qt = 0; qt < NQT; ++qt)
@@ -549,14 +584,13 @@ __device__ __forceinline__ void lds_compute_unit(const FineArgs &a, const FineSm
                                                               acc[qt], 0, 0, 0);
         if ((uu & 3) == 3) __builtin_amdgcn_sched_barrier(0);
     }
-    if (gi == NG - 1) {
+    if (valid && gi == NG - 1) {
         const int64_t base = r0 + (int64_t)tt * kRowsPerStep;
         step_end<NQT, NPL>(a, sm, acc, tt, base, r1, nqg,
                            tid_value(lu.tid, a.tid == nullptr, base, r1), o, st);
     }
 }
-
-template <typename KT, int U, int NQT, int NPL>
+template <typename KT, int U, int NQT, int NPL, bool SPREAD>
 __device__ __forceinline__ void pass_lds(const FineArgs &a, const FineSmem &sm, int64_t p0,
                                          bool single, int64_t r0, int64_t r1, int32_t qbeg,
                                          int32_t qg0, int32_t nqg) {
@@ -583,8 +617,10 @@ __device__ __forceinline__ void pass_lds(const FineArgs &a, const FineSmem &sm, 
 
     pass_begin(a, sm, qbeg, qg0, nqg);
     // stage the queries as MFMA B fragments: [k-step][query tile][lane], eight
-    // fragments per thread loaded before any is stored (indices past the end
-    // load the last fragment again and store nothing)
+    // fragments per thread loaded before any is stored. Indices past the end
+    // load and store the last fragment again (the same value), so that every
+    // load is consumed on every path: a load left pending on one path would
+    // make the compiler drain all loads in flight at the head of the unit loop.
     {
         constexpr int kBatch = 8;
         const int nfrag = KS * NQT * kWave;
@@ -597,13 +633,21 @@ __device__ __forceinline__ void pass_lds(const FineArgs &a, const FineSmem &sm, 
                 const int qt = rem >> 6, ln = rem & 63;
                 const int n = qt * 16 + (ln & 15), k = 32 * s + 8 * (ln >> 4);
                 f[b] = load8(Q + (int64_t)sm.qrow[n < nqg ? n : 0] * d + k);
-                if (n >= nqg) f[b] = zero8();
             }
+            // padding columns (no query) are zeroed at the store: a select on
+            // a loaded value where it is loaded would wait for every load
 #pragma unroll
-            for (int b = 0; b < kBatch; ++b)
-                if (i0 + b * kFineThreads < nfrag) sm.qs[i0 + b * kFineThreads] = f[b];
+            for (int b = 0; b < kBatch; ++b) {
+                const int idx = min(i0 + b * kFineThreads, nfrag - 1);
+                const int rem = idx % (NQT * kWave);
+                const int n = (rem >> 6) * 16 + (rem & 15);
+                sm.qs[idx] = n < nqg ? f[b] : zero8();
+            }
         }
     }
+    // The first ring units are in: no path enters the unit loop with a load
+    // outstanding.
+    wait_vmcnt<0>();
     __syncthreads();
 
     OwnedLane o;
@@ -613,15 +657,22 @@ __device__ __forceinline__ void pass_lds(const FineArgs &a, const FineSmem &sm, 
     f32x4_t acc[NQT];
 #pragma unroll
     for (int qt = 0; qt < NQT; ++qt) acc[qt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    // Whole iterations only: units past the end are multiplied too (on the
+    // last unit's keys, loaded again) and have no step end. On the way back
+    // to the loop head every ring slot loaded in an iteration has then been
+    // consumed in it on every path; a slot still loading on some path would
+    // make the compiler wait for every load in flight at each iteration.
     for (int u = 0; u < total; u += R) {
 #pragma unroll
-        for (int j = 0; j < R; ++j) {
-            lds_load_unit<KT, U>(ring[(j + R - 1) % R], K, a.tid_src, d, NG,
-                              min(u + j + R - 1, total - 1), r0, r1);
-            if (u + j < total)
-                lds_compute_unit<KT, U, NQT, NPL>(a, sm, ring[j], NG, u + j, r0, r1, nqg, acc, o, st);
-        }
+        for (int j = 0; j < R; ++j)
+            lds_compute_unit<KT, U, NQT, NPL, SPREAD>(a, sm, ring[j], ring[(j + R - 1) % R], K,
+                                              min(u + j + R - 1, total - 1), NG, u + j,
+                                              u + j < total, r0, r1, nqg, acc, o, st);
     }
+    // the ring's last loads (re-reads of the last unit) are not used: wait for
+    // them here, so that no path reaches the next pass's unit loop with ring
+    // registers still loading
+    wait_vmcnt<0>();
     pass_end<NQT, NPL>(a, sm, p0, qbeg, single, qg0, nqg, o, st);
 }
 
@@ -658,11 +709,13 @@ __device__ __forceinline__ void for_each_item(const FineArgs &a, int32_t *s_next
         body(item_pass(a.items[w]));
         if (threadIdx.x == 0) s_next[parity] = (int32_t)gridDim.x + nxt;
         __syncthreads();
-        w = s_next[parity];
+        // uniform: the item is then read with scalar loads, which do not
+        // count against the vector loads the unit loop waits for
+        w = __builtin_amdgcn_readfirstlane(s_next[parity]);
     }
 }
 
-template <typename KT, int U, int NPL>
+template <typename KT, int U, int NPL, bool SPREAD>
 __device__ __forceinline__ void stream_lds_body(const FineArgs &a, int32_t qs_bytes,
                                                 unsigned char *smem_raw, int32_t *s_next) {
     const FineSmem sm = fine_carve(smem_raw, qs_bytes, a.qmax, a.cap, a.ntile);
@@ -670,10 +723,10 @@ __device__ __forceinline__ void stream_lds_body(const FineArgs &a, int32_t qs_by
         for (int32_t qg0 = 0; qg0 < it.nq; qg0 += a.qmax) {
             const int32_t nqg = min(a.qmax, it.nq - qg0);
             switch ((nqg + 15) >> 4) {
-                case 1: pass_lds<KT, U, 1, NPL>(a, sm, it.p0, it.single, it.r0, it.r1, it.qbeg, qg0, nqg); break;
-                case 2: pass_lds<KT, U, 2, NPL>(a, sm, it.p0, it.single, it.r0, it.r1, it.qbeg, qg0, nqg); break;
-                case 3: pass_lds<KT, U, 3, NPL>(a, sm, it.p0, it.single, it.r0, it.r1, it.qbeg, qg0, nqg); break;
-                default: pass_lds<KT, U, 4, NPL>(a, sm, it.p0, it.single, it.r0, it.r1, it.qbeg, qg0, nqg); break;
+                case 1: pass_lds<KT, U, 1, NPL, SPREAD>(a, sm, it.p0, it.single, it.r0, it.r1, it.qbeg, qg0, nqg); break;
+                case 2: pass_lds<KT, U, 2, NPL, SPREAD>(a, sm, it.p0, it.single, it.r0, it.r1, it.qbeg, qg0, nqg); break;
+                case 3: pass_lds<KT, U, 3, NPL, SPREAD>(a, sm, it.p0, it.single, it.r0, it.r1, it.qbeg, qg0, nqg); break;
+                default: pass_lds<KT, U, 4, NPL, SPREAD>(a, sm, it.p0, it.single, it.r0, it.r1, it.qbeg, qg0, nqg); break;
             }
         }
     });
@@ -684,7 +737,7 @@ template <typename KT, int NPL>
 __global__ __launch_bounds__(kFineThreads) void stream_lds(FineArgs a, int32_t qs_bytes) {
     extern __shared__ __align__(16) unsigned char smem_raw[];
     __shared__ int32_t s_next[2];
-    stream_lds_body<KT, AFrag<KT>::U, NPL>(a, qs_bytes, smem_raw, s_next);
+    stream_lds_body<KT, AFrag<KT>::U, NPL, true>(a, qs_bytes, smem_raw, s_next);
 }
 
 // Two blocks per CU when their LDS fits (small query groups): registers
@@ -696,7 +749,7 @@ __global__ __launch_bounds__(kFineThreads) __attribute__((amdgpu_waves_per_eu(2,
 void stream_lds2(FineArgs a, int32_t qs_bytes) {
     extern __shared__ __align__(16) unsigned char smem_raw[];
     __shared__ int32_t s_next[2];
-    stream_lds_body<KT, 8, NPL>(a, qs_bytes, smem_raw, s_next);
+    stream_lds_body<KT, 8, NPL, false>(a, qs_bytes, smem_raw, s_next);
 }
 
 template <typename T, bool BF16, int NPL>
