@@ -334,6 +334,15 @@ size_t route_fused_lds(int32_t G, int64_t n) {
     return (size_t)(3 * G + 1) * 8 + (size_t)(6 * G + 4) * 4 + (size_t)n * 2;
 }
 
+// Position in the item table of the w-th full-length chunk (cluster by
+// cluster) among n_full: a fixed permutation (multiplication by a prime above
+// any item count, modulo n_full) that spreads each cluster's chunks over the
+// table, so that the blocks reach a cluster's chunks at different times and
+// the later ones start from the bounds the earlier ones published.
+__device__ __forceinline__ int32_t full_slot(int32_t w, int32_t n_full) {
+    return (int32_t)(((uint64_t)w * 2147483629ull) % (uint64_t)n_full);
+}
+
 // Work item j (a chunk of ch = 2^lch rows) of cluster g, whose segment starts
 // at bank row a0 and has len rows, with nq queries listed from qb and its
 // partials from pb.
@@ -362,7 +371,7 @@ constexpr uint16_t kNoCluster = 0xffff;   // selection out of range (G < kNoClus
 // LDS, so global memory is read once, at the start.
 __global__ __launch_bounds__(kPlanThreads) void route_fused(PlanArgs pa, const int32_t *sel,
                                                             int64_t n, int32_t *qlist,
-                                                            int32_t *pos, SlotOut out,
+                                                            int32_t *pos, uint64_t *bound, SlotOut out,
                                                             WorkItem *items, MergeGroup *groups,
                                                             int2 *units, int32_t *mlist) {
     extern __shared__ int64_t lds[];
@@ -419,6 +428,7 @@ __global__ __launch_bounds__(kPlanThreads) void route_fused(PlanArgs pa, const i
     const int32_t *lwst = m.wstart;
     for (int64_t e = t; e < n; e += kPlanThreads) {
         const uint16_t h = lsel[e];
+        bound[e] = 0;
         if (h != kNoCluster) {
             const int32_t g = h;
             const int32_t qb = m.qoff[g];
@@ -448,8 +458,8 @@ __global__ __launch_bounds__(kPlanThreads) void route_fused(PlanArgs pa, const i
             if (lwst[mid] <= w) lo = mid; else hi = mid;
         }
         const int32_t g = lo, qb = m.qoff[g];
-        items[w] = make_item(g, w - lwst[g], loff[g], loff[g + 1] - loff[g], lch, qb,
-                             m.qoff[g + 1] - qb, lpb[g]);
+        items[full_slot(w, n_full)] = make_item(g, w - lwst[g], loff[g], loff[g + 1] - loff[g],
+                                                lch, qb, m.qoff[g + 1] - qb, lpb[g]);
     }
     for (int32_t g = t; g < G; g += kPlanThreads) {   // the shorter last chunks
         const int32_t wl = m.wlast[g];
@@ -501,8 +511,10 @@ __global__ __launch_bounds__(256) void route_items(PlanArgs pa, const int32_t *q
         const int32_t gs = pa.gstart[g], ng = pa.gstart[g + 1] - gs;
         const int64_t pb = pa.pbase[g], ub = pa.ubase[g];
         const int64_t nfull = len >> lch;
+        const int32_t n_full = pa.wstart[pa.G];
         for (int64_t j = lane; j < nch; j += kWave)
-            items[j < nfull ? w0 + j : wl] = make_item((int32_t)g, j, a, len, lch, qb, nq, pb);
+            items[j < nfull ? full_slot(w0 + (int32_t)j, n_full) : wl] =
+                make_item((int32_t)g, j, a, len, lch, qb, nq, pb);
         for (int32_t jg = lane; jg < ng; jg += kWave) {
             MergeGroup mg;
             mg.p0 = pb + jg * R * nq;
@@ -519,10 +531,12 @@ __global__ __launch_bounds__(256) void route_items(PlanArgs pa, const int32_t *q
 }
 
 __global__ void route_scatter(const int32_t *sel, int64_t n, int32_t G, const int32_t *qoff,
-                              int32_t *cursor, int32_t *qlist, int32_t *pos, SlotOut out) {
+                              int32_t *cursor, int32_t *qlist, int32_t *pos, uint64_t *bound,
+                              SlotOut out) {
     for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < n;
          e += (int64_t)gridDim.x * blockDim.x) {
         const int32_t g = sel[e];
+        bound[e] = 0;
         if (g >= 0 && g < G) {
             const int32_t slot = atomicAdd(&cursor[g], 1);
             qlist[qoff[g] + slot] = (int32_t)e;
@@ -778,6 +792,7 @@ AttendWs attend_layout(void *ws, int32_t d, int32_t G, int64_t N, int32_t key_by
     w.units = cv.take<int2>(w.u_cap);
     w.qlist = cv.take<int32_t>(bc);
     w.pos = cv.take<int32_t>(bc);
+    w.bound = cv.take<uint64_t>(bc);
     w.plan = cv.take<Plan>(1);
     w.items = cv.take<WorkItem>(w.w_max);
     w.groups = cv.take<MergeGroup>(w.g_max);
@@ -888,14 +903,14 @@ hipError_t launch_attend(int32_t key_dtype, int32_t compute_dtype, int32_t d, in
                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)route_lds);
         if (e0 != hipSuccess) return e0;
         hipLaunchKernelGGL(route_fused, dim3(1), dim3(kPlanThreads), route_lds, s, pa, sel, bc,
-                           w.qlist, w.pos, so, w.items, w.groups, w.units, w.mlist);
+                           w.qlist, w.pos, w.bound, so, w.items, w.groups, w.units, w.mlist);
     } else {
         hipLaunchKernelGGL(route_init, dim3((G + 255) / 256 < 1024 ? (G + 255) / 256 : 1024),
                            dim3(256), 0, s, G, w.cnt, w.cursor, w.plan);
         hipLaunchKernelGGL(route_count, dim3(gblocks), dim3(256), 0, s, sel, bc, G, w.cnt, w.plan);
         hipLaunchKernelGGL(route_plan, dim3(1), dim3(kPlanThreads), 0, s, pa, w.cnt);
         hipLaunchKernelGGL(route_scatter, dim3(gblocks), dim3(256), 0, s, sel, bc, G, w.qoff,
-                           w.cursor, w.qlist, w.pos, so);
+                           w.cursor, w.qlist, w.pos, w.bound, so);
         hipLaunchKernelGGL(route_items, dim3((G + 3) / 4 < 2048 ? (G + 3) / 4 : 2048), dim3(256), 0,
                            s, pa, w.qlist, w.items, w.groups, w.units, w.mlist);
     }
@@ -915,6 +930,7 @@ hipError_t launch_attend(int32_t key_dtype, int32_t compute_dtype, int32_t d, in
     fa.cap = fine_cap(k);
     fa.cexp = cexp;
     fa.qlist = w.qlist;
+    fa.bound = w.bound;
     fa.items = w.items;
     fa.plan = w.plan;
     fa.pm = w.pm;

@@ -105,6 +105,7 @@ struct AttendWs {
     int2 *units;       // [u_cap] level-one work: (group, query position)
     int32_t *qlist;    // [B*c] (query, slot) entries grouped by cluster
     int32_t *pos;      // [B*c] position of each entry inside its cluster's list
+    uint64_t *bound;   // [B*c] per pair: a key at or below its k-th best, raised as chunks finish
     Plan *plan;
     WorkItem *items;   // [w_max]
     MergeGroup *groups;// [g_max]

@@ -58,6 +58,7 @@ struct FineArgs {
     float *pm, *pz;
     int32_t *pc;
     uint64_t *pk;
+    uint64_t *bound;   // [B*c] per pair: a key at most its k-th best (shared by its chunks)
     float *slot_max, *slot_sum, *cand_score;   // final per-slot outputs (single-chunk clusters)
     int32_t *cand_id;
 };
@@ -148,11 +149,6 @@ struct OwnedLane {
     uint64_t theta;
 };
 
-__device__ __forceinline__ void owned_reset(OwnedLane &o) {
-    o.cnt = 0;
-    o.theta = 0;
-}
-
 // Softmax statistics in the MFMA result layout: lane (r16, kg) keeps, for
 // query column qt*16 + r16, the running max and sum of exp((s - max)/tau)
 // over its rows (4 kg + e of each of the wave's 16-row tiles). The rows a
@@ -199,13 +195,28 @@ __device__ __forceinline__ void stats_update(Stats<NQT> &st, const f32x4_t (&acc
 
 // Per-pass set-up: the (query, slot) pairs of the pass and their query rows.
 __device__ __forceinline__ void pass_begin(const FineArgs &a, const FineSmem &sm, int32_t qbeg,
-                                           int32_t qg0, int32_t nqg) {
+                                           int32_t qg0, int32_t nqg, bool single) {
     for (int n = threadIdx.x; n < nqg; n += kFineThreads) {
         const int32_t e = a.qlist[qbeg + qg0 + n];
         sm.qpair[n] = e;
         sm.qrow[n] = e / a.c;
+        // a chunk of a longer segment starts from the pair's shared bound
+        sm.otheta[n] = single ? 0 : __hip_atomic_load(a.bound + e, __ATOMIC_RELAXED,
+                                                      __HIP_MEMORY_SCOPE_AGENT);
     }
     __syncthreads();
+}
+
+// The owned query's buffer starts empty, with the threshold handed over from
+// the pair's shared bound.
+template <int NQT>
+__device__ __forceinline__ void owned_begin(const FineSmem &sm, int nqg, OwnedLane &o) {
+    constexpr int RG = OwnerMap<NQT>::RG;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, jq = lane / RG;
+    const int qw = (nqg + kFineWaves - 1) / kFineWaves;
+    const int n = wave * qw + jq;
+    o.cnt = 0;
+    o.theta = jq < qw && n < nqg ? sm.otheta[n] : 0;
 }
 
 // This wave's MFMA results for one step into the score tile: the lane holds
@@ -294,7 +305,7 @@ __device__ __forceinline__ void owner_epilogue(const FineArgs &a, const FineSmem
             const Compacted c1 = compact_cold<NPL>(sm.buf + (size_t)n0 * a.cap, c0, a.k, kWave);
             if (jq == l0 / RG) {
                 o.cnt = c1.n;
-                o.theta = c1.theta;
+                o.theta = c1.theta > o.theta ? c1.theta : o.theta;
             }
         }
         mine = 0;
@@ -365,7 +376,10 @@ __device__ __forceinline__ void pass_end(const FineArgs &a, const FineSmem &sm, 
     const int jq = lane / RG, rg = lane % RG;
     const int qw = (nqg + kFineWaves - 1) / kFineWaves;
     const int n = wave * qw + jq;
-    if (jq < qw && n < nqg && rg == 0) sm.ocnt[n] = o.cnt;
+    if (jq < qw && n < nqg && rg == 0) {
+        sm.ocnt[n] = o.cnt;
+        sm.otheta[n] = o.theta;
+    }
     __syncthreads();           // every wave is done with the score tile, which the statistics reuse
     // statistics: the four row groups of a lane column, then the waves in order
 #pragma unroll
@@ -415,9 +429,16 @@ __device__ __forceinline__ void pass_end(const FineArgs &a, const FineSmem &sm, 
                 a.slot_sum[e] = Zq;
             }
         } else {
+            uint64_t th = sm.otheta[q];
             if (cn > a.k) {
-                cn = compact_cold<NPL>(b, cn, a.k, a.cap - a.k).n;
+                const Compacted c = compact_cold<NPL>(b, cn, a.k, a.cap - a.k);
+                cn = c.n;
+                th = c.theta > th ? c.theta : th;
             }
+            // At least k keys of this partial (or of the one the bound came
+            // from) are at or above th, so no key below it can be among the
+            // pair's top k: later chunks of the segment start from it.
+            if (lane == 0 && th != 0) atomicMax(a.bound + sm.qpair[q], th);
             const int64_t p = p0 + qg0 + q;
             for (int i = lane; i < a.k; i += kWave) a.pk[p * a.k + i] = i < cn ? b[i] : 0;
             if (lane == 0) {
@@ -439,7 +460,7 @@ __device__ __forceinline__ void pass_generic(const FineArgs &a, const FineSmem &
     const int d = a.d;
     const T *K = static_cast<const T *>(a.keys);
     const T *Q = static_cast<const T *>(a.q);
-    pass_begin(a, sm, qbeg, qg0, nqg);
+    pass_begin(a, sm, qbeg, qg0, nqg, single);
     const T *qp[NQT];
 #pragma unroll
     for (int qt = 0; qt < NQT; ++qt) {
@@ -447,7 +468,7 @@ __device__ __forceinline__ void pass_generic(const FineArgs &a, const FineSmem &
         qp[qt] = Q + (int64_t)sm.qrow[n < nqg ? n : 0] * d;
     }
     OwnedLane o;
-    owned_reset(o);
+    owned_begin<NQT>(sm, nqg, o);
     Stats<NQT> st;
     stats_reset<NQT>(st);
     int step = 0;
@@ -615,7 +636,7 @@ __device__ __forceinline__ void pass_lds(const FineArgs &a, const FineSmem &sm, 
     for (int j = 0; j < R - 1; ++j)
         lds_load_unit<KT, U>(ring[j], K, a.tid_src, d, NG, min(j, total - 1), r0, r1);
 
-    pass_begin(a, sm, qbeg, qg0, nqg);
+    pass_begin(a, sm, qbeg, qg0, nqg, single);
     // stage the queries as MFMA B fragments: [k-step][query tile][lane], eight
     // fragments per thread loaded before any is stored. Indices past the end
     // load and store the last fragment again (the same value), so that every
@@ -651,7 +672,7 @@ __device__ __forceinline__ void pass_lds(const FineArgs &a, const FineSmem &sm, 
     __syncthreads();
 
     OwnedLane o;
-    owned_reset(o);
+    owned_begin<NQT>(sm, nqg, o);
     Stats<NQT> st;
     stats_reset<NQT>(st);
     f32x4_t acc[NQT];
