@@ -101,19 +101,14 @@ __global__ __launch_bounds__(kGemmThreads) void coarse_gemm(const __bf16 *__rest
 #pragma unroll
         for (int j = 0; j < 4; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-    // kStages - 1 stages in flight ahead of the one being multiplied; past the
-    // end the last stage is requested again into a buffer nobody reads, so that
-    // every wave issues the same loads and the counts below stay exact.
-#pragma unroll
-    for (int s0 = 0; s0 < kStages - 1; ++s0)
-        gemm_issue_stage(q, ck, m0, n0, B, G, d, min(s0, nk - 1) * BK, lds + s0 * kStageBytes);
-    for (int ks = 0; ks < nk; ++ks) {
-        wait_vmcnt<(kStages - 2) * kLoadsPerWave>();    // this wave's part of stage ks has landed
-        __builtin_amdgcn_s_barrier();                     // everyone's has; stage ks-1 is read
-        gemm_issue_stage(q, ck, m0, n0, B, G, d, min(ks + kStages - 1, nk - 1) * BK,
-                         lds + ((ks + kStages - 1) % kStages) * kStageBytes);
+    // Software pipeline over K stages of 32: while the MFMAs of stage ks run
+    // (its fragments already in registers), the fragments of stage ks + 1 are
+    // read from LDS between them, and stages ks + 1 .. ks + 4 are in flight
+    // or landed in the four LDS buffers. Past the end the last stage is
+    // requested again into a buffer nobody reads, so that every wave issues
+    // the same loads and the counts below stay exact.
+    auto read_frags = [&](int ks, bf16x8_t (&a)[8], bf16x8_t (&b)[4]) {
         const unsigned char *st = lds + (ks % kStages) * kStageBytes;
-        bf16x8_t a[8], b[4];
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
             const int row = wm * 128 + i * 16 + r16;
@@ -124,13 +119,45 @@ __global__ __launch_bounds__(kGemmThreads) void coarse_gemm(const __bf16 *__rest
             const int row = BM + wn * 64 + j * 16 + r16;
             b[j] = *reinterpret_cast<const bf16x8_t *>(st + row * 64 + 16 * gemm_slot(row, kg));
         }
+    };
+    // One stage: wait until stage ks + 1 has landed for every wave and every
+    // wave's reads of stage ks are done, refill stage ks's buffer with stage
+    // ks + 4, then multiply stage ks while reading stage ks + 1.
+    auto stage = [&](int ks, const bf16x8_t (&a)[8], const bf16x8_t (&b)[4], bf16x8_t (&na)[8],
+                     bf16x8_t (&nb)[4]) {
+        wait_vmcnt<(kStages - 2) * kLoadsPerWave>();
+        __builtin_amdgcn_s_waitcnt(0xC07F);               // lgkmcnt(0): this wave's LDS reads are in
+        __builtin_amdgcn_s_barrier();
+        gemm_issue_stage(q, ck, m0, n0, B, G, d, min(ks + kStages, nk - 1) * BK,
+                         lds + (ks % kStages) * kStageBytes);
+        const unsigned char *st = lds + ((ks + 1) % kStages) * kStageBytes;
 #pragma unroll
-        for (int i = 0; i < 8; ++i)
+        for (int i = 0; i < 8; ++i) {
 #pragma unroll
             for (int j = 0; j < 4; ++j)
                 acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+            const int row = wm * 128 + i * 16 + r16;
+            na[i] = *reinterpret_cast<const bf16x8_t *>(st + row * 64 + 16 * gemm_slot(row, kg));
+            if (i < 4) {
+                const int rb = BM + wn * 64 + i * 16 + r16;
+                nb[i] = *reinterpret_cast<const bf16x8_t *>(st + rb * 64 + 16 * gemm_slot(rb, kg));
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    };
+#pragma unroll
+    for (int s0 = 0; s0 < kStages; ++s0)
+        gemm_issue_stage(q, ck, m0, n0, B, G, d, min(s0, nk - 1) * BK, lds + s0 * kStageBytes);
+    wait_vmcnt<(kStages - 1) * kLoadsPerWave>();          // stage 0 has landed for this wave
+    __builtin_amdgcn_s_barrier();
+    bf16x8_t a0[8], b0[4], a1[8], b1[4];
+    read_frags(0, a0, b0);
+    int ks = 0;
+    for (; ks + 2 <= nk; ks += 2) {
+        stage(ks, a0, b0, a1, b1);
+        stage(ks + 1, a1, b1, a0, b0);
     }
-
+    if (ks < nk) stage(ks, a0, b0, a1, b1);
     // D[m][n]: this lane holds rows 4*kg + e of each 16x16 tile, column r16.
 #pragma unroll
     for (int i = 0; i < 8; ++i)

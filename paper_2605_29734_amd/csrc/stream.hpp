@@ -278,17 +278,30 @@ __device__ __forceinline__ void owner_epilogue(const FineArgs &a, const FineSmem
     const float *trow = tile + kWave + nn * kTileRow + rg * QP;
     const int32_t *tids = reinterpret_cast<const int32_t *>(tile) + rg * QP;
     const int64_t valid = active ? r1 - base - rg * QP : 0;   // of this lane's rows, those that exist
+    f32x4_t s4[QP / 4];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int i4 = 0; i4 < QP; i4 += 4) {
+        s4[i4 / 4] = *reinterpret_cast<const f32x4_t *>(trow + i4);
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            if (i4 + e < valid) mx = fmaxf(mx, s4[i4 / 4][e]);
+    }
+    // Past a buffer's first steps few rows beat its threshold: a lane whose
+    // best score is below the threshold's score has no candidate (keys order
+    // by score first), and a wave with no such lane is done with the step.
+    if (!__ballot(mx != -INFINITY && ord_of(mx) >= (uint32_t)(o.theta >> 32))) return;
     uint64_t key[QP];
     int mine = 0;
 #pragma unroll
     for (int i4 = 0; i4 < QP; i4 += 4) {
-        const f32x4_t s4 = *reinterpret_cast<const f32x4_t *>(trow + i4);
         const int4 t4 = *reinterpret_cast<const int4 *>(tids + i4);
         const int32_t tv[4] = {t4.x, t4.y, t4.z, t4.w};
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             const int i = i4 + e;
-            const uint64_t kk = ((uint64_t)ord_of(s4[e]) << 32) | (uint64_t)(~(uint32_t)tv[e]);
+            const uint64_t kk =
+                ((uint64_t)ord_of(s4[i4 / 4][e]) << 32) | (uint64_t)(~(uint32_t)tv[e]);
             key[i] = i < valid ? kk : 0;
             mine += key[i] > o.theta;
         }
