@@ -70,43 +70,63 @@ struct PlanArgs {
     int32_t group;            // chunk partials per level-one merge group
 };
 
+// One DPP move of a 64-bit value (both halves with the same control); lanes
+// outside row_mask, or reading outside their row, get 0.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ int64_t dpp64(int64_t x) {
+    const int lo = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)x, CTRL, ROW_MASK, 0xF, true);
+    const int hi = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)((uint64_t)x >> 32), CTRL, ROW_MASK,
+                                               0xF, true);
+    return (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
+}
+
+// Inclusive prefix sum within each 16-lane row (row_shr 1, 2, 4, 8).
+__device__ __forceinline__ int64_t row_scan64(int64_t x) {
+    x += dpp64<0x111, 0xF>(x);
+    x += dpp64<0x112, 0xF>(x);
+    x += dpp64<0x114, 0xF>(x);
+    x += dpp64<0x118, 0xF>(x);
+    return x;
+}
+
+// Inclusive prefix sum over the wave: rows, then row_bcast:15 into rows 1
+// and 3 and row_bcast:31 into rows 2 and 3.
+__device__ __forceinline__ int64_t wave_scan64(int64_t x) {
+    x = row_scan64(x);
+    x += dpp64<0x142, 0xA>(x);
+    x += dpp64<0x143, 0xC>(x);
+    return x;
+}
+
 // Exclusive scan and total of N values per thread over the 1024-thread block,
-// in two barriers: each wave scans with shuffles, one lane per value scans the
-// wave totals. s: LDS of at least 16 * N int64. v becomes the exclusive prefix.
+// in two barriers: each wave scans with DPP, then the 16 wave totals of each
+// value are scanned by one 16-lane row. s: LDS of at least 17 * N int64. v
+// becomes the exclusive prefix.
 template <int N>
 __device__ void block_scan_n(int64_t (&v)[N], int64_t (&total)[N], int64_t *s) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     constexpr int waves = kPlanThreads / kWave;
+    static_assert(waves == 16, "the wave totals are scanned by one 16-lane row per value");
     int64_t x[N];
 #pragma unroll
-    for (int i = 0; i < N; ++i) x[i] = v[i];
-#pragma unroll
-    for (int o = 1; o < kWave; o <<= 1) {
-#pragma unroll
-        for (int i = 0; i < N; ++i) {
-            const int64_t y = __shfl_up(x[i], o);
-            if (lane >= o) x[i] += y;
-        }
-    }
+    for (int i = 0; i < N; ++i) x[i] = wave_scan64(v[i]);
     if (lane == kWave - 1) {
 #pragma unroll
         for (int i = 0; i < N; ++i) s[wave * N + i] = x[i];
     }
     __syncthreads();
-    if (threadIdx.x < N) {          // one thread per value: prefix over the waves, in place
-        int64_t run = 0;
-        for (int w = 0; w < waves; ++w) {
-            const int64_t c = s[w * N + threadIdx.x];
-            s[w * N + threadIdx.x] = run;
-            run += c;
-        }
-        s[waves * N + threadIdx.x] = run;
+    if (threadIdx.x < waves * N) {  // row = one value, lane in row = one wave
+        const int vi = threadIdx.x >> 4, w = threadIdx.x & 15;
+        const int64_t c = s[w * N + vi];
+        const int64_t incl = row_scan64(c);
+        s[waves * N + w * N + vi] = incl - c;
+        if (w == waves - 1) s[2 * waves * N + vi] = incl;
     }
     __syncthreads();
 #pragma unroll
     for (int i = 0; i < N; ++i) {
-        v[i] = s[wave * N + i] + x[i] - v[i];
-        total[i] = s[waves * N + i];
+        v[i] = s[waves * N + wave * N + i] + x[i] - v[i];
+        total[i] = s[2 * waves * N + i];
     }
     __syncthreads();
 }
@@ -179,24 +199,41 @@ __device__ int64_t plan_chunks(const PlanArgs &pa, CntOf cnt_of, const int64_t *
     const int32_t per = (G + kPlanThreads - 1) / kPlanThreads;
     const int32_t g0 = min((int32_t)G, t * per), g1 = min((int32_t)G, g0 + per);
     const int lmin = 63 - __builtin_clzll((unsigned long long)pa.chunk_min);   // chunk_min is a power of two
-    int64_t q[1] = {0}, qtot[1];
-    int64_t p[kChunkCands];
-#pragma unroll
-    for (int i = 0; i < kChunkCands; ++i) p[i] = 0;
-    for (int32_t g = g0; g < g1; ++g) {
-        const int64_t c = cnt_of(g), len = off[g + 1] - off[g];
-        q[0] += c;
-        if (c > 0 && len > 0) {
-#pragma unroll
-            for (int i = 0; i < kChunkCands; ++i)
-                p[i] += c * ((len + (int64_t(1) << (lmin + i)) - 1) >> (lmin + i));
+    // Partials for candidate length chunk_min * 2^i: sum over the thread's
+    // clusters of (queries) x (chunks). They only fall as i grows, so the
+    // first four candidates are tried together (the usual answer) and the
+    // rest by bisection; the last candidate always fits.
+    auto partials = [&](int i) {
+        int64_t p = 0;
+        for (int32_t g = g0; g < g1; ++g) {
+            const int64_t c = cnt_of(g), len = off[g + 1] - off[g];
+            if (c > 0 && len > 0) p += c * ((len + (int64_t(1) << (lmin + i)) - 1) >> (lmin + i));
         }
-    }
+        return p;
+    };
+    int64_t q[1] = {0}, qtot[1];
+    for (int32_t g = g0; g < g1; ++g) q[0] += cnt_of(g);
     block_scan_n<1>(q, qtot, s);
-    block_sum_n<kChunkCands>(p, s);
-    int cand = kChunkCands - 1;
-    for (int i = kChunkCands - 1; i >= 0; --i)
-        if (p[i] <= pa.p_cap) cand = i;
+    constexpr int kFirst = 4;
+    int64_t p4[kFirst];
+#pragma unroll
+    for (int i = 0; i < kFirst; ++i) p4[i] = partials(i);
+    block_sum_n<kFirst>(p4, s);
+    int cand = -1;
+#pragma unroll
+    for (int i = kFirst - 1; i >= 0; --i)
+        if (p4[i] <= pa.p_cap) cand = i;
+    if (cand < 0) {
+        int lo = kFirst, hi = kChunkCands - 1;     // the answer is in [lo, hi]
+        while (lo < hi) {
+            const int mid = (lo + hi) >> 1;
+            int64_t pm[1] = {partials(mid)};
+            block_sum_n<1>(pm, s);
+            if (pm[0] <= pa.p_cap) hi = mid;
+            else lo = mid + 1;
+        }
+        cand = lo;
+    }
     const int lch = lmin + cand;
     const int64_t ch = int64_t(1) << lch;
 
