@@ -10,8 +10,9 @@
 //   stages in flight, rows swizzled so that fragment reads are free of bank
 //   conflicts (d % 32 == 0); tiles ordered so that the blocks of one XCD share
 //   query rows in their L2. fp32 inputs are rounded to bf16 once per call.
-// Too few 256 x 256 tiles to fill the GPU, or d not a multiple of 32: 64 x 64
-//   tiles read directly from global memory in MFMA fragment layout.
+// Too few 256 x 256 tiles to fill the GPU, or d not a multiple of 32: one wave
+//   per 32 x 32 tile, operands read directly from global memory in MFMA
+//   fragment layout, eight k-steps requested at a time.
 // fp32 arithmetic (small configurations): a direct MFMA kernel on
 //   v_mfma_f32_16x16x4f32.
 // The scores go to a [B][G] fp32 workspace; the top-c selection is the
@@ -172,17 +173,44 @@ __global__ __launch_bounds__(kGemmThreads) void coarse_gemm(const __bf16 *__rest
     wait_vmcnt<0>();      // no load may still be writing LDS when the block ends
 }
 
-// Small problems (fewer 256 x 256 tiles than compute units): 64 x 64 block
-// tiles, 4 waves of 32 x 32, operands read directly in MFMA fragment layout.
+// A fragment as loaded (bf16 as is; fp32 rounded to bf16 when used).
 template <typename T>
-__global__ __launch_bounds__(256) void coarse_small_bf16(const T *__restrict__ q,
-                                                         const T *__restrict__ ck, int32_t B,
-                                                         int32_t G, int32_t d,
-                                                         float *__restrict__ S) {
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+struct RawFrag;
+template <>
+struct RawFrag<__bf16> {
+    uint4 v;
+    __device__ __forceinline__ void load(const __bf16 *p) { v = *reinterpret_cast<const uint4 *>(p); }
+    __device__ __forceinline__ bf16x8_t get() const { return __builtin_bit_cast(bf16x8_t, v); }
+};
+template <>
+struct RawFrag<float> {
+    float4 lo, hi;
+    __device__ __forceinline__ void load(const float *p) {
+        lo = reinterpret_cast<const float4 *>(p)[0];
+        hi = reinterpret_cast<const float4 *>(p)[1];
+    }
+    __device__ __forceinline__ bf16x8_t get() const {
+        bf16x8_t r;
+        r[0] = (__bf16)lo.x; r[1] = (__bf16)lo.y; r[2] = (__bf16)lo.z; r[3] = (__bf16)lo.w;
+        r[4] = (__bf16)hi.x; r[5] = (__bf16)hi.y; r[6] = (__bf16)hi.z; r[7] = (__bf16)hi.w;
+        return r;
+    }
+};
+
+// Small problems (fewer 256 x 256 tiles than compute units): one wave per
+// 32 x 32 tile, operands read directly in MFMA fragment layout. A batch of
+// k-steps is requested before any is used (addresses clamped into the row,
+// past-the-end fragments zeroed where they are used), so a batch costs one
+// memory round trip rather than one per k-step.
+template <typename T>
+__global__ __launch_bounds__(kWave) void coarse_small_bf16(const T *__restrict__ q,
+                                                           const T *__restrict__ ck, int32_t B,
+                                                           int32_t G, int32_t d,
+                                                           float *__restrict__ S) {
+    constexpr int kSteps = sizeof(T) == 4 ? 4 : 8;
+    const int lane = threadIdx.x & 63;
     const int r16 = lane & 15, kg = lane >> 4;
-    const int64_t row0 = (int64_t)blockIdx.y * 64 + (wave >> 1) * 32;
-    const int64_t col0 = (int64_t)blockIdx.x * 64 + (wave & 1) * 32;
+    const int64_t row0 = (int64_t)blockIdx.y * 32, col0 = (int64_t)blockIdx.x * 32;
     const T *qp[2], *cp[2];
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
@@ -195,20 +223,35 @@ __global__ __launch_bounds__(256) void coarse_small_bf16(const T *__restrict__ q
     for (int i = 0; i < 2; ++i)
 #pragma unroll
         for (int j = 0; j < 2; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    for (int k0 = 0; k0 < d; k0 += 32) {
-        const int k = k0 + kg * 8;
-        const bool ok = k < d;
-        bf16x8_t a[2], b[2];
+    const int nks = (d + 31) / 32;
+    for (int s0 = 0; s0 < nks; s0 += kSteps) {
+        RawFrag<T> fa[kSteps][2], fb[kSteps][2];
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            a[i] = ok ? load8(qp[i] + k) : zero8();
-            b[i] = ok ? load8(cp[i] + k) : zero8();
+        for (int st = 0; st < kSteps; ++st) {
+            const int k = min(32 * (s0 + st) + 8 * kg, d - 8);
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                fa[st][i].load(qp[i] + k);
+                fb[st][i].load(cp[i] + k);
+            }
         }
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
+        for (int st = 0; st < kSteps; ++st) {
+            // steps past the end multiply zeros: no branch for the compiler to
+            // sink the loads into
+            const bool ok = 32 * (s0 + st) + 8 * kg < d;
+            bf16x8_t a[2], b[2];
 #pragma unroll
-            for (int j = 0; j < 2; ++j)
-                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+            for (int i = 0; i < 2; ++i) {
+                a[i] = ok ? fa[st][i].get() : zero8();
+                b[i] = ok ? fb[st][i].get() : zero8();
+            }
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+        }
     }
 #pragma unroll
     for (int i = 0; i < 2; ++i)
@@ -291,14 +334,14 @@ hipError_t launch_coarse(int32_t key_dtype, int32_t compute_dtype, int32_t d, in
                            B, G, d, w.scores);
         if (ev.after) hipEventRecord(ev.after, s);
     } else if ((int64_t)((B + BM - 1) / BM) * ((G + BN - 1) / BN) < n_cu || d % BK != 0) {
-        const dim3 grid((G + 63) / 64, (B + 63) / 64);
+        const dim3 grid((G + 31) / 32, (B + 31) / 32);
         if (ev.before) hipEventRecord(ev.before, s);
         if (key_dtype == kF32)
-            hipLaunchKernelGGL(coarse_small_bf16<float>, grid, dim3(256), 0, s,
+            hipLaunchKernelGGL(coarse_small_bf16<float>, grid, dim3(kWave), 0, s,
                                static_cast<const float *>(q),
                                static_cast<const float *>(coarse_keys), B, G, d, w.scores);
         else
-            hipLaunchKernelGGL(coarse_small_bf16<__bf16>, grid, dim3(256), 0, s,
+            hipLaunchKernelGGL(coarse_small_bf16<__bf16>, grid, dim3(kWave), 0, s,
                                static_cast<const __bf16 *>(q),
                                static_cast<const __bf16 *>(coarse_keys), B, G, d, w.scores);
         if (ev.after) hipEventRecord(ev.after, s);
