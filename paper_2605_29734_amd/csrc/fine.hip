@@ -29,6 +29,29 @@ constexpr int64_t kChunkFloor = 64;
 constexpr size_t kRouteLdsBytes = 128 * 1024;  // per-cluster tables of the fused routing kernel
 constexpr int64_t kFusedRoutePairs = 16384;     // above this many pairs, route with many blocks
 constexpr int64_t kChunkCeil = 4096;
+constexpr int kMergeWaves = 4;                   // waves per merge block
+constexpr int kMergeBatch = 8;                   // 64-entry groups per merge request
+
+// Chunk partials per level-one merge group for a cluster of nch chunks whose
+// partials hold kp key slots each (k rounded up to a power of two): 0 (no
+// groups) when one merge request reads all of them, else about sqrt(nch),
+// so that the two merge levels read about as many keys each and a long
+// cluster's merge is not a long chain of requests in one wave.
+__host__ __device__ inline int64_t group_span(int64_t nch, int64_t kp) {
+    if (nch * kp <= (int64_t)kMergeBatch * kWave) return 0;
+    int64_t r = 2;
+    while (r * r < nch) r *= 2;                   // power-of-two bracket, then refine
+    int64_t lo = r / 2;
+    while (lo + 1 < r) {
+        const int64_t mid = (lo + r) / 2;
+        if (mid * mid >= nch) r = mid; else lo = mid;
+    }
+    return r < 2 ? 2 : r;
+}
+__host__ __device__ inline int64_t group_count(int64_t nch, int64_t kp) {
+    const int64_t r = group_span(nch, kp);
+    return r ? (nch + r - 1) / r : 0;
+}
 
 // ---------------------------------------------------------------------------
 // routing
@@ -67,7 +90,7 @@ struct PlanArgs {
     int64_t *ubase;           // [G]
     Plan *plan;
     int64_t chunk_min, p_cap;
-    int32_t group;            // chunk partials per level-one merge group
+    int32_t kp;               // key slots per partial (k rounded up to a power of two)
 };
 
 // One DPP move of a 64-bit value (both halves with the same control); lanes
@@ -243,7 +266,7 @@ __device__ int64_t plan_chunks(const PlanArgs &pa, CntOf cnt_of, const int64_t *
     // short ones fill the end. Bucket b holds lengths in [ch >> (b+1), ch >> b)
     // (the last one everything shorter). Counts that fit 32 bits are scanned
     // two per 64-bit value: (full items, level-one groups), bucket pairs.
-    const int64_t R = pa.group;
+    const int64_t kp = pa.kp;
     constexpr int NW = 4 + kLenBuckets / 2;
     int64_t w[NW], wt[NW];   // items | groups << 32, partials, level-one, merge list, buckets
 #pragma unroll
@@ -252,7 +275,7 @@ __device__ int64_t plan_chunks(const PlanArgs &pa, CntOf cnt_of, const int64_t *
         const int64_t c = cnt_of(g), len = off[g + 1] - off[g];
         const int64_t nch = (c > 0 && len > 0) ? (len + ch - 1) >> lch : 0;
         const int64_t nfull = c > 0 ? len >> lch : 0;
-        const int64_t ng = nch > R ? (nch + R - 1) / R : 0;
+        const int64_t ng = group_count(nch, kp);
         w[0] += nfull + (ng << 32);
         w[1] += nch * c;
         w[2] += ng * c;
@@ -282,7 +305,7 @@ __device__ int64_t plan_chunks(const PlanArgs &pa, CntOf cnt_of, const int64_t *
         const int64_t c = cnt_of(g), len = off[g + 1] - off[g];
         const int64_t nch = (c > 0 && len > 0) ? (len + ch - 1) >> lch : 0;
         const int64_t nfull = c > 0 ? len >> lch : 0;
-        const int64_t ng = nch > R ? (nch + R - 1) / R : 0;
+        const int64_t ng = group_count(nch, kp);
         int32_t wl = -1;
         if (nch > nfull) {
             const int b = len_bucket(len - (nfull << lch), lch);
@@ -371,6 +394,32 @@ size_t route_fused_lds(int32_t G, int64_t n) {
     return (size_t)(3 * G + 1) * 8 + (size_t)(6 * G + 4) * 4 + (size_t)n * 2;
 }
 
+// The merge's description of pair e, position i in the list of its cluster
+// (nch chunks in level-one groups of r, none if r is 0; nq queries; partials
+// from pb, level-one results from ub).
+__device__ __forceinline__ MergeSlot merge_slot(int64_t e, int32_t i, int64_t nch, int64_t r,
+                                                int32_t nq, int64_t pb, int64_t ub) {
+    MergeSlot ms;
+    ms.e = (int32_t)e;
+    ms.stride = nq;
+    ms.level = r > 0;
+    ms.n = (int32_t)(r > 0 ? (nch + r - 1) / r : nch);
+    ms.p0 = (r > 0 ? ub : pb) + i;
+    return ms;
+}
+
+// Level-one group jg of a cluster (nch chunks, groups of r, nq queries,
+// partials from pb, results from ub).
+__device__ __forceinline__ MergeGroup merge_group_of(int32_t jg, int64_t nch, int64_t r,
+                                                     int32_t nq, int64_t pb, int64_t ub) {
+    MergeGroup mg;
+    mg.p0 = pb + jg * r * nq;
+    mg.u0 = ub + (int64_t)jg * nq;
+    mg.npart = (int32_t)(nch - jg * r < r ? nch - jg * r : r);
+    mg.nq = nq;
+    return mg;
+}
+
 // Position in the item table of the w-th full-length chunk (cluster by
 // cluster) among n_full: a fixed permutation (multiplication by a prime above
 // any item count, modulo n_full) that spreads each cluster's chunks over the
@@ -410,7 +459,7 @@ __global__ __launch_bounds__(kPlanThreads) void route_fused(PlanArgs pa, const i
                                                             int64_t n, int32_t *qlist,
                                                             int32_t *pos, uint64_t *bound, SlotOut out,
                                                             WorkItem *items, MergeGroup *groups,
-                                                            int2 *units, int32_t *mlist) {
+                                                            int2 *units, MergeSlot *mlist) {
     extern __shared__ int64_t lds[];
     __shared__ int64_t s[(kPlanThreads / kWave + 1) * kChunkCands];
     __shared__ int32_t s_bad;
@@ -461,7 +510,7 @@ __global__ __launch_bounds__(kPlanThreads) void route_fused(PlanArgs pa, const i
         pa.plan->bad_sel = s_bad;
     }
     __syncthreads();
-    const int64_t R = pa.group;
+    const int64_t kp = pa.kp;
     const int32_t *lwst = m.wstart;
     for (int64_t e = t; e < n; e += kPlanThreads) {
         const uint16_t h = lsel[e];
@@ -475,8 +524,11 @@ __global__ __launch_bounds__(kPlanThreads) void route_fused(PlanArgs pa, const i
             pos[e] = i;
             const int64_t len = loff[g + 1] - loff[g];
             const int64_t nch = (len + ch - 1) >> lch;
-            if (nch != 1) mlist[m.mstart[g] + i] = (int32_t)e;
-            if (nch > R) {                 // this pair's level-one units, one per group
+            const int64_t r = group_span(nch, kp);
+            if (nch != 1)
+                mlist[m.mstart[g] + i] =
+                    merge_slot(e, i, nch, r, m.qoff[g + 1] - qb, lpb[g], lub[g]);
+            if (r > 0) {                   // this pair's level-one units, one per group
                 const int32_t nq = m.qoff[g + 1] - qb, gs = m.gstart[g];
                 const int32_t ng = m.gstart[g + 1] - gs;
                 const int64_t ub = lub[g];
@@ -510,15 +562,9 @@ __global__ __launch_bounds__(kPlanThreads) void route_fused(PlanArgs pa, const i
         if (ng == 0) continue;
         const int32_t nq = m.qoff[g + 1] - m.qoff[g];
         const int64_t nch = (loff[g + 1] - loff[g] + ch - 1) >> lch;
-        const int64_t pb = lpb[g], ub = lub[g];
-        for (int32_t jg = 0; jg < ng; ++jg) {
-            MergeGroup mg;
-            mg.p0 = pb + jg * R * nq;
-            mg.u0 = ub + (int64_t)jg * nq;
-            mg.npart = (int32_t)(nch - jg * R < R ? nch - jg * R : R);
-            mg.nq = nq;
-            groups[gs + jg] = mg;
-        }
+        const int64_t r = group_span(nch, kp);
+        for (int32_t jg = 0; jg < ng; ++jg)
+            groups[gs + jg] = merge_group_of(jg, nch, r, nq, lpb[g], lub[g]);
     }
 }
 
@@ -528,20 +574,23 @@ __global__ __launch_bounds__(kPlanThreads) void route_fused(PlanArgs pa, const i
 // one wave per cluster, spread over the lanes.
 __global__ __launch_bounds__(256) void route_items(PlanArgs pa, const int32_t *qlist,
                                                    WorkItem *items, MergeGroup *groups,
-                                                   int2 *units, int32_t *mlist) {
+                                                   int2 *units, MergeSlot *mlist) {
     const int lane = threadIdx.x & 63;
     const int64_t ch = pa.plan->chunk;
     const int lch = 63 - __builtin_clzll((unsigned long long)ch);
-    const int64_t R = pa.group;
+    const int64_t kp = pa.kp;
     for (int64_t g = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); g < pa.G;
          g += (int64_t)gridDim.x * 4) {
         const int32_t qb = pa.qoff[g], nq = pa.qoff[g + 1] - qb;
         if (nq == 0) continue;
         const int64_t a = pa.off[g], len = pa.off[g + 1] - a;
         const int64_t nch = (len + ch - 1) >> lch;
+        const int64_t r = group_span(nch, kp);
         if (nch != 1) {
             const int32_t m0 = pa.mstart[g];
-            for (int32_t i = lane; i < nq; i += kWave) mlist[m0 + i] = qlist[qb + i];
+            const int64_t pb = pa.pbase[g], ub = pa.ubase[g];
+            for (int32_t i = lane; i < nq; i += kWave)
+                mlist[m0 + i] = merge_slot(qlist[qb + i], i, nch, r, nq, pb, ub);
         }
         if (nch == 0) continue;
         const int32_t w0 = pa.wstart[g], wl = pa.wlast[g];
@@ -552,14 +601,8 @@ __global__ __launch_bounds__(256) void route_items(PlanArgs pa, const int32_t *q
         for (int64_t j = lane; j < nch; j += kWave)
             items[j < nfull ? full_slot(w0 + (int32_t)j, n_full) : wl] =
                 make_item((int32_t)g, j, a, len, lch, qb, nq, pb);
-        for (int32_t jg = lane; jg < ng; jg += kWave) {
-            MergeGroup mg;
-            mg.p0 = pb + jg * R * nq;
-            mg.u0 = ub + (int64_t)jg * nq;
-            mg.npart = (int32_t)(nch - jg * R < R ? nch - jg * R : R);
-            mg.nq = nq;
-            groups[gs + jg] = mg;
-        }
+        for (int32_t jg = lane; jg < ng; jg += kWave)
+            groups[gs + jg] = merge_group_of(jg, nch, r, nq, pb, ub);
         for (int64_t x = lane; x < (int64_t)ng * nq; x += kWave) {
             const int32_t jg = (int32_t)(x / nq), i = (int32_t)(x - (int64_t)jg * nq);
             units[ub + x] = make_int2(gs + jg, i);
@@ -593,10 +636,8 @@ __global__ void route_scatter(const int32_t *sel, int64_t n, int32_t G, const in
 // wave has to read more than `group` partials; the pair then merges its
 // level-one results.
 struct MergeArgs {
-    const int32_t *sel;
-    const int64_t *off;
-    const int32_t *qoff, *pos, *mlist;
-    const int64_t *pbase, *ubase;
+    const MergeSlot *mlist;
+    const uint64_t *bound;            // per pair: a key at most its k-th best (from the stream)
     const Plan *plan;
     const MergeGroup *groups;
     const int2 *units;
@@ -607,14 +648,26 @@ struct MergeArgs {
     int32_t *uc;
     uint64_t *uk;
     int64_t n_pairs;
-    int32_t G, k, group;
+    int32_t k;
     float cexp;
     float *slot_max, *slot_sum, *cand_score;
     int32_t *cand_id;
 };
 
-constexpr int kMergeWaves = 4;
-constexpr int kMergeBatch = 8;
+
+// compact_select out of line for the merge loop (one copy; the loop body
+// stays small).
+struct MergeCompacted {
+    int n;
+    uint64_t theta;
+};
+template <int NPL>
+__device__ __noinline__ MergeCompacted merge_compact(uint64_t *buf, int n, int k) {
+    MergeCompacted r;
+    r.theta = 0;
+    r.n = compact_select<NPL>(buf, n, k, kWave, threadIdx.x & 63, r.theta);
+    return r;
+}
 
 // One wave merges n partial results (m, Z, count, k keys) found at
 // p0 + i * stride: (m, Z) lane-parallel; the keys 8 x 64 at a time through a
@@ -625,10 +678,29 @@ template <int NPL>
 __device__ __forceinline__ int merge_partials(const float *pm, const float *pz, const int32_t *pc,
                                               const uint64_t *pk, int64_t p0, int64_t stride,
                                               int64_t n, int k, float cexp, uint64_t *buf,
-                                              float &M, float &Z) {
+                                              float &M, float &Z, uint64_t theta0 = 0) {
     constexpr int cap = NPL * kWave;
     const int lane = threadIdx.x & 63;
     const uint64_t lt_mask = (1ull << lane) - 1;
+    // entries f = j * kp + r with kp = k rounded up to a power of two: the
+    // partial and the key within it come from a shift and a mask
+    const int lk = 31 - __builtin_clz((unsigned)(2 * k - 1));
+    const int64_t kp = int64_t(1) << lk;
+    const int64_t total = n * kp;
+    // a batch of 8 x 64 entries, requested unconditionally (entries past the
+    // end read the workspace's first key and are dropped where they are used;
+    // p0 itself may lie past the partials when n is 0)
+    auto request = [&](int64_t base, uint64_t (&kv)[kMergeBatch]) {
+#pragma unroll
+        for (int u = 0; u < kMergeBatch; ++u) {
+            const int64_t f = base + u * kWave + lane;
+            const int64_t jj = f >> lk, r = f & (kp - 1);
+            const bool ok = f < total && r < k;
+            kv[u] = pk[ok ? (p0 + jj * stride) * k + r : 0];
+        }
+    };
+    uint64_t cur[kMergeBatch], nxt[kMergeBatch];
+    request(0, cur);                       // in flight with the statistics
     M = -INFINITY;
     Z = 0.0f;
     for (int64_t jj = lane; jj < n; jj += kWave)
@@ -638,34 +710,26 @@ __device__ __forceinline__ int merge_partials(const float *pm, const float *pz, 
         mz_merge(M, Z, m2, z2, cexp);
     }
     int cnt = 0;
-    uint64_t theta = 0;
-    // entries f = j * kp + r with kp = k rounded up to a power of two: the
-    // partial and the key within it come from a shift and a mask
-    const int lk = 31 - __builtin_clz((unsigned)(2 * k - 1));
-    const int64_t kp = int64_t(1) << lk;
-    const int64_t total = n * kp;
+    uint64_t theta = theta0;
     for (int64_t base = 0; base < total; base += kWave * kMergeBatch) {
-        uint64_t key[kMergeBatch];
+        request(base + kWave * kMergeBatch, nxt);   // the next batch while this one is filtered
 #pragma unroll
         for (int u = 0; u < kMergeBatch; ++u) {
             const int64_t f = base + u * kWave + lane;
-            const int64_t jj = f >> lk, r = f & (kp - 1);
-            const bool ok = f < total && r < k;
-            const int64_t src = ok ? (p0 + jj * stride) * k + r : p0 * k;
-            const uint64_t kv = pk[src];
-            key[u] = ok ? kv : 0;
-        }
-#pragma unroll
-        for (int u = 0; u < kMergeBatch; ++u) {
-            const bool pass = key[u] > theta;
+            const uint64_t key = f < total && (f & (kp - 1)) < k ? cur[u] : 0;
+            const bool pass = key > theta;
             const uint64_t mask = __ballot(pass);
-            if (pass) buf[cnt + __popcll(mask & lt_mask)] = key[u];
+            if (pass) buf[cnt + __popcll(mask & lt_mask)] = key;
             cnt += __popcll(mask);
             if (cnt > cap - kWave) {
                 wave_lds_sync();
-                cnt = compact_select<NPL>(buf, cnt, k, kWave, lane, theta);
+                const MergeCompacted mc = merge_compact<NPL>(buf, cnt, k);
+                cnt = mc.n;
+                theta = mc.theta > theta ? mc.theta : theta;
             }
         }
+#pragma unroll
+        for (int u = 0; u < kMergeBatch; ++u) cur[u] = nxt[u];
     }
     (void)pc;
     wave_lds_sync();
@@ -714,20 +778,20 @@ __global__ __launch_bounds__(kWave * kMergeWaves) void slot_merge(MergeArgs a) {
     const int64_t n_merge = a.plan->n_merge;
     for (int64_t u = (int64_t)blockIdx.x * kMergeWaves + wave; u < n_merge;
          u += (int64_t)gridDim.x * kMergeWaves) {
-        const int64_t e = a.mlist[u];
-        const int32_t g = a.sel[e];
-        const int64_t len = a.off[g + 1] - a.off[g];
-        const int64_t CH = a.plan->chunk;
-        const int64_t nch = (len + CH - 1) / CH;
-        const int64_t nq = a.qoff[g + 1] - a.qoff[g];
+        const MergeSlot ms = a.mlist[u];
+        const int64_t e = ms.e;
+        // keys below the pair's bound cannot be in its top k; the bound itself
+        // can (it may be the k-th key), hence one below it
+        const uint64_t b = a.bound[e];
+        const uint64_t theta0 = b ? b - 1 : 0;
         float M, Z;
         int cnt;
-        if (nch > a.group)
-            cnt = merge_partials<NPL>(a.um, a.uz, a.uc, a.uk, a.ubase[g] + a.pos[e], nq,
-                                      (nch + a.group - 1) / a.group, a.k, a.cexp, buf, M, Z);
+        if (ms.level)
+            cnt = merge_partials<NPL>(a.um, a.uz, a.uc, a.uk, ms.p0, ms.stride, ms.n, a.k, a.cexp,
+                                      buf, M, Z, theta0);
         else
-            cnt = merge_partials<NPL>(a.pm, a.pz, a.pc, a.pk, a.pbase[g] + a.pos[e], nq, nch, a.k,
-                                      a.cexp, buf, M, Z);
+            cnt = merge_partials<NPL>(a.pm, a.pz, a.pc, a.pk, ms.p0, ms.stride, ms.n, a.k, a.cexp,
+                                      buf, M, Z, theta0);
         uint64_t v[NPL];
 #pragma unroll
         for (int q = 0; q < NPL; ++q) v[q] = (q * kWave + lane < cnt) ? buf[q * kWave + lane] : 0;
@@ -797,13 +861,6 @@ static size_t lds_budget() {
     return (size_t)bytes;
 }
 
-// Chunk partials per level-one merge group: about 4096 keys per wave.
-static int merge_group(int k) {
-    int r = 8;
-    while (r * 2 * k <= 4096 && r < 256) r *= 2;
-    return r;
-}
-
 AttendWs attend_layout(void *ws, int32_t d, int32_t G, int64_t N, int32_t key_bytes, int32_t B,
                        int32_t c, int32_t k, size_t *bytes) {
     (void)d;
@@ -813,9 +870,11 @@ AttendWs attend_layout(void *ws, int32_t d, int32_t G, int64_t N, int32_t key_by
     const int64_t bc = (int64_t)B * c;
     w.p_cap = 4 * bc;
     w.w_max = N / kChunkFloor + G + 1;
-    w.group = merge_group(k);
-    w.g_max = 2 * w.w_max / w.group + 1;
-    w.u_cap = 2 * w.p_cap / w.group + 1;
+    // a cluster of nch chunks forms at most nch / 2 + 1 level-one groups
+    // (groups of at least two partials, only when nch >= 2)
+    w.kp = next_pow2(k);
+    w.g_max = w.w_max / 2 + G + 1;
+    w.u_cap = w.p_cap / 2 + bc;
     w.cnt = cv.take<int32_t>(G);
     w.cursor = cv.take<int32_t>(G);
     w.qoff = cv.take<int32_t>(G + 1);
@@ -825,7 +884,7 @@ AttendWs attend_layout(void *ws, int32_t d, int32_t G, int64_t N, int32_t key_by
     w.pbase = cv.take<int64_t>(G);
     w.ubase = cv.take<int64_t>(G);
     w.mstart = cv.take<int32_t>(G + 1);
-    w.mlist = cv.take<int32_t>(bc);
+    w.mlist = cv.take<MergeSlot>(bc);
     w.units = cv.take<int2>(w.u_cap);
     w.qlist = cv.take<int32_t>(bc);
     w.pos = cv.take<int32_t>(bc);
@@ -931,7 +990,7 @@ hipError_t launch_attend(int32_t key_dtype, int32_t compute_dtype, int32_t d, in
     pa.plan = w.plan;
     pa.chunk_min = chunk_floor_rows(N, n_cu);
     pa.p_cap = w.p_cap;
-    pa.group = w.group;
+    pa.kp = w.kp;
     const SlotOut so{slot_max, slot_sum, cand_score, cand_id, k};
     const size_t route_lds = route_fused_lds(G, bc);
     static_assert((3 * (size_t)kNoCluster + 1) * 8 > kRouteLdsBytes, "fused routing keeps cluster ids in 16 bits");
@@ -982,16 +1041,11 @@ hipError_t launch_attend(int32_t key_dtype, int32_t compute_dtype, int32_t d, in
     if (err != hipSuccess) return err;
 
     MergeArgs ma{};
-    ma.sel = sel;
-    ma.off = seg_offsets;
-    ma.qoff = w.qoff;
-    ma.pos = w.pos;
-    ma.pbase = w.pbase;
-    ma.ubase = w.ubase;
     ma.plan = w.plan;
     ma.groups = w.groups;
     ma.units = w.units;
     ma.mlist = w.mlist;
+    ma.bound = w.bound;
     ma.pm = w.pm;
     ma.pz = w.pz;
     ma.pc = w.pc;
@@ -1001,9 +1055,7 @@ hipError_t launch_attend(int32_t key_dtype, int32_t compute_dtype, int32_t d, in
     ma.uc = w.uc;
     ma.uk = w.uk;
     ma.n_pairs = bc;
-    ma.G = G;
     ma.k = k;
-    ma.group = w.group;
     ma.cexp = cexp;
     ma.slot_max = slot_max;
     ma.slot_sum = slot_sum;

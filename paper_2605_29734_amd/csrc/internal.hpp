@@ -50,6 +50,17 @@ struct MergeGroup {
     int32_t nq;        // queries of the cluster
 };
 
+// One (query, slot) pair the merge finishes (its cluster has more chunks than
+// one, or none): n partial results at p0 + j * stride, from the chunk
+// partials or, for clusters with level-one groups, from the group results.
+struct MergeSlot {
+    int64_t p0;
+    int32_t e;         // pair index (query * c + slot)
+    int32_t n;         // partial results to merge
+    int32_t stride;    // queries of the cluster
+    int32_t level;     // 1: the partials are level-one group results
+};
+
 // Carves a workspace into 256-byte aligned pieces; with base == nullptr it
 // only measures.
 struct Carve {
@@ -101,7 +112,7 @@ struct AttendWs {
     int64_t *pbase;    // [G]   first partial of each cluster
     int64_t *ubase;    // [G]   first level-one merge result of each cluster
     int32_t *mstart;   // [G+1] first entry of each cluster in mlist
-    int32_t *mlist;    // [B*c] pairs to merge (their cluster has several chunks)
+    MergeSlot *mlist;  // [B*c] pairs to merge (their cluster has several chunks, or none)
     int2 *units;       // [u_cap] level-one work: (group, query position)
     int32_t *qlist;    // [B*c] (query, slot) entries grouped by cluster
     int32_t *pos;      // [B*c] position of each entry inside its cluster's list
@@ -120,7 +131,7 @@ struct AttendWs {
     int64_t w_max;     // bound on work items
     int64_t g_max;     // bound on level-one groups
     int64_t u_cap;     // bound on level-one results
-    int32_t group;     // chunk partials per level-one group
+    int32_t kp;        // key slots per partial (k rounded up to a power of two)
 };
 AttendWs attend_layout(void *ws, int32_t d, int32_t G, int64_t N, int32_t key_bytes, int32_t B,
                        int32_t c, int32_t k, size_t *bytes);
