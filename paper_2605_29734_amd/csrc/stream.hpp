@@ -41,6 +41,11 @@ constexpr int kFineThreads = 256;      // 4 waves
 constexpr int kFineWaves = kFineThreads / kWave;
 constexpr int kRowsPerWave = 16;       // one MFMA tile of key rows per wave per step
 constexpr int kRowsPerStep = kRowsPerWave * kFineWaves;   // rows per block per step
+
+// The wave's index among the four waves of its role: the block's waves in
+// the four-wave kernels; in the producer/consumer kernel each role has four
+// (waves 0-3 stream keys, waves 4-7 keep the top-k buffers).
+__device__ __forceinline__ int fine_wave() { return (threadIdx.x >> 6) & (kFineWaves - 1); }
 constexpr int kMaxQueryTiles = 4;      // at most 64 queries per pass over a chunk
 constexpr int kRing = 3;               // key load units in the LDS kernel's prefetch ring
 
@@ -102,6 +107,7 @@ struct StreamLaunch {
     int64_t max_grid;             // no more blocks than work items
     size_t smem;
     int32_t qs_bytes;
+    bool producer_consumer;       // eight-wave producer/consumer blocks (bf16 keys, one block per CU)
     KernelEvents ev;
     hipStream_t stream;
 };
@@ -196,7 +202,7 @@ __device__ __forceinline__ void stats_update(Stats<NQT> &st, const f32x4_t (&acc
 // Per-pass set-up: the (query, slot) pairs of the pass and their query rows.
 __device__ __forceinline__ void pass_begin(const FineArgs &a, const FineSmem &sm, int32_t qbeg,
                                            int32_t qg0, int32_t nqg, bool single) {
-    for (int n = threadIdx.x; n < nqg; n += kFineThreads) {
+    for (int n = threadIdx.x; n < nqg; n += blockDim.x) {
         const int32_t e = a.qlist[qbeg + qg0 + n];
         sm.qpair[n] = e;
         sm.qrow[n] = e / a.c;
@@ -212,7 +218,7 @@ __device__ __forceinline__ void pass_begin(const FineArgs &a, const FineSmem &sm
 template <int NQT>
 __device__ __forceinline__ void owned_begin(const FineSmem &sm, int nqg, OwnedLane &o) {
     constexpr int RG = OwnerMap<NQT>::RG;
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, jq = lane / RG;
+    const int lane = threadIdx.x & 63, wave = fine_wave(), jq = lane / RG;
     const int qw = (nqg + kFineWaves - 1) / kFineWaves;
     const int n = wave * qw + jq;
     o.cnt = 0;
@@ -225,7 +231,7 @@ __device__ __forceinline__ void owned_begin(const FineSmem &sm, int nqg, OwnedLa
 template <int NQT>
 __device__ __forceinline__ void tile_write(float *tile, const f32x4_t (&acc)[NQT], int32_t tid) {
     constexpr int ROW = kTileRow;
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, r16 = lane & 15, kg = lane >> 4;
+    const int lane = threadIdx.x & 63, wave = fine_wave(), r16 = lane & 15, kg = lane >> 4;
 #pragma unroll
     for (int qt = 0; qt < NQT; ++qt)
         *reinterpret_cast<f32x4_t *>(tile + kWave + (qt * 16 + r16) * ROW + wave * kRowsPerWave +
@@ -269,7 +275,7 @@ __device__ __forceinline__ void owner_epilogue(const FineArgs &a, const FineSmem
                                                const float *tile, int64_t base, int64_t r1,
                                                int nqg, OwnedLane &o) {
     constexpr int QP = OwnerMap<NQT>::QP, RG = OwnerMap<NQT>::RG;
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63, wave = fine_wave();
     const int jq = lane / RG, rg = lane % RG;
     const int qw = (nqg + kFineWaves - 1) / kFineWaves;
     const int n = wave * qw + jq;
@@ -351,12 +357,28 @@ __device__ __forceinline__ void step_end(const FineArgs &a, const FineSmem &sm,
                                          const f32x4_t (&acc)[NQT], int step, int64_t base,
                                          int64_t r1, int nqg, int32_t tid, OwnedLane &o,
                                          Stats<NQT> &st) {
-    stats_update<NQT>(st, acc, base + (threadIdx.x >> 6) * kRowsPerWave, r1, a.cexp);
+    stats_update<NQT>(st, acc, base + fine_wave() * kRowsPerWave, r1, a.cexp);
     float *tile = sm.st + (size_t)(a.ntile == 2 ? step & 1 : 0) * fine_tile_floats(a.qmax);
     if (a.ntile == 1) __syncthreads();      // the previous step's reads are done
     tile_write<NQT>(tile, acc, tid);
     __syncthreads();
     owner_epilogue<NQT, NPL>(a, sm, tile, base, r1, nqg, o);
+}
+
+// A producer wave's share of a step's end in the producer/consumer kernel:
+// statistics, then the scores into the tile for the consumer waves (after the
+// consumers are done with the tile when only one fits). The consumers make
+// the same barriers in the same order, once per step.
+template <int NQT>
+__device__ __forceinline__ void producer_step_end(const FineArgs &a, const FineSmem &sm,
+                                                  const f32x4_t (&acc)[NQT], int step,
+                                                  int64_t base, int64_t r1, int32_t tid,
+                                                  Stats<NQT> &st) {
+    stats_update<NQT>(st, acc, base + fine_wave() * kRowsPerWave, r1, a.cexp);
+    float *tile = sm.st + (size_t)(a.ntile == 2 ? step & 1 : 0) * fine_tile_floats(a.qmax);
+    if (a.ntile == 1) __syncthreads();      // the consumers are done with the previous step
+    tile_write<NQT>(tile, acc, tid);
+    __syncthreads();
 }
 
 // Caller id of row base + lane of a step (rows past the chunk clamped). The
@@ -380,16 +402,19 @@ __device__ __forceinline__ int32_t tid_value(int32_t loaded, bool identity, int6
 // chunk's best k keys unsorted and zero-padded, and (max, sum). The lanes'
 // statistics are merged within each group and handed over through LDS with
 // the counts, then the buffers are written out query by query.
-template <int NQT, int NPL>
+// PC: producer/consumer block (waves 0-3 hold the statistics, waves 4-7 the
+// buffers); otherwise every wave holds both.
+template <int NQT, int NPL, bool PC = false>
 __device__ __forceinline__ void pass_end(const FineArgs &a, const FineSmem &sm, int64_t p0,
                                          int32_t qbeg, bool single, int32_t qg0, int32_t nqg,
                                          OwnedLane &o, Stats<NQT> &st) {
     constexpr int RG = OwnerMap<NQT>::RG;
-    const int t = threadIdx.x, lane = t & 63, wave = t >> 6, r16 = lane & 15, kg = lane >> 4;
+    const int t = threadIdx.x, lane = t & 63, wave = fine_wave(), r16 = lane & 15, kg = lane >> 4;
+    const bool stats_here = !PC || t < kFineThreads, buffers_here = !PC || t >= kFineThreads;
     const int jq = lane / RG, rg = lane % RG;
     const int qw = (nqg + kFineWaves - 1) / kFineWaves;
     const int n = wave * qw + jq;
-    if (jq < qw && n < nqg && rg == 0) {
+    if (buffers_here && jq < qw && n < nqg && rg == 0) {
         sm.ocnt[n] = o.cnt;
         sm.otheta[n] = o.theta;
     }
@@ -403,13 +428,13 @@ __device__ __forceinline__ void pass_end(const FineArgs &a, const FineSmem &sm, 
             mz_merge(st.m[qt], st.z[qt], m2, z2, a.cexp);
         }
         const int q = qt * 16 + r16;
-        if (kg == 0 && q < nqg) {
+        if (stats_here && kg == 0 && q < nqg) {
             sm.wm[wave * a.qmax + q] = st.m[qt];
             sm.wz[wave * a.qmax + q] = st.z[qt];
         }
     }
     __syncthreads();
-    for (int q = t; q < nqg; q += kFineThreads) {
+    for (int q = t; q < nqg; q += blockDim.x) {
         float M = -INFINITY, Z = 0.0f;
         for (int w = 0; w < kFineWaves; ++w)
             mz_merge(M, Z, sm.wm[w * a.qmax + q], sm.wz[w * a.qmax + q], a.cexp);
@@ -417,8 +442,10 @@ __device__ __forceinline__ void pass_end(const FineArgs &a, const FineSmem &sm, 
         sm.oz[q] = Z;
     }
     __syncthreads();
-    const int n1 = min(nqg, (wave + 1) * qw);
-    for (int q = wave * qw; q < n1; ++q) {
+    // the buffers are written out by every wave of the block
+    const int nw = blockDim.x >> 6, wo = t >> 6, qwo = (nqg + nw - 1) / nw;
+    const int n1 = min(nqg, (wo + 1) * qwo);
+    for (int q = wo * qwo; q < n1; ++q) {
         uint64_t *b = sm.buf + (size_t)q * a.cap;
         int cn = sm.ocnt[q];
         const float Mq = sm.om[q], Zq = sm.oz[q];
@@ -562,7 +589,7 @@ struct LoadUnit {
 template <typename KT, int U>
 __device__ __forceinline__ const KT *unit_keys(const KT *__restrict__ K, int d, int NG, int u,
                                                int64_t r0, int64_t r1, int64_t &base) {
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, r16 = lane & 15, kg = lane >> 4;
+    const int lane = threadIdx.x & 63, wave = fine_wave(), r16 = lane & 15, kg = lane >> 4;
     const int tt = u / NG, gi = u - tt * NG;
     base = r0 + (int64_t)tt * kRowsPerStep;
     const int64_t row = min(base + wave * kRowsPerWave + r16, r1 - 1);
@@ -586,7 +613,7 @@ __device__ __forceinline__ void lds_load_unit(LoadUnit<KT, U> &lu, const KT *__r
 // while it multiplies, instead of issuing a whole unit at once and leaving
 // the pipeline to drain; without it (two blocks per CU, whose waves cover for
 // each other) the unit is requested before the MFMAs.
-template <typename KT, int U, int NQT, int NPL, bool SPREAD>
+template <typename KT, int U, int NQT, int NPL, bool SPREAD, bool PC = false>
 __device__ __forceinline__ void lds_compute_unit(const FineArgs &a, const FineSmem &sm,
                                                  const LoadUnit<KT, U> &lu, LoadUnit<KT, U> &nx,
                                                  const KT *__restrict__ K, int nu, int NG, int u,
@@ -620,15 +647,22 @@ __device__ __forceinline__ void lds_compute_unit(const FineArgs &a, const FineSm
     }
     if (valid && gi == NG - 1) {
         const int64_t base = r0 + (int64_t)tt * kRowsPerStep;
-        step_end<NQT, NPL>(a, sm, acc, tt, base, r1, nqg,
-                           tid_value(lu.tid, a.tid == nullptr, base, r1), o, st);
+        const int32_t tid = tid_value(lu.tid, a.tid == nullptr, base, r1);
+        if constexpr (PC) producer_step_end<NQT>(a, sm, acc, tt, base, r1, tid, st);
+        else step_end<NQT, NPL>(a, sm, acc, tt, base, r1, nqg, tid, o, st);
     }
 }
-template <typename KT, int U, int NQT, int NPL, bool SPREAD>
+// PC: producer/consumer block of eight waves. Waves 0-3 stream the keys
+// (loads, MFMAs, statistics, score tiles) and never stop to keep top-k
+// buffers; waves 4-7 run the owner epilogue of each step's tile while the
+// producers multiply the next. Both sides meet once per step at a barrier
+// (twice when only one score tile fits in LDS).
+template <typename KT, int U, int NQT, int NPL, bool SPREAD, bool PC = false>
 __device__ __forceinline__ void pass_lds(const FineArgs &a, const FineSmem &sm, int64_t p0,
                                          bool single, int64_t r0, int64_t r1, int32_t qbeg,
                                          int32_t qg0, int32_t nqg) {
     const int t = threadIdx.x;
+    const bool producer = !PC || t < kFineThreads;
     const int d = a.d;
     const KT *__restrict__ K = static_cast<const KT *>(a.keys);
     const KT *__restrict__ Q = static_cast<const KT *>(a.q);
@@ -643,11 +677,13 @@ __device__ __forceinline__ void pass_lds(const FineArgs &a, const FineSmem &sm, 
     // stays unconditional and the compiler can wait for exactly one unit at a
     // time. The first units are requested before the queries are staged.
     // the largest top-k buffers leave fewer registers for the ring
-    constexpr int R = NPL < 8 ? kRing : (sizeof(KT) == 4 ? 2 : 3);
+    constexpr int R = PC ? 4 : NPL < 8 ? kRing : (sizeof(KT) == 4 ? 2 : 3);
     LoadUnit<KT, U> ring[R];
+    if (producer) {
 #pragma unroll
-    for (int j = 0; j < R - 1; ++j)
-        lds_load_unit<KT, U>(ring[j], K, a.tid_src, d, NG, min(j, total - 1), r0, r1);
+        for (int j = 0; j < R - 1; ++j)
+            lds_load_unit<KT, U>(ring[j], K, a.tid_src, d, NG, min(j, total - 1), r0, r1);
+    }
 
     pass_begin(a, sm, qbeg, qg0, nqg, single);
     // stage the queries as MFMA B fragments: [k-step][query tile][lane], eight
@@ -658,11 +694,12 @@ __device__ __forceinline__ void pass_lds(const FineArgs &a, const FineSmem &sm, 
     {
         constexpr int kBatch = 8;
         const int nfrag = KS * NQT * kWave;
-        for (int i0 = t; i0 < nfrag; i0 += kFineThreads * kBatch) {
+        const int nt = blockDim.x;
+        for (int i0 = t; i0 < nfrag; i0 += nt * kBatch) {
             bf16x8_t f[kBatch];
 #pragma unroll
             for (int b = 0; b < kBatch; ++b) {
-                const int idx = min(i0 + b * kFineThreads, nfrag - 1);
+                const int idx = min(i0 + b * nt, nfrag - 1);
                 const int s = idx / (NQT * kWave), rem = idx - s * NQT * kWave;
                 const int qt = rem >> 6, ln = rem & 63;
                 const int n = qt * 16 + (ln & 15), k = 32 * s + 8 * (ln >> 4);
@@ -672,7 +709,7 @@ __device__ __forceinline__ void pass_lds(const FineArgs &a, const FineSmem &sm, 
             // a loaded value where it is loaded would wait for every load
 #pragma unroll
             for (int b = 0; b < kBatch; ++b) {
-                const int idx = min(i0 + b * kFineThreads, nfrag - 1);
+                const int idx = min(i0 + b * nt, nfrag - 1);
                 const int rem = idx % (NQT * kWave);
                 const int n = (rem >> 6) * 16 + (rem & 15);
                 sm.qs[idx] = n < nqg ? f[b] : zero8();
@@ -696,18 +733,29 @@ __device__ __forceinline__ void pass_lds(const FineArgs &a, const FineSmem &sm, 
     // to the loop head every ring slot loaded in an iteration has then been
     // consumed in it on every path; a slot still loading on some path would
     // make the compiler wait for every load in flight at each iteration.
-    for (int u = 0; u < total; u += R) {
+    if (producer) {
+        for (int u = 0; u < total; u += R) {
 #pragma unroll
-        for (int j = 0; j < R; ++j)
-            lds_compute_unit<KT, U, NQT, NPL, SPREAD>(a, sm, ring[j], ring[(j + R - 1) % R], K,
-                                              min(u + j + R - 1, total - 1), NG, u + j,
-                                              u + j < total, r0, r1, nqg, acc, o, st);
+            for (int j = 0; j < R; ++j)
+                lds_compute_unit<KT, U, NQT, NPL, SPREAD, PC>(
+                    a, sm, ring[j], ring[(j + R - 1) % R], K, min(u + j + R - 1, total - 1), NG,
+                    u + j, u + j < total, r0, r1, nqg, acc, o, st);
+        }
+    } else {
+        // consumers: one step's tile at a time, in step order
+        for (int step = 0; step < T; ++step) {
+            const float *tile =
+                sm.st + (size_t)(a.ntile == 2 ? step & 1 : 0) * fine_tile_floats(a.qmax);
+            if (a.ntile == 1) __syncthreads();
+            __syncthreads();
+            owner_epilogue<NQT, NPL>(a, sm, tile, r0 + (int64_t)step * kRowsPerStep, r1, nqg, o);
+        }
     }
     // the ring's last loads (re-reads of the last unit) are not used: wait for
     // them here, so that no path reaches the next pass's unit loop with ring
     // registers still loading
     wait_vmcnt<0>();
-    pass_end<NQT, NPL>(a, sm, p0, qbeg, single, qg0, nqg, o, st);
+    pass_end<NQT, NPL, PC>(a, sm, p0, qbeg, single, qg0, nqg, o, st);
 }
 
 // Work loop shared by both kernels: items (cluster, chunk) from the planned
@@ -749,7 +797,7 @@ __device__ __forceinline__ void for_each_item(const FineArgs &a, int32_t *s_next
     }
 }
 
-template <typename KT, int U, int NPL, bool SPREAD>
+template <typename KT, int U, int NPL, bool SPREAD, bool PC = false>
 __device__ __forceinline__ void stream_lds_body(const FineArgs &a, int32_t qs_bytes,
                                                 unsigned char *smem_raw, int32_t *s_next) {
     const FineSmem sm = fine_carve(smem_raw, qs_bytes, a.qmax, a.cap, a.ntile);
@@ -757,10 +805,10 @@ __device__ __forceinline__ void stream_lds_body(const FineArgs &a, int32_t qs_by
         for (int32_t qg0 = 0; qg0 < it.nq; qg0 += a.qmax) {
             const int32_t nqg = min(a.qmax, it.nq - qg0);
             switch ((nqg + 15) >> 4) {
-                case 1: pass_lds<KT, U, 1, NPL, SPREAD>(a, sm, it.p0, it.single, it.r0, it.r1, it.qbeg, qg0, nqg); break;
-                case 2: pass_lds<KT, U, 2, NPL, SPREAD>(a, sm, it.p0, it.single, it.r0, it.r1, it.qbeg, qg0, nqg); break;
-                case 3: pass_lds<KT, U, 3, NPL, SPREAD>(a, sm, it.p0, it.single, it.r0, it.r1, it.qbeg, qg0, nqg); break;
-                default: pass_lds<KT, U, 4, NPL, SPREAD>(a, sm, it.p0, it.single, it.r0, it.r1, it.qbeg, qg0, nqg); break;
+                case 1: pass_lds<KT, U, 1, NPL, SPREAD, PC>(a, sm, it.p0, it.single, it.r0, it.r1, it.qbeg, qg0, nqg); break;
+                case 2: pass_lds<KT, U, 2, NPL, SPREAD, PC>(a, sm, it.p0, it.single, it.r0, it.r1, it.qbeg, qg0, nqg); break;
+                case 3: pass_lds<KT, U, 3, NPL, SPREAD, PC>(a, sm, it.p0, it.single, it.r0, it.r1, it.qbeg, qg0, nqg); break;
+                default: pass_lds<KT, U, 4, NPL, SPREAD, PC>(a, sm, it.p0, it.single, it.r0, it.r1, it.qbeg, qg0, nqg); break;
             }
         }
     });
@@ -786,6 +834,17 @@ void stream_lds2(FineArgs a, int32_t qs_bytes) {
     stream_lds_body<KT, 8, NPL, false>(a, qs_bytes, smem_raw, s_next);
 }
 
+// Producer/consumer blocks of eight waves, one per CU (LDS-bound launches):
+// four waves stream the keys with 8-k-step units in a ring of four (spread
+// between the MFMAs), four keep the top-k buffers. Registers are capped at
+// two waves per SIMD, which the two roles share.
+template <typename KT, int NPL>
+__global__ __launch_bounds__(2 * kFineThreads) void stream_pc(FineArgs a, int32_t qs_bytes) {
+    extern __shared__ __align__(16) unsigned char smem_raw[];
+    __shared__ int32_t s_next[2];
+    stream_lds_body<KT, 8, NPL, true, true>(a, qs_bytes, smem_raw, s_next);
+}
+
 template <typename T, bool BF16, int NPL>
 __global__ __launch_bounds__(kFineThreads) void stream_generic(FineArgs a) {
     extern __shared__ __align__(16) unsigned char smem_raw[];
@@ -805,7 +864,7 @@ __global__ __launch_bounds__(kFineThreads) void stream_generic(FineArgs a) {
 }
 
 template <typename Kern, typename... Args>
-hipError_t launch_stream_kernel(Kern kern, const StreamLaunch &l, Args... args) {
+hipError_t launch_stream_kernel_n(Kern kern, int threads, const StreamLaunch &l, Args... args) {
     // allow more than 64 KiB of dynamic LDS (a function attribute, not a stream operation)
     hipError_t err = hipFuncSetAttribute((const void *)kern,
                                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)l.smem);
@@ -813,19 +872,34 @@ hipError_t launch_stream_kernel(Kern kern, const StreamLaunch &l, Args... args) 
     // as many blocks as are resident at once (registers and LDS), no more:
     // the rest of the work is handed out by the item counter
     int per_cu = 0;
-    err = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, kFineThreads, l.smem);
+    err = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, threads, l.smem);
     if (err != hipSuccess) return err;
     int64_t grid = (int64_t)l.n_cu * (per_cu > 0 ? per_cu : 1);
     if (grid > l.max_grid) grid = l.max_grid;
     if (grid < 1) grid = 1;
     if (l.ev.before) hipEventRecord(l.ev.before, l.stream);
-    hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(kFineThreads), l.smem, l.stream, args...);
+    hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(threads), l.smem, l.stream, args...);
     if (l.ev.after) hipEventRecord(l.ev.after, l.stream);
     return hipGetLastError();
+}
+template <typename Kern, typename... Args>
+hipError_t launch_stream_kernel(Kern kern, const StreamLaunch &l, Args... args) {
+    return launch_stream_kernel_n(kern, kFineThreads, l, args...);
 }
 
 template <typename KT>
 hipError_t launch_stream_lds_t(int npl, bool two_per_cu, const StreamLaunch &l) {
+    if constexpr (sizeof(KT) == 2) {
+        if (l.producer_consumer) {
+            switch (npl) {
+                case 2: return launch_stream_kernel_n(stream_pc<KT, 2>, 2 * kFineThreads, l, l.fa,
+                                                      l.qs_bytes);
+                case 4: return launch_stream_kernel_n(stream_pc<KT, 4>, 2 * kFineThreads, l, l.fa,
+                                                      l.qs_bytes);
+            }
+            return hipErrorInvalidValue;
+        }
+    }
     if (two_per_cu) {
         switch (npl) {
             case 2: return launch_stream_kernel(stream_lds2<KT, 2>, l, l.fa, l.qs_bytes);
