@@ -445,16 +445,26 @@ __device__ __forceinline__ void pass_end(const FineArgs &a, const FineSmem &sm, 
     // the buffers are written out by every wave of the block
     const int nw = blockDim.x >> 6, wo = t >> 6, qwo = (nqg + nw - 1) / nw;
     const int n1 = min(nqg, (wo + 1) * qwo);
-    for (int q = wo * qwo; q < n1; ++q) {
-        uint64_t *b = sm.buf + (size_t)q * a.cap;
-        int cn = sm.ocnt[q];
-        const float Mq = sm.om[q], Zq = sm.oz[q];
-        if (single) {
+    if (single) {
+        // final sorted results
+        for (int q = wo * qwo; q < n1; ++q) {
+            int cn = sm.ocnt[q];
+            uint64_t *b = sm.buf + (size_t)q * a.cap;
             const int64_t e = sm.qpair[q];
             uint64_t v[NPL];
+            if constexpr (NPL == 2) {
+                // k <= 64: cut the buffer to at most 64 keys (all the top k)
+                // when it holds more, then sort one 64-key register
+                if (cn > kWave) cn = compact_cold<NPL>(b, cn, a.k, a.cap - kWave).n;
+                v[0] = lane < cn ? b[lane] : 0;
+                v[1] = 0;
+                uint64_t(&v1)[1] = *reinterpret_cast<uint64_t(*)[1]>(&v[0]);
+                wave_sort_regs<1>(v1, lane);
+            } else {
 #pragma unroll
-            for (int j = 0; j < NPL; ++j) v[j] = (j * kWave + lane < cn) ? b[j * kWave + lane] : 0;
-            wave_sort_regs<NPL>(v, lane);
+                for (int j = 0; j < NPL; ++j) v[j] = (j * kWave + lane < cn) ? b[j * kWave + lane] : 0;
+                wave_sort_regs<NPL>(v, lane);
+            }
 #pragma unroll
             for (int j = 0; j < NPL; ++j) {
                 const int r = j * kWave + lane;
@@ -465,27 +475,33 @@ __device__ __forceinline__ void pass_end(const FineArgs &a, const FineSmem &sm, 
                 }
             }
             if (lane == 0) {
-                a.slot_max[e] = Mq;
-                a.slot_sum[e] = Zq;
+                a.slot_max[e] = sm.om[q];
+                a.slot_sum[e] = sm.oz[q];
             }
-        } else {
-            uint64_t th = sm.otheta[q];
-            if (cn > a.k) {
-                const Compacted c = compact_cold<NPL>(b, cn, a.k, a.cap - a.k);
-                cn = c.n;
-                th = c.theta > th ? c.theta : th;
-            }
-            // At least k keys of this partial (or of the one the bound came
-            // from) are at or above th, so no key below it can be among the
-            // pair's top k: later chunks of the segment start from it.
-            if (lane == 0 && th != 0) atomicMax(a.bound + sm.qpair[q], th);
-            const int64_t p = p0 + qg0 + q;
-            for (int i = lane; i < a.k; i += kWave) a.pk[p * a.k + i] = i < cn ? b[i] : 0;
-            if (lane == 0) {
-                a.pc[p] = cn;
-                a.pm[p] = Mq;
-                a.pz[p] = Zq;
-            }
+            wave_lds_sync();
+        }
+        return;
+    }
+    for (int q = wo * qwo; q < n1; ++q) {
+        uint64_t *b = sm.buf + (size_t)q * a.cap;
+        int cn = sm.ocnt[q];
+        const float Mq = sm.om[q], Zq = sm.oz[q];
+        uint64_t th = sm.otheta[q];
+        if (cn > a.k) {
+            const Compacted c = compact_cold<NPL>(b, cn, a.k, a.cap - a.k);
+            cn = c.n;
+            th = c.theta > th ? c.theta : th;
+        }
+        // At least k keys of this partial (or of the one the bound came
+        // from) are at or above th, so no key below it can be among the
+        // pair's top k: later chunks of the segment start from it.
+        if (lane == 0 && th != 0) atomicMax(a.bound + sm.qpair[q], th);
+        const int64_t p = p0 + qg0 + q;
+        for (int i = lane; i < a.k; i += kWave) a.pk[p * a.k + i] = i < cn ? b[i] : 0;
+        if (lane == 0) {
+            a.pc[p] = cn;
+            a.pm[p] = Mq;
+            a.pz[p] = Zq;
         }
         wave_lds_sync();
     }
@@ -831,7 +847,8 @@ __global__ __launch_bounds__(kFineThreads) __attribute__((amdgpu_waves_per_eu(2,
 void stream_lds2(FineArgs a, int32_t qs_bytes) {
     extern __shared__ __align__(16) unsigned char smem_raw[];
     __shared__ int32_t s_next[2];
-    stream_lds_body<KT, 8, NPL, false>(a, qs_bytes, smem_raw, s_next);
+    // fp32 fragments take twice the registers: half-length units
+    stream_lds_body<KT, sizeof(KT) == 4 ? 4 : 8, NPL, false>(a, qs_bytes, smem_raw, s_next);
 }
 
 // Producer/consumer blocks of eight waves, one per CU (LDS-bound launches):
