@@ -389,9 +389,10 @@ __global__ __launch_bounds__(kPlanThreads) void route_plan(PlanArgs pa, const in
 
 // Bytes of the LDS tables of the fused routing kernel for G clusters and n
 // (query, slot) pairs: offsets, partial and level-one bases, counts, four
-// starts tables, the last-chunk items, then the pairs' clusters as 16-bit ids.
+// starts tables, the last-chunk items, then the pairs' clusters as 16-bit ids
+// and their 16-bit positions in their clusters' lists.
 size_t route_fused_lds(int32_t G, int64_t n) {
-    return (size_t)(3 * G + 1) * 8 + (size_t)(6 * G + 4) * 4 + (size_t)n * 2;
+    return (size_t)(3 * G + 1) * 8 + (size_t)(6 * G + 4) * 4 + (size_t)n * 4;
 }
 
 // The merge's description of pair e, position i in the list of its cluster
@@ -476,6 +477,7 @@ __global__ __launch_bounds__(kPlanThreads) void route_fused(PlanArgs pa, const i
     m.pbase = lpb;
     m.ubase = lub;
     uint16_t *lsel = reinterpret_cast<uint16_t *>(m.wlast + G);
+    uint16_t *lpos = lsel + n;                 // position of each pair in its cluster's list
     for (int64_t e0 = t; e0 < n; e0 += 8 * kPlanThreads) {   // 8 loads in flight per thread
         int32_t g[8];
 #pragma unroll
@@ -496,15 +498,13 @@ __global__ __launch_bounds__(kPlanThreads) void route_fused(PlanArgs pa, const i
     int32_t bad = 0;
     for (int64_t e = t; e < n; e += kPlanThreads) {
         const uint16_t h = lsel[e];
-        if (h != kNoCluster) atomicAdd(&lcnt[h], 1);
+        if (h != kNoCluster) lpos[e] = (uint16_t)atomicAdd(&lcnt[h], 1);
         else ++bad;
     }
     if (bad) atomicAdd(&s_bad, bad);
     __syncthreads();
     const int64_t ch = plan_chunks<true>(pa, LdsCnt{lcnt}, loff, s, m);
     const int lch = 63 - __builtin_clzll((unsigned long long)ch);
-    __syncthreads();
-    for (int32_t g = t; g < G; g += kPlanThreads) lcnt[g] = m.qoff[g];
     if (t == 0) {
         pa.plan->next = 0;
         pa.plan->bad_sel = s_bad;
@@ -518,8 +518,8 @@ __global__ __launch_bounds__(kPlanThreads) void route_fused(PlanArgs pa, const i
         if (h != kNoCluster) {
             const int32_t g = h;
             const int32_t qb = m.qoff[g];
-            const int32_t at = atomicAdd(&lcnt[g], 1);
-            const int32_t i = at - qb;
+            const int32_t i = lpos[e];
+            const int32_t at = qb + i;
             qlist[at] = (int32_t)e;
             pos[e] = i;
             const int64_t len = loff[g + 1] - loff[g];

@@ -17,6 +17,7 @@ namespace {
 
 constexpr int kTopkWaves = 4;
 constexpr int kTopkBatch = 8;          // 64-entry groups loaded before they are offered
+constexpr int kTopkStatLists = 1;      // 64-list groups of statistics loaded with the keys
 
 struct TopkArgs {
     int64_t rows, n;              // entries per row = lists * k_in
@@ -42,6 +43,16 @@ __global__ __launch_bounds__(kWave * kTopkWaves) void topk_rows(TopkArgs a) {
     const float *sc = a.score + row * a.n;
     const int32_t *ids = a.id ? a.id + row * a.n : nullptr;
     const uint64_t lt_mask = (1ull << lane) - 1;
+
+    // the row's list statistics, requested with the first keys
+    float lm[kTopkStatLists], lz[kTopkStatLists];
+#pragma unroll
+    for (int i = 0; i < kTopkStatLists; ++i) {
+        const int l = i * kWave + lane;
+        const bool ok = a.slot_max && l < a.lists;
+        lm[i] = ok ? a.slot_max[row * a.lists + l] : -INFINITY;
+        lz[i] = ok ? a.slot_sum[row * a.lists + l] : 0.0f;
+    }
 
     int cnt = 0, total = 0;
     uint64_t theta = 0;
@@ -74,7 +85,9 @@ __global__ __launch_bounds__(kWave * kTopkWaves) void topk_rows(TopkArgs a) {
     // merged softmax statistics of the row's lists
     float M = -INFINITY, Z = 0.0f;
     if (a.slot_max) {
-        for (int l = lane; l < a.lists; l += kWave)
+#pragma unroll
+        for (int i = 0; i < kTopkStatLists; ++i) mz_merge(M, Z, lm[i], lz[i], a.cexp);
+        for (int l = kTopkStatLists * kWave + lane; l < a.lists; l += kWave)
             mz_merge(M, Z, a.slot_max[row * a.lists + l], a.slot_sum[row * a.lists + l], a.cexp);
         for (int sh = 32; sh >= 1; sh >>= 1) {
             const float m2 = __shfl_xor(M, sh), z2 = __shfl_xor(Z, sh);
