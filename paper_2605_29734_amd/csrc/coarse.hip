@@ -159,6 +159,10 @@ __global__ __launch_bounds__(kGemmThreads) void coarse_gemm(const __bf16 *__rest
         stage(ks + 1, a1, b1, a0, b0);
     }
     if (ks < nk) stage(ks, a0, b0, a1, b1);
+    // No load may still be writing LDS when the block ends. Waiting here,
+    // before the stores (the counter covers both), lets the block end while
+    // its stores drain and the next block on the CU starts.
+    wait_vmcnt<0>();
     // D[m][n]: this lane holds rows 4*kg + e of each 16x16 tile, column r16.
 #pragma unroll
     for (int i = 0; i < 8; ++i)
@@ -170,7 +174,6 @@ __global__ __launch_bounds__(kGemmThreads) void coarse_gemm(const __bf16 *__rest
                 const int64_t c = n0 + wn * 64 + j * 16 + r16;
                 if (r < B && c < G) S[r * G + c] = acc[i][j][e];
             }
-    wait_vmcnt<0>();      // no load may still be writing LDS when the block ends
 }
 
 // A fragment as loaded (bf16 as is; fp32 rounded to bf16 when used).
