@@ -158,29 +158,36 @@ def test_attend_out_of_range_selection_is_empty():
         np.testing.assert_array_equal(a[~bad], b[~bad])
 
 
-@pytest.mark.parametrize("B,G,d,c", [(4096, 4096, 64, 256), (4000, 4099, 160, 256)])
-def test_coarse_gemm_every_row(B, G, d, c):
-    """The 256 x 256-tile coarse GEMM (at least one tile per CU; ragged B and G,
-    a G that is not a multiple of 4, two and five 32-wide K stages): every row's
-    top-c scores and cluster ids against the oracle's full score matrix over the
-    same bf16 operands. Checked: the ids are distinct clusters, each score is the
-    oracle's score of its id, and the sorted scores are the oracle's c largest,
-    all within 1e-4 (fp32 accumulation of at most 160 products of unit rows)."""
+@pytest.mark.parametrize("B,G,d,c,storage", [
+    (4096, 4096, 64, 256, "bf16"),     # 256 x 256-tile GEMM: one tile per CU, two K stages
+    (4000, 4099, 160, 256, "bf16"),    # ragged tiles, G % 4 != 0, five K stages
+    (300, 1000, 200, 256, "bf16"),     # 32 x 32-tile GEMM, d % 32 != 0, ragged B and G
+    (300, 1000, 200, 5, "bf16"),       # the same with many radix-select cuts per row
+    (70, 4099, 64, 100, "f32"),        # fp32 storage rounded to bf16
+    (64, 20000, 128, 40, "bf16"),      # long rows for the row top-k
+])
+def test_coarse_every_row(B, G, d, c, storage):
+    """Coarse retrieval over every row against the oracle's full score matrix
+    over the same bf16-rounded operands, for each kernel path (chosen by the
+    shape): the ids are distinct clusters, each score is the oracle's score of
+    its id, and the sorted scores are the oracle's c largest, all within 1e-4
+    (fp32 accumulation of at most 200 products of unit rows)."""
     from paper_2605_29734_amd import htam
-    say(f"[case] coarse GEMM B={B} G={G} d={d} c={c}")
-    rng = np.random.default_rng(B + G + d)
+    say(f"[case] coarse B={B} G={G} d={d} c={c} storage={storage}")
+    rng = np.random.default_rng(B + G + d + c)
     unit = lambda n: (lambda x: x / np.linalg.norm(x, axis=1, keepdims=True))(   # noqa: E731
         rng.standard_normal((n, d)))
     dev = torch.device("cuda:0")
-    q = torch.from_numpy(unit(B).astype(np.float32)).to(dev).to(torch.bfloat16)
-    ck = torch.from_numpy(unit(G).astype(np.float32)).to(dev).to(torch.bfloat16)
-    bank = htam.Bank(coarse_keys=ck, fine_keys=torch.zeros(1, d, dtype=torch.bfloat16, device=dev),
+    dt = torch.bfloat16 if storage == "bf16" else torch.float32
+    q = torch.from_numpy(unit(B).astype(np.float32)).to(dev).to(dt)
+    ck = torch.from_numpy(unit(G).astype(np.float32)).to(dev).to(dt)
+    bank = htam.Bank(coarse_keys=ck, fine_keys=torch.zeros(1, d, dtype=dt, device=dev),
                      seg_offsets=torch.zeros(G + 1, dtype=torch.int64, device=dev),
                      transition_id=None, compute="bf16")
     sel, ss = htam.htam_retrieve_coarse(bank, q, c)
     torch.cuda.synchronize()
     sel, ss = to_np(sel), to_np(ss)
-    ref = oracle.scores(to_np(q), to_np(ck))
+    ref = oracle.scores(oracle.round_bf16(to_np(q)), oracle.round_bf16(to_np(ck)))
     assert sel.min() >= 0 and sel.max() < G
     assert all(len(np.unique(row)) == c for row in sel)
     rows = np.arange(B)[:, None]
