@@ -820,11 +820,14 @@ __global__ __launch_bounds__(kWave * kMergeWaves) void slot_merge(MergeArgs a) {
 // ---------------------------------------------------------------------------
 static int fine_cap(int k) { return next_pow2(k + kRowsPerStep); }
 
-// Shortest chunk: the bank's rows spread over about 4 chunks per compute unit
-// (a power of two between kChunkFloor and kChunkCeil rows); the planning
-// kernel doubles it while the partial results would not fit.
+// Shortest chunk: the bank's rows spread over about one chunk per compute
+// unit (a power of two between kChunkFloor and kChunkCeil rows); the planning
+// kernel doubles it while the partial results would not fit. On a small bank
+// (the ceiling not reached) the selected clusters' chunks then number about as
+// many as the blocks the stream kernel keeps resident, so most items start at
+// once and no block runs a chain of short ones.
 static int64_t chunk_floor_rows(int64_t N, int n_cu) {
-    const int64_t target = N / ((int64_t)(n_cu > 0 ? n_cu : 1) * 4);
+    const int64_t target = N / (int64_t)(n_cu > 0 ? n_cu : 1);
     int64_t ch = kChunkFloor;
     while (ch * 2 <= target && ch * 2 <= kChunkCeil) ch *= 2;
     return ch;
