@@ -31,14 +31,16 @@ constexpr int64_t kFusedRoutePairs = 16384;     // above this many pairs, route 
 constexpr int64_t kChunkCeil = 4096;
 constexpr int kMergeWaves = 4;                   // waves per merge block
 constexpr int kMergeBatch = 8;                   // 64-entry groups per merge request
+constexpr int kMergeDirect = 4;                  // requests a one-level merge may take
 
 // Chunk partials per level-one merge group for a cluster of nch chunks whose
 // partials hold kp key slots each (k rounded up to a power of two): 0 (no
-// groups) when one merge request reads all of them, else about sqrt(nch),
-// so that the two merge levels read about as many keys each and a long
-// cluster's merge is not a long chain of requests in one wave.
+// groups) when kMergeDirect merge requests read all of them (a short chain of
+// prefetched requests costs less than a second merge level), else about
+// sqrt(nch), so that the two merge levels read about as many keys each and a
+// long cluster's merge is not a long chain of requests in one wave.
 __host__ __device__ inline int64_t group_span(int64_t nch, int64_t kp) {
-    if (nch * kp <= (int64_t)kMergeBatch * kWave) return 0;
+    if (nch * kp <= (int64_t)kMergeDirect * kMergeBatch * kWave) return 0;
     int64_t r = 2;
     while (r * r < nch) r *= 2;                   // power-of-two bracket, then refine
     int64_t lo = r / 2;
