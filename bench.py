@@ -8,9 +8,12 @@ and their weights (htam_topk). Inputs (bank, queries) are resident in HBM
 before the timed region; the bank build is offline and untimed.
 
 Prints one JSON line: queries/s for the workload, the roofline position of the
-dominant kernel (the bank stream, HBM-bound), measured with HIP events around
-that kernel inside the timed region, and the CPU oracle timed on a sample of the
-same workload on the host's cores.
+dominant kernel (the bank stream, HBM-bound), measured with HIP events stamped
+at that kernel's start and end inside the timed region (on every
+--event-every-th timed step: a timed dispatch costs the step a few
+microseconds, which the small workloads would otherwise show in their
+throughput), and the CPU oracle timed on a sample of the same workload on the
+host's cores.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--gpus 1]
 """
@@ -135,6 +138,8 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--event-every", type=int, default=8, metavar="E",
+                    help="stamp the kernel timing events on every E-th timed step")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run plain copies of MIB MiB (counter calibration) and exit")
     args = ap.parse_args()
@@ -166,9 +171,11 @@ def main():
     torch.cuda.synchronize()
 
     K = args.steps
+    E = max(1, args.event_every)
+    n_ev = (K + E - 1) // E              # timed steps i with i % E == 0
     mk = lambda: torch.cuda.Event(enable_timing=True)   # noqa: E731
-    ev_s = [(mk(), mk()) for _ in range(K)]
-    ev_c = [(mk(), mk()) for _ in range(K)]
+    ev_s = [(mk(), mk()) for _ in range(n_ev)]
+    ev_c = [(mk(), mk()) for _ in range(n_ev)]
     for a, b in ev_s + ev_c:        # materialise the events before handing them to the library
         a.record()
         b.record()
@@ -178,10 +185,15 @@ def main():
     t0 = time.perf_counter()
     start.record()
     for i in range(K):
-        htam.lib.htam_set_kernel_events(htam.HTAM_KERNEL_STREAM, ev_s[i][0].cuda_event,
-                                        ev_s[i][1].cuda_event)
-        htam.lib.htam_set_kernel_events(htam.HTAM_KERNEL_COARSE, ev_c[i][0].cuda_event,
-                                        ev_c[i][1].cuda_event)
+        if i % E == 0:
+            j = i // E
+            htam.lib.htam_set_kernel_events(htam.HTAM_KERNEL_STREAM, ev_s[j][0].cuda_event,
+                                            ev_s[j][1].cuda_event)
+            htam.lib.htam_set_kernel_events(htam.HTAM_KERNEL_COARSE, ev_c[j][0].cuda_event,
+                                            ev_c[j][1].cuda_event)
+        elif i % E == 1:
+            htam.lib.htam_set_kernel_events(htam.HTAM_KERNEL_STREAM, None, None)
+            htam.lib.htam_set_kernel_events(htam.HTAM_KERNEL_COARSE, None, None)
         r.run(q)
     end.record()
     torch.cuda.synchronize()
@@ -189,8 +201,8 @@ def main():
     htam.lib.htam_set_kernel_events(htam.HTAM_KERNEL_STREAM, None, None)
     htam.lib.htam_set_kernel_events(htam.HTAM_KERNEL_COARSE, None, None)
     ms_step = start.elapsed_time(end) / K
-    t_stream = sum(a.elapsed_time(b) for a, b in ev_s) / K * 1e-3
-    t_coarse = sum(a.elapsed_time(b) for a, b in ev_c) / K * 1e-3
+    t_stream = sum(a.elapsed_time(b) for a, b in ev_s) / n_ev * 1e-3
+    t_coarse = sum(a.elapsed_time(b) for a, b in ev_c) / n_ev * 1e-3
 
     # algorithmic bytes of one bank-stream launch: every row of every selected
     # segment read once, plus the queries
@@ -230,7 +242,8 @@ def main():
                    "coarse_mfma_frac": coarse_flops / t_coarse / 1e12 / MFMA_BF16_PEAK_TFLOPS,
                    "fine_stream_ms": t_stream * 1e3,
                    "scored_pairs_per_step": pairs,
-                   "step_ms_event": ms_step, "step_ms_wall": wall / K * 1e3},
+                   "step_ms_event": ms_step, "step_ms_wall": wall / K * 1e3,
+                   "kernel_timed_steps": n_ev},
     }
     if not args.no_cpu_baseline:
         log("[bench] CPU oracle baseline")

@@ -226,10 +226,11 @@ htam_status htam_topk(int32_t n_rows, int32_t n_lists, int32_t k_in, const float
 /*
  * Diagnostics: kernel timing hooks. After htam_set_kernel_events(which, before,
  * after) with two hipEvent_t handles (passed as void *), every later call on
- * the calling thread that launches kernel `which` records `before` on the
- * call's stream just before that kernel and `after` just after it, so that
- * hipEventElapsedTime gives the kernel's own duration. NULL handles switch the
- * hook off. The events are owned by the caller.
+ * the calling thread that launches kernel `which` has `before` stamped at that
+ * kernel's start and `after` at its end (by the kernel's own dispatch, through
+ * hipExtLaunchKernel), so that hipEventElapsedTime gives the kernel's own
+ * duration. NULL handles switch the hook off. The events are owned by the
+ * caller.
  *   HTAM_KERNEL_COARSE  the coarse scoring kernel (htam_retrieve_coarse);
  *   HTAM_KERNEL_STREAM  the bank-streaming kernel (htam_attend_transitions).
  */

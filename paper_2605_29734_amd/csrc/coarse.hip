@@ -331,23 +331,19 @@ hipError_t launch_coarse(int32_t key_dtype, int32_t compute_dtype, int32_t d, in
                          int32_t *sel, float *sel_score, const CoarseWs &w, int n_cu,
                          KernelEvents ev, hipStream_t s) {
     if (compute_dtype == kF32) {
-        if (ev.before) hipEventRecord(ev.before, s);
-        hipLaunchKernelGGL(coarse_f32, dim3((G + 63) / 64, (B + 63) / 64), dim3(256), 0, s,
-                           static_cast<const float *>(q), static_cast<const float *>(coarse_keys),
-                           B, G, d, w.scores);
-        if (ev.after) hipEventRecord(ev.after, s);
+        launch_timed(coarse_f32, dim3((G + 63) / 64, (B + 63) / 64), dim3(256), 0, s, ev,
+                     static_cast<const float *>(q), static_cast<const float *>(coarse_keys), B, G,
+                     d, w.scores);
     } else if ((int64_t)((B + BM - 1) / BM) * ((G + BN - 1) / BN) < n_cu || d % BK != 0) {
         const dim3 grid((G + 31) / 32, (B + 31) / 32);
-        if (ev.before) hipEventRecord(ev.before, s);
         if (key_dtype == kF32)
-            hipLaunchKernelGGL(coarse_small_bf16<float>, grid, dim3(kWave), 0, s,
-                               static_cast<const float *>(q),
-                               static_cast<const float *>(coarse_keys), B, G, d, w.scores);
+            launch_timed(coarse_small_bf16<float>, grid, dim3(kWave), 0, s, ev,
+                         static_cast<const float *>(q), static_cast<const float *>(coarse_keys), B,
+                         G, d, w.scores);
         else
-            hipLaunchKernelGGL(coarse_small_bf16<__bf16>, grid, dim3(kWave), 0, s,
-                               static_cast<const __bf16 *>(q),
-                               static_cast<const __bf16 *>(coarse_keys), B, G, d, w.scores);
-        if (ev.after) hipEventRecord(ev.after, s);
+            launch_timed(coarse_small_bf16<__bf16>, grid, dim3(kWave), 0, s, ev,
+                         static_cast<const __bf16 *>(q), static_cast<const __bf16 *>(coarse_keys),
+                         B, G, d, w.scores);
     } else {
         const __bf16 *q16 = static_cast<const __bf16 *>(q);
         const __bf16 *c16 = static_cast<const __bf16 *>(coarse_keys);
@@ -365,10 +361,8 @@ hipError_t launch_coarse(int32_t key_dtype, int32_t compute_dtype, int32_t d, in
                                              (int)kGemmLds);
         if (err != hipSuccess) return err;
         const int tiles = ((B + BM - 1) / BM) * ((G + BN - 1) / BN);
-        if (ev.before) hipEventRecord(ev.before, s);
-        hipLaunchKernelGGL(coarse_gemm, dim3(tiles), dim3(kGemmThreads), kGemmLds, s, q16, c16, B, G,
-                           d, w.scores);
-        if (ev.after) hipEventRecord(ev.after, s);
+        launch_timed(coarse_gemm, dim3(tiles), dim3(kGemmThreads), kGemmLds, s, ev, q16, c16, B, G,
+                     d, w.scores);
     }
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;

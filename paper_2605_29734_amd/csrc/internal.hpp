@@ -1,6 +1,7 @@
 // Internal interface between the host API (htam_api.cpp) and the kernel
 // translation units: workspace layouts and kernel launchers.
 #pragma once
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 #include <stdint.h>
@@ -9,10 +10,23 @@ namespace htam {
 
 enum DType : int32_t { kF32 = 0, kBF16 = 1 };
 
-// Optional events recorded around one kernel (timing hooks of the C ABI).
+// Optional events stamped at the start and the end of one kernel (timing
+// hooks of the C ABI).
 struct KernelEvents {
     hipEvent_t before = nullptr, after = nullptr;
 };
+
+// Launches kern; with events, through hipExtLaunchKernel, which stamps them
+// from the kernel's own dispatch (no marker packets of their own around it).
+template <typename Kern, typename... Args>
+inline void launch_timed(Kern kern, dim3 grid, dim3 block, size_t smem, hipStream_t s,
+                         KernelEvents ev, Args... args) {
+    if (ev.before || ev.after)
+        hipExtLaunchKernelGGL(kern, grid, block, (std::uint32_t)smem, s, ev.before, ev.after, 0u,
+                              args...);
+    else
+        hipLaunchKernelGGL(kern, grid, block, smem, s, args...);
+}
 
 // Routing plan written on the device by the planning kernel of the fine stage.
 struct Plan {

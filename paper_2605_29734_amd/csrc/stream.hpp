@@ -894,9 +894,7 @@ hipError_t launch_stream_kernel_n(Kern kern, int threads, const StreamLaunch &l,
     int64_t grid = (int64_t)l.n_cu * (per_cu > 0 ? per_cu : 1);
     if (grid > l.max_grid) grid = l.max_grid;
     if (grid < 1) grid = 1;
-    if (l.ev.before) hipEventRecord(l.ev.before, l.stream);
-    hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(threads), l.smem, l.stream, args...);
-    if (l.ev.after) hipEventRecord(l.ev.after, l.stream);
+    launch_timed(kern, dim3((unsigned)grid), dim3(threads), l.smem, l.stream, l.ev, args...);
     return hipGetLastError();
 }
 template <typename Kern, typename... Args>
