@@ -32,15 +32,16 @@ constexpr int64_t kChunkCeil = 4096;
 constexpr int kMergeWaves = 4;                   // waves per merge block
 constexpr int kMergeBatch = 8;                   // 64-entry groups per merge request
 constexpr int kMergeDirect = 4;                  // requests a one-level merge may take
+constexpr int kMergeDirectSmall = 8;             // the same where it rules out level one
 
 // Chunk partials per level-one merge group for a cluster of nch chunks whose
 // partials hold kp key slots each (k rounded up to a power of two): 0 (no
-// groups) when kMergeDirect merge requests read all of them (a short chain of
-// prefetched requests costs less than a second merge level), else about
-// sqrt(nch), so that the two merge levels read about as many keys each and a
-// long cluster's merge is not a long chain of requests in one wave.
-__host__ __device__ inline int64_t group_span(int64_t nch, int64_t kp) {
-    if (nch * kp <= (int64_t)kMergeDirect * kMergeBatch * kWave) return 0;
+// groups) when they hold at most `direct` keys (a one-level merge: a short
+// chain of prefetched requests costs less than a second merge level), else
+// about sqrt(nch), so that the two merge levels read about as many keys each
+// and a long cluster's merge is not a long chain of requests in one wave.
+__host__ __device__ inline int64_t group_span(int64_t nch, int64_t kp, int64_t direct) {
+    if (nch * kp <= direct) return 0;
     int64_t r = 2;
     while (r * r < nch) r *= 2;                   // power-of-two bracket, then refine
     int64_t lo = r / 2;
@@ -50,8 +51,8 @@ __host__ __device__ inline int64_t group_span(int64_t nch, int64_t kp) {
     }
     return r < 2 ? 2 : r;
 }
-__host__ __device__ inline int64_t group_count(int64_t nch, int64_t kp) {
-    const int64_t r = group_span(nch, kp);
+__host__ __device__ inline int64_t group_count(int64_t nch, int64_t kp, int64_t direct) {
+    const int64_t r = group_span(nch, kp, direct);
     return r ? (nch + r - 1) / r : 0;
 }
 
@@ -92,6 +93,7 @@ struct PlanArgs {
     int64_t *ubase;           // [G]
     Plan *plan;
     int64_t chunk_min, p_cap;
+    int64_t direct;           // most keys a one-level merge of a pair reads
     int32_t kp;               // key slots per partial (k rounded up to a power of two)
 };
 
@@ -277,7 +279,7 @@ __device__ int64_t plan_chunks(const PlanArgs &pa, CntOf cnt_of, const int64_t *
         const int64_t c = cnt_of(g), len = off[g + 1] - off[g];
         const int64_t nch = (c > 0 && len > 0) ? (len + ch - 1) >> lch : 0;
         const int64_t nfull = c > 0 ? len >> lch : 0;
-        const int64_t ng = group_count(nch, kp);
+        const int64_t ng = group_count(nch, kp, pa.direct);
         w[0] += nfull + (ng << 32);
         w[1] += nch * c;
         w[2] += ng * c;
@@ -307,7 +309,7 @@ __device__ int64_t plan_chunks(const PlanArgs &pa, CntOf cnt_of, const int64_t *
         const int64_t c = cnt_of(g), len = off[g + 1] - off[g];
         const int64_t nch = (c > 0 && len > 0) ? (len + ch - 1) >> lch : 0;
         const int64_t nfull = c > 0 ? len >> lch : 0;
-        const int64_t ng = group_count(nch, kp);
+        const int64_t ng = group_count(nch, kp, pa.direct);
         int32_t wl = -1;
         if (nch > nfull) {
             const int b = len_bucket(len - (nfull << lch), lch);
@@ -526,7 +528,7 @@ __global__ __launch_bounds__(kPlanThreads) void route_fused(PlanArgs pa, const i
             pos[e] = i;
             const int64_t len = loff[g + 1] - loff[g];
             const int64_t nch = (len + ch - 1) >> lch;
-            const int64_t r = group_span(nch, kp);
+            const int64_t r = group_span(nch, kp, pa.direct);
             if (nch != 1)
                 mlist[m.mstart[g] + i] =
                     merge_slot(e, i, nch, r, m.qoff[g + 1] - qb, lpb[g], lub[g]);
@@ -564,7 +566,7 @@ __global__ __launch_bounds__(kPlanThreads) void route_fused(PlanArgs pa, const i
         if (ng == 0) continue;
         const int32_t nq = m.qoff[g + 1] - m.qoff[g];
         const int64_t nch = (loff[g + 1] - loff[g] + ch - 1) >> lch;
-        const int64_t r = group_span(nch, kp);
+        const int64_t r = group_span(nch, kp, pa.direct);
         for (int32_t jg = 0; jg < ng; ++jg)
             groups[gs + jg] = merge_group_of(jg, nch, r, nq, lpb[g], lub[g]);
     }
@@ -587,7 +589,7 @@ __global__ __launch_bounds__(256) void route_items(PlanArgs pa, const int32_t *q
         if (nq == 0) continue;
         const int64_t a = pa.off[g], len = pa.off[g + 1] - a;
         const int64_t nch = (len + ch - 1) >> lch;
-        const int64_t r = group_span(nch, kp);
+        const int64_t r = group_span(nch, kp, pa.direct);
         if (nch != 1) {
             const int32_t m0 = pa.mstart[g];
             const int64_t pb = pa.pbase[g], ub = pa.ubase[g];
@@ -966,10 +968,12 @@ static unsigned merge_grid(int64_t bound, int n_cu) {
 }
 
 template <int NPL>
-static hipError_t launch_merge(const MergeArgs &ma, int64_t u_cap, int n_cu, hipStream_t s) {
+static hipError_t launch_merge(const MergeArgs &ma, int64_t u_cap, bool groups, int n_cu,
+                               hipStream_t s) {
     const size_t smem = (size_t)kMergeWaves * NPL * kWave * 8;
-    hipLaunchKernelGGL(group_merge<NPL>, dim3(merge_grid(u_cap, n_cu)), dim3(kWave * kMergeWaves),
-                       smem, s, ma);
+    if (groups)
+        hipLaunchKernelGGL(group_merge<NPL>, dim3(merge_grid(u_cap, n_cu)),
+                           dim3(kWave * kMergeWaves), smem, s, ma);
     hipLaunchKernelGGL(slot_merge<NPL>, dim3(merge_grid(ma.n_pairs, n_cu)),
                        dim3(kWave * kMergeWaves), smem, s, ma);
     return hipGetLastError();
@@ -998,6 +1002,15 @@ hipError_t launch_attend(int32_t key_dtype, int32_t compute_dtype, int32_t d, in
     pa.chunk_min = chunk_floor_rows(N, n_cu);
     pa.p_cap = w.p_cap;
     pa.kp = w.kp;
+    // One merge level everywhere, and no level-one launch, when up to
+    // kMergeDirectSmall requests cover even a segment of all N rows cut at
+    // the shortest chunk the planner may choose (small banks); else level one
+    // above kMergeDirect requests, where longer one-level chains would set
+    // the merge kernel's length.
+    const int64_t nch_max = (N + pa.chunk_min - 1) / pa.chunk_min;
+    const int64_t req = (int64_t)kMergeBatch * kWave;
+    const bool groups = group_span(nch_max, pa.kp, kMergeDirectSmall * req) > 0;
+    pa.direct = (groups ? kMergeDirect : kMergeDirectSmall) * req;
     const SlotOut so{slot_max, slot_sum, cand_score, cand_id, k};
     const size_t route_lds = route_fused_lds(G, bc);
     static_assert((3 * (size_t)kNoCluster + 1) * 8 > kRouteLdsBytes, "fused routing keeps cluster ids in 16 bits");
@@ -1069,9 +1082,9 @@ hipError_t launch_attend(int32_t key_dtype, int32_t compute_dtype, int32_t d, in
     ma.cand_score = cand_score;
     ma.cand_id = cand_id;
     switch (next_pow2(k + kWave) / kWave) {
-        case 2: return launch_merge<2>(ma, w.u_cap, n_cu, s);
-        case 4: return launch_merge<4>(ma, w.u_cap, n_cu, s);
-        default: return launch_merge<8>(ma, w.u_cap, n_cu, s);
+        case 2: return launch_merge<2>(ma, w.u_cap, groups, n_cu, s);
+        case 4: return launch_merge<4>(ma, w.u_cap, groups, n_cu, s);
+        default: return launch_merge<8>(ma, w.u_cap, groups, n_cu, s);
     }
 }
 
