@@ -198,11 +198,15 @@ __device__ void block_sum_n(int64_t (&v)[N], int64_t *s) {
 // (query, slot) then has one partial and p_cap >= B*c).
 constexpr int kChunkCands = 26;
 
-// Buckets of the clusters' shorter last chunks by length (item order).
+// Buckets of the clusters' shorter last chunks (item order): by length
+// (longest first), and within a length, clusters of more than one query tile
+// (16 queries) before the others, whose items cost less per row.
 constexpr int kLenBuckets = 8;
-__device__ __forceinline__ int len_bucket(int64_t len, int lch) {   // 0 < len < 2^lch
-    const int b = lch - 1 - (63 - __builtin_clzll((unsigned long long)len));
-    return b < kLenBuckets - 1 ? b : kLenBuckets - 1;
+constexpr int kItemBuckets = 2 * kLenBuckets;
+__device__ __forceinline__ int item_bucket(int64_t len, int lch, int64_t nq) {   // 0 < len < 2^lch
+    int b = lch - 1 - (63 - __builtin_clzll((unsigned long long)len));
+    b = b < kLenBuckets - 1 ? b : kLenBuckets - 1;
+    return 2 * b + (nq > 16 ? 0 : 1);
 }
 
 // LDS copies of the per-cluster tables the planning step writes (fused routing).
@@ -265,13 +269,14 @@ __device__ int64_t plan_chunks(const PlanArgs &pa, CntOf cnt_of, const int64_t *
     const int64_t ch = int64_t(1) << lch;
 
     // Items: first every full-length chunk, cluster by cluster; then each
-    // cluster's shorter last chunk, in buckets by length (longest first), so
-    // that the dynamic work counter hands out the longest items first and the
-    // short ones fill the end. Bucket b holds lengths in [ch >> (b+1), ch >> b)
-    // (the last one everything shorter). Counts that fit 32 bits are scanned
-    // two per 64-bit value: (full items, level-one groups), bucket pairs.
+    // cluster's shorter last chunk, in buckets by length (longest first) and
+    // query tiles (item_bucket), so that the dynamic work counter hands out
+    // the costliest items first and the cheap ones fill the end. Length
+    // bucket b holds lengths in [ch >> (b+1), ch >> b) (the last one
+    // everything shorter). Counts that fit 32 bits are scanned two per 64-bit
+    // value: (full items, level-one groups), bucket pairs.
     const int64_t kp = pa.kp;
-    constexpr int NW = 4 + kLenBuckets / 2;
+    constexpr int NW = 4 + kItemBuckets / 2;
     int64_t w[NW], wt[NW];   // items | groups << 32, partials, level-one, merge list, buckets
 #pragma unroll
     for (int i = 0; i < NW; ++i) w[i] = 0;
@@ -285,20 +290,20 @@ __device__ int64_t plan_chunks(const PlanArgs &pa, CntOf cnt_of, const int64_t *
         w[2] += ng * c;
         w[3] += nch != 1 ? c : 0;        // empty segments are finished by the merge too
         if (nch > nfull) {
-            const int b = len_bucket(len - (nfull << lch), lch);
+            const int b = item_bucket(len - (nfull << lch), lch, c);
 #pragma unroll
-            for (int i = 0; i < kLenBuckets / 2; ++i)
+            for (int i = 0; i < kItemBuckets / 2; ++i)
                 if ((b >> 1) == i) w[4 + i] += int64_t(1) << (32 * (b & 1));
         }
     }
     block_scan_n<NW>(w, wt, s);
     const int64_t n_full = wt[0] & 0xffffffff;
     // next item of each bucket of last chunks, for this thread's clusters
-    int32_t bnext[kLenBuckets];
+    int32_t bnext[kItemBuckets];
     {
         int64_t at = n_full;
 #pragma unroll
-        for (int b = 0; b < kLenBuckets; ++b) {
+        for (int b = 0; b < kItemBuckets; ++b) {
             bnext[b] = (int32_t)(at + ((w[4 + b / 2] >> (32 * (b & 1))) & 0xffffffff));
             at += (wt[4 + b / 2] >> (32 * (b & 1))) & 0xffffffff;
         }
@@ -312,9 +317,9 @@ __device__ int64_t plan_chunks(const PlanArgs &pa, CntOf cnt_of, const int64_t *
         const int64_t ng = group_count(nch, kp, pa.direct);
         int32_t wl = -1;
         if (nch > nfull) {
-            const int b = len_bucket(len - (nfull << lch), lch);
+            const int b = item_bucket(len - (nfull << lch), lch, c);
 #pragma unroll
-            for (int i = 0; i < kLenBuckets; ++i)
+            for (int i = 0; i < kItemBuckets; ++i)
                 if (b == i) wl = bnext[i]++;
         }
         const int32_t ws = (int32_t)(w[0] & 0xffffffff), gs = (int32_t)(w[0] >> 32);
