@@ -90,6 +90,14 @@ __device__ __forceinline__ void wave_lds_sync() {
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
 }
 
+// Block barrier for LDS only: this thread's LDS operations complete, then the
+// workgroup barrier; its global loads stay in flight (__syncthreads would wait
+// for them). The memory clobber keeps the compiler from moving memory
+// accesses across it.
+__device__ __forceinline__ void block_lds_barrier() {
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
 
 // ---------------------------------------------------------------------------
 // Register-resident sorting networks over one wave. A list of 64*NPL keys is

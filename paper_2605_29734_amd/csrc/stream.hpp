@@ -200,17 +200,49 @@ __device__ __forceinline__ void stats_update(Stats<NQT> &st, const f32x4_t (&acc
 }
 
 // Per-pass set-up: the (query, slot) pairs of the pass and their query rows.
-__device__ __forceinline__ void pass_begin(const FineArgs &a, const FineSmem &sm, int32_t qbeg,
-                                           int32_t qg0, int32_t nqg, bool single) {
-    for (int n = threadIdx.x; n < nqg; n += blockDim.x) {
+// A query's shared bound as loaded by pass_begin, for pass_bound to store.
+struct PassBound {
+    uint64_t v = 0;
+    int n = -1;            // the query whose bound this thread holds, -1: none
+};
+
+// Start of a pass: the pass's pair indices and query rows into LDS, and each
+// query's starting threshold: 0 for a cluster that is one chunk, else the
+// pair's shared bound (a chunk of a longer segment starts from it). Thread n
+// handles query n (nqg <= qmax <= blocks' thread count). With kDefer the
+// bound load is left in flight (the barrier here waits for LDS only) and the
+// caller stores it with pass_bound before its next block-wide barrier, so
+// that the load overlaps the query staging.
+template <bool kDefer>
+__device__ __forceinline__ PassBound pass_begin(const FineArgs &a, const FineSmem &sm,
+                                                int32_t qbeg, int32_t qg0, int32_t nqg,
+                                                bool single) {
+    PassBound pb;
+    if (qg0 > 0) {
+        // a later pass over the same item: every wave must be done writing
+        // the previous pass's results out, which reads these same slots
+        block_lds_barrier();
+    }
+    const int n = threadIdx.x;
+    if (n < nqg) {
         const int32_t e = a.qlist[qbeg + qg0 + n];
         sm.qpair[n] = e;
         sm.qrow[n] = e / a.c;
-        // a chunk of a longer segment starts from the pair's shared bound
-        sm.otheta[n] = single ? 0 : __hip_atomic_load(a.bound + e, __ATOMIC_RELAXED,
-                                                      __HIP_MEMORY_SCOPE_AGENT);
+        pb.v = single ? 0 : __hip_atomic_load(a.bound + e, __ATOMIC_RELAXED,
+                                              __HIP_MEMORY_SCOPE_AGENT);
+        pb.n = n;
+        if constexpr (!kDefer) sm.otheta[n] = pb.v;
     }
-    __syncthreads();
+    if constexpr (kDefer) {
+        block_lds_barrier();
+    } else {
+        __syncthreads();
+    }
+    return pb;
+}
+
+__device__ __forceinline__ void pass_bound(const FineSmem &sm, const PassBound &pb) {
+    if (pb.n >= 0) sm.otheta[pb.n] = pb.v;
 }
 
 // The owned query's buffer starts empty, with the threshold handed over from
@@ -516,7 +548,7 @@ __device__ __forceinline__ void pass_generic(const FineArgs &a, const FineSmem &
     const int d = a.d;
     const T *K = static_cast<const T *>(a.keys);
     const T *Q = static_cast<const T *>(a.q);
-    pass_begin(a, sm, qbeg, qg0, nqg, single);
+    pass_begin<false>(a, sm, qbeg, qg0, nqg, single);
     const T *qp[NQT];
 #pragma unroll
     for (int qt = 0; qt < NQT; ++qt) {
@@ -701,7 +733,7 @@ __device__ __forceinline__ void pass_lds(const FineArgs &a, const FineSmem &sm, 
             lds_load_unit<KT, U>(ring[j], K, a.tid_src, d, NG, min(j, total - 1), r0, r1);
     }
 
-    pass_begin(a, sm, qbeg, qg0, nqg, single);
+    const PassBound pb = pass_begin<true>(a, sm, qbeg, qg0, nqg, single);
     // stage the queries as MFMA B fragments: [k-step][query tile][lane], eight
     // fragments per thread loaded before any is stored. Indices past the end
     // load and store the last fragment again (the same value), so that every
@@ -732,6 +764,7 @@ __device__ __forceinline__ void pass_lds(const FineArgs &a, const FineSmem &sm, 
             }
         }
     }
+    pass_bound(sm, pb);
     // The first ring units are in: no path enters the unit loop with a load
     // outstanding.
     wait_vmcnt<0>();
