@@ -195,3 +195,31 @@ def test_coarse_every_row(B, G, d, c, storage):
     assert np.all(np.diff(ss, axis=1) <= 0)
     top = -np.sort(-ref, axis=1)[:, :c]
     np.testing.assert_allclose(ss, top, rtol=0, atol=1e-4)
+
+
+def test_level_one_merge_groups():
+    """A bank large enough for two merge levels (level-one groups of chunk
+    partials): one 1.5M-row cluster next to 15 of 33K rows, k = 128. The
+    partial buffer (4 B c entries) sets the chunk at 65,536 rows, so the large
+    cluster is 23 chunks whose partials (23 x 128 keys) exceed what one merge
+    level reads. Every query against the oracle."""
+    sizes = tuple([1_500_000] + [33_000] * 15)
+    spec = synth.Spec("groups", B=128, d=64, G=len(sizes), N=sum(sizes), top_c=2, top_k=128,
+                      tau=0.5, storage="bf16", compute="bf16", sizes="fixed", fixed_sizes=sizes)
+    run_case(spec, gen_device="cuda", check_build=False)
+
+
+def test_level_one_merge_groups_selected():
+    """The workload above selects its large cluster (so the two-level merge ran)."""
+    from paper_2605_29734_amd import htam
+    sizes = tuple([1_500_000] + [33_000] * 15)
+    spec = synth.Spec("groups", B=128, d=64, G=len(sizes), N=sum(sizes), top_c=2, top_k=128,
+                      tau=0.5, storage="bf16", compute="bf16", sizes="fixed", fixed_sizes=sizes)
+    w = synth.make(spec, device="cuda", seed=0)
+    bank = htam.Bank(coarse_keys=w.coarse_keys, fine_keys=torch.zeros(1, spec.d, dtype=torch.bfloat16,
+                                                                       device="cuda"),
+                     seg_offsets=torch.zeros(spec.G + 1, dtype=torch.int64, device="cuda"),
+                     transition_id=None, compute="bf16")
+    sel, _ = htam.htam_retrieve_coarse(bank, w.queries, spec.top_c)
+    torch.cuda.synchronize()
+    assert int((sel == 0).sum()) >= 4
