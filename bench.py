@@ -145,8 +145,9 @@ def main():
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py runs on exactly one GPU: multi-GPU runs are not part of this build "
-              "(how the path would shard is described in DESIGN.md)", file=sys.stderr)
+        print("bench.py measures one GPU; runs over several GPUs are not supported "
+              "(one process per GPU, each streaming its own shard of the clusters, is the "
+              "intended split)", file=sys.stderr)
         sys.exit(2)
 
     if args.copy_calibration:

@@ -18,7 +18,8 @@ LIB = os.path.join(PKG, "libhtam.so")
 OBJ_DIR = os.path.join(ROOT, "_build", "htam")
 ARCH = "gfx950"
 FLAGS = ["-O3", "-std=c++17", "-fPIC", "-fvisibility=hidden", f"--offload-arch={ARCH}",
-         # packed fp32 instructions stay off (toolchain notes)
+         # packed fp32 instructions stay off: some of their forms have given wrong
+         # results on this toolchain, with no error
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
          "-I", os.path.join(ROOT, "include")]
 
