@@ -822,6 +822,83 @@ __global__ __launch_bounds__(kWave * kMergeWaves) void slot_merge(MergeArgs a) {
     }
 }
 
+// One-level merges on a small bank (no level-one groups): the four waves of a
+// block share a pair. Wave w merges the w-th quarter of its chunk partials
+// into its own buffer (keys above the pair's bound, cut to k as it fills);
+// wave 0 then merges the four (m, Z) and passes the other buffers' keys
+// through the same filter into its own, sorts and writes the slot. A long
+// cluster's merge is then about a quarter of the chain of requests.
+template <int NPL>
+__global__ __launch_bounds__(kWave * kMergeWaves) void slot_merge_shared(MergeArgs a) {
+    extern __shared__ __align__(16) uint64_t mbuf[];
+    __shared__ float s_m[kMergeWaves], s_z[kMergeWaves];
+    __shared__ int32_t s_c[kMergeWaves];
+    constexpr int cap = NPL * kWave;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const uint64_t lt_mask = (1ull << lane) - 1;
+    uint64_t *buf = mbuf + wave * cap;
+    const int64_t n_merge = a.plan->n_merge;
+    for (int64_t u = blockIdx.x; u < n_merge; u += gridDim.x) {      // block-uniform
+        const MergeSlot ms = a.mlist[u];
+        const int64_t e = ms.e;
+        const uint64_t b = a.bound[e];
+        const uint64_t theta0 = b ? b - 1 : 0;   // the bound itself may be the k-th key
+        const int64_t per = ((int64_t)ms.n + kMergeWaves - 1) / kMergeWaves;
+        const int64_t j0 = min((int64_t)ms.n, wave * per), j1 = min((int64_t)ms.n, j0 + per);
+        float M, Z;
+        const int cnt = merge_partials<NPL>(a.pm, a.pz, a.pc, a.pk, ms.p0 + j0 * ms.stride,
+                                            ms.stride, j1 - j0, a.k, a.cexp, buf, M, Z, theta0);
+        if (lane == 0) {
+            s_m[wave] = M;
+            s_z[wave] = Z;
+            s_c[wave] = cnt;
+        }
+        __syncthreads();
+        if (wave == 0) {
+            float Mt = -INFINITY, Zt = 0.0f;
+#pragma unroll
+            for (int w = 0; w < kMergeWaves; ++w) mz_merge(Mt, Zt, s_m[w], s_z[w], a.cexp);
+            int c0 = s_c[0];
+            uint64_t theta = theta0;
+            for (int w = 1; w < kMergeWaves; ++w) {
+                const int cw = s_c[w];
+                for (int base = 0; base < cw; base += kWave) {
+                    const uint64_t key = base + lane < cw ? mbuf[w * cap + base + lane] : 0;
+                    const bool pass = key > theta;
+                    const uint64_t mask = __ballot(pass);
+                    if (pass) buf[c0 + __popcll(mask & lt_mask)] = key;
+                    c0 += __popcll(mask);
+                    if (c0 > cap - kWave) {
+                        wave_lds_sync();
+                        const MergeCompacted mc = merge_compact<NPL>(buf, c0, a.k);
+                        c0 = mc.n;
+                        theta = mc.theta > theta ? mc.theta : theta;
+                    }
+                }
+            }
+            wave_lds_sync();
+            uint64_t v[NPL];
+#pragma unroll
+            for (int q = 0; q < NPL; ++q) v[q] = (q * kWave + lane < c0) ? buf[q * kWave + lane] : 0;
+            wave_sort_regs<NPL>(v, lane);
+#pragma unroll
+            for (int q = 0; q < NPL; ++q) {
+                const int r = q * kWave + lane;
+                if (r < a.k) {
+                    const uint64_t key = r < c0 ? v[q] : 0;
+                    a.cand_score[e * a.k + r] = key ? key_score(key) : -INFINITY;
+                    a.cand_id[e * a.k + r] = key ? key_id(key) : -1;
+                }
+            }
+            if (lane == 0) {
+                a.slot_max[e] = Mt;
+                a.slot_sum[e] = Zt;
+            }
+        }
+        __syncthreads();           // the buffers and s_* are reused by the next pair
+    }
+}
+
 }  // namespace
 
 // ---------------------------------------------------------------------------
@@ -976,11 +1053,15 @@ template <int NPL>
 static hipError_t launch_merge(const MergeArgs &ma, int64_t u_cap, bool groups, int n_cu,
                                hipStream_t s) {
     const size_t smem = (size_t)kMergeWaves * NPL * kWave * 8;
-    if (groups)
-        hipLaunchKernelGGL(group_merge<NPL>, dim3(merge_grid(u_cap, n_cu)),
-                           dim3(kWave * kMergeWaves), smem, s, ma);
-    hipLaunchKernelGGL(slot_merge<NPL>, dim3(merge_grid(ma.n_pairs, n_cu)),
-                       dim3(kWave * kMergeWaves), smem, s, ma);
+    const dim3 block(kWave * kMergeWaves);
+    if (groups) {
+        hipLaunchKernelGGL(group_merge<NPL>, dim3(merge_grid(u_cap, n_cu)), block, smem, s, ma);
+        hipLaunchKernelGGL(slot_merge<NPL>, dim3(merge_grid(ma.n_pairs, n_cu)), block, smem, s, ma);
+    } else {
+        // one level only: the waves of a block share each pair
+        hipLaunchKernelGGL(slot_merge_shared<NPL>, dim3(merge_grid(ma.n_pairs, n_cu)), block, smem,
+                           s, ma);
+    }
     return hipGetLastError();
 }
 
