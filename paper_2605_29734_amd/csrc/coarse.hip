@@ -201,39 +201,41 @@ struct RawFrag<float> {
 };
 
 // Small problems (fewer 256 x 256 tiles than compute units): one wave per
-// 32 x 32 tile, operands read directly in MFMA fragment layout. A batch of
-// k-steps is requested before any is used (addresses clamped into the row,
-// past-the-end fragments zeroed where they are used), so a batch costs one
-// memory round trip rather than one per k-step.
-template <typename T>
+// TM*16 x TM*16 tile, operands read directly in MFMA fragment layout. A batch
+// of k-steps is requested before any is used (addresses clamped into the
+// row, past-the-end fragments zeroed where they are used), so a batch costs
+// one memory round trip rather than one per k-step. TM = 1 (16 x 16 tiles,
+// twice the k-steps per batch) when 32 x 32 tiles would leave compute units
+// idle: four times the waves, and half the round trips each.
+template <typename T, int TM>
 __global__ __launch_bounds__(kWave) void coarse_small_bf16(const T *__restrict__ q,
                                                            const T *__restrict__ ck, int32_t B,
                                                            int32_t G, int32_t d,
                                                            float *__restrict__ S) {
-    constexpr int kSteps = sizeof(T) == 4 ? 4 : 8;
+    constexpr int kSteps = (sizeof(T) == 4 ? 4 : 8) * (TM == 1 ? 2 : 1);
     const int lane = threadIdx.x & 63;
     const int r16 = lane & 15, kg = lane >> 4;
-    const int64_t row0 = (int64_t)blockIdx.y * 32, col0 = (int64_t)blockIdx.x * 32;
-    const T *qp[2], *cp[2];
+    const int64_t row0 = (int64_t)blockIdx.y * 16 * TM, col0 = (int64_t)blockIdx.x * 16 * TM;
+    const T *qp[TM], *cp[TM];
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
+    for (int i = 0; i < TM; ++i) {
         const int64_t r = row0 + 16 * i + r16, c = col0 + 16 * i + r16;
         qp[i] = q + (r < B ? r : B - 1) * d;
         cp[i] = ck + (c < G ? c : G - 1) * d;
     }
-    f32x4_t acc[2][2];
+    f32x4_t acc[TM][TM];
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        for (int j = 0; j < TM; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     const int nks = (d + 31) / 32;
     for (int s0 = 0; s0 < nks; s0 += kSteps) {
-        RawFrag<T> fa[kSteps][2], fb[kSteps][2];
+        RawFrag<T> fa[kSteps][TM], fb[kSteps][TM];
 #pragma unroll
         for (int st = 0; st < kSteps; ++st) {
             const int k = min(32 * (s0 + st) + 8 * kg, d - 8);
 #pragma unroll
-            for (int i = 0; i < 2; ++i) {
+            for (int i = 0; i < TM; ++i) {
                 fa[st][i].load(qp[i] + k);
                 fb[st][i].load(cp[i] + k);
             }
@@ -243,23 +245,23 @@ __global__ __launch_bounds__(kWave) void coarse_small_bf16(const T *__restrict__
             // steps past the end multiply zeros: no branch for the compiler to
             // sink the loads into
             const bool ok = 32 * (s0 + st) + 8 * kg < d;
-            bf16x8_t a[2], b[2];
+            bf16x8_t a[TM], b[TM];
 #pragma unroll
-            for (int i = 0; i < 2; ++i) {
+            for (int i = 0; i < TM; ++i) {
                 a[i] = ok ? fa[st][i].get() : zero8();
                 b[i] = ok ? fb[st][i].get() : zero8();
             }
 #pragma unroll
-            for (int i = 0; i < 2; ++i)
+            for (int i = 0; i < TM; ++i)
 #pragma unroll
-                for (int j = 0; j < 2; ++j)
+                for (int j = 0; j < TM; ++j)
                     acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
         }
     }
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+        for (int j = 0; j < TM; ++j)
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
                 const int64_t r = row0 + 16 * i + 4 * kg + e, c = col0 + 16 * j + r16;
@@ -335,15 +337,24 @@ hipError_t launch_coarse(int32_t key_dtype, int32_t compute_dtype, int32_t d, in
                      static_cast<const float *>(q), static_cast<const float *>(coarse_keys), B, G,
                      d, w.scores);
     } else if ((int64_t)((B + BM - 1) / BM) * ((G + BN - 1) / BN) < n_cu || d % BK != 0) {
-        const dim3 grid((G + 31) / 32, (B + 31) / 32);
-        if (key_dtype == kF32)
-            launch_timed(coarse_small_bf16<float>, grid, dim3(kWave), 0, s, ev,
-                         static_cast<const float *>(q), static_cast<const float *>(coarse_keys), B,
-                         G, d, w.scores);
+        const bool small_tiles = (int64_t)((G + 31) / 32) * ((B + 31) / 32) < n_cu;
+        const int tile = small_tiles ? 16 : 32;
+        const dim3 grid((G + tile - 1) / tile, (B + tile - 1) / tile);
+        const float *qf = static_cast<const float *>(q), *cf = static_cast<const float *>(coarse_keys);
+        const __bf16 *qb = static_cast<const __bf16 *>(q);
+        const __bf16 *cb = static_cast<const __bf16 *>(coarse_keys);
+        if (key_dtype == kF32 && small_tiles)
+            launch_timed(coarse_small_bf16<float, 1>, grid, dim3(kWave), 0, s, ev, qf, cf, B, G, d,
+                         w.scores);
+        else if (key_dtype == kF32)
+            launch_timed(coarse_small_bf16<float, 2>, grid, dim3(kWave), 0, s, ev, qf, cf, B, G, d,
+                         w.scores);
+        else if (small_tiles)
+            launch_timed(coarse_small_bf16<__bf16, 1>, grid, dim3(kWave), 0, s, ev, qb, cb, B, G, d,
+                         w.scores);
         else
-            launch_timed(coarse_small_bf16<__bf16>, grid, dim3(kWave), 0, s, ev,
-                         static_cast<const __bf16 *>(q), static_cast<const __bf16 *>(coarse_keys),
-                         B, G, d, w.scores);
+            launch_timed(coarse_small_bf16<__bf16, 2>, grid, dim3(kWave), 0, s, ev, qb, cb, B, G, d,
+                         w.scores);
     } else {
         const __bf16 *q16 = static_cast<const __bf16 *>(q);
         const __bf16 *c16 = static_cast<const __bf16 *>(coarse_keys);

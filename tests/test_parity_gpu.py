@@ -165,6 +165,8 @@ def test_attend_out_of_range_selection_is_empty():
     (300, 1000, 200, 5, "bf16"),       # the same with many radix-select cuts per row
     (70, 4099, 64, 100, "f32"),        # fp32 storage rounded to bf16
     (64, 20000, 128, 40, "bf16"),      # long rows for the row top-k
+    (100, 300, 200, 50, "bf16"),       # 16 x 16-tile GEMM (few tiles), ragged, d % 32 != 0
+    (50, 500, 96, 20, "f32"),          # the same with fp32 storage
 ])
 def test_coarse_every_row(B, G, d, c, storage):
     """Coarse retrieval over every row against the oracle's full score matrix
