@@ -134,9 +134,20 @@ __device__ void block_scan_n(int64_t (&v)[N], int64_t (&total)[N], int64_t *s) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     constexpr int waves = kPlanThreads / kWave;
     static_assert(waves == 16, "the wave totals are scanned by one 16-lane row per value");
-    int64_t x[N];
+    // a wave whose values are all zero (threads past the last cluster) skips
+    // the DPP scans: 16 waves share one CU here
+    bool any = false;
 #pragma unroll
-    for (int i = 0; i < N; ++i) x[i] = wave_scan64(v[i]);
+    for (int i = 0; i < N; ++i) any |= v[i] != 0;
+    const bool live = __ballot(any) != 0;
+    int64_t x[N];
+    if (live) {
+#pragma unroll
+        for (int i = 0; i < N; ++i) x[i] = wave_scan64(v[i]);
+    } else {
+#pragma unroll
+        for (int i = 0; i < N; ++i) x[i] = 0;
+    }
     if (lane == kWave - 1) {
 #pragma unroll
         for (int i = 0; i < N; ++i) s[wave * N + i] = x[i];
@@ -176,9 +187,13 @@ template <int N>
 __device__ void block_sum_n(int64_t (&v)[N], int64_t *s) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     constexpr int waves = kPlanThreads / kWave;
+    bool any = false;
+#pragma unroll
+    for (int i = 0; i < N; ++i) any |= v[i] != 0;
+    const bool live = __ballot(any) != 0;      // all-zero waves skip the DPP sums
 #pragma unroll
     for (int i = 0; i < N; ++i) {
-        const int64_t x = wave_sum64(v[i]);
+        const int64_t x = live ? wave_sum64(v[i]) : 0;
         if (lane == 0) s[wave * N + i] = x;
     }
     __syncthreads();
@@ -248,7 +263,15 @@ __device__ int64_t plan_chunks(const PlanArgs &pa, CntOf cnt_of, const int64_t *
     constexpr int kFirst = 4;
     int64_t p4[kFirst];
 #pragma unroll
-    for (int i = 0; i < kFirst; ++i) p4[i] = partials(i);
+    for (int i = 0; i < kFirst; ++i) p4[i] = 0;
+    for (int32_t g = g0; g < g1; ++g) {        // the four in one pass over the clusters
+        const int64_t c = cnt_of(g), len = off[g + 1] - off[g];
+        if (c > 0 && len > 0) {
+#pragma unroll
+            for (int i = 0; i < kFirst; ++i)
+                p4[i] += c * ((len + (int64_t(1) << (lmin + i)) - 1) >> (lmin + i));
+        }
+    }
     block_sum_n<kFirst>(p4, s);
     int cand = -1;
 #pragma unroll
