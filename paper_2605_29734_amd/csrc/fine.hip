@@ -234,8 +234,9 @@ struct PlanMirror {
 // Chunk length and work numbering from the per-cluster query counts (read
 // through cnt_of) and the segment offsets `off` (global or LDS): the chunk is
 // the smallest candidate length for which the partial results fit in p_cap.
-// Writes qoff, wstart, wlast, gstart, mstart, pbase, ubase and the plan, and
-// the same tables to the LDS mirror m when kMirror. Clusters are split into contiguous
+// Writes qoff, wstart, wlast, gstart, mstart, pbase and ubase (to global
+// memory, or with kMirror only to the LDS mirror m, for the fused routing
+// that uses them in the same block) and the plan. Clusters are split into contiguous
 // ranges, one per thread. Returns the chunk length (in every thread).
 template <bool kMirror, typename CntOf>
 __device__ int64_t plan_chunks(const PlanArgs &pa, CntOf cnt_of, const int64_t *off, int64_t *s,
@@ -346,14 +347,17 @@ __device__ int64_t plan_chunks(const PlanArgs &pa, CntOf cnt_of, const int64_t *
                 if (b == i) wl = bnext[i]++;
         }
         const int32_t ws = (int32_t)(w[0] & 0xffffffff), gs = (int32_t)(w[0] >> 32);
-        pa.qoff[g] = (int32_t)qrun;
-        pa.wstart[g] = ws;
-        pa.wlast[g] = wl;
-        pa.pbase[g] = w[1];
-        pa.gstart[g] = gs;
-        pa.ubase[g] = w[2];
-        pa.mstart[g] = (int32_t)w[3];
-        if (kMirror) {
+        // the tables go to global memory for the multi-block routing kernels,
+        // or only to the LDS mirror when the same block goes on to use them
+        if (!kMirror) {
+            pa.qoff[g] = (int32_t)qrun;
+            pa.wstart[g] = ws;
+            pa.wlast[g] = wl;
+            pa.pbase[g] = w[1];
+            pa.gstart[g] = gs;
+            pa.ubase[g] = w[2];
+            pa.mstart[g] = (int32_t)w[3];
+        } else {
             m.qoff[g] = (int32_t)qrun;
             m.wstart[g] = ws;
             m.wlast[g] = wl;
@@ -369,11 +373,12 @@ __device__ int64_t plan_chunks(const PlanArgs &pa, CntOf cnt_of, const int64_t *
         w[3] += nch != 1 ? c : 0;
     }
     if (t == kPlanThreads - 1) {
-        pa.qoff[G] = (int32_t)qtot[0];
-        pa.wstart[G] = (int32_t)n_full;
-        pa.gstart[G] = (int32_t)(wt[0] >> 32);
-        pa.mstart[G] = (int32_t)wt[3];
-        if (kMirror) {
+        if (!kMirror) {
+            pa.qoff[G] = (int32_t)qtot[0];
+            pa.wstart[G] = (int32_t)n_full;
+            pa.gstart[G] = (int32_t)(wt[0] >> 32);
+            pa.mstart[G] = (int32_t)wt[3];
+        } else {
             m.qoff[G] = (int32_t)qtot[0];
             m.wstart[G] = (int32_t)n_full;
             m.gstart[G] = (int32_t)(wt[0] >> 32);
