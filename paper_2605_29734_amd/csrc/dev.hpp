@@ -216,6 +216,26 @@ __device__ __forceinline__ void wave_sort_regs(uint64_t (&v)[NPL], int lane) {
     BitonicSort<1, NPL, Log2Npl<NPL>::value>::run(w, lane);
 }
 
+// Loads the n keys of an LDS buffer (n wave-uniform, at most 64 NPL) into v
+// sorted descending (register j holds ranks 64 j + lane; empty slots 0).
+// Up to 64 keys are sorted as one register, a fraction of the cost of all NPL.
+template <int NPL>
+__device__ __forceinline__ void sort_buffer(const uint64_t *buf, int n, uint64_t (&v)[NPL],
+                                            int lane) {
+    n = __builtin_amdgcn_readfirstlane(n);
+    if (NPL > 1 && n <= kWave) {
+        uint64_t one[1] = {lane < n ? buf[lane] : 0};
+        wave_sort_regs<1>(one, lane);
+        v[0] = one[0];
+#pragma unroll
+        for (int q = 1; q < NPL; ++q) v[q] = 0;
+    } else {
+#pragma unroll
+        for (int q = 0; q < NPL; ++q) v[q] = (q * kWave + lane < n) ? buf[q * kWave + lane] : 0;
+        wave_sort_regs<NPL>(v, lane);
+    }
+}
+
 // a, b: sorted descending. Leaves in a the 64*NPL largest of a and b, sorted.
 template <int NPL>
 __device__ __forceinline__ void wave_merge_top(uint64_t (&a)[NPL], const uint64_t (&b)[NPL],

@@ -830,9 +830,7 @@ __global__ __launch_bounds__(kWave * kMergeWaves) void slot_merge(MergeArgs a) {
             cnt = merge_partials<NPL>(a.pm, a.pz, a.pc, a.pk, ms.p0, ms.stride, ms.n, a.k, a.cexp,
                                       buf, M, Z, theta0);
         uint64_t v[NPL];
-#pragma unroll
-        for (int q = 0; q < NPL; ++q) v[q] = (q * kWave + lane < cnt) ? buf[q * kWave + lane] : 0;
-        wave_sort_regs<NPL>(v, lane);
+        sort_buffer<NPL>(buf, cnt, v, lane);
 #pragma unroll
         for (int q = 0; q < NPL; ++q) {
             const int r = q * kWave + lane;
@@ -906,9 +904,7 @@ __global__ __launch_bounds__(kWave * kMergeWaves) void slot_merge_shared(MergeAr
             }
             wave_lds_sync();
             uint64_t v[NPL];
-#pragma unroll
-            for (int q = 0; q < NPL; ++q) v[q] = (q * kWave + lane < c0) ? buf[q * kWave + lane] : 0;
-            wave_sort_regs<NPL>(v, lane);
+            sort_buffer<NPL>(buf, c0, v, lane);
 #pragma unroll
             for (int q = 0; q < NPL; ++q) {
                 const int r = q * kWave + lane;

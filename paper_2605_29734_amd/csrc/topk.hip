@@ -97,9 +97,7 @@ __global__ __launch_bounds__(kWave * kTopkWaves) void topk_rows(TopkArgs a) {
 
     wave_lds_sync();
     uint64_t v[NPL];
-#pragma unroll
-    for (int q = 0; q < NPL; ++q) v[q] = (q * kWave + lane < cnt) ? buf[q * kWave + lane] : 0;
-    wave_sort_regs<NPL>(v, lane);
+    sort_buffer<NPL>(buf, cnt, v, lane);
     const int kept = cnt < a.top_k ? cnt : a.top_k;
 #pragma unroll
     for (int q = 0; q < NPL; ++q) {
