@@ -832,13 +832,21 @@ __device__ __forceinline__ ItemPass item_pass(const WorkItem &wi) {
 // Runs body(item) for every item this block takes. s_next: two LDS words.
 template <typename Body>
 __device__ __forceinline__ void for_each_item(const FineArgs &a, int32_t *s_next, Body &&body) {
+    // The block's own first item (the grid is at most the item table's
+    // capacity) is requested together with the item count, not after it.
+    // The counter is used only when there are more items than blocks:
+    // otherwise no block takes a second item, and the blocks' atomics on the
+    // one counter at start would hold up each block's first loads (the
+    // loads complete in order behind its contended atomic).
     const int64_t n_items = a.plan->n_items;
+    const WorkItem first = a.items[blockIdx.x];
+    const bool more = n_items > (int64_t)gridDim.x;
     int64_t w = blockIdx.x;
     for (int parity = 0; w < n_items; parity ^= 1) {
         int32_t nxt = 0;
-        if (threadIdx.x == 0) nxt = atomicAdd(&a.plan->next, 1);    // consumed after the item
-        body(item_pass(a.items[w]));
-        if (threadIdx.x == 0) s_next[parity] = (int32_t)gridDim.x + nxt;
+        if (more && threadIdx.x == 0) nxt = atomicAdd(&a.plan->next, 1);   // consumed after the item
+        body(item_pass(w == (int64_t)blockIdx.x ? first : a.items[w]));
+        if (threadIdx.x == 0) s_next[parity] = more ? (int32_t)gridDim.x + nxt : (int32_t)n_items;
         __syncthreads();
         // uniform: the item is then read with scalar loads, which do not
         // count against the vector loads the unit loop waits for
