@@ -34,7 +34,10 @@ sys.path.insert(0, ROOT)
 METRIC = "retrieval queries/sec at fixed bank size; % HBM roofline and % MFMA peak"
 HBM_PEAK_GBS = 8000.0           # MI355X HBM3E
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
-DEFAULT_WORKLOAD = "zipf_bf16"  # 256 queries, d = 512, 256 clusters, 65,536 records
+# the largest single-GPU workload: 8,192 queries, d = 2,048, 16,384 clusters,
+# 4,194,304 fp32 records (34.4 GB, far beyond the 256 MB last-level cache, so
+# every step streams the bank from HBM)
+DEFAULT_WORKLOAD = "before_after_f32"
 
 
 def log(msg):
@@ -86,24 +89,35 @@ def copy_calibration(mib: int, launches: int = 5):
     print(json.dumps({"copy_bytes_per_launch": n, "launches": launches}), flush=True)
 
 
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(spec, w, bank, target_s: float):
-    """Time the CPU oracle on a sample of the workload's queries (host copies excluded)."""
+    """Time the CPU oracle on a seeded uniform sample of 256 of the workload's
+    queries (all of them when there are fewer): coarse scores over every
+    cluster, selection, and the fine stage over the selected segments. Rows
+    are independent, so queries/s on the sample is the oracle's rate on the
+    workload. Host copies of the touched segments are made before the clock
+    starts."""
     import oracle
     cores = int(os.environ.get("OMP_NUM_THREADS") or len(os.sched_getaffinity(0)))
     q = w.queries.float().cpu().numpy()
     c = w.coarse_keys.float().cpu().numpy()
     off = bank.seg_offsets.cpu().numpy()
     tid = bank.transition_id.cpu().numpy()
-    # sample: as many queries as keep the touched bank rows near 2^20
-    head = min(spec.B, 256)
-    qh = oracle.round_bf16(q[:head]) if spec.compute == "bf16" else q[:head]
+    n_rows = min(spec.B, 256)
+    rows = np.sort(np.random.default_rng(0).choice(spec.B, size=n_rows, replace=False))
+    qh = oracle.round_bf16(q[rows]) if spec.compute == "bf16" else q[rows]
     ch = oracle.round_bf16(c) if spec.compute == "bf16" else c
     sel, _ = oracle.coarse(qh, ch, spec.top_c)
-    lens = np.diff(off)
-    per_query = lens[sel].sum(1)
-    n = int(np.searchsorted(np.cumsum(per_query), 1 << 20)) + 1
-    rows = np.arange(min(head, max(n, 1)))
-    touched = np.unique(sel[rows])
+    touched = np.unique(sel)
     seg = {}
     for g in touched:                      # host copies of the touched segments, untimed
         a, b = int(off[g]), int(off[g + 1])
@@ -124,15 +138,16 @@ def cpu_baseline(spec, w, bank, target_s: float):
         if el >= target_s:
             break
     return {"value": done / el, "unit": "queries/s", "cores": cores, "kind": "oracle",
-            "sample": f"{rows.size} of {spec.B} queries x {done // rows.size} passes "
-                      f"({el:.1f} s; coarse scores over all {spec.G} clusters, fine stage over "
-                      f"the selected segments, fp64)"}
+            "cpu_model": cpu_model(),
+            "sample": f"{rows.size} of {spec.B} queries (seeded uniform subset) x "
+                      f"{done // rows.size} passes ({el:.1f} s; coarse scores over all {spec.G} "
+                      f"clusters, fine stage over the selected segments, fp64)"}
 
 
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--steps", type=int, default=40)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--seed", type=int, default=0)
@@ -177,33 +192,50 @@ def main():
     mk = lambda: torch.cuda.Event(enable_timing=True)   # noqa: E731
     ev_s = [(mk(), mk()) for _ in range(n_ev)]
     ev_c = [(mk(), mk()) for _ in range(n_ev)]
+    # per step: start, coarse done, attend done, end (= the next step's start)
+    marks = [[mk() for _ in range(3)] for _ in range(K)] + [[mk()]]
     for a, b in ev_s + ev_c:        # materialise the events before handing them to the library
         a.record()
         b.record()
-    start, end = mk(), mk()
     torch.cuda.synchronize()
+    lib, ks, kc = htam.lib, htam.HTAM_KERNEL_STREAM, htam.HTAM_KERNEL_COARSE
     log(f"[bench] timing {K} steps")
     t0 = time.perf_counter()
-    start.record()
     for i in range(K):
         if i % E == 0:
             j = i // E
-            htam.lib.htam_set_kernel_events(htam.HTAM_KERNEL_STREAM, ev_s[j][0].cuda_event,
-                                            ev_s[j][1].cuda_event)
-            htam.lib.htam_set_kernel_events(htam.HTAM_KERNEL_COARSE, ev_c[j][0].cuda_event,
-                                            ev_c[j][1].cuda_event)
+            lib.htam_set_kernel_events(ks, ev_s[j][0].cuda_event, ev_s[j][1].cuda_event)
+            lib.htam_set_kernel_events(kc, ev_c[j][0].cuda_event, ev_c[j][1].cuda_event)
         elif i % E == 1:
-            htam.lib.htam_set_kernel_events(htam.HTAM_KERNEL_STREAM, None, None)
-            htam.lib.htam_set_kernel_events(htam.HTAM_KERNEL_COARSE, None, None)
-        r.run(q)
-    end.record()
+            lib.htam_set_kernel_events(ks, None, None)
+            lib.htam_set_kernel_events(kc, None, None)
+        marks[i][0].record()
+        htam.htam_retrieve_coarse(r.bank, q, r.c, out=r.sel, ws=r.ws_coarse)
+        marks[i][1].record()
+        htam.htam_attend_transitions(r.bank, q, r.sel[0], r.tau, r.k, out=r.slots, ws=r.ws_attend)
+        marks[i][2].record()
+        htam.htam_topk(r.slots[2], r.slots[3], r.k, r.slots[0], r.slots[1], r.tau, out=r.rows)
+    marks[K][0].record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    htam.lib.htam_set_kernel_events(htam.HTAM_KERNEL_STREAM, None, None)
-    htam.lib.htam_set_kernel_events(htam.HTAM_KERNEL_COARSE, None, None)
-    ms_step = start.elapsed_time(end) / K
-    t_stream = sum(a.elapsed_time(b) for a, b in ev_s) / n_ev * 1e-3
-    t_coarse = sum(a.elapsed_time(b) for a, b in ev_c) / n_ev * 1e-3
+    lib.htam_set_kernel_events(ks, None, None)
+    lib.htam_set_kernel_events(kc, None, None)
+    step_ms = [marks[i][0].elapsed_time(marks[i + 1][0]) for i in range(K)]
+    ms_total = marks[0][0].elapsed_time(marks[K][0])
+    ms_step = ms_total / K
+    med = lambda xs: float(np.median(xs))        # noqa: E731
+    coarse_stage = [marks[i][0].elapsed_time(marks[i][1]) for i in range(K)]
+    attend_stage = [marks[i][1].elapsed_time(marks[i][2]) for i in range(K)]
+    topk_stage = [marks[i][2].elapsed_time(marks[i + 1][0]) for i in range(K)]
+    stream_ms = [a.elapsed_time(b) for a, b in ev_s]
+    gemm_ms = [a.elapsed_time(b) for a, b in ev_c]
+    # on the stamped steps: routing = attend start -> stream start, merges =
+    # stream end -> attend end
+    route_ms = [marks[j * E][1].elapsed_time(ev_s[j][0]) for j in range(n_ev)]
+    merge_ms = [ev_s[j][1].elapsed_time(marks[j * E][2]) for j in range(n_ev)]
+    t_stream = sum(stream_ms) / n_ev * 1e-3
+    t_coarse = sum(gemm_ms) / n_ev * 1e-3
+    t_coarse_stage = med(coarse_stage) * 1e-3
 
     # algorithmic bytes of one bank-stream launch: every row of every selected
     # segment read once, plus the queries
@@ -216,10 +248,11 @@ def main():
     achieved = alg_bytes / t_stream / 1e9
     coarse_flops = 2.0 * spec.B * spec.G * spec.d
     pairs = int((off[sel + 1] - off[sel]).sum())
+    tflops = lambda t: coarse_flops / t / 1e12    # noqa: E731
 
     res = {
         "metric": METRIC,
-        "value": spec.B * K / wall,
+        "value": spec.B * K / (ms_total * 1e-3),
         "unit": "queries/s",
         "n_gpus": 1,
         "steps": K,
@@ -238,13 +271,21 @@ def main():
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "traffic": stream_kernel_traffic(spec.name),
                      "alg_bytes_per_launch": alg_bytes, "launch_ms": t_stream * 1e3},
-        "stages": {"coarse_scores_ms": t_coarse * 1e3,
-                   "coarse_tflops": coarse_flops / t_coarse / 1e12,
-                   "coarse_mfma_frac": coarse_flops / t_coarse / 1e12 / MFMA_BF16_PEAK_TFLOPS,
+        "stages": {"step_ms_median": med(step_ms), "step_ms_min": min(step_ms),
+                   "step_ms_wall": wall / K * 1e3,
+                   "coarse_stage_ms_median": med(coarse_stage),
+                   "coarse_stage_mfma_frac": tflops(t_coarse_stage) / MFMA_BF16_PEAK_TFLOPS,
+                   "coarse_gemm_ms": t_coarse * 1e3,
+                   "coarse_gemm_mfma_frac": tflops(t_coarse) / MFMA_BF16_PEAK_TFLOPS,
+                   "attend_stage_ms_median": med(attend_stage),
+                   "route_ms_median": med(route_ms),
                    "fine_stream_ms": t_stream * 1e3,
+                   "fine_stream_hbm_frac": achieved / HBM_PEAK_GBS,
+                   "slot_merge_ms_median": med(merge_ms),
+                   "final_topk_ms_median": med(topk_stage),
                    "scored_pairs_per_step": pairs,
-                   "step_ms_event": ms_step, "step_ms_wall": wall / K * 1e3,
-                   "kernel_timed_steps": n_ev},
+                   "kernel_timed_steps": n_ev,
+                   "source_sha256": kernel_source_sha256()},
     }
     if not args.no_cpu_baseline:
         log("[bench] CPU oracle baseline")

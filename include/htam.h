@@ -30,6 +30,14 @@
  *   - HTAM_ERR_DEVICE reports a HIP error seen while enqueueing; the message
  *     is available from htam_last_error() on the calling thread.
  *   - Inputs must be finite. NaN or infinite scores give unspecified rankings.
+ *   - The bank's segment offsets are checked on the device by the first kernel
+ *     that reads them, before any record is indexed through them: offsets
+ *     that are not a partition of the rows (off[0] = 0, nondecreasing,
+ *     off[G] = N) give empty slots and no bank read. With the environment
+ *     variable HTAM_VALIDATE set (to anything but "" or "0"),
+ *     htam_attend_transitions waits for that check and returns
+ *     HTAM_ERR_VALUE for malformed offsets or for selected cluster ids
+ *     outside [0, G); this is the only case in which it synchronises.
  *   - Calls are stateless: concurrent calls on distinct streams with
  *     distinct output and workspace buffers are safe.
  */
@@ -54,7 +62,8 @@ typedef enum {
     HTAM_ERR_NULL = -1,      /* a required pointer is NULL                        */
     HTAM_ERR_SHAPE = -2,     /* a size or count is out of its documented range    */
     HTAM_ERR_DTYPE = -3,     /* unsupported dtype or dtype combination            */
-    HTAM_ERR_VALUE = -4,     /* bad value: tau, or invalid records found in build */
+    HTAM_ERR_VALUE = -4,     /* bad value: tau, invalid records found in build,
+                                bad offsets or selections (HTAM_VALIDATE)          */
     HTAM_ERR_WORKSPACE = -5, /* workspace NULL or smaller than the size asked for */
     HTAM_ERR_ALIGN = -6,     /* a pointer is not 16-byte aligned                  */
     HTAM_ERR_DEVICE = -7     /* HIP runtime error (see htam_last_error)           */
@@ -175,7 +184,9 @@ size_t htam_retrieve_coarse_workspace_size(const htam_bank *bank, int32_t n_quer
  *
  *   sel_cluster  [n_queries][top_c] int32, each in [0, G) (as produced by
  *                htam_retrieve_coarse; a query's clusters must be distinct
- *                for the union of htam_topk to be a set).
+ *                for the union of htam_topk to be a set). An id outside
+ *                [0, G) gives an empty slot (HTAM_ERR_VALUE under
+ *                HTAM_VALIDATE).
  *   tau          temperature, finite and > 0.
  *   top_k        1 <= top_k <= HTAM_MAX_TOP_K.
  *   ws, ws_bytes workspace of htam_attend_transitions_workspace_size() bytes.

@@ -38,8 +38,14 @@ __device__ __forceinline__ int32_t key_id(uint64_t k) { return (int32_t)(~(uint3
 // Z = sum exp((s - m) / tau). Evaluated as exp2((s - m) * c), c = log2(e)/tau.
 // (m, Z) (+) (m', Z') = (M, Z e^{(m-M)/tau} + Z' e^{(m'-M)/tau}), M = max(m, m').
 // An empty set is (-inf, 0).
+// Contraction into fused multiply-adds is off here and in the stream's
+// statistics update: every product and sum is rounded on its own, in source
+// order, so the bits of a (query, slot)'s statistics do not depend on which
+// inlined or templated copy of the code computed them (a query's place in its
+// cluster's list, and so its pass and query tile, depends on atomic order).
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ void mz_merge(float &m, float &z, float m2, float z2, float c) {
+#pragma clang fp contract(off)
     if (m2 == -INFINITY) return;
     if (m == -INFINITY) { m = m2; z = z2; return; }
     float M = fmaxf(m, m2);

@@ -68,6 +68,7 @@ __global__ void route_init(int32_t G, int32_t *cnt, int32_t *cursor, Plan *plan)
     if (blockIdx.x == 0 && threadIdx.x == 0) {
         plan->next = 0;
         plan->bad_sel = 0;
+        plan->bad_off = 0;
     }
 }
 
@@ -83,6 +84,7 @@ __global__ void route_count(const int32_t *sel, int64_t n, int32_t G, int32_t *c
 // Inputs and outputs of the planning step (device pointers).
 struct PlanArgs {
     int32_t G;
+    int64_t n_rows;           // N, the bank's rows
     const int64_t *off;
     int32_t *qoff;            // [G+1]
     int32_t *wstart;          // [G+1] first full-length chunk item of each cluster
@@ -418,9 +420,38 @@ struct SlotOut {
     }
 };
 
-// Planning step of the multi-kernel routing (counts in global memory).
+// The bank's segment offsets (global or LDS) must partition its rows:
+// off[0] = 0, nondecreasing, off[G] = N (Eq. local nodes: every record has
+// one parent). Checked by the whole block before any row is indexed through
+// them; returns the verdict in every thread.
+__device__ __forceinline__ bool offsets_bad(const int64_t *off, int32_t G, int64_t N) {
+    int bad = 0;
+    for (int32_t g = threadIdx.x; g < G; g += blockDim.x) bad |= off[g] > off[g + 1];
+    if (threadIdx.x == 0) bad |= off[0] != 0 || off[G] != N;
+    return __syncthreads_or(bad) != 0;
+}
+
+// A plan with no work: nothing is streamed or merged (malformed offsets).
+__device__ __forceinline__ void plan_nothing(Plan *plan) {
+    plan->chunk = 1;
+    plan->n_items = 0;
+    plan->n_parts = 0;
+    plan->n_groups = 0;
+    plan->n_l1 = 0;
+    plan->n_merge = 0;
+    plan->next = 0;
+    plan->bad_off = 1;
+}
+
+// Planning step of the multi-kernel routing (counts in global memory). With
+// malformed offsets the plan is empty and the scatter gives every pair an
+// empty slot.
 __global__ __launch_bounds__(kPlanThreads) void route_plan(PlanArgs pa, const int32_t *cnt) {
     __shared__ int64_t s[(kPlanThreads / kWave + 1) * kChunkCands];
+    if (offsets_bad(pa.off, pa.G, pa.n_rows)) {
+        if (threadIdx.x == 0) plan_nothing(pa.plan);
+        return;
+    }
     plan_chunks<false>(pa, GlobalCnt{cnt}, pa.off, s, PlanMirror{});
 }
 
@@ -532,6 +563,17 @@ __global__ __launch_bounds__(kPlanThreads) void route_fused(PlanArgs pa, const i
     for (int32_t g = t; g < G; g += kPlanThreads) lcnt[g] = 0;
     if (t == 0) s_bad = 0;
     __syncthreads();
+    if (offsets_bad(loff, G, pa.n_rows)) {     // before any row is indexed through them
+        if (t == 0) {
+            plan_nothing(pa.plan);
+            pa.plan->bad_sel = 0;
+        }
+        for (int64_t e = t; e < n; e += kPlanThreads) {
+            bound[e] = 0;
+            out.empty(e);
+        }
+        return;
+    }
     int32_t bad = 0;
     for (int64_t e = t; e < n; e += kPlanThreads) {
         const uint16_t h = lsel[e];
@@ -545,6 +587,7 @@ __global__ __launch_bounds__(kPlanThreads) void route_fused(PlanArgs pa, const i
     if (t == 0) {
         pa.plan->next = 0;
         pa.plan->bad_sel = s_bad;
+        pa.plan->bad_off = 0;
     }
     __syncthreads();
     const int64_t kp = pa.kp;
@@ -613,6 +656,7 @@ __global__ __launch_bounds__(256) void route_items(PlanArgs pa, const int32_t *q
                                                    WorkItem *items, MergeGroup *groups,
                                                    int2 *units, MergeSlot *mlist) {
     const int lane = threadIdx.x & 63;
+    if (pa.plan->bad_off) return;              // malformed offsets: no work
     const int64_t ch = pa.plan->chunk;
     const int lch = 63 - __builtin_clzll((unsigned long long)ch);
     const int64_t kp = pa.kp;
@@ -649,12 +693,13 @@ __global__ __launch_bounds__(256) void route_items(PlanArgs pa, const int32_t *q
 
 __global__ void route_scatter(const int32_t *sel, int64_t n, int32_t G, const int32_t *qoff,
                               int32_t *cursor, int32_t *qlist, int32_t *pos, uint64_t *bound,
-                              SlotOut out) {
+                              SlotOut out, const Plan *plan) {
+    const bool none = plan->bad_off != 0;      // malformed offsets: every slot empty
     for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < n;
          e += (int64_t)gridDim.x * blockDim.x) {
         const int32_t g = sel[e];
         bound[e] = 0;
-        if (g >= 0 && g < G) {
+        if (!none && g >= 0 && g < G) {
             const int32_t slot = atomicAdd(&cursor[g], 1);
             qlist[qoff[g] + slot] = (int32_t)e;
             pos[e] = slot;
@@ -1100,6 +1145,7 @@ hipError_t launch_attend(int32_t key_dtype, int32_t compute_dtype, int32_t d, in
     const int gblocks = (int)((bc + 255) / 256 < 4096 ? (bc + 255) / 256 : 4096);
     PlanArgs pa{};
     pa.G = G;
+    pa.n_rows = N;
     pa.off = seg_offsets;
     pa.qoff = w.qoff;
     pa.wstart = w.wstart;
@@ -1136,7 +1182,7 @@ hipError_t launch_attend(int32_t key_dtype, int32_t compute_dtype, int32_t d, in
         hipLaunchKernelGGL(route_count, dim3(gblocks), dim3(256), 0, s, sel, bc, G, w.cnt, w.plan);
         hipLaunchKernelGGL(route_plan, dim3(1), dim3(kPlanThreads), 0, s, pa, w.cnt);
         hipLaunchKernelGGL(route_scatter, dim3(gblocks), dim3(256), 0, s, sel, bc, G, w.qoff,
-                           w.cursor, w.qlist, w.pos, w.bound, so);
+                           w.cursor, w.qlist, w.pos, w.bound, so, w.plan);
         hipLaunchKernelGGL(route_items, dim3((G + 3) / 4 < 2048 ? (G + 3) / 4 : 2048), dim3(256), 0,
                            s, pa, w.qlist, w.items, w.groups, w.units, w.mlist);
     }

@@ -5,6 +5,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <string>
 
 #include "../../include/htam.h"
@@ -87,6 +88,14 @@ htam_status check_tau(float tau) {
     if (!std::isfinite(tau) || !(tau > 0.0f))
         return fail(HTAM_ERR_VALUE, "tau = %g: need a finite tau > 0", (double)tau);
     return HTAM_OK;
+}
+
+// HTAM_VALIDATE set to anything but "" or "0": the fine stage waits for its
+// planning step and reports malformed bank offsets and out-of-range selected
+// cluster ids as HTAM_ERR_VALUE (read at every call).
+bool validate_mode() {
+    const char *v = std::getenv("HTAM_VALIDATE");
+    return v && v[0] && !(v[0] == '0' && v[1] == 0);
 }
 
 // Compute units of the current device (cached per device).
@@ -226,13 +235,26 @@ HTAM_API htam_status htam_attend_transitions(const htam_bank *bank, const void *
     const htam::AttendWs w =
         htam::attend_layout(ws, bank->d, bank->n_clusters, bank->n_transitions,
                             dtype_bytes(bank->key_dtype), n_queries, top_c, top_k, nullptr);
-    return device_status(
+    const htam_status st = device_status(
         htam::launch_attend(bank->key_dtype, bank->compute_dtype, bank->d, bank->n_clusters,
                             bank->n_transitions, bank->fine_keys, bank->seg_offsets,
                             bank->transition_id, q, n_queries, sel_cluster, top_c, tau, top_k,
                             slot_max, slot_sum, cand_score, cand_id, w, n_cu,
                             g_events[HTAM_KERNEL_STREAM], stream),
         "htam_attend_transitions");
+    if (st != HTAM_OK || !validate_mode()) return st;
+    htam::Plan plan{};
+    hipError_t e = hipMemcpyAsync(&plan, w.plan, sizeof plan, hipMemcpyDeviceToHost, stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(stream);
+    if (e != hipSuccess) return device_status(e, "htam_attend_transitions (validation)");
+    if (plan.bad_off)
+        return fail(HTAM_ERR_VALUE, "bank->seg_offsets is not a partition of [0, %lld): need "
+                    "off[0] = 0, nondecreasing, off[G] = N (no record was read)",
+                    (long long)bank->n_transitions);
+    if (plan.bad_sel)
+        return fail(HTAM_ERR_VALUE, "%d selected cluster ids lie outside [0, %d) (their slots are empty)",
+                    plan.bad_sel, bank->n_clusters);
+    return ok();
 }
 
 // ---------------------------------------------------------------------------

@@ -38,6 +38,8 @@ struct Plan {
     int64_t n_merge;   // (query, slot) pairs whose cluster spans more than one chunk
     int32_t next;      // dynamic work counter of the streaming kernel
     int32_t bad_sel;   // count of selected cluster ids out of range
+    int32_t bad_off;   // 1 if the bank's segment offsets are not a partition of [0, N)
+    int32_t pad;
 };
 
 // One work item of the bank stream: a chunk of one selected cluster's segment,

@@ -179,6 +179,7 @@ __device__ __forceinline__ void stats_reset(Stats<NQT> &st) {
 template <int NQT>
 __device__ __forceinline__ void stats_update(Stats<NQT> &st, const f32x4_t (&acc)[NQT],
                                              int64_t rt, int64_t r1, float cexp) {
+#pragma clang fp contract(off)
     const int kg = (threadIdx.x & 63) >> 4;
     const int64_t nvalid = r1 - (rt + 4 * kg);    // rows of this lane's four that exist
 #pragma unroll

@@ -63,6 +63,8 @@ def run_case(spec, seed=0, rows=None, tau=None, gen_device="cpu", check_build=Tr
         torch.cuda.synchronize()
         for k in gpu:
             assert np.array_equal(gpu[k], again[k], equal_nan=True), f"{k} differs between runs"
+    if callable(rows):      # rows chosen after the GPU run, from its full outputs
+        rows = rows(gpu, np.diff(off))
     if rows is not None:
         rows = np.asarray(rows)
         gpu = {k: v[rows] for k, v in gpu.items()}
@@ -78,4 +80,6 @@ def run_case(spec, seed=0, rows=None, tau=None, gen_device="cpu", check_build=Tr
     rep = parity.check(gpu, to_np(q), to_np(ck), off, spec.top_c, spec.top_k, tau, spec.compute,
                        fetch, gather, transition_id=tid, rows=rows)
     say(f"[ok] {spec.name}: {dict(rep)}")
+    rep["sel"] = gpu["sel"]
+    rep["sizes"] = np.diff(off)
     return rep

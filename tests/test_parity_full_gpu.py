@@ -1,31 +1,57 @@
 """GPU parity at the full workload sizes, in the launch configuration the bench
-times: the whole batch runs on the GPU, and a seeded sample of queries is
-checked against the CPU oracle (rows are independent, so a sample is exact
-for the rows it covers). The oracle streams the sampled rows' segments from
-the device cluster by cluster."""
+times: the whole batch runs on the GPU, and the CPU oracle checks every query
+of the smaller workloads and a seeded uniform subset of 256 queries (seed 0)
+of the two largest (rows are independent, so a subset is exact for the rows
+it covers). The oracle streams the checked rows' segments from the device
+cluster by cluster."""
 import numpy as np
 import pytest
 import torch
 
-from gpu_cases import run_case
+from gpu_cases import run_case, say
 from paper_2605_29734_amd import synth
 
 pytestmark = pytest.mark.gpu
 S = synth.SPECS
 
 
-def _rows(spec, n, seed=0):
-    return np.sort(np.random.default_rng(seed).choice(spec.B, size=n, replace=False))
+def _subset(spec, n, seed=0):
+    return np.sort(np.random.default_rng(seed).choice(spec.B, size=min(n, spec.B), replace=False))
 
 
-@pytest.mark.parametrize("name,n_rows", [
-    ("zipf_bf16", 256),             # every query of the benchmarked workload
-    ("mixture_bf16", 48),
-    ("zipf_large_bf16", 24),
-    ("before_after_f32", 24),
-])
-def test_full_size_sampled(name, n_rows):
-    spec = S[name]
-    run_case(spec, rows=_rows(spec, min(n_rows, spec.B)), gen_device="cuda",
-             check_build=name == "zipf_bf16")
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("name", ["zipf_bf16", "mixture_bf16"])
+def test_full_size_every_query(name):
+    run_case(S[name], gen_device="cuda", check_build=name == "zipf_bf16")
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.timeout(900)
+def test_full_size_zipf_large_subset():
+    """256 seeded queries, plus (if none of them did) the first query that
+    selected the largest cluster (1.35M rows, 329 chunks), so that its
+    two-level merge is checked at full size."""
+    spec = S["zipf_large_bf16"]
+    base = _subset(spec, 256)
+    chosen = {}
+
+    def rows(gpu, sizes):
+        big = int(np.argmax(sizes))
+        hits = np.nonzero((gpu["sel"] == big).any(axis=1))[0]
+        assert hits.size > 0, "no query selected the largest cluster"
+        r = base if np.isin(hits, base).any() else np.union1d(base, hits[:1])
+        chosen["big"], chosen["rows"] = big, r
+        return r
+
+    rep = run_case(spec, rows=rows, gen_device="cuda", check_build=False)
+    assert (rep["sel"] == chosen["big"]).any(), "the checked rows miss the largest cluster"
+    say(f"[ok] largest cluster {chosen['big']} ({int(rep['sizes'][chosen['big']])} rows) "
+        f"checked in {int((rep['sel'] == chosen['big']).any(axis=1).sum())} rows")
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.timeout(900)
+def test_full_size_before_after_subset():
+    spec = S["before_after_f32"]
+    run_case(spec, rows=_subset(spec, 256), gen_device="cuda", check_build=False)
     torch.cuda.empty_cache()
