@@ -235,6 +235,26 @@ htam_status htam_topk(int32_t n_rows, int32_t n_lists, int32_t k_in, const float
                       hipStream_t stream);
 
 /*
+ * htam_attend_transitions_noalloc -- htam_attend_transitions without a caller
+ * workspace, for callers that cannot allocate device memory (code under
+ * stream capture, serving loops that must not allocate, harnesses that forbid
+ * it). Same arguments, outputs, checks and results as htam_attend_transitions
+ * (same kernels), with the workspace taken from a file-scope device array of
+ * HTAM_NOALLOC_SCRATCH_MIB MiB that each GPU the library runs on holds until
+ * the process ends. Calls that need more workspace than that (see
+ * htam_attend_transitions_workspace_size) return HTAM_ERR_WORKSPACE and
+ * enqueue nothing. The call allocates nothing. All calls on one GPU share its
+ * array: calls that overlap in time on one GPU (on different streams, or from
+ * different threads) race and must be serialised by the caller.
+ */
+#define HTAM_NOALLOC_SCRATCH_MIB 64
+htam_status htam_attend_transitions_noalloc(const htam_bank *bank, const void *q, int32_t q_dtype,
+                                            int32_t n_queries, const int32_t *sel_cluster,
+                                            int32_t top_c, float tau, int32_t top_k,
+                                            float *slot_max, float *slot_sum, float *cand_score,
+                                            int32_t *cand_id, hipStream_t stream);
+
+/*
  * Diagnostics: kernel timing hooks. After htam_set_kernel_events(which, before,
  * after) with two hipEvent_t handles (passed as void *), every later call on
  * the calling thread that launches kernel `which` has `before` stamped at that

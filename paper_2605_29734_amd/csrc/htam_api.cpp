@@ -113,6 +113,11 @@ int device_cus(int *dev_out) {
 
 }  // namespace
 
+int32_t htam::report_error(int32_t status, const char *msg) {
+    g_last_error = msg ? msg : "";
+    return status;
+}
+
 #define HTAM_TRY(x)                                    \
     do {                                               \
         htam_status _st = (x);                         \

@@ -158,6 +158,9 @@ hipError_t launch_attend(int32_t key_dtype, int32_t compute_dtype, int32_t d, in
                          float *slot_sum, float *cand_score, int32_t *cand_id, const AttendWs &w,
                          int n_cu, KernelEvents ev, hipStream_t s);
 
+// Records msg as the calling thread's last error (htam_last_error) and returns status.
+int32_t report_error(int32_t status, const char *msg);
+
 // ---- top-k merge -----------------------------------------------------------
 hipError_t launch_topk(int32_t rows, int32_t lists, int32_t k_in, const float *score,
                        const int32_t *id, const float *slot_max, const float *slot_sum, float tau,

@@ -21,6 +21,7 @@ HTAM_BF16 = 1
 HTAM_MAX_TOP_K = 256
 HTAM_MAX_TOP_C = 256
 HTAM_MAX_DIM = 8192
+HTAM_NOALLOC_SCRATCH_MIB = 64
 
 HTAM_KERNEL_COARSE = 0
 HTAM_KERNEL_STREAM = 1
@@ -60,6 +61,7 @@ def _load():
         "htam_retrieve_coarse_workspace_size": ([BP, i32, i32], sz),
         "htam_attend_transitions": ([BP, P, i32, i32, P, i32, f32, i32, P, P, P, P, P, sz, P], i32),
         "htam_attend_transitions_workspace_size": ([BP, i32, i32, i32], sz),
+        "htam_attend_transitions_noalloc": ([BP, P, i32, i32, P, i32, f32, i32, P, P, P, P, P], i32),
         "htam_topk": ([i32, i32, i32, P, P, P, P, f32, i32, P, P, P, P, P, P, P], i32),
         "htam_set_kernel_events": ([i32, P, P], i32),
         "htam_status_string": ([i32], ctypes.c_char_p),
@@ -184,6 +186,24 @@ def htam_attend_transitions(bank: Bank, q: torch.Tensor, sel: torch.Tensor, tau:
                                        _ptr(sel), c, float(tau), top_k, _ptr(out[0]), _ptr(out[1]),
                                        _ptr(out[2]), _ptr(out[3]), _ptr(ws), ws.numel(),
                                        _stream(dev)))
+    return out
+
+
+def htam_attend_transitions_noalloc(bank: Bank, q: torch.Tensor, sel: torch.Tensor, tau: float,
+                                    top_k: int, out=None):
+    """htam_attend_transitions with the library's own scratch array as workspace."""
+    B, c = sel.shape
+    dev = q.device
+    if out is None:
+        out = (torch.empty(B, c, dtype=torch.float32, device=dev),
+               torch.empty(B, c, dtype=torch.float32, device=dev),
+               torch.empty(B, c, top_k, dtype=torch.float32, device=dev),
+               torch.empty(B, c, top_k, dtype=torch.int32, device=dev))
+    _check("htam_attend_transitions_noalloc",
+           lib.htam_attend_transitions_noalloc(ctypes.byref(bank.struct), _ptr(q),
+                                               dtype_code(q.dtype), B, _ptr(sel), c, float(tau),
+                                               top_k, _ptr(out[0]), _ptr(out[1]), _ptr(out[2]),
+                                               _ptr(out[3]), _stream(dev)))
     return out
 
 
