@@ -157,6 +157,42 @@ def build_bank(cluster_of, n_clusters: int):
 
 
 # ---------------------------------------------------------------------------
+# flat memory retrieval (the baseline without a hierarchy)
+# ---------------------------------------------------------------------------
+def flat(q, keys, tau: float, top_k: int, compute: str, transition_id=None,
+         chunk_rows: int = 65536) -> dict:
+    """Flat memory retrieval: every record of the memory is a candidate of
+    every query, with no coarse level (the "Flat Memory Retrieval" baseline
+    of Table 1 and App. C.4; the "w/o hierarchy" ablation of Sec. 5.5).
+    O0 quantisation, O4 scores <q_b, k_j> over all N records, O5 the
+    temperature softmax over all N, O6 the top-k by (-score, caller id).
+
+    q [B][d], keys [N][d] (fp32 arrays; bf16 storage passed widened),
+    transition_id [N] (None = row index). Returns id, score, weight, m, Z,
+    count per query, like the row outputs of retrieve().
+    """
+    q = _f32(q)
+    kk = _f32(keys)
+    if compute == "bf16":
+        quant = round_bf16
+    elif compute == "f32":
+        def quant(x):
+            return _f32(x)
+    else:
+        raise ValueError(compute)
+    qh = quant(q)
+    N = kk.shape[0]
+    parts = [scores(qh, quant(kk[a:min(N, a + chunk_rows)])) for a in range(0, N, chunk_rows)]
+    S = np.concatenate(parts, axis=1) if parts else np.zeros((q.shape[0], 0))
+    ids = (np.arange(N) if transition_id is None else np.asarray(transition_id)).astype(np.int32)
+    B = q.shape[0]
+    off = np.arange(B + 1, dtype=np.int64) * N
+    r = attend_rows(off, S.reshape(-1), np.tile(ids, B), tau, top_k)
+    r["qh"] = qh
+    return r
+
+
+# ---------------------------------------------------------------------------
 # the whole retrieval, composed in the paper's order
 # ---------------------------------------------------------------------------
 def retrieve(q, c, seg_offsets, top_c: int, top_k: int, tau: float, compute: str,

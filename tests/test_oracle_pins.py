@@ -207,6 +207,44 @@ def test_top_c_equal_G_is_flat_retrieval(tau):
         assert r["m"][b] == pytest.approx(m, abs=1e-12)
 
 
+@pytest.mark.parametrize("tau,compute", [(0.07, "f32"), (1.0, "bf16")])
+def test_flat_is_brute_force(tau, compute):
+    """oracle.flat against a full numpy sort and softmax over every record."""
+    rng = np.random.default_rng(21)
+    B, N, d, k = 6, 50, 24, 11
+    q, keys = _unit(rng, B, d), _unit(rng, N, d)
+    keys[7] = keys[3]                                  # an exact tie: lower caller id first
+    tid = rng.permutation(N).astype(np.int32)
+    r = oracle.flat(q, keys, tau, k, compute, transition_id=tid)
+    qq, kq = (oracle.round_bf16(q), oracle.round_bf16(keys)) if compute == "bf16" else (q, keys)
+    S = qq.astype(np.float64) @ kq.astype(np.float64).T
+    for b in range(B):
+        order = np.lexsort((tid, -S[b]))[:k]
+        e = np.exp((S[b] - S[b].max()) / tau)
+        np.testing.assert_array_equal(r["id"][b], tid[order])
+        np.testing.assert_allclose(r["score"][b], S[b, order], rtol=0, atol=1e-12)
+        np.testing.assert_allclose(r["weight"][b], e[order] / e.sum(), rtol=1e-12)
+        assert r["Z"][b] == pytest.approx(e.sum(), rel=1e-12) and r["count"][b] == k
+
+
+def test_flat_equals_hierarchy_with_every_cluster():
+    """Selecting every cluster (top_c = G) leaves the hierarchy nothing to
+    exclude: its row outputs are flat retrieval's, and with fewer clusters
+    selected the flat top-1 can only be at least as good."""
+    rng = np.random.default_rng(22)
+    B, G, d, k = 5, 7, 16, 6
+    off, keys, tid = _bank(rng, G, rng.integers(1, 9, G), d)
+    q, C = _unit(rng, B, d), _unit(rng, G, d)
+    f = oracle.flat(q, keys, 0.5, k, "f32", transition_id=tid)
+    h = oracle.retrieve(q, C, off, G, k, 0.5, "f32", keys=keys, transition_id=tid)
+    for key in ("id", "count"):
+        np.testing.assert_array_equal(f[key], h[key])
+    for key in ("score", "weight", "m", "Z"):        # sums taken in another order
+        np.testing.assert_allclose(f[key], h[key], rtol=1e-12, atol=1e-300)
+    h2 = oracle.retrieve(q, C, off, 2, k, 0.5, "f32", keys=keys, transition_id=tid)
+    assert np.all(f["score"][:, 0] >= h2["score"][:, 0])
+
+
 def test_hierarchy_masks_unselected_clusters():
     """The best record overall sits in a cluster that is not selected: it must not appear."""
     rng = np.random.default_rng(6)
