@@ -71,7 +71,9 @@ typedef enum {
 
 /* Limits checked by the calls. */
 #define HTAM_MAX_TOP_K 256   /* 1 <= top_k <= HTAM_MAX_TOP_K                      */
-#define HTAM_MAX_TOP_C 256   /* 1 <= top_c <= min(n_clusters, HTAM_MAX_TOP_C)     */
+#define HTAM_MAX_TOP_C 256   /* 1 <= top_c <= min(n_clusters, HTAM_MAX_TOP_C);
+                                selecting every cluster of a larger bank is
+                                htam_retrieve_flat                              */
 #define HTAM_MAX_DIM 8192    /* 8 <= d <= HTAM_MAX_DIM, d % 8 == 0                */
 
 /*
@@ -233,6 +235,38 @@ htam_status htam_topk(int32_t n_rows, int32_t n_lists, int32_t k_in, const float
                       float tau, int32_t top_k, int32_t *out_id, float *out_score,
                       float *out_weight, float *row_max, float *row_sum, int32_t *out_count,
                       hipStream_t stream);
+
+/*
+ * htam_retrieve_flat -- flat memory retrieval: the baseline without a
+ * hierarchy, in which every record of the memory is a candidate of every
+ * query (the "Flat Memory Retrieval" row of Table 1 and App. C.4; the
+ * "w/o hierarchy" ablation of Sec. 5.5). Scores are <q_b, k_j> over all N
+ * rows of fine_keys (seg_offsets and coarse_keys are not read), the weights
+ * the temperature softmax over all N, and the result the top_k records by
+ * descending score, ties to the lower caller id. It equals the row outputs of
+ * the hierarchical path when every cluster is selected.
+ *
+ *   q            [n_queries][d], element type q_dtype (as in the other calls).
+ *   tau          temperature, finite and > 0.
+ *   top_k        1 <= top_k <= HTAM_MAX_TOP_K.
+ *   out_id, out_score [n_queries][top_k] out: by descending score, ties to
+ *                the lower caller id, padded with (-1, -inf) when N < top_k.
+ *   out_weight   [n_queries][top_k] out or NULL: exp((s - row_max)/tau)/row_sum
+ *                (padding 0).
+ *   row_max, row_sum [n_queries] out or NULL: max over all N scores, and the
+ *                sum of exp((s - row_max)/tau) (-inf and 0 when N = 0).
+ *   out_count    [n_queries] out or NULL: min(top_k, N).
+ *   ws, ws_bytes workspace of htam_retrieve_flat_workspace_size() bytes
+ *                (the score buffer is bounded: the bank is scored in bands).
+ * The kernel timing hook HTAM_KERNEL_COARSE stamps this call's score GEMM
+ * launches (the last band's when there are several).
+ */
+htam_status htam_retrieve_flat(const htam_bank *bank, const void *q, int32_t q_dtype,
+                               int32_t n_queries, float tau, int32_t top_k, int32_t *out_id,
+                               float *out_score, float *out_weight, float *row_max,
+                               float *row_sum, int32_t *out_count, void *ws, size_t ws_bytes,
+                               hipStream_t stream);
+size_t htam_retrieve_flat_workspace_size(const htam_bank *bank, int32_t n_queries, int32_t top_k);
 
 /*
  * htam_attend_transitions_noalloc -- htam_attend_transitions without a caller

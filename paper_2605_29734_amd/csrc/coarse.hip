@@ -16,7 +16,9 @@
 // fp32 arithmetic (small configurations): a direct MFMA kernel on
 //   v_mfma_f32_16x16x4f32.
 // The scores go to a [B][G] fp32 workspace; the top-c selection is the
-// row-wise top-k kernel with implicit ids.
+// row-wise top-k kernel with implicit ids; rows longer than 2048 clusters go
+// through the segmented top-k first (2048 clusters per wave, held in
+// registers) and then a merge of the segments' lists.
 #include "dev.hpp"
 #include "internal.hpp"
 
@@ -31,11 +33,15 @@ constexpr int kStageBytes = (BM + BN) * BK * 2;           // 32 KiB: 512 rows x 
 constexpr size_t kGemmLds = (size_t)kStages * kStageBytes;
 constexpr int kLoadsPerWave = (BM + BN) * BK / 8 / kWave / (kGemmThreads / kWave);   // 4
 
-// fp32 -> bf16 (round to nearest even), 8 elements per thread.
-__global__ void to_bf16(const float *__restrict__ x, __bf16 *__restrict__ y, int64_t n8) {
-    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n8;
-         i += (int64_t)gridDim.x * blockDim.x)
-        reinterpret_cast<bf16x8_t *>(y)[i] = load8(x + i * 8);
+// fp32 -> bf16 (round to nearest even) of two arrays in one launch (the
+// queries and the coarse keys), 8 elements per thread.
+__global__ void to_bf16(const float *__restrict__ x0, __bf16 *__restrict__ y0, int64_t n0,
+                        const float *__restrict__ x1, __bf16 *__restrict__ y1, int64_t n1) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n0 + n1;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        if (i < n0) reinterpret_cast<bf16x8_t *>(y0)[i] = load8(x0 + i * 8);
+        else reinterpret_cast<bf16x8_t *>(y1)[i - n0] = load8(x1 + (i - n0) * 8);
+    }
 }
 
 // Tile of block b: the blocks that run on one XCD (b % 8) take consecutive
@@ -316,69 +322,88 @@ __global__ __launch_bounds__(256) void coarse_f32(const float *__restrict__ q,
 
 }  // namespace
 
+
 CoarseWs coarse_layout(void *ws, int32_t B, int32_t G, int32_t d, int32_t key_dtype,
-                       int32_t compute_dtype, size_t *bytes) {
+                       int32_t compute_dtype, int32_t top_c, size_t *bytes) {
     Carve cv(ws);
     CoarseWs w{};
     w.scores = cv.take<float>((size_t)B * G);
     const bool convert = compute_dtype == kBF16 && key_dtype == kF32;
     w.q16 = convert ? cv.take<__bf16>((size_t)B * d) : nullptr;
     w.c16 = convert ? cv.take<__bf16>((size_t)G * d) : nullptr;
+    // score rows longer than one segment of the segmented top-k are cut into
+    // segments (one wave each, then a merge of the segments' lists): many
+    // short units keep far more loads in flight than one wave per row
+    const int32_t seg = seg_topk_cols();
+    w.n_seg = G > seg ? (G + seg - 1) / seg : 1;
+    const size_t np = w.n_seg > 1 ? (size_t)B * w.n_seg * seg_topk_slots(top_c) : 0;
+    w.p_score = np ? cv.take<float>(np) : nullptr;
+    w.p_id = np ? cv.take<int32_t>(np) : nullptr;
     if (bytes) *bytes = cv.off + 256;
     return w;
 }
 
-hipError_t launch_coarse(int32_t key_dtype, int32_t compute_dtype, int32_t d, int32_t G,
-                         const void *coarse_keys, const void *q, int32_t B, int32_t top_c,
-                         int32_t *sel, float *sel_score, const CoarseWs &w, int n_cu,
-                         KernelEvents ev, hipStream_t s) {
+hipError_t launch_scores(int32_t key_dtype, int32_t compute_dtype, int32_t d, int64_t n,
+                         const void *keys, const void *q, int32_t B, float *S, __bf16 *q16,
+                         __bf16 *k16, bool convert_q, int n_cu, KernelEvents ev, hipStream_t s) {
+    const int32_t G = (int32_t)n;
     if (compute_dtype == kF32) {
         launch_timed(coarse_f32, dim3((G + 63) / 64, (B + 63) / 64), dim3(256), 0, s, ev,
-                     static_cast<const float *>(q), static_cast<const float *>(coarse_keys), B, G,
-                     d, w.scores);
+                     static_cast<const float *>(q), static_cast<const float *>(keys), B, G, d, S);
     } else if ((int64_t)((B + BM - 1) / BM) * ((G + BN - 1) / BN) < n_cu || d % BK != 0) {
         const bool small_tiles = (int64_t)((G + 31) / 32) * ((B + 31) / 32) < n_cu;
         const int tile = small_tiles ? 16 : 32;
         const dim3 grid((G + tile - 1) / tile, (B + tile - 1) / tile);
-        const float *qf = static_cast<const float *>(q), *cf = static_cast<const float *>(coarse_keys);
+        const float *qf = static_cast<const float *>(q), *cf = static_cast<const float *>(keys);
         const __bf16 *qb = static_cast<const __bf16 *>(q);
-        const __bf16 *cb = static_cast<const __bf16 *>(coarse_keys);
+        const __bf16 *cb = static_cast<const __bf16 *>(keys);
         if (key_dtype == kF32 && small_tiles)
-            launch_timed(coarse_small_bf16<float, 1>, grid, dim3(kWave), 0, s, ev, qf, cf, B, G, d,
-                         w.scores);
+            launch_timed(coarse_small_bf16<float, 1>, grid, dim3(kWave), 0, s, ev, qf, cf, B, G, d, S);
         else if (key_dtype == kF32)
-            launch_timed(coarse_small_bf16<float, 2>, grid, dim3(kWave), 0, s, ev, qf, cf, B, G, d,
-                         w.scores);
+            launch_timed(coarse_small_bf16<float, 2>, grid, dim3(kWave), 0, s, ev, qf, cf, B, G, d, S);
         else if (small_tiles)
-            launch_timed(coarse_small_bf16<__bf16, 1>, grid, dim3(kWave), 0, s, ev, qb, cb, B, G, d,
-                         w.scores);
+            launch_timed(coarse_small_bf16<__bf16, 1>, grid, dim3(kWave), 0, s, ev, qb, cb, B, G, d, S);
         else
-            launch_timed(coarse_small_bf16<__bf16, 2>, grid, dim3(kWave), 0, s, ev, qb, cb, B, G, d,
-                         w.scores);
+            launch_timed(coarse_small_bf16<__bf16, 2>, grid, dim3(kWave), 0, s, ev, qb, cb, B, G, d, S);
     } else {
-        const __bf16 *q16 = static_cast<const __bf16 *>(q);
-        const __bf16 *c16 = static_cast<const __bf16 *>(coarse_keys);
+        const __bf16 *qa = static_cast<const __bf16 *>(q);
+        const __bf16 *ka = static_cast<const __bf16 *>(keys);
         if (key_dtype == kF32) {
-            const int64_t nq = (int64_t)B * d / 8, nc = (int64_t)G * d / 8;
-            hipLaunchKernelGGL(to_bf16, dim3((unsigned)((nq + 255) / 256 < 4096 ? (nq + 255) / 256 : 4096)),
-                               dim3(256), 0, s, static_cast<const float *>(q), w.q16, nq);
-            hipLaunchKernelGGL(to_bf16, dim3((unsigned)((nc + 255) / 256 < 4096 ? (nc + 255) / 256 : 4096)),
-                               dim3(256), 0, s, static_cast<const float *>(coarse_keys), w.c16, nc);
-            q16 = w.q16;
-            c16 = w.c16;
+            const int64_t nq = convert_q ? (int64_t)B * d / 8 : 0, nc = (int64_t)G * d / 8;
+            const int64_t nb = (nq + nc + 255) / 256;
+            hipLaunchKernelGGL(to_bf16, dim3((unsigned)(nb < 8192 ? nb : 8192)), dim3(256), 0, s,
+                               static_cast<const float *>(q), q16, nq,
+                               static_cast<const float *>(keys), k16, nc);
+            qa = q16;
+            ka = k16;
         }
         hipError_t err = hipFuncSetAttribute((const void *)coarse_gemm,
                                              hipFuncAttributeMaxDynamicSharedMemorySize,
                                              (int)kGemmLds);
         if (err != hipSuccess) return err;
         const int tiles = ((B + BM - 1) / BM) * ((G + BN - 1) / BN);
-        launch_timed(coarse_gemm, dim3(tiles), dim3(kGemmThreads), kGemmLds, s, ev, q16, c16, B, G,
-                     d, w.scores);
+        launch_timed(coarse_gemm, dim3(tiles), dim3(kGemmThreads), kGemmLds, s, ev, qa, ka, B, G,
+                     d, S);
     }
-    hipError_t err = hipGetLastError();
+    return hipGetLastError();
+}
+
+hipError_t launch_coarse(int32_t key_dtype, int32_t compute_dtype, int32_t d, int32_t G,
+                         const void *coarse_keys, const void *q, int32_t B, int32_t top_c,
+                         int32_t *sel, float *sel_score, const CoarseWs &w, int n_cu,
+                         KernelEvents ev, hipStream_t s) {
+    hipError_t err = launch_scores(key_dtype, compute_dtype, d, G, coarse_keys, q, B, w.scores,
+                                   w.q16, w.c16, true, n_cu, ev, s);
     if (err != hipSuccess) return err;
-    return launch_topk(B, 1, G, w.scores, nullptr, nullptr, nullptr, 1.0f, top_c, sel, sel_score,
-                       nullptr, nullptr, nullptr, nullptr, s);
+    if (w.n_seg == 1)
+        return launch_topk(B, 1, G, w.scores, nullptr, nullptr, nullptr, 1.0f, top_c, sel,
+                           sel_score, nullptr, nullptr, nullptr, nullptr, s);
+    // each (query, segment) keeps its best top_c, then the segments' lists are merged
+    err = launch_seg_topk(B, G, G, w.scores, nullptr, 0, top_c, 1.0f, w.p_score, w.p_id, nullptr,
+                          nullptr, w.n_seg, 0, s);
+    if (err != hipSuccess) return err;
+    return launch_topk(B, w.n_seg, seg_topk_slots(top_c), w.p_score, w.p_id, nullptr, nullptr,
+                       1.0f, top_c, sel, sel_score, nullptr, nullptr, nullptr, nullptr, s);
 }
 
 }  // namespace htam

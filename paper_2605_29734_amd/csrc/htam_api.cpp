@@ -172,11 +172,10 @@ HTAM_API htam_status htam_memory_build(int64_t n, int32_t n_clusters, int32_t d,
 // ---------------------------------------------------------------------------
 HTAM_API size_t htam_retrieve_coarse_workspace_size(const htam_bank *bank, int32_t n_queries,
                                                     int32_t top_c) {
-    (void)top_c;
-    if (!bank || n_queries < 0 || bank->n_clusters < 1) return 0;
+    if (!bank || n_queries < 0 || bank->n_clusters < 1 || top_c < 1) return 0;
     size_t bytes = 0;
     htam::coarse_layout(nullptr, n_queries, bank->n_clusters, bank->d, bank->key_dtype,
-                        bank->compute_dtype, &bytes);
+                        bank->compute_dtype, top_c, &bytes);
     return bytes;
 }
 
@@ -195,7 +194,8 @@ HTAM_API htam_status htam_retrieve_coarse(const htam_bank *bank, const void *q, 
     const int n_cu = device_cus(nullptr);
     if (n_cu <= 0) return fail(HTAM_ERR_DEVICE, "no HIP device");
     const htam::CoarseWs w = htam::coarse_layout(ws, n_queries, bank->n_clusters, bank->d,
-                                                 bank->key_dtype, bank->compute_dtype, nullptr);
+                                                 bank->key_dtype, bank->compute_dtype, top_c,
+                                                 nullptr);
     return device_status(htam::launch_coarse(bank->key_dtype, bank->compute_dtype, bank->d,
                                              bank->n_clusters, bank->coarse_keys, q, n_queries,
                                              top_c, sel_cluster, sel_score, w, n_cu,
@@ -260,6 +260,41 @@ HTAM_API htam_status htam_attend_transitions(const htam_bank *bank, const void *
         return fail(HTAM_ERR_VALUE, "%d selected cluster ids lie outside [0, %d) (their slots are empty)",
                     plan.bad_sel, bank->n_clusters);
     return ok();
+}
+
+// ---------------------------------------------------------------------------
+HTAM_API size_t htam_retrieve_flat_workspace_size(const htam_bank *bank, int32_t n_queries,
+                                                  int32_t top_k) {
+    if (!bank || n_queries < 0 || top_k < 1 || bank->d < 8 || bank->n_transitions < 0) return 0;
+    size_t bytes = 0;
+    htam::flat_layout(nullptr, bank->d, bank->n_transitions, bank->key_dtype, bank->compute_dtype,
+                      n_queries, top_k, &bytes);
+    return bytes;
+}
+
+HTAM_API htam_status htam_retrieve_flat(const htam_bank *bank, const void *q, int32_t q_dtype,
+                                        int32_t n_queries, float tau, int32_t top_k,
+                                        int32_t *out_id, float *out_score, float *out_weight,
+                                        float *row_max, float *row_sum, int32_t *out_count,
+                                        void *ws, size_t ws_bytes, hipStream_t stream) {
+    HTAM_TRY(check_bank(bank));
+    HTAM_TRY(check_query(bank, q, q_dtype, n_queries));
+    if (top_k < 1 || top_k > HTAM_MAX_TOP_K)
+        return fail(HTAM_ERR_SHAPE, "top_k = %d out of [1, %d]", top_k, HTAM_MAX_TOP_K);
+    HTAM_TRY(check_tau(tau));
+    if (n_queries == 0) return ok();
+    if (!out_id || !out_score) return fail(HTAM_ERR_NULL, "out_id / out_score is NULL");
+    HTAM_TRY(check_ws(ws, ws_bytes, htam_retrieve_flat_workspace_size(bank, n_queries, top_k)));
+    const int n_cu = device_cus(nullptr);
+    if (n_cu <= 0) return fail(HTAM_ERR_DEVICE, "no HIP device");
+    const htam::FlatWs w = htam::flat_layout(ws, bank->d, bank->n_transitions, bank->key_dtype,
+                                             bank->compute_dtype, n_queries, top_k, nullptr);
+    return device_status(htam::launch_flat(bank->key_dtype, bank->compute_dtype, bank->d,
+                                           bank->n_transitions, bank->fine_keys,
+                                           bank->transition_id, q, n_queries, tau, top_k, out_id,
+                                           out_score, out_weight, row_max, row_sum, out_count, w,
+                                           n_cu, g_events[HTAM_KERNEL_COARSE], stream),
+                         "htam_retrieve_flat");
 }
 
 // ---------------------------------------------------------------------------

@@ -109,9 +109,12 @@ struct CoarseWs {
     float *scores;     // [B][G]
     __bf16 *q16;       // [B][d] bf16 copy of fp32 queries (bf16 arithmetic on fp32 storage)
     __bf16 *c16;       // [G][d] bf16 copy of fp32 coarse keys
+    int32_t n_seg;     // segments per score row in the top-c selection
+    float *p_score;    // [B][n_seg][top_c] per-segment selections (n_seg > 1)
+    int32_t *p_id;
 };
 CoarseWs coarse_layout(void *ws, int32_t B, int32_t G, int32_t d, int32_t key_dtype,
-                       int32_t compute_dtype, size_t *bytes);
+                       int32_t compute_dtype, int32_t top_c, size_t *bytes);
 hipError_t launch_coarse(int32_t key_dtype, int32_t compute_dtype, int32_t d, int32_t G,
                          const void *coarse_keys, const void *q, int32_t B, int32_t top_c,
                          int32_t *sel, float *sel_score, const CoarseWs &w, int n_cu,
@@ -157,6 +160,44 @@ hipError_t launch_attend(int32_t key_dtype, int32_t compute_dtype, int32_t d, in
                          const int32_t *sel, int32_t c, float tau, int32_t k, float *slot_max,
                          float *slot_sum, float *cand_score, int32_t *cand_id, const AttendWs &w,
                          int n_cu, KernelEvents ev, hipStream_t s);
+
+// Segmented row top-k: rows of n scores (row_stride apart) cut into n_seg
+// segments of seg_topk_cols() columns; segment s of row r writes a list of
+// seg_topk_slots(top_k) (score, id) entries holding its top_k (unsorted,
+// padded with (-inf, -1)) as list r * o_lists + o_seg0 + s of o_score/o_id
+// [rows][o_lists][slots], and with o_m/o_z non-null its softmax statistics
+// there too. Column j's id is col_id[j] (or id_base + j without col_id).
+int32_t seg_topk_cols();
+int32_t seg_topk_slots(int32_t top_k);
+hipError_t launch_seg_topk(int64_t rows, int64_t row_stride, int64_t n, const float *score,
+                           const int32_t *col_id, int64_t id_base, int32_t top_k, float tau,
+                           float *o_score, int32_t *o_id, float *o_m, float *o_z, int64_t o_lists,
+                           int64_t o_seg0, hipStream_t s);
+
+// S[B][n] = Q K^T over n key rows (row stride n), on the coarse GEMM kernels.
+// With fp32 storage and bf16 arithmetic the 256 x 256-tile kernel reads bf16
+// copies: k16 [n][d] is made here, q16 [B][d] too when convert_q.
+hipError_t launch_scores(int32_t key_dtype, int32_t compute_dtype, int32_t d, int64_t n,
+                         const void *keys, const void *q, int32_t B, float *S, __bf16 *q16,
+                         __bf16 *k16, bool convert_q, int n_cu, KernelEvents ev, hipStream_t s);
+
+// ---- flat retrieval (every record a candidate) --------------------------------
+struct FlatWs {
+    int64_t band;      // key rows scored per GEMM launch (a multiple of the segment length)
+    int64_t n_lists;   // per-query partial lists over all bands
+    float *scores;     // [B][band]
+    __bf16 *q16, *k16; // bf16 copies (fp32 storage, bf16 arithmetic)
+    float *p_score;    // [B][n_lists][k]
+    int32_t *p_id;
+    float *pm, *pz;    // [B][n_lists]
+};
+FlatWs flat_layout(void *ws, int32_t d, int64_t N, int32_t key_dtype, int32_t compute_dtype,
+                   int32_t B, int32_t k, size_t *bytes);
+hipError_t launch_flat(int32_t key_dtype, int32_t compute_dtype, int32_t d, int64_t N,
+                       const void *fine_keys, const int32_t *transition_id, const void *q,
+                       int32_t B, float tau, int32_t k, int32_t *out_id, float *out_score,
+                       float *out_weight, float *row_max, float *row_sum, int32_t *out_count,
+                       const FlatWs &w, int n_cu, KernelEvents ev, hipStream_t s);
 
 // Records msg as the calling thread's last error (htam_last_error) and returns status.
 int32_t report_error(int32_t status, const char *msg);

@@ -118,7 +118,231 @@ __global__ __launch_bounds__(kWave * kTopkWaves) void topk_rows(TopkArgs a) {
     }
 }
 
+// Segmented row top-k with optional softmax statistics. A unit is one
+// segment of kSegCols consecutive columns of one score row, handled by one
+// wave that loads the whole segment into registers at once (kSegPer scores
+// per lane, every load in flight together; with caller ids, those too).
+//
+// Candidates: with top_k <= 64, only scores at or above T, the top_k-th
+// largest of the 64 lanes' maximum scores, can be in the segment's top-k
+// (those maxima are top_k entries scoring at least T). T comes from a radix
+// select over the lane maxima, one ballot per bit. Random scores leave a few
+// more than top_k candidates; each is written straight to the unit's output
+// list (k_slot >= top_k slots, unsorted, padded with (-inf, -1)) at its
+// ballot prefix position. A superset of the segment's top-k is all the row
+// merge (topk_rows) needs. Only if the candidates overflow the list (many
+// ties, or top_k > 64 where no bound is taken) does the unit fall back to
+// the LDS buffer with radix-select compaction of topk_rows and write its
+// exact top_k, sorted.
+//
+// Statistics: the segment's maximum (the largest lane maximum), then one sum
+// of exp((s - max)/tau) per lane, written for the row merge.
+//
+// The work per score is a compare and a ballot for most scores: a wave64
+// VALU instruction issues over four cycles, so the instruction count, not
+// the memory traffic, decides whether this kernel keeps up with HBM.
+constexpr int kSegCols = 2048;
+constexpr int kSegPer = kSegCols / kWave;  // 32 scores per lane
+
+struct SegArgs {
+    int64_t rows, row_stride;      // score rows and the elements between them
+    int64_t n;                     // columns per row
+    int64_t units;                 // rows * n_seg
+    int32_t n_seg, top_k, k_slot;
+    int32_t stats;                 // 1: also the segment's softmax statistics
+    float cexp;                    // log2(e) / tau
+    const float *score;
+    const int32_t *col_id;         // column j's id is col_id[j] (IDS), else id_base + j
+    int64_t id_base;
+    float *o_score;                // [rows][o_lists][k_slot], this call's lists from o_seg0
+    int32_t *o_id;
+    float *o_m, *o_z;              // [rows][o_lists] (stats only)
+    int64_t o_lists, o_seg0;
+};
+
+struct SegCompacted {
+    int n;
+    uint64_t theta;
+};
+template <int NPL>
+__device__ __noinline__ SegCompacted seg_compact(uint64_t *buf, int n, int k) {
+    SegCompacted r;
+    r.theta = 0;
+    r.n = compact_select<NPL>(buf, n, k, kWave, threadIdx.x & 63, r.theta);
+    return r;
+}
+
+template <int NPL, bool IDS>
+__global__ __launch_bounds__(kWave * kTopkWaves) void seg_topk(SegArgs a) {
+    extern __shared__ __align__(16) uint64_t tbuf[];
+    constexpr int cap = NPL * kWave;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int64_t u = (int64_t)blockIdx.x * kTopkWaves + wave;
+    if (u >= a.units) return;               // no block-wide synchronisation below
+    const int64_t row = u / a.n_seg, seg = u - row * a.n_seg;
+    const int64_t ol = row * a.o_lists + a.o_seg0 + seg;    // output list
+    const int64_t c0 = seg * kSegCols;
+    const int len = (int)min((int64_t)kSegCols, a.n - c0);
+    const float *sc = a.score + row * a.row_stride + c0;
+    const uint64_t lt_mask = (1ull << lane) - 1;
+    float *os = a.o_score + ol * a.k_slot;
+    int32_t *oi = a.o_id + ol * a.k_slot;
+
+    // column j * 64 + lane in register j (unconditional loads clamped into
+    // the segment; past-the-end columns become -inf and are never candidates)
+    float s[kSegPer];
+    int32_t id[IDS ? kSegPer : 1];
+#pragma unroll
+    for (int j = 0; j < kSegPer; ++j) s[j] = sc[min(j * kWave + lane, len - 1)];
+    if constexpr (IDS) {
+#pragma unroll
+        for (int j = 0; j < kSegPer; ++j) id[j] = a.col_id[c0 + min(j * kWave + lane, len - 1)];
+    }
+    if (len < kSegCols) {
+#pragma unroll
+        for (int j = 0; j < kSegPer; ++j)
+            if (j * kWave + lane >= len) s[j] = -INFINITY;
+    }
+    if constexpr (IDS) {
+#pragma unroll
+        for (int j = 0; j < kSegPer; ++j)
+            if (id[j] < 0) s[j] = -INFINITY;          // not a record
+    }
+    float lmax = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < kSegPer; ++j) lmax = fmaxf(lmax, s[j]);
+
+    // T: the top_k-th largest lane maximum, bit by bit on the ordered bits
+    float T = -INFINITY;
+    if (a.top_k <= kWave) {
+        const uint32_t o = lmax == -INFINITY ? 0u : ord_of(lmax);
+        uint32_t t = 0;
+        for (int bit = 31; bit >= 0; --bit) {
+            const uint32_t cand = t | (1u << bit);
+            if (__popcll(__ballot(o >= cand)) >= a.top_k) t = cand;
+        }
+        if (t) T = score_of_ord(t);
+    }
+    // candidates straight to the output list
+    int cnt = 0;
+#pragma unroll
+    for (int j = 0; j < kSegPer; ++j) {
+        const bool pass = s[j] >= T && s[j] != -INFINITY;
+        const uint64_t mask = __ballot(pass);
+        if (mask) {
+            const int pos = cnt + __popcll(mask & lt_mask);
+            if (pass && pos < a.k_slot) {
+                os[pos] = s[j];
+                oi[pos] = IDS ? id[j] : (int32_t)(a.id_base + c0 + j * kWave + lane);
+            }
+            cnt += __popcll(mask);
+        }
+    }
+    if (cnt <= a.k_slot) {
+        for (int r = cnt + lane; r < a.k_slot; r += kWave) {
+            os[r] = -INFINITY;
+            oi[r] = -1;
+        }
+    } else {
+        // overflow: the exact top_k through the LDS buffer, sorted
+        uint64_t *buf = tbuf + wave * cap;
+        int bc = 0;
+        uint64_t theta = 0;
+#pragma unroll
+        for (int j = 0; j < kSegPer; ++j) {
+            const bool ok = s[j] >= T && s[j] != -INFINITY;
+            const int32_t cid = IDS ? id[j] : (int32_t)(a.id_base + c0 + j * kWave + lane);
+            const uint64_t key = ok ? make_key(s[j], cid) : 0;
+            const bool in = key > theta;
+            const uint64_t mask = __ballot(in);
+            if (in) buf[bc + __popcll(mask & lt_mask)] = key;
+            bc += __popcll(mask);
+            if (bc > cap - kWave) {
+                wave_lds_sync();
+                const SegCompacted c = seg_compact<NPL>(buf, bc, a.top_k);
+                bc = c.n;
+                theta = c.theta > theta ? c.theta : theta;
+            }
+        }
+        wave_lds_sync();
+        uint64_t v[NPL];
+        sort_buffer<NPL>(buf, bc, v, lane);
+#pragma unroll
+        for (int q = 0; q < NPL; ++q) {
+            const int r = q * kWave + lane;
+            if (r < a.top_k) {
+                const bool ok = r < bc;
+                oi[r] = ok ? key_id(v[q]) : -1;
+                os[r] = ok ? key_score(v[q]) : -INFINITY;
+            }
+        }
+        for (int r = a.top_k + lane; r < a.k_slot; r += kWave) {
+            os[r] = -INFINITY;
+            oi[r] = -1;
+        }
+    }
+    if (a.stats) {
+        float M = lmax;
+        for (int sh = 32; sh >= 1; sh >>= 1) M = fmaxf(M, __shfl_xor(M, sh));
+        float z = 0.0f;
+        if (M != -INFINITY) {
+#pragma clang fp contract(off)
+#pragma unroll
+            for (int j = 0; j < kSegPer; ++j)
+                if (s[j] != -INFINITY) z += fast_exp2((s[j] - M) * a.cexp);
+        }
+        for (int sh = 32; sh >= 1; sh >>= 1) z += __shfl_xor(z, sh);
+        if (lane == 0) {
+            a.o_m[ol] = M;
+            a.o_z[ol] = z;
+        }
+    }
+}
+
 }  // namespace
+
+int32_t seg_topk_cols() { return kSegCols; }
+int32_t seg_topk_slots(int32_t top_k) { return top_k < kWave ? kWave : top_k; }
+
+hipError_t launch_seg_topk(int64_t rows, int64_t row_stride, int64_t n, const float *score,
+                           const int32_t *col_id, int64_t id_base, int32_t top_k, float tau,
+                           float *o_score, int32_t *o_id, float *o_m, float *o_z, int64_t o_lists,
+                           int64_t o_seg0, hipStream_t s) {
+    if (rows == 0 || n == 0) return hipSuccess;
+    SegArgs a{};
+    a.rows = rows;
+    a.row_stride = row_stride;
+    a.n = n;
+    a.n_seg = (int32_t)((n + kSegCols - 1) / kSegCols);
+    a.units = rows * a.n_seg;
+    a.top_k = top_k;
+    a.k_slot = seg_topk_slots(top_k);
+    a.stats = o_m != nullptr;
+    a.cexp = 1.4426950408889634f / tau;
+    a.score = score;
+    a.col_id = col_id;
+    a.id_base = id_base;
+    a.o_score = o_score;
+    a.o_id = o_id;
+    a.o_m = o_m;
+    a.o_z = o_z;
+    a.o_lists = o_lists;
+    a.o_seg0 = o_seg0;
+    const int npl = next_pow2(top_k + kWave) / kWave;
+    const dim3 grid((unsigned)((a.units + kTopkWaves - 1) / kTopkWaves)), block(kWave * kTopkWaves);
+    const size_t smem = (size_t)kTopkWaves * npl * kWave * 8;
+    const bool ids = col_id != nullptr;
+    switch (npl * 2 + (ids ? 1 : 0)) {
+        case 4: hipLaunchKernelGGL((seg_topk<2, false>), grid, block, smem, s, a); break;
+        case 5: hipLaunchKernelGGL((seg_topk<2, true>), grid, block, smem, s, a); break;
+        case 8: hipLaunchKernelGGL((seg_topk<4, false>), grid, block, smem, s, a); break;
+        case 9: hipLaunchKernelGGL((seg_topk<4, true>), grid, block, smem, s, a); break;
+        case 16: hipLaunchKernelGGL((seg_topk<8, false>), grid, block, smem, s, a); break;
+        case 17: hipLaunchKernelGGL((seg_topk<8, true>), grid, block, smem, s, a); break;
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
 
 hipError_t launch_topk(int32_t rows, int32_t lists, int32_t k_in, const float *score,
                        const int32_t *id, const float *slot_max, const float *slot_sum, float tau,

@@ -61,6 +61,8 @@ def _load():
         "htam_retrieve_coarse_workspace_size": ([BP, i32, i32], sz),
         "htam_attend_transitions": ([BP, P, i32, i32, P, i32, f32, i32, P, P, P, P, P, sz, P], i32),
         "htam_attend_transitions_workspace_size": ([BP, i32, i32, i32], sz),
+        "htam_retrieve_flat": ([BP, P, i32, i32, f32, i32, P, P, P, P, P, P, P, sz, P], i32),
+        "htam_retrieve_flat_workspace_size": ([BP, i32, i32], sz),
         "htam_attend_transitions_noalloc": ([BP, P, i32, i32, P, i32, f32, i32, P, P, P, P, P], i32),
         "htam_topk": ([i32, i32, i32, P, P, P, P, f32, i32, P, P, P, P, P, P, P], i32),
         "htam_set_kernel_events": ([i32, P, P], i32),
@@ -186,6 +188,28 @@ def htam_attend_transitions(bank: Bank, q: torch.Tensor, sel: torch.Tensor, tau:
                                        _ptr(sel), c, float(tau), top_k, _ptr(out[0]), _ptr(out[1]),
                                        _ptr(out[2]), _ptr(out[3]), _ptr(ws), ws.numel(),
                                        _stream(dev)))
+    return out
+
+
+def htam_retrieve_flat(bank: Bank, q: torch.Tensor, tau: float, top_k: int, out=None, ws=None):
+    """Flat retrieval over every record. Returns (id, score, weight, row_max, row_sum, count)."""
+    B = q.shape[0]
+    dev = q.device
+    if out is None:
+        out = (torch.empty(B, top_k, dtype=torch.int32, device=dev),
+               torch.empty(B, top_k, dtype=torch.float32, device=dev),
+               torch.empty(B, top_k, dtype=torch.float32, device=dev),
+               torch.empty(B, dtype=torch.float32, device=dev),
+               torch.empty(B, dtype=torch.float32, device=dev),
+               torch.empty(B, dtype=torch.int32, device=dev))
+    if ws is None:
+        ws = _workspace(lib.htam_retrieve_flat_workspace_size(ctypes.byref(bank.struct), B, top_k),
+                        dev)
+    _check("htam_retrieve_flat",
+           lib.htam_retrieve_flat(ctypes.byref(bank.struct), _ptr(q), dtype_code(q.dtype), B,
+                                  float(tau), top_k, _ptr(out[0]), _ptr(out[1]), _ptr(out[2]),
+                                  _ptr(out[3]), _ptr(out[4]), _ptr(out[5]), _ptr(ws), ws.numel(),
+                                  _stream(dev)))
     return out
 
 

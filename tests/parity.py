@@ -216,3 +216,57 @@ def check(gpu: dict, q, c, seg_offsets, top_c: int, top_k: int, tau: float, comp
             rep.worst("weight_err", e)
         assert np.all(gpu["weight"][r, n:] == 0.0)
     return rep
+
+
+def check_rows(gpu: dict, ref: dict, qh, key_rows, tau: float, compute: str, rtol=None,
+               tag: str = "row") -> Report:
+    """Row outputs (id, score, weight, m, Z, count) of a GPU retrieval against the
+    oracle's over the same candidates, by the P2/P3 rules: ids match except at
+    the k-th boundary within the window, scores within rtol * |s| plus the
+    window, weights within rtol, max within rtol * |m| plus the top-1 window,
+    log Z within rtol, counts exact. key_rows(ids) returns the quantised keys
+    of caller ids (fp32, [len][d])."""
+    if rtol is None:
+        rtol = 2e-2 if compute == "bf16" else 1e-5
+    n_acc = qh.shape[1] if compute == "bf16" else qh.shape[1] + 1
+    rep = Report(rows=gpu["id"].shape[0])
+    for r in range(gpu["id"].shape[0]):
+        kept = int(ref["count"][r])
+        assert int(gpu["count"][r]) == kept, f"{tag} {r}: count {gpu['count'][r]} vs {kept}"
+        ig, sg = gpu["id"][r], gpu["score"][r].astype(np.float64)
+        assert np.all(ig[kept:] == -1) and np.all(np.isneginf(sg[kept:])), f"{tag} {r}: padding"
+        if kept == 0:
+            assert gpu["m"][r] == -np.inf and gpu["Z"][r] == 0.0 and np.all(gpu["weight"][r] == 0)
+            continue
+        ig, sg = ig[:kept], sg[:kept]
+        ir = ref["id"][r, :kept]
+        assert len(set(ig.tolist())) == kept and np.all(np.diff(sg) <= 0), f"{tag} {r}: ids/order"
+        ids = np.unique(np.concatenate([ig, ir]))
+        kv = dict(zip(ids.tolist(), np.asarray(key_rows(ids), dtype=np.float64)))
+        qv = qh[r].astype(np.float64)
+        s_ref = {i: float(kv[i] @ qv) for i in ids.tolist()}
+        win = {i: float(window(np.abs(qv) @ np.abs(kv[i]), s_ref[i], n_acc)) for i in ids.tolist()}
+        diff = set(ig.tolist()) ^ set(ir.tolist())
+        kth = int(ir[-1])
+        for i in diff:
+            assert abs(s_ref[i] - s_ref[kth]) <= win[i] + win[kth], \
+                f"{tag} {r}: id {i} ({s_ref[i]}) vs k-th {s_ref[kth]}"
+        if diff:
+            rep.bump("tie_events", len(diff) // 2)
+        for i, s in zip(ig.tolist(), sg.tolist()):
+            allow = rtol * abs(s_ref[i]) + win[i]
+            assert abs(s - s_ref[i]) <= allow, f"{tag} {r}: id {i} score {s} vs {s_ref[i]}"
+            rep.worst("score_err", abs(s - s_ref[i]) / allow)
+        mr, zr = float(ref["m"][r]), float(ref["Z"][r])
+        top = int(ir[0])
+        assert abs(float(gpu["m"][r]) - mr) <= rtol * abs(mr) + win[top], f"{tag} {r}: max"
+        e = abs(np.log(float(gpu["Z"][r])) - np.log(zr))
+        assert e <= rtol, f"{tag} {r}: log Z {np.log(float(gpu['Z'][r]))} vs {np.log(zr)}"
+        rep.worst("logZ_err", e)
+        for a, i in enumerate(ig.tolist()):
+            w_ref = np.exp((s_ref[i] - mr) / tau) / zr
+            e = abs(float(gpu["weight"][r, a]) - w_ref) / max(w_ref, 1e-30)
+            assert e <= rtol, f"{tag} {r}: weight of {i}: {gpu['weight'][r, a]} vs {w_ref}"
+            rep.worst("weight_err", e)
+        assert np.all(gpu["weight"][r, kept:] == 0.0)
+    return rep

@@ -117,3 +117,21 @@ def test_workspace_sizes():
     assert a > 4 * 4096 * 32 * 64 * 8                  # partial top-k lists dominate
     assert htam.lib.htam_attend_transitions_workspace_size(ctypes.byref(b), 4096, 0, 64) == 0
     assert htam.lib.htam_memory_build_workspace_size(-1, 4) == 0
+
+
+def test_flat_rejects_bad_arguments():
+    f = htam.lib.htam_retrieve_flat
+    b = _bank()
+    args = lambda **kw: dict(dict(B=4, tau=1.0, k=8, ws=FAKE, wsb=1 << 40, qd=htam.HTAM_BF16), **kw)  # noqa: E731
+
+    def call(**kw):
+        a = args(**kw)
+        return f(ctypes.byref(b), FAKE, a["qd"], a["B"], a["tau"], a["k"], FAKE, FAKE, None, None,
+                 None, None, a["ws"], a["wsb"], None)
+    assert call(tau=0.0) == -4
+    assert call(k=0) == -2
+    assert call(k=htam.HTAM_MAX_TOP_K + 1) == -2
+    assert call(qd=htam.HTAM_F32) == -3
+    assert call(wsb=64) == -5
+    assert call(B=0) == 0
+    assert htam.lib.htam_retrieve_flat_workspace_size(ctypes.byref(b), 4, 8) > 0
