@@ -286,3 +286,56 @@ def retrieve(q, c, seg_offsets, top_c: int, top_k: int, tau: float, compute: str
     out.update(per_row)
     out["qh"] = qh
     return out
+
+
+# ---------------------------------------------------------------------------
+# prefix-aware transition scoring of the global directions
+# ---------------------------------------------------------------------------
+def prefix_weights(length: int, lam: float) -> np.ndarray:
+    """Position-aware weights of a prefix of `length` directions (Eq. prefix_weight):
+    alpha_i = exp(-lam * (length - i)) for i = 1..length; the most recent
+    direction (i = length) has weight 1."""
+    i = np.arange(1, length + 1, dtype=np.float64)
+    return np.exp(-float(lam) * (length - i))
+
+
+def coarse_prefix(q, c, edge_keys, prefix, lam: float, top_c: int, compute: str):
+    """Prefix-aware coarse scores and top-c selection (Sec. 4.3, Eq. score with
+    Eq. prefix_weight; App. A.1 and App. B.2 for the edge memories).
+
+    The score of direction g for query b with prefix p_b = (g_1, ..., g_L) is
+    sum_{i=1..L} alpha_i * phi(g_i, g), alpha_i = exp(-lam (L - i)), where the
+    state-conditioned transition utility read from edge E_G(g_i, g) is the
+    inner product <q_b, E[g_i][g]> (the linear scorer of App. B.6 in embedding
+    space). A query with an empty prefix (the first step, which reads no edge)
+    is scored by its node keys, <q_b, c_g>.
+
+    q [B][d], c [G][d], edge_keys [G][G][d] (edge_keys[src][dst]), prefix
+    [B][Lmax] int (a row's prefix ends at its first entry outside [0, G)).
+    Returns (sel [B][top_c], sel_score, S [B][G]) with the selection ordered by
+    (-score, g). Computed in double over the (bf16-quantised) operands.
+    """
+    quant = round_bf16 if compute == "bf16" else _f32
+    qh = quant(q).astype(np.float64)
+    ch = quant(c).astype(np.float64)
+    eh = quant(edge_keys).astype(np.float64)
+    G = ch.shape[0]
+    prefix = np.asarray(prefix)
+    B = qh.shape[0]
+    S = np.empty((B, G))
+    for b in range(B):
+        row = prefix[b]
+        L = 0
+        while L < row.size and 0 <= row[L] < G:
+            L += 1
+        if L == 0:
+            S[b] = ch @ qh[b]
+        else:
+            alpha = prefix_weights(L, lam)
+            S[b] = sum(alpha[i] * (eh[row[i]] @ qh[b]) for i in range(L))
+    sel = np.empty((B, top_c), dtype=np.int32)
+    sel_score = np.empty((B, top_c))
+    for b in range(B):
+        order = np.lexsort((np.arange(G), -S[b]))[:top_c]
+        sel[b], sel_score[b] = order, S[b, order]
+    return sel, sel_score, S

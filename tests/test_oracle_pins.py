@@ -394,3 +394,92 @@ def test_build_is_stable_counting_sort():
 def test_build_rejects_bad_cluster_id():
     with pytest.raises(ValueError):
         oracle.build_bank([0, 3, 1], 3)
+
+
+# ---------------------------------------------------------------------------
+# prefix-aware transition scoring (Eq. score, Eq. prefix_weight)
+# ---------------------------------------------------------------------------
+def _prefix_inputs(rng, B, G, d, Lmax):
+    q, C = _unit(rng, B, d), _unit(rng, G, d)
+    E = (rng.standard_normal((G, G, d)) / np.sqrt(d)).astype(np.float32)
+    lengths = rng.integers(0, Lmax + 1, B)
+    P = np.full((B, Lmax), -1, dtype=np.int32)
+    for b in range(B):
+        P[b, :lengths[b]] = rng.integers(0, G, lengths[b])
+    return q, C, E, P, lengths
+
+
+def test_prefix_worked_example_exact():
+    ex = json.load(open(os.path.join(GOLDEN, "prefix_example.json")))
+    sel, ss, S = oracle.coarse_prefix(np.asarray(ex["queries"], np.float32),
+                                      np.asarray(ex["coarse_keys"], np.float32),
+                                      np.asarray(ex["edge_keys"], np.float32),
+                                      np.asarray(ex["prefix"]), math.log(2.0), ex["top_c"], "f32")
+    np.testing.assert_allclose(S, _arr(ex["scores"]), rtol=1e-15, atol=1e-15)
+    np.testing.assert_array_equal(sel, ex["sel"])
+
+
+def test_prefix_weights_closed_form():
+    a = oracle.prefix_weights(4, math.log(3.0))
+    np.testing.assert_allclose(a, [1 / 27, 1 / 9, 1 / 3, 1], rtol=1e-14)
+    assert oracle.prefix_weights(0, 1.0).size == 0
+    np.testing.assert_array_equal(oracle.prefix_weights(3, 0.0), [1, 1, 1])
+
+
+def test_prefix_one_term_with_node_edges_is_plain_coarse():
+    """Edge keys that repeat the node keys, E[s][g] = c_g, and a one-term
+    prefix (alpha = 1): the prefix score is the one-term score <q, c_g>."""
+    rng = np.random.default_rng(31)
+    B, G, d = 9, 12, 16
+    q, C = _unit(rng, B, d), _unit(rng, G, d)
+    E = np.broadcast_to(C, (G, G, d)).copy()
+    P = rng.integers(0, G, (B, 1)).astype(np.int32)
+    sel, ss, S = oracle.coarse_prefix(q, C, E, P, 0.7, 4, "f32")
+    sel0, ss0 = oracle.coarse(q, C, 4)
+    np.testing.assert_array_equal(sel, sel0)
+    np.testing.assert_allclose(ss, ss0, rtol=1e-13, atol=1e-15)
+
+
+@pytest.mark.parametrize("compute", ["f32", "bf16"])
+def test_prefix_against_direct_sums(compute):
+    """lam = 0 adds every term with weight 1; a large lam keeps only the most
+    recent term; an empty prefix scores the node keys; ids outside [0, G)
+    end a prefix."""
+    rng = np.random.default_rng(32)
+    B, G, d, L = 10, 7, 24, 4
+    q, C, E, P, lengths = _prefix_inputs(rng, B, G, d, L)
+    P[0] = [3, 5, G, 1]                                 # ends after two entries
+    lengths[0] = 2
+    qq, cq, eq = ((oracle.round_bf16(q), oracle.round_bf16(C), oracle.round_bf16(E))
+                  if compute == "bf16" else (q, C, E))
+    qq, cq, eq = (x.astype(np.float64) for x in (qq, cq, eq))
+    for lam in (0.0, 60.0):
+        _, _, S = oracle.coarse_prefix(q, C, E, P, lam, 3, compute)
+        for b in range(B):
+            L_b = lengths[b]
+            if L_b == 0:
+                ref = cq @ qq[b]
+            elif lam == 0.0:
+                ref = sum(eq[P[b, i]] @ qq[b] for i in range(L_b))
+            else:
+                ref = eq[P[b, L_b - 1]] @ qq[b]
+            np.testing.assert_allclose(S[b], ref, rtol=1e-12, atol=1e-20)
+
+
+def test_prefix_relabel_invariance():
+    """Renaming the global directions (node keys, both edge axes and the
+    prefixes permuted together) renames the selection and nothing else."""
+    rng = np.random.default_rng(33)
+    B, G, d = 8, 9, 12
+    q, C, E, P, _ = _prefix_inputs(rng, B, G, d, 3)
+    pi = rng.permutation(G)
+    C2 = np.empty_like(C)
+    C2[pi] = C
+    E2 = np.empty_like(E)
+    E2[np.ix_(pi, pi)] = E
+    P2 = np.where(P >= 0, pi[np.maximum(P, 0)], -1)
+    sel, ss, S = oracle.coarse_prefix(q, C, E, P, 0.5, 4, "f32")
+    sel2, ss2, S2 = oracle.coarse_prefix(q, C2, E2, P2, 0.5, 4, "f32")
+    np.testing.assert_array_equal(sel2, pi[sel])
+    np.testing.assert_allclose(ss2, ss, rtol=1e-13)
+    np.testing.assert_allclose(S2[:, pi], S, rtol=1e-13)
