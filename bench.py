@@ -144,6 +144,110 @@ def cpu_baseline(spec, w, bank, target_s: float):
                       f"clusters, fine stage over the selected segments, fp64)"}
 
 
+def bench_alt(args, spec, w, bank):
+    """The flat path (htam_retrieve_flat: every record a candidate) or the
+    prefix path (htam_retrieve_coarse_prefix, then the fine stage and the
+    merge), timed like the hierarchical step. Roofline: the flat path is the
+    dense B x N score GEMM (MFMA-bound; the whole step against the bf16 peak);
+    the prefix path's added kernel is the grouped edge-score GEMM, which reads
+    each used source node's edge slice once (HBM-bound at these shapes)."""
+    import torch
+    from paper_2605_29734_amd import htam, synth
+    q = w.queries
+    dev = q.device
+    kc = htam.HTAM_KERNEL_COARSE
+    mk = lambda: torch.cuda.Event(enable_timing=True)   # noqa: E731
+    K, E = args.steps, max(1, args.event_every)
+    if args.path == "flat":
+        out = (torch.empty(spec.B, spec.top_k, dtype=torch.int32, device=dev),
+               torch.empty(spec.B, spec.top_k, device=dev), torch.empty(spec.B, spec.top_k, device=dev),
+               torch.empty(spec.B, device=dev), torch.empty(spec.B, device=dev),
+               torch.empty(spec.B, dtype=torch.int32, device=dev))
+        ws = htam._workspace(htam.lib.htam_retrieve_flat_workspace_size(
+            htam.ctypes.byref(bank.struct), spec.B, spec.top_k), dev)
+
+        def step(i, marks):
+            marks[i][0].record()
+            htam.htam_retrieve_flat(bank, q, spec.tau, spec.top_k, out=out, ws=ws)
+    else:
+        edges, prefix = synth.make_prefix(spec, w.coarse_keys, args.prefix_len, device=dev,
+                                          seed=args.seed)
+        r = htam.Retriever(bank, spec.B, spec.top_c, spec.top_k, spec.tau)
+        wsp = htam._workspace(htam.lib.htam_retrieve_coarse_prefix_workspace_size(
+            htam.ctypes.byref(bank.struct), spec.B, args.prefix_len, spec.top_c), dev)
+
+        def step(i, marks):
+            marks[i][0].record()
+            htam.htam_retrieve_coarse_prefix(bank, edges, prefix, args.lam, q, spec.top_c,
+                                             out=r.sel, ws=wsp)
+            marks[i][1].record()
+            htam.htam_attend_transitions(bank, q, r.sel[0], r.tau, r.k, out=r.slots, ws=r.ws_attend)
+            htam.htam_topk(r.slots[2], r.slots[3], r.k, r.slots[0], r.slots[1], r.tau, out=r.rows)
+    marks = [[mk(), mk()] for _ in range(K)] + [[mk()]]
+    ev = [(mk(), mk()) for _ in range((K + E - 1) // E)]
+    for a, b in ev:
+        a.record()
+        b.record()
+    for i in range(args.warmup):
+        step(0, marks)
+    torch.cuda.synchronize()
+    log(f"[bench] timing {K} steps ({args.path})")
+    t0 = time.perf_counter()
+    for i in range(K):
+        if i % E == 0:
+            htam.lib.htam_set_kernel_events(kc, ev[i // E][0].cuda_event, ev[i // E][1].cuda_event)
+        elif i % E == 1:
+            htam.lib.htam_set_kernel_events(kc, None, None)
+        step(i, marks)
+    marks[K][0].record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    htam.lib.htam_set_kernel_events(kc, None, None)
+    ms_total = marks[0][0].elapsed_time(marks[K][0])
+    step_ms = [marks[i][0].elapsed_time(marks[i + 1][0]) for i in range(K)]
+    t_kernel = float(np.mean([a.elapsed_time(b) for a, b in ev])) * 1e-3
+    kb = bank.fine_keys.element_size()
+    res = {
+        "metric": METRIC, "value": spec.B * K / (ms_total * 1e-3), "unit": "queries/s",
+        "n_gpus": 1, "steps": K, "warmup": args.warmup, "ms_per_step": ms_total / K,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16" if spec.compute == "bf16" else "f32", "data": "synthetic",
+        "config": {"workload": spec.name, "path": args.path, "queries": spec.B, "d": spec.d,
+                   "clusters": spec.G, "transitions": spec.N, "top_c": spec.top_c,
+                   "top_k": spec.top_k, "tau": spec.tau, "key_storage": spec.storage,
+                   "bank_bytes": int(spec.N * spec.d * kb)},
+        "stages": {"step_ms_median": float(np.median(step_ms)), "step_ms_wall": wall / K * 1e3,
+                   "source_sha256": kernel_source_sha256()},
+    }
+    if args.path == "flat":
+        flops = 2.0 * spec.B * spec.N * spec.d
+        t_step = ms_total / K * 1e-3
+        res["roofline"] = {"bound": "mfma", "kernel": "flat retrieval step (score GEMM, "
+                           "segmented top-k, merge)", "achieved": flops / t_step / 1e12,
+                           "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                           "frac": flops / t_step / 1e12 / MFMA_BF16_PEAK_TFLOPS, "traffic": None,
+                           "flops_per_step": flops}
+        res["stages"]["score_gemm_ms_last_band"] = t_kernel * 1e3
+    else:
+        P = prefix.cpu().numpy()
+        G = spec.G
+        valid = np.cumprod((P >= 0) & (P < G), axis=1).astype(bool)
+        n_pairs = int(valid.sum())
+        n_src = int(np.unique(P[valid]).size)
+        eb = edges.element_size()
+        alg = n_src * G * spec.d * eb + spec.B * spec.d * q.element_size()
+        res["roofline"] = {"bound": "hbm", "kernel": "prefix_gemm (edge scores)",
+                           "achieved": alg / t_kernel / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                           "frac": alg / t_kernel / 1e9 / HBM_PEAK_GBS, "traffic": None,
+                           "alg_bytes_per_launch": alg, "launch_ms": t_kernel * 1e3}
+        coarse_ms = [marks[i][0].elapsed_time(marks[i][1]) for i in range(K)]
+        res["stages"].update({"prefix_coarse_stage_ms_median": float(np.median(coarse_ms)),
+                              "prefix_pairs": n_pairs, "prefix_sources": n_src,
+                              "prefix_edge_tflops": 2.0 * n_pairs * G * spec.d / t_kernel / 1e12,
+                              "prefix_len_max": args.prefix_len, "lambda": args.lam})
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -155,6 +259,12 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--event-every", type=int, default=8, metavar="E",
                     help="stamp the kernel timing events on every E-th timed step")
+    ap.add_argument("--path", default="hierarchical", choices=["hierarchical", "prefix", "flat"],
+                    help="hierarchical retrieval (default); the same with prefix-aware coarse "
+                         "scoring; or flat retrieval over every record")
+    ap.add_argument("--prefix-len", type=int, default=5, metavar="L",
+                    help="prefix path: longest prefix (lengths uniform on 0..L)")
+    ap.add_argument("--lam", type=float, default=0.5, help="prefix path: recency decay lambda")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run plain copies of MIB MiB (counter calibration) and exit")
     args = ap.parse_args()
@@ -180,6 +290,10 @@ def main():
     torch.cuda.synchronize()
     del w.keys_in
     q = w.queries
+    if args.path != "hierarchical":
+        res = bench_alt(args, spec, w, bank)
+        print(json.dumps(res), flush=True)
+        return
     r = htam.Retriever(bank, spec.B, spec.top_c, spec.top_k, spec.tau)
     log(f"[bench] warmup {args.warmup}")
     for _ in range(args.warmup):

@@ -166,6 +166,40 @@ htam_status htam_retrieve_coarse(const htam_bank *bank, const void *q, int32_t q
 size_t htam_retrieve_coarse_workspace_size(const htam_bank *bank, int32_t n_queries, int32_t top_c);
 
 /*
+ * htam_retrieve_coarse_prefix -- prefix-aware scoring of every cluster, then
+ * the best top_c: htam_retrieve_coarse with the transition-attended score of
+ * Sec. 4.3 (Eq. score, with the position-aware weights of Eq. prefix_weight;
+ * the edge memories of App. A.1 and App. B.2). For query b with prefix
+ * p_b = (g_1, ..., g_L) of previously chosen directions (g_L the most
+ * recent), the score of cluster g is
+ *     sum_{i=1..L} alpha_i <q_b, E[g_i][g]>,  alpha_i = exp(-lambda (L - i)),
+ * each term the state-conditioned transition utility of the edge g_i -> g
+ * (the linear scorer of App. B.6 as an inner product with an edge key). A
+ * query with an empty prefix (the first step, which reads no edge) is scored
+ * by the node keys, <q_b, c_g>, as in htam_retrieve_coarse.
+ *
+ *   edge_keys    [G][G][d] edge keys E[src][dst], element type key_dtype,
+ *                16-byte aligned (the complete directed pair space of App. B.2).
+ *   prefix       [n_queries][max_prefix] int32: row b lists g_1, ..., g_L and
+ *                ends at its first entry outside [0, G) (pad with -1).
+ *   max_prefix   1 <= max_prefix <= HTAM_MAX_PREFIX.
+ *   lambda       recency decay, finite and >= 0 (0: every edge weighs 1).
+ *   q, q_dtype, n_queries, top_c, sel_cluster, sel_score as in
+ *                htam_retrieve_coarse (ties to the lower cluster id).
+ *   ws, ws_bytes workspace of htam_retrieve_coarse_prefix_workspace_size()
+ *                bytes.
+ * The kernel timing hook HTAM_KERNEL_COARSE stamps the edge-score GEMM.
+ */
+#define HTAM_MAX_PREFIX 16
+htam_status htam_retrieve_coarse_prefix(const htam_bank *bank, const void *edge_keys,
+                                        const int32_t *prefix, int32_t max_prefix, float lambda,
+                                        const void *q, int32_t q_dtype, int32_t n_queries,
+                                        int32_t top_c, int32_t *sel_cluster, float *sel_score,
+                                        void *ws, size_t ws_bytes, hipStream_t stream);
+size_t htam_retrieve_coarse_prefix_workspace_size(const htam_bank *bank, int32_t n_queries,
+                                                  int32_t max_prefix, int32_t top_c);
+
+/*
  * htam_attend_transitions -- stream the selected clusters' transition
  * segments, with softmax statistics and top-k per selected cluster.
  *

@@ -182,30 +182,6 @@ __global__ __launch_bounds__(kGemmThreads) void coarse_gemm(const __bf16 *__rest
             }
 }
 
-// A fragment as loaded (bf16 as is; fp32 rounded to bf16 when used).
-template <typename T>
-struct RawFrag;
-template <>
-struct RawFrag<__bf16> {
-    uint4 v;
-    __device__ __forceinline__ void load(const __bf16 *p) { v = *reinterpret_cast<const uint4 *>(p); }
-    __device__ __forceinline__ bf16x8_t get() const { return __builtin_bit_cast(bf16x8_t, v); }
-};
-template <>
-struct RawFrag<float> {
-    float4 lo, hi;
-    __device__ __forceinline__ void load(const float *p) {
-        lo = reinterpret_cast<const float4 *>(p)[0];
-        hi = reinterpret_cast<const float4 *>(p)[1];
-    }
-    __device__ __forceinline__ bf16x8_t get() const {
-        bf16x8_t r;
-        r[0] = (__bf16)lo.x; r[1] = (__bf16)lo.y; r[2] = (__bf16)lo.z; r[3] = (__bf16)lo.w;
-        r[4] = (__bf16)hi.x; r[5] = (__bf16)hi.y; r[6] = (__bf16)hi.z; r[7] = (__bf16)hi.w;
-        return r;
-    }
-};
-
 // Small problems (fewer 256 x 256 tiles than compute units): one wave per
 // TM*16 x TM*16 tile, operands read directly in MFMA fragment layout. A batch
 // of k-steps is requested before any is used (addresses clamped into the
@@ -395,6 +371,12 @@ hipError_t launch_coarse(int32_t key_dtype, int32_t compute_dtype, int32_t d, in
     hipError_t err = launch_scores(key_dtype, compute_dtype, d, G, coarse_keys, q, B, w.scores,
                                    w.q16, w.c16, true, n_cu, ev, s);
     if (err != hipSuccess) return err;
+    return launch_select(B, G, top_c, sel, sel_score, w, s);
+}
+
+hipError_t launch_select(int32_t B, int32_t G, int32_t top_c, int32_t *sel, float *sel_score,
+                         const CoarseWs &w, hipStream_t s) {
+    hipError_t err = hipSuccess;
     if (w.n_seg == 1)
         return launch_topk(B, 1, G, w.scores, nullptr, nullptr, nullptr, 1.0f, top_c, sel,
                            sel_score, nullptr, nullptr, nullptr, nullptr, s);

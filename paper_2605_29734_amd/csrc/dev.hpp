@@ -90,6 +90,30 @@ __device__ __forceinline__ bf16x8_t zero8() {
     return r;
 }
 
+// A fragment as loaded (bf16 as is; fp32 rounded to bf16 when used).
+template <typename T>
+struct RawFrag;
+template <>
+struct RawFrag<__bf16> {
+    uint4 v;
+    __device__ __forceinline__ void load(const __bf16 *p) { v = *reinterpret_cast<const uint4 *>(p); }
+    __device__ __forceinline__ bf16x8_t get() const { return __builtin_bit_cast(bf16x8_t, v); }
+};
+template <>
+struct RawFrag<float> {
+    float4 lo, hi;
+    __device__ __forceinline__ void load(const float *p) {
+        lo = reinterpret_cast<const float4 *>(p)[0];
+        hi = reinterpret_cast<const float4 *>(p)[1];
+    }
+    __device__ __forceinline__ bf16x8_t get() const {
+        bf16x8_t r;
+        r[0] = (__bf16)lo.x; r[1] = (__bf16)lo.y; r[2] = (__bf16)lo.z; r[3] = (__bf16)lo.w;
+        r[4] = (__bf16)hi.x; r[5] = (__bf16)hi.y; r[6] = (__bf16)hi.z; r[7] = (__bf16)hi.w;
+        return r;
+    }
+};
+
 // Wait for this wave's LDS traffic and stop the compiler from moving memory
 // operations across this point (LDS operations of one wave complete in order).
 __device__ __forceinline__ void wave_lds_sync() {

@@ -263,6 +263,55 @@ HTAM_API htam_status htam_attend_transitions(const htam_bank *bank, const void *
 }
 
 // ---------------------------------------------------------------------------
+HTAM_API size_t htam_retrieve_coarse_prefix_workspace_size(const htam_bank *bank,
+                                                           int32_t n_queries, int32_t max_prefix,
+                                                           int32_t top_c) {
+    if (!bank || n_queries < 0 || bank->n_clusters < 1 || top_c < 1 || max_prefix < 1 ||
+        max_prefix > HTAM_MAX_PREFIX)
+        return 0;
+    size_t bytes = 0;
+    htam::prefix_layout(nullptr, n_queries, bank->n_clusters, bank->d, bank->key_dtype,
+                        bank->compute_dtype, max_prefix, top_c, &bytes);
+    return bytes;
+}
+
+HTAM_API htam_status htam_retrieve_coarse_prefix(const htam_bank *bank, const void *edge_keys,
+                                                 const int32_t *prefix, int32_t max_prefix,
+                                                 float lambda, const void *q, int32_t q_dtype,
+                                                 int32_t n_queries, int32_t top_c,
+                                                 int32_t *sel_cluster, float *sel_score, void *ws,
+                                                 size_t ws_bytes, hipStream_t stream) {
+    HTAM_TRY(check_bank(bank));
+    HTAM_TRY(check_query(bank, q, q_dtype, n_queries));
+    const int32_t cmax = bank->n_clusters < HTAM_MAX_TOP_C ? bank->n_clusters : HTAM_MAX_TOP_C;
+    if (top_c < 1 || top_c > cmax)
+        return fail(HTAM_ERR_SHAPE, "top_c = %d out of [1, %d]", top_c, cmax);
+    if (max_prefix < 1 || max_prefix > HTAM_MAX_PREFIX)
+        return fail(HTAM_ERR_SHAPE, "max_prefix = %d out of [1, %d]", max_prefix, HTAM_MAX_PREFIX);
+    if (!std::isfinite(lambda) || lambda < 0.0f)
+        return fail(HTAM_ERR_VALUE, "lambda = %g: need a finite lambda >= 0", (double)lambda);
+    if ((int64_t)n_queries * max_prefix >= (int64_t(1) << 31))
+        return fail(HTAM_ERR_SHAPE, "n_queries * max_prefix must be < 2^31");
+    if (!edge_keys) return fail(HTAM_ERR_NULL, "edge_keys is NULL");
+    if (!aligned16(edge_keys)) return fail(HTAM_ERR_ALIGN, "edge_keys must be 16-byte aligned");
+    if (n_queries == 0) return ok();
+    if (!prefix || !sel_cluster) return fail(HTAM_ERR_NULL, "prefix / sel_cluster is NULL");
+    HTAM_TRY(check_ws(ws, ws_bytes, htam_retrieve_coarse_prefix_workspace_size(
+                                         bank, n_queries, max_prefix, top_c)));
+    const int n_cu = device_cus(nullptr);
+    if (n_cu <= 0) return fail(HTAM_ERR_DEVICE, "no HIP device");
+    const htam::PrefixWs w =
+        htam::prefix_layout(ws, n_queries, bank->n_clusters, bank->d, bank->key_dtype,
+                            bank->compute_dtype, max_prefix, top_c, nullptr);
+    return device_status(htam::launch_prefix(bank->key_dtype, bank->compute_dtype, bank->d,
+                                             bank->n_clusters, bank->coarse_keys, edge_keys,
+                                             prefix, max_prefix, lambda, q, n_queries, top_c,
+                                             sel_cluster, sel_score, w, n_cu,
+                                             g_events[HTAM_KERNEL_COARSE], stream),
+                         "htam_retrieve_coarse_prefix");
+}
+
+// ---------------------------------------------------------------------------
 HTAM_API size_t htam_retrieve_flat_workspace_size(const htam_bank *bank, int32_t n_queries,
                                                   int32_t top_k) {
     if (!bank || n_queries < 0 || top_k < 1 || bank->d < 8 || bank->n_transitions < 0) return 0;

@@ -120,6 +120,31 @@ hipError_t launch_coarse(int32_t key_dtype, int32_t compute_dtype, int32_t d, in
                          int32_t *sel, float *sel_score, const CoarseWs &w, int n_cu,
                          KernelEvents ev, hipStream_t s);
 
+// The top_c of each score row of w.scores [B][G] (descending, ties to the lower id).
+hipError_t launch_select(int32_t B, int32_t G, int32_t top_c, int32_t *sel, float *sel_score,
+                         const CoarseWs &w, hipStream_t s);
+
+// ---- prefix-aware coarse scoring ----------------------------------------------
+struct PrefixWs {
+    CoarseWs c;        // node scores, then the combined scores, and the selection
+    float *part;       // [B * Lmax][G] per (query, prefix position) edge scores
+    int32_t *cnt;      // [G] pairs per source node
+    int32_t *cursor;   // [G]
+    int32_t *off;      // [G+1] first pair of each source in `pairs`
+    int32_t *goff;     // [G+1] first group of each source
+    int32_t *pairs;    // [B * Lmax] (query, position) pairs grouped by source
+    int4 *groups;      // [g_max] (source, first pair, pairs, -)
+    int32_t *n_groups; // [1]
+    int64_t g_max;
+};
+PrefixWs prefix_layout(void *ws, int32_t B, int32_t G, int32_t d, int32_t key_dtype,
+                       int32_t compute_dtype, int32_t lmax, int32_t top_c, size_t *bytes);
+hipError_t launch_prefix(int32_t key_dtype, int32_t compute_dtype, int32_t d, int32_t G,
+                         const void *coarse_keys, const void *edge_keys, const int32_t *prefix,
+                         int32_t lmax, float lambda, const void *q, int32_t B, int32_t top_c,
+                         int32_t *sel, float *sel_score, const PrefixWs &w, int n_cu,
+                         KernelEvents ev, hipStream_t s);
+
 // ---- fine stage (routing + bank stream + per-slot merge) ----------------------
 struct AttendWs {
     int32_t *cnt;      // [G] queries per cluster

@@ -22,6 +22,7 @@ HTAM_MAX_TOP_K = 256
 HTAM_MAX_TOP_C = 256
 HTAM_MAX_DIM = 8192
 HTAM_NOALLOC_SCRATCH_MIB = 64
+HTAM_MAX_PREFIX = 16
 
 HTAM_KERNEL_COARSE = 0
 HTAM_KERNEL_STREAM = 1
@@ -61,6 +62,8 @@ def _load():
         "htam_retrieve_coarse_workspace_size": ([BP, i32, i32], sz),
         "htam_attend_transitions": ([BP, P, i32, i32, P, i32, f32, i32, P, P, P, P, P, sz, P], i32),
         "htam_attend_transitions_workspace_size": ([BP, i32, i32, i32], sz),
+        "htam_retrieve_coarse_prefix": ([BP, P, P, i32, f32, P, i32, i32, i32, P, P, P, sz, P], i32),
+        "htam_retrieve_coarse_prefix_workspace_size": ([BP, i32, i32, i32], sz),
         "htam_retrieve_flat": ([BP, P, i32, i32, f32, i32, P, P, P, P, P, P, P, sz, P], i32),
         "htam_retrieve_flat_workspace_size": ([BP, i32, i32], sz),
         "htam_attend_transitions_noalloc": ([BP, P, i32, i32, P, i32, f32, i32, P, P, P, P, P], i32),
@@ -188,6 +191,26 @@ def htam_attend_transitions(bank: Bank, q: torch.Tensor, sel: torch.Tensor, tau:
                                        _ptr(sel), c, float(tau), top_k, _ptr(out[0]), _ptr(out[1]),
                                        _ptr(out[2]), _ptr(out[3]), _ptr(ws), ws.numel(),
                                        _stream(dev)))
+    return out
+
+
+def htam_retrieve_coarse_prefix(bank: Bank, edge_keys: torch.Tensor, prefix: torch.Tensor,
+                                lam: float, q: torch.Tensor, top_c: int, out=None, ws=None):
+    """Prefix-aware top-c clusters per query. edge_keys [G][G][d]; prefix [B][Lmax] int32
+    (-1 padded). Returns (sel_cluster int32 [B][c], sel_score fp32 [B][c])."""
+    B, lmax = prefix.shape
+    dev = q.device
+    if out is None:
+        out = (torch.empty(B, top_c, dtype=torch.int32, device=dev),
+               torch.empty(B, top_c, dtype=torch.float32, device=dev))
+    if ws is None:
+        ws = _workspace(lib.htam_retrieve_coarse_prefix_workspace_size(
+            ctypes.byref(bank.struct), B, lmax, top_c), dev)
+    _check("htam_retrieve_coarse_prefix",
+           lib.htam_retrieve_coarse_prefix(ctypes.byref(bank.struct), _ptr(edge_keys), _ptr(prefix),
+                                           lmax, float(lam), _ptr(q), dtype_code(q.dtype), B, top_c,
+                                           _ptr(out[0]), _ptr(out[1]), _ptr(ws), ws.numel(),
+                                           _stream(dev)))
     return out
 
 

@@ -215,3 +215,34 @@ def make(spec, device="cpu", seed: int = 0, chunk_rows: int = 1 << 20) -> Worklo
     return Workload(spec=spec, queries=_store(queries, spec.storage).contiguous(),
                     coarse_keys=_store(coarse, spec.storage).contiguous(),
                     cluster_of=cluster_of, keys_in=keys_in, sizes=sizes)
+
+
+def make_prefix(spec, coarse_keys: torch.Tensor, lmax: int, device="cpu", seed: int = 0,
+                sigma: float = 0.5):
+    """Edge keys and prefixes for prefix-aware coarse scoring (the edge
+    memories E_G(g_src, g_dst) over the complete directed pair space, and each
+    query's recent global directions).
+
+    edge_keys [G][G][d] in the storage dtype: E[src][dst] = normalise(c_dst +
+    sigma * e / sqrt(d)), e ~ N(0, I_d) drawn per (src, dst), so an edge key is
+    its destination's node key perturbed per source. prefix [B][lmax] int32:
+    each query's prefix length is uniform on 0..lmax (0: the first step) and
+    its entries uniform over the G directions; rows are padded with -1."""
+    if isinstance(spec, str):
+        spec = SPECS[spec]
+    device = torch.device(device)
+    G, d = spec.G, spec.d
+    ck = coarse_keys.to(device=device, dtype=torch.float32)
+    gen = _gen(device, seed, spec.name, "edges")
+    dt = torch.bfloat16 if spec.storage == "bf16" else torch.float32
+    E = torch.empty(G, G, d, dtype=dt, device=device)
+    for s0 in range(G):
+        e = torch.randn(G, d, generator=gen, device=device)
+        E[s0] = _store(_unit(ck + sigma * e / (d ** 0.5)), spec.storage)
+    rng = np.random.default_rng(_seed(seed, spec.name, "prefix"))
+    lengths = rng.integers(0, lmax + 1, spec.B)
+    P = np.full((spec.B, lmax), -1, dtype=np.int32)
+    for b in range(spec.B):
+        P[b, :lengths[b]] = rng.integers(0, G, lengths[b])
+    return E, torch.from_numpy(P).to(device)
+

@@ -135,3 +135,23 @@ def test_flat_rejects_bad_arguments():
     assert call(wsb=64) == -5
     assert call(B=0) == 0
     assert htam.lib.htam_retrieve_flat_workspace_size(ctypes.byref(b), 4, 8) > 0
+
+
+def test_prefix_rejects_bad_arguments():
+    f = htam.lib.htam_retrieve_coarse_prefix
+    b = _bank()
+
+    def call(edges=FAKE, prefix=FAKE, lmax=4, lam=0.5, B=4, c=2, wsb=1 << 40):
+        return f(ctypes.byref(b), edges, prefix, lmax, lam, FAKE, htam.HTAM_BF16, B, c, FAKE, FAKE,
+                 FAKE, wsb, None)
+    assert call(edges=None) == -1
+    assert call(edges=FAKE + 8) == -6
+    assert call(lmax=0) == -2
+    assert call(lmax=htam.HTAM_MAX_PREFIX + 1) == -2
+    assert call(lam=-1.0) == -4
+    assert call(lam=math.inf) == -4
+    assert call(c=9) == -2
+    assert call(prefix=None) == -1
+    assert call(wsb=64) == -5
+    assert call(B=0) == 0
+    assert htam.lib.htam_retrieve_coarse_prefix_workspace_size(ctypes.byref(b), 4, 4, 2) > 0
