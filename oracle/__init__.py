@@ -339,3 +339,45 @@ def coarse_prefix(q, c, edge_keys, prefix, lam: float, top_c: int, compute: str)
         order = np.lexsort((np.arange(G), -S[b]))[:top_c]
         sel[b], sel_score[b] = order, S[b, order]
     return sel, sel_score, S
+
+
+# ---------------------------------------------------------------------------
+# the stochastic direction policy mu_g, sampled c times without replacement
+# ---------------------------------------------------------------------------
+def policy(S, eps: float, tau_g: float) -> np.ndarray:
+    """The direction policy of Eq. global direction over every cluster:
+    mu(g) = eps / G + (1 - eps) exp(S[g] / tau_g) / sum_g' exp(S[g'] / tau_g),
+    row by row, in double."""
+    S = np.asarray(S, dtype=np.float64)
+    z = (S - S.max(axis=-1, keepdims=True)) / tau_g
+    soft = np.exp(z) / np.exp(z).sum(axis=-1, keepdims=True)
+    return eps / S.shape[-1] + (1.0 - eps) * soft
+
+
+def gumbel_of_bits(x) -> np.ndarray:
+    """Standard Gumbel variate of a uniform 32-bit word x: u = (x + 1/2) / 2^32
+    in (0, 1), G = -log(-log u)."""
+    u = (np.asarray(x, dtype=np.float64) + 0.5) / 4294967296.0
+    return -np.log(-np.log(u))
+
+
+def coarse_sampled(q, c, top_c: int, eps: float, tau_g: float, noise, compute: str):
+    """Direction choice by sampling the policy mu_g (Eq. global direction;
+    Alg. 1 Step 2, g_t ~ mu_g) top_c times without replacement, by the
+    Gumbel-top-k construction (Kool et al., ICML 2019): perturb log mu(g) with
+    independent standard Gumbel variates and keep the top_c, which is a draw
+    of top_c clusters one after another without replacement from mu.
+
+    Scores are the one-term coarse scores <q_b, c_g> (O0/O1). noise [B][G]
+    uint32 supplies the uniform words (one per query and cluster). Returns
+    (sel [B][top_c] ordered by descending perturbed key, ties to the lower
+    cluster id; their raw scores; the keys [B][G]; S [B][G])."""
+    quant = round_bf16 if compute == "bf16" else _f32
+    qh, ch = quant(q), quant(c)
+    S = scores(qh, ch)
+    keys = np.log(policy(S, eps, tau_g)) + gumbel_of_bits(noise)
+    B, G = S.shape
+    sel = np.empty((B, top_c), dtype=np.int32)
+    for b in range(B):
+        sel[b] = np.lexsort((np.arange(G), -keys[b]))[:top_c]
+    return sel, np.take_along_axis(S, sel, axis=1), keys, S

@@ -483,3 +483,65 @@ def test_prefix_relabel_invariance():
     np.testing.assert_array_equal(sel2, pi[sel])
     np.testing.assert_allclose(ss2, ss, rtol=1e-13)
     np.testing.assert_allclose(S2[:, pi], S, rtol=1e-13)
+
+
+# ---------------------------------------------------------------------------
+# the sampled direction policy (Eq. global direction, Gumbel-top-k)
+# ---------------------------------------------------------------------------
+def test_policy_limits():
+    """eps = 0 is the softmax (scipy's), eps = 1 the uniform distribution, and
+    every row sums to 1."""
+    from scipy.special import softmax
+    rng = np.random.default_rng(41)
+    S = rng.standard_normal((5, 13))
+    np.testing.assert_allclose(oracle.policy(S, 0.0, 0.3), softmax(S / 0.3, axis=1), rtol=1e-13)
+    np.testing.assert_allclose(oracle.policy(S, 1.0, 0.3), np.full((5, 13), 1 / 13), rtol=1e-13)
+    np.testing.assert_allclose(oracle.policy(S, 0.25, 2.0).sum(axis=1), 1.0, rtol=1e-13)
+
+
+def test_gumbel_of_bits():
+    """u = 1/2 gives -log(log 2); the variates of evenly spread words have the
+    Gumbel mean (Euler's constant) and variance pi^2/6."""
+    assert oracle.gumbel_of_bits(np.uint32(2 ** 31) - 1)[()] == pytest.approx(
+        -math.log(-math.log(0.5 - 0.5 / 2 ** 32)), rel=1e-15)
+    x = (np.arange(1 << 20, dtype=np.uint64) << 12).astype(np.uint32)
+    g = oracle.gumbel_of_bits(x)
+    assert g.mean() == pytest.approx(np.euler_gamma, abs=2e-3)
+    assert g.var() == pytest.approx(math.pi ** 2 / 6, rel=5e-3)
+
+
+def test_sampled_with_constant_noise_is_greedy():
+    """Equal noise for every cluster leaves the order of log mu, which is the
+    order of the scores: the greedy top-c."""
+    rng = np.random.default_rng(42)
+    q, C = _unit(rng, 7, 16), _unit(rng, 30, 16)
+    noise = np.full((7, 30), 123456789, dtype=np.uint32)
+    sel, ss, _, _ = oracle.coarse_sampled(q, C, 5, 0.2, 0.5, noise, "f32")
+    sel0, ss0 = oracle.coarse(q, C, 5)
+    np.testing.assert_array_equal(sel, sel0)
+    np.testing.assert_allclose(ss, ss0, rtol=1e-13)
+
+
+def test_sampled_frequencies_follow_the_policy():
+    """Many independent draws for one query: the first pick is distributed as
+    mu, and the ordered pair of the first two picks as sequential sampling
+    without replacement, mu(a) mu(b) / (1 - mu(a)) (chi-square, 1e-4 level)."""
+    from scipy.stats import chi2
+    rng = np.random.default_rng(43)
+    G, n = 6, 60000
+    q, C = _unit(rng, 1, 8), _unit(rng, G, 8)
+    Q = np.repeat(q, n, axis=0)
+    noise = rng.integers(0, 2 ** 32, (n, G), dtype=np.uint64).astype(np.uint32)
+    sel, _, _, S = oracle.coarse_sampled(Q, C, 2, 0.3, 0.1, noise, "f32")
+    mu = oracle.policy(S[:1], 0.3, 0.1)[0]
+    obs = np.bincount(sel[:, 0], minlength=G)
+    stat = ((obs - n * mu) ** 2 / (n * mu)).sum()
+    assert stat < chi2.ppf(1 - 1e-4, G - 1)
+    pair = sel[:, 0] * G + sel[:, 1]
+    exp2 = np.array([mu[a] * mu[b] / (1 - mu[a]) if a != b else 0.0
+                     for a in range(G) for b in range(G)]) * n
+    obs2 = np.bincount(pair, minlength=G * G)
+    m = exp2 > 0
+    assert np.all(obs2[~m] == 0)
+    stat2 = ((obs2[m] - exp2[m]) ** 2 / exp2[m]).sum()
+    assert stat2 < chi2.ppf(1 - 1e-4, m.sum() - 1)
