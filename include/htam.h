@@ -166,6 +166,37 @@ htam_status htam_retrieve_coarse(const htam_bank *bank, const void *q, int32_t q
 size_t htam_retrieve_coarse_workspace_size(const htam_bank *bank, int32_t n_queries, int32_t top_c);
 
 /*
+ * htam_retrieve_coarse_sampled -- the stochastic direction choice of Alg. 1,
+ * Step 2 (g_t ~ mu_g), drawn top_c times without replacement. The policy of
+ * Eq. global direction over every cluster,
+ *     mu(g) = epsilon / G + (1 - epsilon) softmax(score / tau_g)(g),
+ * (epsilon-uniform exploration plus the temperature softmax of the one-term
+ * coarse scores <q_b, c_g>) is sampled by the Gumbel-top-k construction:
+ * cluster g's key is log mu(g) + Gumbel(u_bg), and the top_c keys are a draw
+ * of top_c clusters one after another without replacement from mu.
+ *
+ *   epsilon      exploration weight, 0 <= epsilon <= 1.
+ *   tau_g        policy temperature, finite and > 0 (as tau_g -> 0 with
+ *                epsilon = 0 the draw becomes the greedy top_c).
+ *   noise        [n_queries][G] uint32 uniform words (u = (x + 1/2) / 2^32),
+ *                or NULL: the library draws them from Philox4x32-10 with key
+ *                (seed low, seed high) and counter (g / 4, b, offset low,
+ *                offset high), word g % 4, so a draw depends only on
+ *                (seed, offset, b, g) (use a new offset for a new draw).
+ *   sel_cluster  [n_queries][top_c] out: the drawn clusters in draw order
+ *                (descending key; ties to the lower cluster id).
+ *   sel_score    [n_queries][top_c] out or NULL: their coarse scores.
+ *   ws, ws_bytes workspace of htam_retrieve_coarse_sampled_workspace_size().
+ */
+htam_status htam_retrieve_coarse_sampled(const htam_bank *bank, const void *q, int32_t q_dtype,
+                                         int32_t n_queries, int32_t top_c, float epsilon,
+                                         float tau_g, const uint32_t *noise, uint64_t seed,
+                                         uint64_t offset, int32_t *sel_cluster, float *sel_score,
+                                         void *ws, size_t ws_bytes, hipStream_t stream);
+size_t htam_retrieve_coarse_sampled_workspace_size(const htam_bank *bank, int32_t n_queries,
+                                                   int32_t top_c);
+
+/*
  * htam_retrieve_coarse_prefix -- prefix-aware scoring of every cluster, then
  * the best top_c: htam_retrieve_coarse with the transition-attended score of
  * Sec. 4.3 (Eq. score, with the position-aware weights of Eq. prefix_weight;

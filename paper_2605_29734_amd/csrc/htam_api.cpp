@@ -263,6 +263,49 @@ HTAM_API htam_status htam_attend_transitions(const htam_bank *bank, const void *
 }
 
 // ---------------------------------------------------------------------------
+HTAM_API size_t htam_retrieve_coarse_sampled_workspace_size(const htam_bank *bank,
+                                                            int32_t n_queries, int32_t top_c) {
+    if (!bank || n_queries < 0 || bank->n_clusters < 1 || top_c < 1) return 0;
+    size_t bytes = 0;
+    htam::sampled_layout(nullptr, n_queries, bank->n_clusters, bank->d, bank->key_dtype,
+                         bank->compute_dtype, top_c, &bytes);
+    return bytes;
+}
+
+HTAM_API htam_status htam_retrieve_coarse_sampled(const htam_bank *bank, const void *q,
+                                                  int32_t q_dtype, int32_t n_queries, int32_t top_c,
+                                                  float epsilon, float tau_g,
+                                                  const uint32_t *noise, uint64_t seed,
+                                                  uint64_t offset, int32_t *sel_cluster,
+                                                  float *sel_score, void *ws, size_t ws_bytes,
+                                                  hipStream_t stream) {
+    HTAM_TRY(check_bank(bank));
+    HTAM_TRY(check_query(bank, q, q_dtype, n_queries));
+    const int32_t cmax = bank->n_clusters < HTAM_MAX_TOP_C ? bank->n_clusters : HTAM_MAX_TOP_C;
+    if (top_c < 1 || top_c > cmax)
+        return fail(HTAM_ERR_SHAPE, "top_c = %d out of [1, %d]", top_c, cmax);
+    if (!std::isfinite(epsilon) || epsilon < 0.0f || epsilon > 1.0f)
+        return fail(HTAM_ERR_VALUE, "epsilon = %g: need 0 <= epsilon <= 1", (double)epsilon);
+    if (!std::isfinite(tau_g) || !(tau_g > 0.0f))
+        return fail(HTAM_ERR_VALUE, "tau_g = %g: need a finite tau_g > 0", (double)tau_g);
+    if (n_queries == 0) return ok();
+    if (!sel_cluster) return fail(HTAM_ERR_NULL, "sel_cluster is NULL");
+    HTAM_TRY(check_ws(ws, ws_bytes,
+                      htam_retrieve_coarse_sampled_workspace_size(bank, n_queries, top_c)));
+    const int n_cu = device_cus(nullptr);
+    if (n_cu <= 0) return fail(HTAM_ERR_DEVICE, "no HIP device");
+    const htam::SampledWs w = htam::sampled_layout(ws, n_queries, bank->n_clusters, bank->d,
+                                                   bank->key_dtype, bank->compute_dtype, top_c,
+                                                   nullptr);
+    return device_status(htam::launch_sampled(bank->key_dtype, bank->compute_dtype, bank->d,
+                                              bank->n_clusters, bank->coarse_keys, q, n_queries,
+                                              top_c, epsilon, tau_g, noise, seed, offset,
+                                              sel_cluster, sel_score, w, n_cu,
+                                              g_events[HTAM_KERNEL_COARSE], stream),
+                         "htam_retrieve_coarse_sampled");
+}
+
+// ---------------------------------------------------------------------------
 HTAM_API size_t htam_retrieve_coarse_prefix_workspace_size(const htam_bank *bank,
                                                            int32_t n_queries, int32_t max_prefix,
                                                            int32_t top_c) {

@@ -145,6 +145,20 @@ hipError_t launch_prefix(int32_t key_dtype, int32_t compute_dtype, int32_t d, in
                          int32_t *sel, float *sel_score, const PrefixWs &w, int n_cu,
                          KernelEvents ev, hipStream_t s);
 
+// ---- sampled direction choice (Gumbel-top-k of the policy) ---------------------
+struct SampledWs {
+    CoarseWs c;        // scores and the selection's buffers
+    float *keys;       // [B][G] perturbed log-policy keys
+    float *sel_key;    // [B][top_c] keys of the selection
+};
+SampledWs sampled_layout(void *ws, int32_t B, int32_t G, int32_t d, int32_t key_dtype,
+                         int32_t compute_dtype, int32_t top_c, size_t *bytes);
+hipError_t launch_sampled(int32_t key_dtype, int32_t compute_dtype, int32_t d, int32_t G,
+                          const void *coarse_keys, const void *q, int32_t B, int32_t top_c,
+                          float eps, float tau_g, const uint32_t *noise, uint64_t seed,
+                          uint64_t offset, int32_t *sel, float *sel_score, const SampledWs &w,
+                          int n_cu, KernelEvents ev, hipStream_t s);
+
 // ---- fine stage (routing + bank stream + per-slot merge) ----------------------
 struct AttendWs {
     int32_t *cnt;      // [G] queries per cluster

@@ -54,6 +54,7 @@ def _load():
     lib = ctypes.CDLL(_LIB_PATH)
     P, i32, i64, f32, sz = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float,
                             ctypes.c_size_t)
+    u64 = ctypes.c_uint64
     BP = ctypes.POINTER(BankStruct)
     sig = {
         "htam_memory_build": ([i64, i32, i32, i32, P, P, P, P, P, P, sz, P], i32),
@@ -62,6 +63,8 @@ def _load():
         "htam_retrieve_coarse_workspace_size": ([BP, i32, i32], sz),
         "htam_attend_transitions": ([BP, P, i32, i32, P, i32, f32, i32, P, P, P, P, P, sz, P], i32),
         "htam_attend_transitions_workspace_size": ([BP, i32, i32, i32], sz),
+        "htam_retrieve_coarse_sampled": ([BP, P, i32, i32, i32, f32, f32, P, u64, u64, P, P, P, sz, P], i32),
+        "htam_retrieve_coarse_sampled_workspace_size": ([BP, i32, i32], sz),
         "htam_retrieve_coarse_prefix": ([BP, P, P, i32, f32, P, i32, i32, i32, P, P, P, sz, P], i32),
         "htam_retrieve_coarse_prefix_workspace_size": ([BP, i32, i32, i32], sz),
         "htam_retrieve_flat": ([BP, P, i32, i32, f32, i32, P, P, P, P, P, P, P, sz, P], i32),
@@ -191,6 +194,28 @@ def htam_attend_transitions(bank: Bank, q: torch.Tensor, sel: torch.Tensor, tau:
                                        _ptr(sel), c, float(tau), top_k, _ptr(out[0]), _ptr(out[1]),
                                        _ptr(out[2]), _ptr(out[3]), _ptr(ws), ws.numel(),
                                        _stream(dev)))
+    return out
+
+
+def htam_retrieve_coarse_sampled(bank: Bank, q: torch.Tensor, top_c: int, eps: float, tau_g: float,
+                                 noise: torch.Tensor | None = None, seed: int = 0, offset: int = 0,
+                                 out=None, ws=None):
+    """Draw top_c clusters per query from the policy mu_g without replacement.
+    noise: [B][G] uint32 words as int32 tensor, or None (Philox from seed, offset).
+    Returns (sel_cluster int32 [B][c], sel_score fp32 [B][c])."""
+    B = q.shape[0]
+    dev = q.device
+    if out is None:
+        out = (torch.empty(B, top_c, dtype=torch.int32, device=dev),
+               torch.empty(B, top_c, dtype=torch.float32, device=dev))
+    if ws is None:
+        ws = _workspace(lib.htam_retrieve_coarse_sampled_workspace_size(
+            ctypes.byref(bank.struct), B, top_c), dev)
+    _check("htam_retrieve_coarse_sampled",
+           lib.htam_retrieve_coarse_sampled(ctypes.byref(bank.struct), _ptr(q), dtype_code(q.dtype), B,
+                                            top_c, float(eps), float(tau_g), _ptr(noise), int(seed),
+                                            int(offset), _ptr(out[0]), _ptr(out[1]), _ptr(ws),
+                                            ws.numel(), _stream(dev)))
     return out
 
 

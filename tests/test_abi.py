@@ -155,3 +155,22 @@ def test_prefix_rejects_bad_arguments():
     assert call(wsb=64) == -5
     assert call(B=0) == 0
     assert htam.lib.htam_retrieve_coarse_prefix_workspace_size(ctypes.byref(b), 4, 4, 2) > 0
+
+
+def test_sampled_rejects_bad_arguments():
+    f = htam.lib.htam_retrieve_coarse_sampled
+    b = _bank()
+
+    def call(eps=0.1, tau=1.0, B=4, c=2, wsb=1 << 40, sel=FAKE):
+        return f(ctypes.byref(b), FAKE, htam.HTAM_BF16, B, c, eps, tau, None, 1, 0, sel, FAKE,
+                 FAKE, wsb, None)
+    assert call(eps=-0.1) == -4
+    assert call(eps=1.5) == -4
+    assert call(eps=math.nan) == -4
+    assert call(tau=0.0) == -4
+    assert call(c=0) == -2
+    assert call(sel=None) == -1
+    assert call(wsb=64) == -5
+    assert call(B=0) == 0
+    assert htam.lib.htam_retrieve_coarse_sampled_workspace_size(ctypes.byref(b), 4, 2) > 0
+
