@@ -144,6 +144,37 @@ htam_status htam_memory_build(int64_t n, int32_t n_clusters, int32_t d, int32_t 
 size_t htam_memory_build_workspace_size(int64_t n, int32_t n_clusters);
 
 /*
+ * htam_memory_merge -- online memory update, record side: fold a delta bank
+ * of newly appended records into the main bank (the memory growth of
+ * Eq. memory_update, Alg. 1 Step 4, kept log-structured). New records are
+ * built into a small delta bank with htam_memory_build; retrieval reads both
+ * banks (htam_attend_transitions on each, the per-slot lists merged by
+ * htam_topk, which gives exactly the union's softmax and top-k); this call
+ * compacts them into one bank: the bank htam_memory_build would make from the
+ * main bank's records followed by the delta's. Per cluster g the output
+ * segment holds main's rows of g, then delta's, each in their order, and
+ * off_out[g] = off_a[g] + off_b[g].
+ *
+ *   n_clusters   G >= 1 (both banks have G segments).
+ *   d, key_dtype key width and element type of both banks and of keys_out.
+ *   keys_a, off_a, id_a, n_a   main bank: [n_a][d] keys, [G+1] offsets,
+ *                [n_a] caller ids (required).
+ *   keys_b, off_b, id_b, n_b   delta bank, the same.
+ *   keys_out [n_a + n_b][d], off_out [G+1], id_out [n_a + n_b] out; keys_out
+ *                must not overlap the inputs.
+ *   ws, ws_bytes workspace of htam_memory_merge_workspace_size() bytes.
+ * Offsets that are not a partition of their bank's rows are detected on the
+ * device before any row is moved, and then nothing is written; under
+ * HTAM_VALIDATE the call waits and returns HTAM_ERR_VALUE for them.
+ */
+htam_status htam_memory_merge(int32_t n_clusters, int32_t d, int32_t key_dtype,
+                              const void *keys_a, const int64_t *off_a, const int32_t *id_a,
+                              int64_t n_a, const void *keys_b, const int64_t *off_b,
+                              const int32_t *id_b, int64_t n_b, void *keys_out, int64_t *off_out,
+                              int32_t *id_out, void *ws, size_t ws_bytes, hipStream_t stream);
+size_t htam_memory_merge_workspace_size(void);
+
+/*
  * htam_retrieve_coarse -- score every cluster and keep the best top_c.
  *
  * Alg. 1, Step 2: the score of each global node for the current state

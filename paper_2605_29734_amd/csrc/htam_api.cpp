@@ -263,6 +263,52 @@ HTAM_API htam_status htam_attend_transitions(const htam_bank *bank, const void *
 }
 
 // ---------------------------------------------------------------------------
+HTAM_API size_t htam_memory_merge_workspace_size(void) { return 256; }
+
+HTAM_API htam_status htam_memory_merge(int32_t n_clusters, int32_t d, int32_t key_dtype,
+                                       const void *keys_a, const int64_t *off_a,
+                                       const int32_t *id_a, int64_t n_a, const void *keys_b,
+                                       const int64_t *off_b, const int32_t *id_b, int64_t n_b,
+                                       void *keys_out, int64_t *off_out, int32_t *id_out,
+                                       void *ws, size_t ws_bytes, hipStream_t stream) {
+    if (n_clusters < 1) return fail(HTAM_ERR_SHAPE, "n_clusters = %d < 1", n_clusters);
+    if (n_a < 0 || n_b < 0 || n_a + n_b >= (int64_t(1) << 31))
+        return fail(HTAM_ERR_SHAPE, "n_a = %lld, n_b = %lld: need n_a, n_b >= 0 and n_a + n_b < 2^31",
+                    (long long)n_a, (long long)n_b);
+    if (!valid_dtype(key_dtype)) return fail(HTAM_ERR_DTYPE, "unknown key_dtype %d", key_dtype);
+    if (d < 8 || d > HTAM_MAX_DIM || d % 8 != 0)
+        return fail(HTAM_ERR_SHAPE, "d = %d: need 8 <= d <= %d and d %% 8 == 0", d, HTAM_MAX_DIM);
+    if (!off_a || !off_b || !off_out) return fail(HTAM_ERR_NULL, "an offset array is NULL");
+    if ((n_a > 0 && (!keys_a || !id_a)) || (n_b > 0 && (!keys_b || !id_b)) ||
+        (n_a + n_b > 0 && (!keys_out || !id_out)))
+        return fail(HTAM_ERR_NULL, "a key or id array is NULL");
+    if (!aligned16(keys_a) || !aligned16(keys_b) || !aligned16(keys_out))
+        return fail(HTAM_ERR_ALIGN, "key arrays must be 16-byte aligned");
+    const size_t rb = (size_t)d * dtype_bytes(key_dtype);
+    auto overlap = [](const void *p, size_t np, const void *q, size_t nq) {
+        const char *a = static_cast<const char *>(p), *b = static_cast<const char *>(q);
+        return np && nq && a < b + nq && b < a + np;
+    };
+    if (overlap(keys_out, (n_a + n_b) * rb, keys_a, n_a * rb) ||
+        overlap(keys_out, (n_a + n_b) * rb, keys_b, n_b * rb))
+        return fail(HTAM_ERR_VALUE, "keys_out overlaps an input bank");
+    HTAM_TRY(check_ws(ws, ws_bytes, htam_memory_merge_workspace_size()));
+    int32_t *bad = static_cast<int32_t *>(ws);
+    hipError_t e = htam::launch_merge_banks(n_clusters, (int32_t)rb, keys_a, off_a, id_a, n_a,
+                                            keys_b, off_b, id_b, n_b, keys_out, off_out, id_out,
+                                            bad, stream);
+    if (e != hipSuccess) return device_status(e, "htam_memory_merge");
+    if (!validate_mode()) return ok();
+    int32_t hb = 0;
+    e = hipMemcpyAsync(&hb, bad, sizeof hb, hipMemcpyDeviceToHost, stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(stream);
+    if (e != hipSuccess) return device_status(e, "htam_memory_merge (validation)");
+    if (hb) return fail(HTAM_ERR_VALUE, "an input bank's offsets are not a partition of its rows "
+                        "(nothing was written)");
+    return ok();
+}
+
+// ---------------------------------------------------------------------------
 HTAM_API size_t htam_retrieve_coarse_sampled_workspace_size(const htam_bank *bank,
                                                             int32_t n_queries, int32_t top_c) {
     if (!bank || n_queries < 0 || bank->n_clusters < 1 || top_c < 1) return 0;

@@ -145,6 +145,15 @@ hipError_t launch_prefix(int32_t key_dtype, int32_t compute_dtype, int32_t d, in
                          int32_t *sel, float *sel_score, const PrefixWs &w, int n_cu,
                          KernelEvents ev, hipStream_t s);
 
+// ---- online memory update: log-structured compaction -----------------------------
+// Merged bank of (a then b) per cluster; *bad (device) is set when either
+// bank's offsets are not a partition of its rows, and nothing is written then.
+hipError_t launch_merge_banks(int32_t G, int32_t row_bytes, const void *keys_a,
+                              const int64_t *off_a, const int32_t *id_a, int64_t n_a,
+                              const void *keys_b, const int64_t *off_b, const int32_t *id_b,
+                              int64_t n_b, void *keys_out, int64_t *off_out, int32_t *id_out,
+                              int32_t *bad, hipStream_t s);
+
 // ---- sampled direction choice (Gumbel-top-k of the policy) ---------------------
 struct SampledWs {
     CoarseWs c;        // scores and the selection's buffers

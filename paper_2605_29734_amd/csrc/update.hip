@@ -1,0 +1,104 @@
+// Online memory update on gfx950, record side (Eq. memory_update: the memory
+// grows by each step's new transition record under its parent direction; Alg.
+// 1, Step 4). Records are appended log-structured: new records are built into
+// a small delta bank (htam_memory_build), retrieval reads the main and the
+// delta bank and merges their per-slot lists, and this compaction folds the
+// delta into the main bank. The result is the bank that htam_memory_build
+// would make from the main bank's records followed by the delta's: segment by
+// segment, the main bank's rows, then the delta's, each in their order.
+//
+// With both banks' offsets a partition of their rows, the destination of a
+// row has a closed form: main row i of cluster g goes to i + off_delta[g]
+// (the delta rows of clusters before g come first), delta row j of cluster g
+// to j + off_main[g + 1] (all main rows of clusters up to g come first). One
+// wave takes 64 rows: each lane finds its row's cluster by binary search over
+// the offsets, then the wave copies the rows with 16-byte accesses.
+#include "dev.hpp"
+#include "internal.hpp"
+
+namespace htam {
+
+namespace {
+
+// Both offset arrays must partition their banks' rows (off[0] = 0,
+// nondecreasing, off[G] = rows); *bad = 1 otherwise. One block.
+__global__ void merge_check(const int64_t *off_a, int64_t n_a, const int64_t *off_b, int64_t n_b,
+                            int32_t G, int32_t *bad) {
+    int b = 0;
+    for (int32_t g = threadIdx.x; g < G; g += blockDim.x)
+        b |= off_a[g] > off_a[g + 1] || off_b[g] > off_b[g + 1];
+    if (threadIdx.x == 0) b |= off_a[0] != 0 || off_a[G] != n_a || off_b[0] != 0 || off_b[G] != n_b;
+    b = __syncthreads_or(b);
+    if (threadIdx.x == 0) *bad = b;
+}
+
+__global__ void merge_offsets(const int64_t *off_a, const int64_t *off_b, int32_t G,
+                              const int32_t *bad, int64_t *off_out) {
+    if (*bad) return;
+    for (int64_t g = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; g <= G;
+         g += (int64_t)gridDim.x * blockDim.x)
+        off_out[g] = off_a[g] + off_b[g];
+}
+
+// Rows of one source bank to their merged positions: row r of cluster g goes
+// to r + shift[g + step] (step 0: the main bank, shift = delta offsets;
+// step 1: the delta bank, shift = main offsets).
+__global__ __launch_bounds__(256) void merge_rows(const uint4 *__restrict__ keys,
+                                                  const int32_t *__restrict__ ids,
+                                                  const int64_t *__restrict__ off, int64_t n,
+                                                  const int64_t *__restrict__ shift, int32_t step,
+                                                  int32_t G, int32_t vpr, const int32_t *bad,
+                                                  uint4 *__restrict__ keys_out,
+                                                  int32_t *__restrict__ ids_out) {
+    if (*bad) return;
+    const int lane = threadIdx.x & 63;
+    const int64_t waves = (int64_t)gridDim.x * (blockDim.x >> 6);
+    for (int64_t r0 = ((int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6)) * kWave; r0 < n;
+         r0 += waves * kWave) {
+        const int64_t r = r0 + lane;
+        int64_t dst = 0;
+        if (r < n) {
+            int32_t lo = 0, hi = G;                 // off[lo] <= r < off[hi]
+            while (hi - lo > 1) {
+                const int32_t mid = (lo + hi) >> 1;
+                if (off[mid] <= r) lo = mid; else hi = mid;
+            }
+            dst = r + shift[lo + step];
+            ids_out[dst] = ids[r];
+        }
+        const int rows = (int)min((int64_t)kWave, n - r0);
+        for (int i = 0; i < rows; ++i) {
+            const int64_t di = __shfl(dst, i);
+            for (int v = lane; v < vpr; v += kWave)
+                keys_out[di * vpr + v] = keys[(r0 + i) * vpr + v];
+        }
+    }
+}
+
+}  // namespace
+
+hipError_t launch_merge_banks(int32_t G, int32_t row_bytes, const void *keys_a,
+                              const int64_t *off_a, const int32_t *id_a, int64_t n_a,
+                              const void *keys_b, const int64_t *off_b, const int32_t *id_b,
+                              int64_t n_b, void *keys_out, int64_t *off_out, int32_t *id_out,
+                              int32_t *bad, hipStream_t s) {
+    hipLaunchKernelGGL(merge_check, dim3(1), dim3(1024), 0, s, off_a, n_a, off_b, n_b, G, bad);
+    hipLaunchKernelGGL(merge_offsets, dim3((G + 256) / 256 < 1024 ? (G + 256) / 256 : 1024),
+                       dim3(256), 0, s, off_a, off_b, G, bad, off_out);
+    const int32_t vpr = row_bytes / 16;
+    auto grid = [](int64_t n) {
+        const int64_t w = (n + kWave - 1) / kWave, b = (w + 3) / 4;
+        return (unsigned)(b < 8192 ? (b > 0 ? b : 1) : 8192);
+    };
+    if (n_a > 0)
+        hipLaunchKernelGGL(merge_rows, dim3(grid(n_a)), dim3(256), 0, s,
+                           static_cast<const uint4 *>(keys_a), id_a, off_a, n_a, off_b, 0, G, vpr,
+                           bad, static_cast<uint4 *>(keys_out), id_out);
+    if (n_b > 0)
+        hipLaunchKernelGGL(merge_rows, dim3(grid(n_b)), dim3(256), 0, s,
+                           static_cast<const uint4 *>(keys_b), id_b, off_b, n_b, off_a, 1, G, vpr,
+                           bad, static_cast<uint4 *>(keys_out), id_out);
+    return hipGetLastError();
+}
+
+}  // namespace htam

@@ -63,6 +63,8 @@ def _load():
         "htam_retrieve_coarse_workspace_size": ([BP, i32, i32], sz),
         "htam_attend_transitions": ([BP, P, i32, i32, P, i32, f32, i32, P, P, P, P, P, sz, P], i32),
         "htam_attend_transitions_workspace_size": ([BP, i32, i32, i32], sz),
+        "htam_memory_merge": ([i32, i32, i32, P, P, P, i64, P, P, P, i64, P, P, P, P, sz, P], i32),
+        "htam_memory_merge_workspace_size": ([], sz),
         "htam_retrieve_coarse_sampled": ([BP, P, i32, i32, i32, f32, f32, P, u64, u64, P, P, P, sz, P], i32),
         "htam_retrieve_coarse_sampled_workspace_size": ([BP, i32, i32], sz),
         "htam_retrieve_coarse_prefix": ([BP, P, P, i32, f32, P, i32, i32, i32, P, P, P, sz, P], i32),
@@ -339,6 +341,50 @@ class Retriever:
                     slot_sum=self.slots[1], slot_score=self.slots[2], slot_id=self.slots[3],
                     id=self.rows[0], score=self.rows[1], weight=self.rows[2], m=self.rows[3],
                     Z=self.rows[4], count=self.rows[5])
+
+
+def htam_memory_merge(main: Bank, delta: Bank) -> Bank:
+    """Compact a delta bank into the main bank (both with transition ids)."""
+    dev = main.device
+    G = main.coarse_keys.shape[0]
+    na, nb = main.fine_keys.shape[0], delta.fine_keys.shape[0]
+    keys = torch.empty(na + nb, main.fine_keys.shape[1], dtype=main.fine_keys.dtype, device=dev)
+    off = torch.empty(G + 1, dtype=torch.int64, device=dev)
+    ids = torch.empty(na + nb, dtype=torch.int32, device=dev)
+    ws = _workspace(lib.htam_memory_merge_workspace_size(), dev)
+    _check("htam_memory_merge",
+           lib.htam_memory_merge(G, main.fine_keys.shape[1], dtype_code(main.fine_keys.dtype),
+                                 _ptr(main.fine_keys), _ptr(main.seg_offsets),
+                                 _ptr(main.transition_id), na, _ptr(delta.fine_keys),
+                                 _ptr(delta.seg_offsets), _ptr(delta.transition_id), nb,
+                                 _ptr(keys), _ptr(off), _ptr(ids), _ptr(ws), ws.numel(),
+                                 _stream(dev)))
+    return Bank(coarse_keys=main.coarse_keys, fine_keys=keys, seg_offsets=off, transition_id=ids,
+                compute=main.compute)
+
+
+def retrieve_two_banks(main: Bank, delta: Bank, q: torch.Tensor, top_c: int, top_k: int,
+                       tau: float) -> dict:
+    """Retrieval over a main bank and a delta bank of recent records (same
+    clusters and coarse keys): one coarse selection, the fine stage on each
+    bank, then each slot's two lists merged and every row's 2 * top_c lists
+    merged by htam_topk -- the result over the union of the two banks."""
+    B = q.shape[0]
+    sel, ss = htam_retrieve_coarse(main, q, top_c)
+    a = htam_attend_transitions(main, q, sel, tau, top_k)
+    b = htam_attend_transitions(delta, q, sel, tau, top_k)
+    # per slot: the two lists of (query, slot) merged
+    sc = torch.stack([a[2], b[2]], dim=2).reshape(B * top_c, 2, top_k).contiguous()
+    si = torch.stack([a[3], b[3]], dim=2).reshape(B * top_c, 2, top_k).contiguous()
+    sm = torch.stack([a[0], b[0]], dim=2).reshape(B * top_c, 2).contiguous()
+    sz = torch.stack([a[1], b[1]], dim=2).reshape(B * top_c, 2).contiguous()
+    slot = htam_topk(sc, si, top_k, sm, sz, tau)
+    row = htam_topk(slot[1].reshape(B, top_c, top_k), slot[0].reshape(B, top_c, top_k), top_k,
+                    slot[3].reshape(B, top_c), slot[4].reshape(B, top_c), tau)
+    return dict(sel=sel, sel_score=ss, slot_id=slot[0].reshape(B, top_c, top_k),
+                slot_score=slot[1].reshape(B, top_c, top_k), slot_max=slot[3].reshape(B, top_c),
+                slot_sum=slot[4].reshape(B, top_c), id=row[0], score=row[1], weight=row[2],
+                m=row[3], Z=row[4], count=row[5])
 
 
 def build_bank(cluster_of: torch.Tensor, keys_in: torch.Tensor, coarse_keys: torch.Tensor,

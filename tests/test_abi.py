@@ -174,3 +174,19 @@ def test_sampled_rejects_bad_arguments():
     assert call(B=0) == 0
     assert htam.lib.htam_retrieve_coarse_sampled_workspace_size(ctypes.byref(b), 4, 2) > 0
 
+
+
+def test_merge_rejects_bad_arguments():
+    f = htam.lib.htam_memory_merge
+
+    def call(G=4, d=64, kd=htam.HTAM_BF16, na=10, nb=5, ka=FAKE, kout=FAKE * 4, ida=FAKE, wsb=256):
+        return f(G, d, kd, ka, FAKE, ida, na, FAKE * 2, FAKE, FAKE, nb, kout, FAKE, FAKE, FAKE,
+                 wsb, None)
+    assert call(G=0) == -2
+    assert call(d=12) == -2
+    assert call(kd=5) == -3
+    assert call(na=-1) == -2
+    assert call(ida=None) == -1
+    assert call(ka=FAKE + 8) == -6
+    assert call(kout=FAKE) == -4                         # output overlaps an input
+    assert call(wsb=4) == -5
