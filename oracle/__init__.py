@@ -381,3 +381,89 @@ def coarse_sampled(q, c, top_c: int, eps: float, tau_g: float, noise, compute: s
     for b in range(B):
         sel[b] = np.lexsort((np.arange(G), -keys[b]))[:top_c]
     return sel, np.take_along_axis(S, sel, axis=1), keys, S
+
+
+# ---------------------------------------------------------------------------
+# online memory update, statistics side (Eq. memory_update; App. B.6)
+# ---------------------------------------------------------------------------
+FEEDBACK_FEATURES = 11     # r_imm, r_fut, pos, succ, comp, corr, safe, cfail, corfail, neg, risk
+STATS_WORDS = 12           # count, then the fixed-point sum of each feature
+FIXED_ONE = 1 << 24        # fixed-point scale of the sums
+
+
+def feedback_update(G: int, n_buckets: int, src, dst, bucket, feat, node, edge, edge_bucket):
+    """Rule-based aggregation of step outcomes into the memory's statistics
+    (Eq. memory_update refreshes the node statistics of V_G(g_t) and the
+    transition-edge feedback of E_G(g_{t-1}, g_t), t > 1; App. B.2 and B.6).
+    Event e adds one observation with features feat[e] (the outcome's
+    r_imm, r_fut and indicator/rate values, App. B.6) to node dst[e], and,
+    when src[e] >= 0 (not the first step), to edge (src[e], dst[e]) and to
+    that edge's state bucket bucket[e]. Sums are kept in fixed point
+    (round-to-nearest-even of x * 2^24, exact int64 additions), so they do not
+    depend on the order of the events. Events with dst or bucket out of range
+    are skipped. Returns updated copies of node [G][12], edge [G][G][12],
+    edge_bucket [G][G][n_buckets][12]."""
+    node, edge, edge_bucket = (np.array(x, dtype=np.int64, copy=True) for x in
+                               (node, edge, edge_bucket))
+    fx = np.rint(np.asarray(feat, dtype=np.float32).astype(np.float64) * FIXED_ONE).astype(np.int64)
+    for e in range(len(dst)):
+        s, d, k = int(src[e]), int(dst[e]), int(bucket[e])
+        if not (0 <= d < G and 0 <= k < n_buckets and s < G):
+            continue
+        rec = np.concatenate([[1], fx[e]])
+        node[d] += rec
+        if s >= 0:
+            edge[s, d] += rec
+            edge_bucket[s, d, k] += rec
+    return node, edge, edge_bucket
+
+
+def feature_vector(stats, h_ctx: float) -> np.ndarray:
+    """z of App. B.6 (Eq. transition_feature_vector) from one statistics record:
+    [r_imm, r_fut, p_pos | p_succ, p_comp, p_corr, p_safe, h_ctx |
+     -p_cfail, -p_corfail, -p_neg, -rho_risk], means over the observations;
+    no observation gives the zero prior."""
+    stats = np.asarray(stats, dtype=np.int64)
+    n = int(stats[0])
+    if n == 0:
+        return np.zeros(STATS_WORDS)
+    m = stats[1:].astype(np.float64) / (n * FIXED_ONE)
+    return np.concatenate([m[:7], [h_ctx], -m[7:]])
+
+
+def transition_utility(edge, edge_bucket, s: int, g: int, k: int, min_count: int, w) -> float:
+    """phi(s -> g | state bucket k) = w^T z: the bucket's statistics when it has
+    at least min_count observations (h_ctx = 1), else the edge's aggregate
+    statistics (h_ctx = 0) (App. B.6, Eq. transition_phi)."""
+    eb = np.asarray(edge_bucket)[s, g, k]
+    if eb[0] >= min_count and eb[0] > 0:
+        z = feature_vector(eb, 1.0)
+    else:
+        z = feature_vector(np.asarray(edge)[s, g], 0.0)
+    return float(np.dot(np.asarray(w, dtype=np.float64), z))
+
+
+def transition_scores(prefix, bucket, lam: float, w, min_count: int, node, edge, edge_bucket):
+    """Scores of every direction by the rule-based scorer: for a query with
+    prefix (g_1..g_L) and state bucket k, score(g) = sum_i alpha_i
+    phi(g_i -> g | k) with alpha_i = exp(-lam (L - i)) (Eq. score,
+    Eq. prefix_weight); an empty prefix uses the node statistics of g
+    (w^T z with h_ctx = 0). Returns [B][G] in double."""
+    node = np.asarray(node)
+    G = node.shape[0]
+    prefix = np.asarray(prefix)
+    B = prefix.shape[0]
+    S = np.zeros((B, G))
+    for b in range(B):
+        L = 0
+        while L < prefix.shape[1] and 0 <= prefix[b, L] < G:
+            L += 1
+        for g in range(G):
+            if L == 0:
+                S[b, g] = float(np.dot(w, feature_vector(node[g], 0.0)))
+            else:
+                a = prefix_weights(L, lam)
+                S[b, g] = sum(a[i] * transition_utility(edge, edge_bucket, int(prefix[b, i]), g,
+                                                        int(bucket[b]), min_count, w)
+                              for i in range(L))
+    return S

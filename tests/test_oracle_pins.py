@@ -545,3 +545,68 @@ def test_sampled_frequencies_follow_the_policy():
     assert np.all(obs2[~m] == 0)
     stat2 = ((obs2[m] - exp2[m]) ** 2 / exp2[m]).sum()
     assert stat2 < chi2.ppf(1 - 1e-4, m.sum() - 1)
+
+
+# ---------------------------------------------------------------------------
+# online memory update: feedback statistics and the rule-based scorer
+# ---------------------------------------------------------------------------
+def _empty_stats(G, NB):
+    W = oracle.STATS_WORDS
+    return (np.zeros((G, W), np.int64), np.zeros((G, G, W), np.int64),
+            np.zeros((G, G, NB, W), np.int64))
+
+
+def test_feedback_worked_example_exact():
+    ex = json.load(open(os.path.join(GOLDEN, "feedback_example.json")))
+    G, NB, mc = ex["G"], ex["n_buckets"], ex["min_count"]
+    node, edge, eb = oracle.feedback_update(G, NB, ex["src"], ex["dst"], ex["bucket"],
+                                            ex["features"], *_empty_stats(G, NB))
+    np.testing.assert_array_equal(node[:, 0], ex["node_count"])
+    assert edge[0, 1, 0] == ex["edge_count_0_1"]
+    np.testing.assert_array_equal(eb[0, 1, :, 0], ex["edge_bucket_count_0_1"])
+    w = np.asarray(ex["w"], np.float64)
+    for k, key in ((0, "phi_0_1_bucket0"), (1, "phi_0_1_bucket1")):
+        assert oracle.transition_utility(edge, eb, 0, 1, k, mc, w) == pytest.approx(_num(ex[key]), abs=1e-12)
+    assert oracle.transition_utility(edge, eb, 1, 0, 0, mc, w) == _num(ex["phi_1_0_bucket0"])
+    S = oracle.transition_scores(np.full((1, 2), -1), [0], 0.5, w, mc, node, edge, eb)
+    np.testing.assert_allclose(S[0], [_num(x) for x in ex["node_score"]], atol=1e-12)
+
+
+def test_feedback_sums_are_order_free_and_exact():
+    """The statistics are integer sums: any order of the events gives the
+    same bits, and the counts are the bincounts."""
+    rng = np.random.default_rng(51)
+    G, NB, n = 5, 3, 400
+    src = rng.integers(-1, G, n)
+    dst = rng.integers(0, G, n)
+    bk = rng.integers(0, NB, n)
+    feat = rng.standard_normal((n, oracle.FEEDBACK_FEATURES)).astype(np.float32)
+    a = oracle.feedback_update(G, NB, src, dst, bk, feat, *_empty_stats(G, NB))
+    p = rng.permutation(n)
+    b = oracle.feedback_update(G, NB, src[p], dst[p], bk[p], feat[p], *_empty_stats(G, NB))
+    for x, y in zip(a, b):
+        np.testing.assert_array_equal(x, y)
+    np.testing.assert_array_equal(a[0][:, 0], np.bincount(dst, minlength=G))
+    fx = np.rint(feat.astype(np.float64) * oracle.FIXED_ONE).astype(np.int64)
+    np.testing.assert_array_equal(a[0][2, 1:], fx[dst == 2].sum(axis=0))
+
+
+def test_transition_scores_prefix_and_fallback():
+    """Prefix weighting as in Eq. prefix_weight over phi; a bucket below
+    min_count falls back to the edge aggregate."""
+    rng = np.random.default_rng(52)
+    G, NB, n = 4, 2, 300
+    src, dst, bk = rng.integers(0, G, n), rng.integers(0, G, n), rng.integers(0, NB, n)
+    feat = rng.random((n, oracle.FEEDBACK_FEATURES)).astype(np.float32)
+    node, edge, eb = oracle.feedback_update(G, NB, src, dst, bk, feat, *_empty_stats(G, NB))
+    w = rng.standard_normal(oracle.STATS_WORDS)
+    P = np.array([[2, 0, 3], [1, -1, -1]])
+    S = oracle.transition_scores(P, [1, 0], 0.7, w, 5, node, edge, eb)
+    a = oracle.prefix_weights(3, 0.7)
+    for g in range(G):
+        ref = sum(a[i] * oracle.transition_utility(edge, eb, P[0, i], g, 1, 5, w) for i in range(3))
+        assert S[0, g] == pytest.approx(ref, rel=1e-13)
+    huge = 10 ** 6                                   # no bucket qualifies: the aggregate
+    S2 = oracle.transition_scores(P[1:], [0], 0.7, w, huge, node, edge, eb)
+    for g in range(G):
+        assert S2[0, g] == pytest.approx(w @ oracle.feature_vector(edge[1, g], 0.0), rel=1e-13)
