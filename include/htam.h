@@ -175,6 +175,58 @@ htam_status htam_memory_merge(int32_t n_clusters, int32_t d, int32_t key_dtype,
 size_t htam_memory_merge_workspace_size(void);
 
 /*
+ * htam_feedback_update -- online memory update, statistics side: the
+ * rule-based aggregation of step outcomes (Eq. memory_update refreshes the
+ * node statistics of V_G(g_t) and the transition-edge feedback of
+ * E_G(g_{t-1}, g_t), t > 1; App. B.2, B.6). A statistics record is
+ * HTAM_STATS_WORDS int64: the count of observations, then the sum of each of
+ * the HTAM_FEEDBACK_FEATURES outcome features in fixed point (x * 2^24,
+ * rounded to nearest even). Features, in order: r_imm and r_fut (log-runtime
+ * gains), then the indicators pos, succ, comp, corr, safe, cfail, corfail,
+ * neg (0 or 1, or rates), then risk. Event e adds one observation to
+ * node_stats[dst[e]] and, when src[e] >= 0 (not a first step), to
+ * edge_stats[src][dst] and edge_bucket_stats[src][dst][bucket[e]]. The sums
+ * are exact integer additions: the result does not depend on event order.
+ * Events with dst or bucket out of range, or src >= G, are skipped.
+ * Features must be finite with |x| < 2^38.
+ *
+ *   src, dst, bucket [n_events] int32; features [n_events][11] fp32;
+ *   node_stats [G][12], edge_stats [G][G][12],
+ *   edge_bucket_stats [G][G][n_buckets][12] int64, caller-owned, updated in
+ *   place (zero them to start an empty memory).
+ */
+#define HTAM_FEEDBACK_FEATURES 11
+#define HTAM_STATS_WORDS 12
+htam_status htam_feedback_update(int32_t n_clusters, int32_t n_buckets, int32_t n_events,
+                                 const int32_t *src, const int32_t *dst, const int32_t *bucket,
+                                 const float *features, int64_t *node_stats, int64_t *edge_stats,
+                                 int64_t *edge_bucket_stats, hipStream_t stream);
+
+/*
+ * htam_transition_scores -- the rule-based direction scores over those
+ * statistics: score_b(g) = sum_{i=1..L} alpha_i phi(g_i -> g | bucket_b),
+ * alpha_i = exp(-lambda (L - i)) (Eq. score, Eq. prefix_weight), with
+ * phi = w^T z (App. B.6, Eq. transition_phi, Eq. transition_feature_vector):
+ * z = [r_imm, r_fut, p_pos, p_succ, p_comp, p_corr, p_safe, h_ctx, -p_cfail,
+ * -p_corfail, -p_neg, -rho_risk], the means of the features over the state
+ * bucket's observations when it has at least min_count of them (h_ctx = 1),
+ * else over all of the edge's (h_ctx = 0); an edge never observed scores 0
+ * (the default prior). A query with an empty prefix scores w^T z of the node
+ * statistics of g (h_ctx = 0), as the first step does.
+ *
+ *   prefix [n_queries][max_prefix] (ends at the first entry outside [0, G)),
+ *   bucket [n_queries] the state bucket of each query (clamped into range),
+ *   w [12] fp32, scores [n_queries][G] fp32 out (select from them with
+ *   htam_topk, cand_id NULL). Arithmetic in double.
+ */
+htam_status htam_transition_scores(int32_t n_clusters, int32_t n_buckets, int32_t n_queries,
+                                   const int32_t *prefix, int32_t max_prefix,
+                                   const int32_t *bucket, float lambda, const float *w,
+                                   int32_t min_count, const int64_t *node_stats,
+                                   const int64_t *edge_stats, const int64_t *edge_bucket_stats,
+                                   float *scores, hipStream_t stream);
+
+/*
  * htam_retrieve_coarse -- score every cluster and keep the best top_c.
  *
  * Alg. 1, Step 2: the score of each global node for the current state

@@ -309,6 +309,52 @@ HTAM_API htam_status htam_memory_merge(int32_t n_clusters, int32_t d, int32_t ke
 }
 
 // ---------------------------------------------------------------------------
+HTAM_API htam_status htam_feedback_update(int32_t n_clusters, int32_t n_buckets, int32_t n_events,
+                                          const int32_t *src, const int32_t *dst,
+                                          const int32_t *bucket, const float *features,
+                                          int64_t *node_stats, int64_t *edge_stats,
+                                          int64_t *edge_bucket_stats, hipStream_t stream) {
+    if (n_clusters < 1 || n_buckets < 1 || n_events < 0)
+        return fail(HTAM_ERR_SHAPE, "n_clusters %d, n_buckets %d, n_events %d: need >= 1, >= 1, >= 0",
+                    n_clusters, n_buckets, n_events);
+    if ((int64_t)n_clusters * n_clusters * n_buckets * HTAM_STATS_WORDS >= (int64_t(1) << 40))
+        return fail(HTAM_ERR_SHAPE, "the edge-bucket statistics would exceed 2^40 words");
+    if (!node_stats || !edge_stats || !edge_bucket_stats)
+        return fail(HTAM_ERR_NULL, "a statistics array is NULL");
+    if (n_events == 0) return ok();
+    if (!src || !dst || !bucket || !features) return fail(HTAM_ERR_NULL, "an event array is NULL");
+    return device_status(htam::launch_feedback_update(n_clusters, n_buckets, n_events, src, dst,
+                                                      bucket, features, node_stats, edge_stats,
+                                                      edge_bucket_stats, stream),
+                         "htam_feedback_update");
+}
+
+HTAM_API htam_status htam_transition_scores(int32_t n_clusters, int32_t n_buckets,
+                                            int32_t n_queries, const int32_t *prefix,
+                                            int32_t max_prefix, const int32_t *bucket, float lambda,
+                                            const float *w, int32_t min_count,
+                                            const int64_t *node_stats, const int64_t *edge_stats,
+                                            const int64_t *edge_bucket_stats, float *scores,
+                                            hipStream_t stream) {
+    if (n_clusters < 1 || n_buckets < 1 || n_queries < 0)
+        return fail(HTAM_ERR_SHAPE, "n_clusters %d, n_buckets %d, n_queries %d", n_clusters,
+                    n_buckets, n_queries);
+    if (max_prefix < 1 || max_prefix > HTAM_MAX_PREFIX)
+        return fail(HTAM_ERR_SHAPE, "max_prefix = %d out of [1, %d]", max_prefix, HTAM_MAX_PREFIX);
+    if (!std::isfinite(lambda) || lambda < 0.0f)
+        return fail(HTAM_ERR_VALUE, "lambda = %g: need a finite lambda >= 0", (double)lambda);
+    if (min_count < 0) return fail(HTAM_ERR_VALUE, "min_count = %d < 0", min_count);
+    if (n_queries == 0) return ok();
+    if (!prefix || !bucket || !w || !node_stats || !edge_stats || !edge_bucket_stats || !scores)
+        return fail(HTAM_ERR_NULL, "an input or output array is NULL");
+    return device_status(htam::launch_transition_scores(n_clusters, n_buckets, n_queries, prefix,
+                                                        max_prefix, bucket, lambda, w, min_count,
+                                                        node_stats, edge_stats, edge_bucket_stats,
+                                                        scores, stream),
+                         "htam_transition_scores");
+}
+
+// ---------------------------------------------------------------------------
 HTAM_API size_t htam_retrieve_coarse_sampled_workspace_size(const htam_bank *bank,
                                                             int32_t n_queries, int32_t top_c) {
     if (!bank || n_queries < 0 || bank->n_clusters < 1 || top_c < 1) return 0;

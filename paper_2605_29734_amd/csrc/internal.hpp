@@ -154,6 +154,18 @@ hipError_t launch_merge_banks(int32_t G, int32_t row_bytes, const void *keys_a,
                               int64_t n_b, void *keys_out, int64_t *off_out, int32_t *id_out,
                               int32_t *bad, hipStream_t s);
 
+// Feedback statistics (record: count, then fixed-point feature sums) and the
+// rule-based transition scores over them.
+hipError_t launch_feedback_update(int32_t G, int32_t NB, int32_t n, const int32_t *src,
+                                  const int32_t *dst, const int32_t *bucket, const float *feat,
+                                  int64_t *node, int64_t *edge, int64_t *edge_bucket,
+                                  hipStream_t s);
+hipError_t launch_transition_scores(int32_t G, int32_t NB, int32_t B, const int32_t *prefix,
+                                    int32_t lmax, const int32_t *bucket, float lambda,
+                                    const float *w, int32_t min_count, const int64_t *node,
+                                    const int64_t *edge, const int64_t *edge_bucket,
+                                    float *scores, hipStream_t s);
+
 // ---- sampled direction choice (Gumbel-top-k of the policy) ---------------------
 struct SampledWs {
     CoarseWs c;        // scores and the selection's buffers

@@ -13,6 +13,10 @@
 // to j + off_main[g + 1] (all main rows of clusters up to g come first). One
 // wave takes 64 rows: each lane finds its row's cluster by binary search over
 // the offsets, then the wave copies the rows with 16-byte accesses.
+//
+// Statistics side (the node, edge and edge-bucket feedback the update
+// refreshes, and the rule-based scorer that reads them) further down.
+#include "../../include/htam.h"
 #include "dev.hpp"
 #include "internal.hpp"
 
@@ -75,7 +79,117 @@ __global__ __launch_bounds__(256) void merge_rows(const uint4 *__restrict__ keys
     }
 }
 
+// ---------------------------------------------------------------------------
+// statistics side: rule-based aggregation of step outcomes (Eq. memory_update
+// refreshes the node statistics of V_G(g_t) and the edge feedback of
+// E_G(g_{t-1}, g_t); App. B.6 reads them as the features z of phi = w^T z)
+// ---------------------------------------------------------------------------
+constexpr int kFeat = HTAM_FEEDBACK_FEATURES;
+constexpr int kWords = HTAM_STATS_WORDS;
+constexpr double kFixedOne = 16777216.0;   // 2^24
+
+// One thread per (event, word): word 0 counts the observation, word 1 + f adds
+// feature f in fixed point (x * 2^24 rounded to nearest even). int64 additions
+// are exact and commute, so the statistics do not depend on event order.
+__global__ void feedback_update(int32_t G, int32_t NB, int32_t n, const int32_t *src,
+                                const int32_t *dst, const int32_t *bucket, const float *feat,
+                                unsigned long long *node, unsigned long long *edge,
+                                unsigned long long *edge_bucket) {
+    for (int64_t x = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; x < (int64_t)n * kWords;
+         x += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t e = x / kWords;
+        const int wd = (int)(x - e * kWords);
+        const int32_t s = src[e], d = dst[e], k = bucket[e];
+        if (d < 0 || d >= G || k < 0 || k >= NB || s >= G) continue;
+        const long long v = wd == 0 ? 1LL : llrint((double)feat[e * kFeat + wd - 1] * kFixedOne);
+        const unsigned long long u = (unsigned long long)v;
+        atomicAdd(node + (int64_t)d * kWords + wd, u);
+        if (s >= 0) {
+            atomicAdd(edge + ((int64_t)s * G + d) * kWords + wd, u);
+            atomicAdd(edge_bucket + (((int64_t)s * G + d) * NB + k) * kWords + wd, u);
+        }
+    }
+}
+
+// w^T z of one statistics record (z: means over its observations, the h_ctx
+// flag in position 7, the four risk features negated; no observation: 0).
+__device__ __forceinline__ double stats_utility(const long long *st, double h, const float *w) {
+    const long long n = st[0];
+    if (n == 0) return 0.0;
+    const double inv = 1.0 / ((double)n * kFixedOne);
+    double acc = 0.0;
+#pragma unroll
+    for (int f = 0; f < kFeat; ++f) {
+        const double m = (double)st[1 + f] * inv;
+        acc += (double)w[f < 7 ? f : f + 1] * (f < 7 ? m : -m);
+    }
+    return acc + (double)w[7] * h;
+}
+
+// score_b(g) = sum_i alpha_i phi(g_i -> g | bucket_b) over b's prefix, phi
+// from the bucket's statistics when it has at least min_count observations
+// (h = 1), else from the edge's (h = 0); an empty prefix scores the node
+// statistics of g (h = 0). One thread per (query, direction); double inside.
+__global__ void transition_scores(int32_t G, int32_t NB, int32_t B, const int32_t *prefix,
+                                  int32_t lmax, const int32_t *bucket, float lambda,
+                                  const float *w, int32_t min_count, const long long *node,
+                                  const long long *edge, const long long *edge_bucket,
+                                  float *scores) {
+    for (int64_t x = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; x < (int64_t)B * G;
+         x += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t b = x / G, g = x - b * G;
+        const int32_t *row = prefix + b * lmax;
+        int L = 0;
+        while (L < lmax && row[L] >= 0 && row[L] < G) ++L;
+        double acc;
+        if (L == 0) {
+            acc = stats_utility(node + g * kWords, 0.0, w);
+        } else {
+            const int32_t k = min(max(bucket[b], 0), NB - 1);
+            acc = 0.0;
+            for (int i = 0; i < L; ++i) {
+                const int64_t eg = (int64_t)row[i] * G + g;
+                const long long *eb = edge_bucket + (eg * NB + k) * kWords;
+                const double phi = (eb[0] > 0 && eb[0] >= min_count)
+                                       ? stats_utility(eb, 1.0, w)
+                                       : stats_utility(edge + eg * kWords, 0.0, w);
+                acc += exp(-(double)lambda * (double)(L - 1 - i)) * phi;
+            }
+        }
+        scores[x] = (float)acc;
+    }
+}
+
 }  // namespace
+
+hipError_t launch_feedback_update(int32_t G, int32_t NB, int32_t n, const int32_t *src,
+                                  const int32_t *dst, const int32_t *bucket, const float *feat,
+                                  int64_t *node, int64_t *edge, int64_t *edge_bucket,
+                                  hipStream_t s) {
+    if (n == 0) return hipSuccess;
+    const int64_t t = (int64_t)n * kWords;
+    hipLaunchKernelGGL(feedback_update, dim3((unsigned)((t + 255) / 256 < 8192 ? (t + 255) / 256 : 8192)),
+                       dim3(256), 0, s, G, NB, n, src, dst, bucket, feat,
+                       reinterpret_cast<unsigned long long *>(node),
+                       reinterpret_cast<unsigned long long *>(edge),
+                       reinterpret_cast<unsigned long long *>(edge_bucket));
+    return hipGetLastError();
+}
+
+hipError_t launch_transition_scores(int32_t G, int32_t NB, int32_t B, const int32_t *prefix,
+                                    int32_t lmax, const int32_t *bucket, float lambda,
+                                    const float *w, int32_t min_count, const int64_t *node,
+                                    const int64_t *edge, const int64_t *edge_bucket,
+                                    float *scores, hipStream_t s) {
+    if (B == 0) return hipSuccess;
+    const int64_t t = (int64_t)B * G;
+    hipLaunchKernelGGL(transition_scores, dim3((unsigned)((t + 255) / 256 < 8192 ? (t + 255) / 256 : 8192)),
+                       dim3(256), 0, s, G, NB, B, prefix, lmax, bucket, lambda, w, min_count,
+                       reinterpret_cast<const long long *>(node),
+                       reinterpret_cast<const long long *>(edge),
+                       reinterpret_cast<const long long *>(edge_bucket), scores);
+    return hipGetLastError();
+}
 
 hipError_t launch_merge_banks(int32_t G, int32_t row_bytes, const void *keys_a,
                               const int64_t *off_a, const int32_t *id_a, int64_t n_a,

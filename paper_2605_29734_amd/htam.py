@@ -63,6 +63,8 @@ def _load():
         "htam_retrieve_coarse_workspace_size": ([BP, i32, i32], sz),
         "htam_attend_transitions": ([BP, P, i32, i32, P, i32, f32, i32, P, P, P, P, P, sz, P], i32),
         "htam_attend_transitions_workspace_size": ([BP, i32, i32, i32], sz),
+        "htam_feedback_update": ([i32, i32, i32, P, P, P, P, P, P, P, P], i32),
+        "htam_transition_scores": ([i32, i32, i32, P, i32, P, f32, P, i32, P, P, P, P, P], i32),
         "htam_memory_merge": ([i32, i32, i32, P, P, P, i64, P, P, P, i64, P, P, P, P, sz, P], i32),
         "htam_memory_merge_workspace_size": ([], sz),
         "htam_retrieve_coarse_sampled": ([BP, P, i32, i32, i32, f32, f32, P, u64, u64, P, P, P, sz, P], i32),
@@ -361,6 +363,42 @@ def htam_memory_merge(main: Bank, delta: Bank) -> Bank:
                                  _stream(dev)))
     return Bank(coarse_keys=main.coarse_keys, fine_keys=keys, seg_offsets=off, transition_id=ids,
                 compute=main.compute)
+
+
+HTAM_FEEDBACK_FEATURES = 11
+HTAM_STATS_WORDS = 12
+
+
+def empty_stats(G: int, n_buckets: int, device):
+    """Zeroed (node, edge, edge_bucket) statistics of an empty memory."""
+    W = HTAM_STATS_WORDS
+    z = lambda *s: torch.zeros(*s, W, dtype=torch.int64, device=device)  # noqa: E731
+    return z(G), z(G, G), z(G, G, n_buckets)
+
+
+def htam_feedback_update(stats, src, dst, bucket, features):
+    """Add step outcomes to (node, edge, edge_bucket) statistics in place."""
+    node, edge, eb = stats
+    G, NB = node.shape[0], eb.shape[2]
+    _check("htam_feedback_update",
+           lib.htam_feedback_update(G, NB, dst.numel(), _ptr(src), _ptr(dst), _ptr(bucket),
+                                    _ptr(features), _ptr(node), _ptr(edge), _ptr(eb),
+                                    _stream(node.device)))
+    return stats
+
+
+def htam_transition_scores(stats, prefix, bucket, lam: float, w, min_count: int, out=None):
+    """Rule-based direction scores [B][G] over the feedback statistics."""
+    node, edge, eb = stats
+    G, NB = node.shape[0], eb.shape[2]
+    B, lmax = prefix.shape
+    if out is None:
+        out = torch.empty(B, G, dtype=torch.float32, device=node.device)
+    _check("htam_transition_scores",
+           lib.htam_transition_scores(G, NB, B, _ptr(prefix), lmax, _ptr(bucket), float(lam),
+                                      _ptr(w), int(min_count), _ptr(node), _ptr(edge), _ptr(eb),
+                                      _ptr(out), _stream(node.device)))
+    return out
 
 
 def retrieve_two_banks(main: Bank, delta: Bank, q: torch.Tensor, top_c: int, top_k: int,

@@ -190,3 +190,16 @@ def test_merge_rejects_bad_arguments():
     assert call(ka=FAKE + 8) == -6
     assert call(kout=FAKE) == -4                         # output overlaps an input
     assert call(wsb=4) == -5
+
+
+def test_feedback_and_transition_scores_reject_bad_arguments():
+    f = htam.lib.htam_feedback_update
+    assert f(0, 2, 5, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None) == -2
+    assert f(4, 2, 5, FAKE, FAKE, FAKE, FAKE, None, FAKE, FAKE, None) == -1
+    assert f(4, 2, 5, None, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None) == -1
+    assert f(4, 2, 0, None, None, None, None, FAKE, FAKE, FAKE, None) == 0
+    s = htam.lib.htam_transition_scores
+    assert s(4, 2, 3, FAKE, 0, FAKE, 0.5, FAKE, 1, FAKE, FAKE, FAKE, FAKE, None) == -2
+    assert s(4, 2, 3, FAKE, 4, FAKE, -0.5, FAKE, 1, FAKE, FAKE, FAKE, FAKE, None) == -4
+    assert s(4, 2, 3, FAKE, 4, FAKE, 0.5, FAKE, -1, FAKE, FAKE, FAKE, FAKE, None) == -4
+    assert s(4, 2, 3, FAKE, 4, FAKE, 0.5, None, 1, FAKE, FAKE, FAKE, FAKE, None) == -1

@@ -78,3 +78,66 @@ def test_merge_refuses_malformed_offsets(monkeypatch):
     with pytest.raises(htam.HtamError) as ei:
         htam.htam_memory_merge(main, bad)
     assert ei.value.status == -4
+
+
+def _events(rng, G, NB, n):
+    src = rng.integers(-1, G, n).astype(np.int32)
+    dst = rng.integers(0, G, n).astype(np.int32)
+    bk = rng.integers(0, NB, n).astype(np.int32)
+    feat = np.concatenate([rng.standard_normal((n, 2)), (rng.random((n, 8)) < 0.5),
+                           rng.random((n, 1))], axis=1).astype(np.float32)
+    return src, dst, bk, feat
+
+
+def test_feedback_statistics_exact_and_order_free():
+    """Integer statistics: the GPU's are the oracle's bits, in any event order
+    (several launches of shuffled batches add up to the same)."""
+    from paper_2605_29734_amd import htam
+    rng = np.random.default_rng(61)
+    G, NB, n = 24, 3, 20000
+    say(f"[case] feedback statistics G={G} buckets={NB} events={n}")
+    src, dst, bk, feat = _events(rng, G, NB, n)
+    dst[:5] = [G, -1, 3, 4, 5]                       # skipped: destination out of range
+    bk[2] = NB                                       # skipped: bucket out of range
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to("cuda")   # noqa: E731
+    st = htam.empty_stats(G, NB, "cuda")
+    htam.htam_feedback_update(st, t(src), t(dst), t(bk), t(feat))
+    st2 = htam.empty_stats(G, NB, "cuda")
+    p = rng.permutation(n)
+    for part in np.array_split(p, 3):
+        htam.htam_feedback_update(st2, t(src[part]), t(dst[part]), t(bk[part]), t(feat[part]))
+    torch.cuda.synchronize()
+    W = oracle.STATS_WORDS
+    ref = oracle.feedback_update(G, NB, src, dst, bk, feat, np.zeros((G, W), np.int64),
+                                 np.zeros((G, G, W), np.int64), np.zeros((G, G, NB, W), np.int64))
+    for a, b, r in zip(st, st2, ref):
+        np.testing.assert_array_equal(to_np(a), r)
+        np.testing.assert_array_equal(to_np(b), r)
+
+
+@pytest.mark.parametrize("min_count,lam", [(3, 0.5), (0, 0.0), (10 ** 6, 2.0)])
+def test_transition_scores_against_oracle(min_count, lam):
+    """The rule-based direction scores (bucket statistics or the edge fallback,
+    prefix weights, node statistics for an empty prefix) and their top-c."""
+    from paper_2605_29734_amd import htam
+    rng = np.random.default_rng(62)
+    G, NB, n, B, L, c = 40, 4, 30000, 64, 5, 6
+    say(f"[case] rule-based transition scores min_count={min_count} lambda={lam}")
+    src, dst, bk, feat = _events(rng, G, NB, n)
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to("cuda")   # noqa: E731
+    st = htam.empty_stats(G, NB, "cuda")
+    htam.htam_feedback_update(st, t(src), t(dst), t(bk), t(feat))
+    lengths = rng.integers(0, L + 1, B)
+    P = np.full((B, L), -1, np.int32)
+    for b in range(B):
+        P[b, :lengths[b]] = rng.integers(0, G, lengths[b])
+    qb = rng.integers(0, NB, B).astype(np.int32)
+    w = rng.standard_normal(oracle.STATS_WORDS).astype(np.float32)
+    S = htam.htam_transition_scores(st, t(P), t(qb), lam, t(w), min_count)
+    sel, ss, *_ = htam.htam_topk(S, None, c)
+    torch.cuda.synchronize()
+    ref = oracle.transition_scores(P, qb, lam, w, min_count, *(to_np(x) for x in st))
+    np.testing.assert_allclose(to_np(S), ref, rtol=1e-6, atol=1e-9)
+    for b in range(B):        # the selection: the c best of the GPU's own scores
+        order = np.lexsort((np.arange(G), -to_np(S)[b].astype(np.float64)))[:c]
+        np.testing.assert_array_equal(to_np(sel)[b], order)
