@@ -248,6 +248,100 @@ def bench_alt(args, spec, w, bank):
     return res
 
 
+def bench_update(args, spec, w):
+    """The online update. The records are split in arrival order into a main
+    bank and a delta bank of recent ones (--delta-frac); the timed step is
+    retrieval over both banks (what queries see between compactions). Also
+    timed: the compaction of the delta into the main bank (htam_memory_merge,
+    HBM-bound: every key row read and written once, the roofline here), the
+    feedback statistics of 2^20 step outcomes, and the rule-based direction
+    scores over them."""
+    import torch
+    from paper_2605_29734_amd import htam
+    q = w.queries
+    dev = q.device
+    n_main = int(spec.N * (1.0 - args.delta_frac))
+    main = htam.build_bank(w.cluster_of[:n_main].contiguous(), w.keys_in[:n_main].contiguous(),
+                           w.coarse_keys, spec.compute)
+    delta = htam.build_bank(w.cluster_of[n_main:].contiguous(), w.keys_in[n_main:].contiguous(),
+                            w.coarse_keys, spec.compute)
+    delta.transition_id += n_main
+    del w.keys_in
+    torch.cuda.synchronize()
+    mk = lambda: torch.cuda.Event(enable_timing=True)   # noqa: E731
+    K = args.steps
+    for _ in range(args.warmup):
+        htam.retrieve_two_banks(main, delta, q, spec.top_c, spec.top_k, spec.tau)
+    torch.cuda.synchronize()
+    log(f"[bench] timing {K} steps (update: main + delta retrieval)")
+    e0, e1 = mk(), mk()
+    t0 = time.perf_counter()
+    e0.record()
+    for _ in range(K):
+        htam.retrieve_two_banks(main, delta, q, spec.top_c, spec.top_k, spec.tau)
+    e1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_total = e0.elapsed_time(e1)
+    # compaction
+    merged = htam.htam_memory_merge(main, delta)
+    torch.cuda.synchronize()
+    reps = 5
+    e0.record()
+    for _ in range(reps):
+        merged = htam.htam_memory_merge(main, delta)
+    e1.record()
+    torch.cuda.synchronize()
+    t_merge = e0.elapsed_time(e1) / reps * 1e-3
+    kb = main.fine_keys.element_size()
+    merge_bytes = 2 * spec.N * (spec.d * kb + 4) + 16 * (spec.G + 1)
+    # statistics: 2^20 outcomes over the bank's clusters (4 state buckets), then
+    # scores for every query over prefixes of up to 5 directions
+    G, NB, n_ev = min(spec.G, 1024), 4, 1 << 20
+    gen = torch.Generator(device=dev).manual_seed(args.seed)
+    src = torch.randint(-1, G, (n_ev,), dtype=torch.int32, device=dev, generator=gen)
+    dst = torch.randint(0, G, (n_ev,), dtype=torch.int32, device=dev, generator=gen)
+    bk = torch.randint(0, NB, (n_ev,), dtype=torch.int32, device=dev, generator=gen)
+    feat = torch.rand(n_ev, htam.HTAM_FEEDBACK_FEATURES, device=dev, generator=gen)
+    st = htam.empty_stats(G, NB, dev)
+    htam.htam_feedback_update(st, src, dst, bk, feat)
+    torch.cuda.synchronize()
+    e0.record()
+    htam.htam_feedback_update(st, src, dst, bk, feat)
+    e1.record()
+    torch.cuda.synchronize()
+    t_fb = e0.elapsed_time(e1) * 1e-3
+    P = torch.randint(-1, G, (spec.B, 5), dtype=torch.int32, device=dev, generator=gen)
+    qb = torch.randint(0, NB, (spec.B,), dtype=torch.int32, device=dev, generator=gen)
+    wv = torch.randn(htam.HTAM_STATS_WORDS, device=dev, generator=gen)
+    S = htam.htam_transition_scores(st, P, qb, 0.5, wv, 8)
+    torch.cuda.synchronize()
+    e0.record()
+    htam.htam_transition_scores(st, P, qb, 0.5, wv, 8, out=S)
+    e1.record()
+    torch.cuda.synchronize()
+    t_ts = e0.elapsed_time(e1) * 1e-3
+    achieved = merge_bytes / t_merge / 1e9
+    return {
+        "metric": METRIC, "value": spec.B * K / (ms_total * 1e-3), "unit": "queries/s",
+        "n_gpus": 1, "steps": K, "warmup": args.warmup, "ms_per_step": ms_total / K,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16" if spec.compute == "bf16" else "f32", "data": "synthetic",
+        "config": {"workload": spec.name, "path": "update", "queries": spec.B, "d": spec.d,
+                   "clusters": spec.G, "transitions": spec.N, "delta_records": spec.N - n_main,
+                   "top_c": spec.top_c, "top_k": spec.top_k, "tau": spec.tau,
+                   "key_storage": spec.storage},
+        "roofline": {"bound": "hbm", "kernel": "htam_memory_merge (compaction)",
+                     "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "alg_bytes_per_launch": merge_bytes, "launch_ms": t_merge * 1e3},
+        "stages": {"step_ms_wall": wall / K * 1e3, "merge_ms": t_merge * 1e3,
+                   "feedback_events_per_s": n_ev / t_fb, "feedback_ms_per_2^20_events": t_fb * 1e3,
+                   "transition_scores_ms": t_ts * 1e3, "stats_clusters": G, "stats_buckets": NB,
+                   "source_sha256": kernel_source_sha256()},
+    }
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -259,9 +353,13 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--event-every", type=int, default=8, metavar="E",
                     help="stamp the kernel timing events on every E-th timed step")
-    ap.add_argument("--path", default="hierarchical", choices=["hierarchical", "prefix", "flat"],
+    ap.add_argument("--path", default="hierarchical",
+                    choices=["hierarchical", "prefix", "flat", "update"],
                     help="hierarchical retrieval (default); the same with prefix-aware coarse "
-                         "scoring; or flat retrieval over every record")
+                         "scoring; flat retrieval over every record; or the online update "
+                         "(retrieval over a main and a delta bank, compaction, statistics)")
+    ap.add_argument("--delta-frac", type=float, default=0.01,
+                    help="update path: share of the records in the delta bank")
     ap.add_argument("--prefix-len", type=int, default=5, metavar="L",
                     help="prefix path: longest prefix (lengths uniform on 0..L)")
     ap.add_argument("--lam", type=float, default=0.5, help="prefix path: recency decay lambda")
@@ -286,10 +384,16 @@ def main():
     dev = torch.device("cuda:0")
     log(f"[bench] workload {spec.name}: generating on {dev}")
     w = synth.make(spec, device=dev, seed=args.seed)
-    bank = htam.build_bank(w.cluster_of, w.keys_in, w.coarse_keys, spec.compute)
-    torch.cuda.synchronize()
-    del w.keys_in
+    bank = None
+    if args.path != "update":
+        bank = htam.build_bank(w.cluster_of, w.keys_in, w.coarse_keys, spec.compute)
+        torch.cuda.synchronize()
+        del w.keys_in
     q = w.queries
+    if args.path == "update":
+        res = bench_update(args, spec, w)
+        print(json.dumps(res), flush=True)
+        return
     if args.path != "hierarchical":
         res = bench_alt(args, spec, w, bank)
         print(json.dumps(res), flush=True)
