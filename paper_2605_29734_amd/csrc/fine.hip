@@ -1095,8 +1095,9 @@ static hipError_t launch_stream(int32_t key_dtype, int32_t compute_dtype, const 
         l.smem = l.qs_bytes + fine_state_bytes(ql, fa0.cap, l.fa.ntile);
         // two blocks per CU when two blocks' LDS fits (and the buffers leave the registers)
         const bool two = npl <= 4 && 2 * (l.smem + 256) <= budget + 256;
-        // one block per CU with bf16 keys: producer/consumer blocks
-        l.producer_consumer = !two && key_dtype == kBF16 && npl <= 4;
+        // one block per CU: producer/consumer blocks (their load units are
+        // 8 k-steps for bf16 keys, 4 for fp32: d % 256 or d % 128)
+        l.producer_consumer = !two && npl <= 4;
         const int unit_k = key_dtype == kF32 ? 8 : 16;
         if (two || l.producer_consumer || fa0.d % (32 * unit_k) == 0)
             return key_dtype == kF32 ? launch_stream_lds_f32(npl, two, l)

@@ -107,7 +107,7 @@ struct StreamLaunch {
     int64_t max_grid;             // no more blocks than work items
     size_t smem;
     int32_t qs_bytes;
-    bool producer_consumer;       // eight-wave producer/consumer blocks (bf16 keys, one block per CU)
+    bool producer_consumer;       // eight-wave producer/consumer blocks (one block per CU)
     KernelEvents ev;
     hipStream_t stream;
 };
@@ -726,7 +726,7 @@ __device__ __forceinline__ void pass_lds(const FineArgs &a, const FineSmem &sm, 
     // stays unconditional and the compiler can wait for exactly one unit at a
     // time. The first units are requested before the queries are staged.
     // the largest top-k buffers leave fewer registers for the ring
-    constexpr int R = PC ? 4 : NPL < 8 ? kRing : (sizeof(KT) == 4 ? 2 : 3);
+    constexpr int R = PC ? (sizeof(KT) == 4 ? 3 : 4) : NPL < 8 ? kRing : (sizeof(KT) == 4 ? 2 : 3);
     LoadUnit<KT, U> ring[R];
     if (producer) {
 #pragma unroll
@@ -894,14 +894,15 @@ void stream_lds2(FineArgs a, int32_t qs_bytes) {
 }
 
 // Producer/consumer blocks of eight waves, one per CU (LDS-bound launches):
-// four waves stream the keys with 8-k-step units in a ring of four (spread
-// between the MFMAs), four keep the top-k buffers. Registers are capped at
-// two waves per SIMD, which the two roles share.
+// four waves stream the keys with 8-k-step units (4 for fp32 keys, whose
+// fragments take twice the registers) in a ring of four (spread between the
+// MFMAs), four keep the top-k buffers. Registers are capped at two waves per
+// SIMD, which the two roles share.
 template <typename KT, int NPL>
 __global__ __launch_bounds__(2 * kFineThreads) void stream_pc(FineArgs a, int32_t qs_bytes) {
     extern __shared__ __align__(16) unsigned char smem_raw[];
     __shared__ int32_t s_next[2];
-    stream_lds_body<KT, 8, NPL, true, true>(a, qs_bytes, smem_raw, s_next);
+    stream_lds_body<KT, sizeof(KT) == 4 ? 4 : 8, NPL, true, true>(a, qs_bytes, smem_raw, s_next);
 }
 
 template <typename T, bool BF16, int NPL>
@@ -946,16 +947,14 @@ hipError_t launch_stream_kernel(Kern kern, const StreamLaunch &l, Args... args) 
 
 template <typename KT>
 hipError_t launch_stream_lds_t(int npl, bool two_per_cu, const StreamLaunch &l) {
-    if constexpr (sizeof(KT) == 2) {
-        if (l.producer_consumer) {
-            switch (npl) {
-                case 2: return launch_stream_kernel_n(stream_pc<KT, 2>, 2 * kFineThreads, l, l.fa,
-                                                      l.qs_bytes);
-                case 4: return launch_stream_kernel_n(stream_pc<KT, 4>, 2 * kFineThreads, l, l.fa,
-                                                      l.qs_bytes);
-            }
-            return hipErrorInvalidValue;
+    if (l.producer_consumer) {
+        switch (npl) {
+            case 2: return launch_stream_kernel_n(stream_pc<KT, 2>, 2 * kFineThreads, l, l.fa,
+                                                  l.qs_bytes);
+            case 4: return launch_stream_kernel_n(stream_pc<KT, 4>, 2 * kFineThreads, l, l.fa,
+                                                  l.qs_bytes);
         }
+        return hipErrorInvalidValue;
     }
     if (two_per_cu) {
         switch (npl) {
