@@ -240,8 +240,8 @@ struct PlanMirror {
 // memory, or with kMirror only to the LDS mirror m, for the fused routing
 // that uses them in the same block) and the plan. Clusters are split into contiguous
 // ranges, one per thread. Returns the chunk length (in every thread).
-template <bool kMirror, typename CntOf>
-__device__ int64_t plan_chunks(const PlanArgs &pa, CntOf cnt_of, const int64_t *off, int64_t *s,
+template <bool kMirror, typename CntOf, typename LenOf>
+__device__ int64_t plan_chunks(const PlanArgs &pa, CntOf cnt_of, LenOf len_of, int64_t *s,
                                PlanMirror m) {
     const int t = threadIdx.x;
     const int32_t G = pa.G;
@@ -255,7 +255,7 @@ __device__ int64_t plan_chunks(const PlanArgs &pa, CntOf cnt_of, const int64_t *
     auto partials = [&](int i) {
         int64_t p = 0;
         for (int32_t g = g0; g < g1; ++g) {
-            const int64_t c = cnt_of(g), len = off[g + 1] - off[g];
+            const int64_t c = cnt_of(g), len = len_of(g);
             if (c > 0 && len > 0) p += c * ((len + (int64_t(1) << (lmin + i)) - 1) >> (lmin + i));
         }
         return p;
@@ -268,7 +268,7 @@ __device__ int64_t plan_chunks(const PlanArgs &pa, CntOf cnt_of, const int64_t *
 #pragma unroll
     for (int i = 0; i < kFirst; ++i) p4[i] = 0;
     for (int32_t g = g0; g < g1; ++g) {        // the four in one pass over the clusters
-        const int64_t c = cnt_of(g), len = off[g + 1] - off[g];
+        const int64_t c = cnt_of(g), len = len_of(g);
         if (c > 0 && len > 0) {
 #pragma unroll
             for (int i = 0; i < kFirst; ++i)
@@ -307,7 +307,7 @@ __device__ int64_t plan_chunks(const PlanArgs &pa, CntOf cnt_of, const int64_t *
 #pragma unroll
     for (int i = 0; i < NW; ++i) w[i] = 0;
     for (int32_t g = g0; g < g1; ++g) {
-        const int64_t c = cnt_of(g), len = off[g + 1] - off[g];
+        const int64_t c = cnt_of(g), len = len_of(g);
         const int64_t nch = (c > 0 && len > 0) ? (len + ch - 1) >> lch : 0;
         const int64_t nfull = c > 0 ? len >> lch : 0;
         const int64_t ng = group_count(nch, kp, pa.direct);
@@ -337,7 +337,7 @@ __device__ int64_t plan_chunks(const PlanArgs &pa, CntOf cnt_of, const int64_t *
     }
     int64_t qrun = q[0];
     for (int32_t g = g0; g < g1; ++g) {
-        const int64_t c = cnt_of(g), len = off[g + 1] - off[g];
+        const int64_t c = cnt_of(g), len = len_of(g);
         const int64_t nch = (c > 0 && len > 0) ? (len + ch - 1) >> lch : 0;
         const int64_t nfull = c > 0 ? len >> lch : 0;
         const int64_t ng = group_count(nch, kp, pa.direct);
@@ -403,6 +403,16 @@ struct LdsCnt {
     const int32_t *cnt;
     __device__ int64_t operator()(int32_t g) const { return cnt[g]; }
 };
+// Segment length of cluster g from the offsets (global or an LDS copy) ...
+struct OffLen {
+    const int64_t *off;
+    __device__ int64_t operator()(int32_t g) const { return off[g + 1] - off[g]; }
+};
+// ... or from an LDS table of lengths.
+struct LdsLen {
+    const int32_t *len;
+    __device__ int64_t operator()(int32_t g) const { return len[g]; }
+};
 
 // Outputs of the fine stage, for pairs the routing finishes itself: a
 // selected cluster id out of range gives an empty slot (no candidates).
@@ -443,16 +453,32 @@ __device__ __forceinline__ void plan_nothing(Plan *plan) {
     plan->bad_off = 1;
 }
 
-// Planning step of the multi-kernel routing (counts in global memory). With
-// malformed offsets the plan is empty and the scatter gives every pair an
-// empty slot.
+// Planning step of the multi-kernel routing. With kStage the clusters'
+// query counts and segment lengths are first staged in LDS (8 bytes per
+// cluster, coalesced loads all in flight together), so that the planning
+// passes over each thread's clusters read LDS instead of waiting on L2 in
+// every iteration; otherwise (too many clusters for the LDS) they read
+// global memory. With malformed offsets the plan is empty and the scatter
+// gives every pair an empty slot.
+template <bool kStage>
 __global__ __launch_bounds__(kPlanThreads) void route_plan(PlanArgs pa, const int32_t *cnt) {
     __shared__ int64_t s[(kPlanThreads / kWave + 1) * kChunkCands];
+    extern __shared__ int32_t stage[];
     if (offsets_bad(pa.off, pa.G, pa.n_rows)) {
         if (threadIdx.x == 0) plan_nothing(pa.plan);
         return;
     }
-    plan_chunks<false>(pa, GlobalCnt{cnt}, pa.off, s, PlanMirror{});
+    if constexpr (kStage) {
+        int32_t *lcnt = stage, *llen = stage + pa.G;
+        for (int32_t g = threadIdx.x; g < pa.G; g += kPlanThreads) {
+            lcnt[g] = cnt[g];
+            llen[g] = (int32_t)(pa.off[g + 1] - pa.off[g]);     // N < 2^31
+        }
+        __syncthreads();
+        plan_chunks<false>(pa, LdsCnt{lcnt}, LdsLen{llen}, s, PlanMirror{});
+    } else {
+        plan_chunks<false>(pa, GlobalCnt{cnt}, OffLen{pa.off}, s, PlanMirror{});
+    }
 }
 
 // Bytes of the LDS tables of the fused routing kernel for G clusters and n
@@ -582,7 +608,7 @@ __global__ __launch_bounds__(kPlanThreads) void route_fused(PlanArgs pa, const i
     }
     if (bad) atomicAdd(&s_bad, bad);
     __syncthreads();
-    const int64_t ch = plan_chunks<true>(pa, LdsCnt{lcnt}, loff, s, m);
+    const int64_t ch = plan_chunks<true>(pa, LdsCnt{lcnt}, OffLen{loff}, s, m);
     const int lch = 63 - __builtin_clzll((unsigned long long)ch);
     if (t == 0) {
         pa.plan->next = 0;
@@ -1181,7 +1207,16 @@ hipError_t launch_attend(int32_t key_dtype, int32_t compute_dtype, int32_t d, in
         hipLaunchKernelGGL(route_init, dim3((G + 255) / 256 < 1024 ? (G + 255) / 256 : 1024),
                            dim3(256), 0, s, G, w.cnt, w.cursor, w.plan);
         hipLaunchKernelGGL(route_count, dim3(gblocks), dim3(256), 0, s, sel, bc, G, w.cnt, w.plan);
-        hipLaunchKernelGGL(route_plan, dim3(1), dim3(kPlanThreads), 0, s, pa, w.cnt);
+        const size_t stage = (size_t)G * 8;
+        if (stage + 8 * 1024 <= lds_budget()) {
+            hipError_t e1 = hipFuncSetAttribute((const void *)route_plan<true>,
+                                                hipFuncAttributeMaxDynamicSharedMemorySize,
+                                                (int)stage);
+            if (e1 != hipSuccess) return e1;
+            hipLaunchKernelGGL(route_plan<true>, dim3(1), dim3(kPlanThreads), stage, s, pa, w.cnt);
+        } else {
+            hipLaunchKernelGGL(route_plan<false>, dim3(1), dim3(kPlanThreads), 0, s, pa, w.cnt);
+        }
         hipLaunchKernelGGL(route_scatter, dim3(gblocks), dim3(256), 0, s, sel, bc, G, w.qoff,
                            w.cursor, w.qlist, w.pos, w.bound, so, w.plan);
         hipLaunchKernelGGL(route_items, dim3((G + 3) / 4 < 2048 ? (G + 3) / 4 : 2048), dim3(256), 0,
