@@ -413,6 +413,19 @@ struct LdsLen {
     const int32_t *len;
     __device__ int64_t operator()(int32_t g) const { return len[g]; }
 };
+// Staged planner tables: one pad word per 16 clusters. A thread plans a
+// contiguous run of clusters (16 of them at G = 16384), so a wave's reads
+// are that run length apart; padded, the stride is odd and the 64 lanes
+// spread over all 32 banks instead of hitting two.
+__device__ __forceinline__ int32_t pad16(int32_t g) { return g + (g >> 4); }
+struct PadCnt {
+    const int32_t *cnt;
+    __device__ int64_t operator()(int32_t g) const { return cnt[pad16(g)]; }
+};
+struct PadLen {
+    const int32_t *len;
+    __device__ int64_t operator()(int32_t g) const { return len[pad16(g)]; }
+};
 
 // Outputs of the fine stage, for pairs the routing finishes itself: a
 // selected cluster id out of range gives an empty slot (no candidates).
@@ -460,23 +473,49 @@ __device__ __forceinline__ void plan_nothing(Plan *plan) {
 // every iteration; otherwise (too many clusters for the LDS) they read
 // global memory. With malformed offsets the plan is empty and the scatter
 // gives every pair an empty slot.
+constexpr int kStagePer = 16;    // clusters per thread the staged planner loads at once
+
 template <bool kStage>
 __global__ __launch_bounds__(kPlanThreads) void route_plan(PlanArgs pa, const int32_t *cnt) {
     __shared__ int64_t s[(kPlanThreads / kWave + 1) * kChunkCands];
     extern __shared__ int32_t stage[];
-    if (offsets_bad(pa.off, pa.G, pa.n_rows)) {
-        if (threadIdx.x == 0) plan_nothing(pa.plan);
-        return;
-    }
     if constexpr (kStage) {
-        int32_t *lcnt = stage, *llen = stage + pa.G;
-        for (int32_t g = threadIdx.x; g < pa.G; g += kPlanThreads) {
-            lcnt[g] = cnt[g];
-            llen[g] = (int32_t)(pa.off[g + 1] - pa.off[g]);     // N < 2^31
+        // every load requested before any is used (G <= kStagePer * threads):
+        // one round trip, and the offsets are checked from the same registers
+        const int t = threadIdx.x;
+        const int32_t G = pa.G;
+        int64_t o0[kStagePer], o1[kStagePer];
+        int32_t c[kStagePer];
+#pragma unroll
+        for (int i = 0; i < kStagePer; ++i) {
+            const int32_t g = min(t + i * kPlanThreads, G - 1);
+            o0[i] = pa.off[g];
+            o1[i] = pa.off[g + 1];
+            c[i] = cnt[g];
+        }
+        int bad = t == 0 && (o0[0] != 0 || pa.off[G] != pa.n_rows);
+#pragma unroll
+        for (int i = 0; i < kStagePer; ++i) bad |= o0[i] > o1[i];
+        if (__syncthreads_or(bad)) {
+            if (t == 0) plan_nothing(pa.plan);
+            return;
+        }
+        int32_t *lcnt = stage, *llen = stage + pad16(G) + 1;
+#pragma unroll
+        for (int i = 0; i < kStagePer; ++i) {
+            const int32_t g = t + i * kPlanThreads;
+            if (g < G) {
+                lcnt[pad16(g)] = c[i];
+                llen[pad16(g)] = (int32_t)(o1[i] - o0[i]);      // N < 2^31
+            }
         }
         __syncthreads();
-        plan_chunks<false>(pa, LdsCnt{lcnt}, LdsLen{llen}, s, PlanMirror{});
+        plan_chunks<false>(pa, PadCnt{lcnt}, PadLen{llen}, s, PlanMirror{});
     } else {
+        if (offsets_bad(pa.off, pa.G, pa.n_rows)) {
+            if (threadIdx.x == 0) plan_nothing(pa.plan);
+            return;
+        }
         plan_chunks<false>(pa, GlobalCnt{cnt}, OffLen{pa.off}, s, PlanMirror{});
     }
 }
@@ -1207,8 +1246,8 @@ hipError_t launch_attend(int32_t key_dtype, int32_t compute_dtype, int32_t d, in
         hipLaunchKernelGGL(route_init, dim3((G + 255) / 256 < 1024 ? (G + 255) / 256 : 1024),
                            dim3(256), 0, s, G, w.cnt, w.cursor, w.plan);
         hipLaunchKernelGGL(route_count, dim3(gblocks), dim3(256), 0, s, sel, bc, G, w.cnt, w.plan);
-        const size_t stage = (size_t)G * 8;
-        if (stage + 8 * 1024 <= lds_budget()) {
+        const size_t stage = ((size_t)G + G / 16 + 1) * 8;
+        if (G <= kStagePer * kPlanThreads && stage + 8 * 1024 <= lds_budget()) {
             hipError_t e1 = hipFuncSetAttribute((const void *)route_plan<true>,
                                                 hipFuncAttributeMaxDynamicSharedMemorySize,
                                                 (int)stage);
