@@ -361,6 +361,45 @@ def gumbel_of_bits(x) -> np.ndarray:
     return -np.log(-np.log(u))
 
 
+_MASK32 = np.uint64(0xFFFFFFFF)
+
+
+def philox4x32_10(counter, key) -> np.ndarray:
+    """Philox4x32 with ten rounds, as Salmon, Moraes, Dror and Shaw define it
+    (SC'11, Sec. 3): counter [..., 4] and key [..., 2] of 32-bit words. A round
+    takes the full 64-bit products of counter words 0 and 2 with the two
+    multipliers; the new counter is (hi(M1 x2) ^ x1 ^ k0, lo(M1 x2),
+    hi(M0 x0) ^ x3 ^ k1, lo(M0 x0)), and the key grows by the two Weyl
+    constants between rounds. Returns the [..., 4] output words."""
+    m0, m1 = np.uint64(0xD2511F53), np.uint64(0xCD9E8D57)
+    w0, w1 = np.uint64(0x9E3779B9), np.uint64(0xBB67AE85)
+    x = [np.asarray(counter, dtype=np.uint64)[..., i] & _MASK32 for i in range(4)]
+    k0 = np.asarray(key, dtype=np.uint64)[..., 0] & _MASK32
+    k1 = np.asarray(key, dtype=np.uint64)[..., 1] & _MASK32
+    for r in range(10):
+        if r:
+            k0, k1 = (k0 + w0) & _MASK32, (k1 + w1) & _MASK32
+        p0, p1 = m0 * x[0], m1 * x[2]          # < 2^64: exact in uint64
+        x = [(p1 >> np.uint64(32)) ^ x[1] ^ k0, p1 & _MASK32,
+             (p0 >> np.uint64(32)) ^ x[3] ^ k1, p0 & _MASK32]
+    return np.stack(x, axis=-1).astype(np.uint32)
+
+
+def philox_words(seed: int, offset: int, B: int, G: int) -> np.ndarray:
+    """The uniform words [B][G] that htam_retrieve_coarse_sampled draws when the
+    caller passes none: the word of (b, g) is output word g % 4 of Philox4x32-10
+    at counter (g / 4, b, offset low, offset high) under key (seed low, seed
+    high), so a draw depends only on (seed, offset, b, g)."""
+    n4 = (G + 3) // 4
+    ctr = np.zeros((B, n4, 4), dtype=np.uint64)
+    ctr[..., 0] = np.arange(n4, dtype=np.uint64)[None, :]
+    ctr[..., 1] = np.arange(B, dtype=np.uint64)[:, None]
+    ctr[..., 2] = offset & 0xFFFFFFFF
+    ctr[..., 3] = (offset >> 32) & 0xFFFFFFFF
+    key = np.array([seed & 0xFFFFFFFF, (seed >> 32) & 0xFFFFFFFF], dtype=np.uint64)
+    return philox4x32_10(ctr, key).reshape(B, n4 * 4)[:, :G]
+
+
 def coarse_sampled(q, c, top_c: int, eps: float, tau_g: float, noise, compute: str):
     """Direction choice by sampling the policy mu_g (Eq. global direction;
     Alg. 1 Step 2, g_t ~ mu_g) top_c times without replacement, by the

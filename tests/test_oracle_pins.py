@@ -510,6 +510,25 @@ def test_gumbel_of_bits():
     assert g.var() == pytest.approx(math.pi ** 2 / 6, rel=5e-3)
 
 
+def test_philox_known_answers():
+    """The oracle's Philox4x32-10 reproduces the published known-answer vectors
+    (tests/golden/philox_kat.json), and the word layout of philox_words puts
+    output word g % 4 of counter (g / 4, b, offset) at (b, g)."""
+    with open(os.path.join(GOLDEN, "philox_kat.json")) as f:
+        kat = json.load(f)["vectors"]
+    h = lambda v: np.array([int(x, 16) for x in v], dtype=np.uint64)   # noqa: E731
+    for v in kat:
+        got = oracle.philox4x32_10(h(v["counter"]), h(v["key"]))
+        np.testing.assert_array_equal(got, h(v["output"]).astype(np.uint32))
+    seed, off = 0x0123456789ABCDEF, (5 << 32) | 7
+    W = oracle.philox_words(seed, off, 3, 10)
+    for b, g in [(0, 0), (2, 9), (1, 4), (2, 3)]:
+        one = oracle.philox4x32_10(np.array([g // 4, b, 7, 5]), np.array([0x89ABCDEF, 0x01234567]))
+        assert W[b, g] == one[g % 4]
+    # Weyl key schedule: the words of a different seed share nothing
+    assert not np.any(oracle.philox_words(seed + 1, off, 3, 10) == W)
+
+
 def test_sampled_with_constant_noise_is_greedy():
     """Equal noise for every cluster leaves the order of log mu, which is the
     order of the scores: the greedy top-c."""

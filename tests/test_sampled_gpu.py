@@ -32,18 +32,27 @@ def _bank(spec, seed):
     ("f32", "f32", 40, 33, 72, 4, 1.0, 1.0),          # uniform: the words decide
     ("bf16", "bf16", 100, 64, 64, 64, 0.5, 0.3),      # every cluster drawn (a full order)
 ])
-def test_sampled_against_oracle(storage, compute, B, G, d, c, eps, tau):
+@pytest.mark.parametrize("source", ["words", "philox"])
+def test_sampled_against_oracle(storage, compute, B, G, d, c, eps, tau, source):
+    """source "words": the caller's uniform words; "philox": the library's own
+    draws, against the oracle fed with Philox4x32-10 words of the same (seed,
+    offset), its implementation pinned by the published known answers."""
     from paper_2605_29734_amd import htam
     spec = synth.Spec("sampled", B=B, d=d, G=G, N=G, top_c=c, top_k=1, tau=1.0, storage=storage,
                       compute=compute, sizes="uniform")
-    say(f"[case] sampled B={B} G={G} d={d} c={c} eps={eps} tau_g={tau} {storage}/{compute}")
+    say(f"[case] sampled B={B} G={G} d={d} c={c} eps={eps} tau_g={tau} {storage}/{compute} {source}")
     bank, q = _bank(spec, seed=G + c)
-    noise = torch.randint(-2 ** 31, 2 ** 31, (B, G), dtype=torch.int32, device="cuda",
-                          generator=torch.Generator(device="cuda").manual_seed(B))
-    sel, ss = htam.htam_retrieve_coarse_sampled(bank, q, c, eps, tau, noise=noise)
+    if source == "words":
+        noise = torch.randint(-2 ** 31, 2 ** 31, (B, G), dtype=torch.int32, device="cuda",
+                              generator=torch.Generator(device="cuda").manual_seed(B))
+        sel, ss = htam.htam_retrieve_coarse_sampled(bank, q, c, eps, tau, noise=noise)
+        words = to_np(noise).view(np.uint32)
+    else:
+        seed, offset = 0xDEADBEEF00000000 + G, (3 << 32) + B
+        sel, ss = htam.htam_retrieve_coarse_sampled(bank, q, c, eps, tau, seed=seed, offset=offset)
+        words = oracle.philox_words(seed, offset, B, G)
     torch.cuda.synchronize()
     sel, ss = to_np(sel), to_np(ss).astype(np.float64)
-    words = to_np(noise).view(np.uint32)
     ref_sel, _, keys, S = oracle.coarse_sampled(to_np(q), to_np(bank.coarse_keys), c, eps, tau,
                                                 words, compute)
     quant = oracle.round_bf16 if compute == "bf16" else (lambda x: np.asarray(x, np.float32))
