@@ -227,6 +227,20 @@ def test_flat_is_brute_force(tau, compute):
         assert r["Z"][b] == pytest.approx(e.sum(), rel=1e-12) and r["count"][b] == k
 
 
+def test_flat_ties_go_to_the_lower_id():
+    """Two records equal to the query tie at the top: the lower caller id comes
+    first, with row indices as ids when the caller gives none."""
+    rng = np.random.default_rng(23)
+    q, keys = _unit(rng, 2, 16), _unit(rng, 12, 16)
+    keys[3] = keys[7] = q[0]
+    keys[9] = keys[2] = q[1]
+    r = oracle.flat(q, keys, 0.5, 2, "f32")
+    np.testing.assert_array_equal(r["id"], [[3, 7], [2, 9]])
+    tid = np.array([50, 40, 30, 20, 10, 0, 1, 2, 3, 4, 5, 6], np.int32)
+    r = oracle.flat(q, keys, 0.5, 2, "f32", transition_id=tid)
+    np.testing.assert_array_equal(r["id"], [[2, 20], [4, 30]])
+
+
 def test_flat_equals_hierarchy_with_every_cluster():
     """Selecting every cluster (top_c = G) leaves the hierarchy nothing to
     exclude: its row outputs are flat retrieval's, and with fewer clusters
@@ -504,6 +518,10 @@ def test_gumbel_of_bits():
     Gumbel mean (Euler's constant) and variance pi^2/6."""
     assert oracle.gumbel_of_bits(np.uint32(2 ** 31) - 1)[()] == pytest.approx(
         -math.log(-math.log(0.5 - 0.5 / 2 ** 32)), rel=1e-15)
+    # the extreme words: u = 2^-33 and u = 1 - 2^-33
+    assert oracle.gumbel_of_bits(np.uint32(0))[()] == pytest.approx(-math.log(33 * math.log(2)), rel=1e-15)
+    assert oracle.gumbel_of_bits(np.uint32(2 ** 32 - 1))[()] == pytest.approx(
+        -math.log(-math.log1p(-2.0 ** -33)), rel=1e-6)
     x = (np.arange(1 << 20, dtype=np.uint64) << 12).astype(np.uint32)
     g = oracle.gumbel_of_bits(x)
     assert g.mean() == pytest.approx(np.euler_gamma, abs=2e-3)
@@ -527,6 +545,19 @@ def test_philox_known_answers():
         assert W[b, g] == one[g % 4]
     # Weyl key schedule: the words of a different seed share nothing
     assert not np.any(oracle.philox_words(seed + 1, off, 3, 10) == W)
+
+
+def test_sampled_ties_go_to_the_lower_id():
+    """Equal scores and equal noise make every key equal: the draw is the
+    clusters in id order."""
+    q = np.zeros((3, 8))
+    q[:, 0] = 1.0
+    C = np.zeros((9, 8))
+    C[:, 1] = 1.0                                    # every score 0
+    noise = np.full((3, 9), 77, dtype=np.uint32)
+    sel, _, keys, _ = oracle.coarse_sampled(q, C, 4, 0.3, 0.7, noise, "f32")
+    assert np.all(keys == keys[0, 0])
+    np.testing.assert_array_equal(sel, np.tile(np.arange(4), (3, 1)))
 
 
 def test_sampled_with_constant_noise_is_greedy():
@@ -589,6 +620,12 @@ def test_feedback_worked_example_exact():
     assert oracle.transition_utility(edge, eb, 1, 0, 0, mc, w) == _num(ex["phi_1_0_bucket0"])
     S = oracle.transition_scores(np.full((1, 2), -1), [0], 0.5, w, mc, node, edge, eb)
     np.testing.assert_allclose(S[0], [_num(x) for x in ex["node_score"]], atol=1e-12)
+    # distinct weights: each entry of z sits at its place in App. B.6's order
+    w = np.asarray(ex["w_distinct"], np.float64)
+    for k, key in ((0, "phi_0_1_bucket0_w_distinct"), (1, "phi_0_1_bucket1_w_distinct")):
+        assert oracle.transition_utility(edge, eb, 0, 1, k, mc, w) == pytest.approx(_num(ex[key]), abs=1e-12)
+    S = oracle.transition_scores(np.full((1, 2), -1), [0], 0.5, w, mc, node, edge, eb)
+    np.testing.assert_allclose(S[0], [_num(x) for x in ex["node_score_w_distinct"]], atol=1e-12)
 
 
 def test_feedback_sums_are_order_free_and_exact():
