@@ -9,7 +9,9 @@ before the timed region; the bank build is offline and untimed.
 
 The default workload is the largest that fits one GPU: 8,192 queries of
 d = 2,048 against 16,384 clusters and 4,194,304 fp32 records (a 34 GB bank,
-far beyond the last-level cache, so every step streams it from HBM).
+far beyond the last-level cache, so every step streams it from HBM). A bank
+that would fit the 256 MB last-level cache is timed over copies of itself
+that together exceed 1 GiB, one per step in turn (--no-rotate: one bank).
 
 Prints one JSON line: queries/s for the workload (whole timed region), the
 roofline position of the dominant kernel (the bank stream, HBM-bound),
@@ -360,6 +362,8 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-rotate", action="store_true",
+                    help="time one bank even when it fits the last-level cache")
     ap.add_argument("--event-every", type=int, default=4, metavar="E",
                     help="stamp the kernel and stage timing events on every E-th timed step")
     ap.add_argument("--path", default="hierarchical",
@@ -408,8 +412,21 @@ def main():
         print(json.dumps(res), flush=True)
         return
     r = htam.Retriever(bank, spec.B, spec.top_c, spec.top_k, spec.tau)
+    # A bank smaller than the last-level cache (256 MB Infinity Cache) would be
+    # read from the cache on every step after the first: rotate over copies
+    # of it that together exceed 1 GiB, so that each step reads its bank from
+    # HBM (the workspaces fit any copy: same shapes).
+    bank_bytes = bank.fine_keys.numel() * bank.fine_keys.element_size()
+    n_copies = 1 if args.no_rotate else min(32, max(1, -(-(1 << 30) // max(bank_bytes, 1))))
+    banks = [bank] + [htam.Bank(coarse_keys=bank.coarse_keys.clone(),
+                                fine_keys=bank.fine_keys.clone(), seg_offsets=bank.seg_offsets,
+                                transition_id=bank.transition_id, compute=bank.compute)
+                      for _ in range(n_copies - 1)]
+    if n_copies > 1:
+        log(f"[bench] rotating over {n_copies} copies of the {bank_bytes / 2**20:.0f} MiB bank")
     log(f"[bench] warmup {args.warmup}")
-    for _ in range(args.warmup):
+    for i in range(max(args.warmup, n_copies)):
+        r.bank = banks[i % n_copies]
         r.run(q)
     torch.cuda.synchronize()
 
@@ -439,11 +456,12 @@ def main():
         # stage boundaries on the stamped steps only: on the small workloads
         # every marker between calls shows in the step time
         stamped = i % E == 0
+        bk = banks[i % n_copies]
         marks[i][0].record()
-        htam.htam_retrieve_coarse(r.bank, q, r.c, out=r.sel, ws=r.ws_coarse)
+        htam.htam_retrieve_coarse(bk, q, r.c, out=r.sel, ws=r.ws_coarse)
         if stamped:
             marks[i][1].record()
-        htam.htam_attend_transitions(r.bank, q, r.sel[0], r.tau, r.k, out=r.slots, ws=r.ws_attend)
+        htam.htam_attend_transitions(bk, q, r.sel[0], r.tau, r.k, out=r.slots, ws=r.ws_attend)
         if stamped:
             marks[i][2].record()
         htam.htam_topk(r.slots[2], r.slots[3], r.k, r.slots[0], r.slots[1], r.tau, out=r.rows)
@@ -499,7 +517,7 @@ def main():
         "config": {"workload": spec.name, "queries": spec.B, "d": spec.d, "clusters": spec.G,
                    "transitions": spec.N, "top_c": spec.top_c, "top_k": spec.top_k,
                    "tau": spec.tau, "key_storage": spec.storage,
-                   "bank_bytes": int(spec.N * spec.d * kb)},
+                   "bank_bytes": int(spec.N * spec.d * kb), "bank_copies": n_copies},
         "roofline": {"bound": "hbm", "kernel": "fine_stream", "achieved": achieved,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "traffic": stream_kernel_traffic(spec.name),
