@@ -234,13 +234,13 @@ struct PlanMirror {
 };
 
 // Chunk length and work numbering from the per-cluster query counts (read
-// through cnt_of) and the segment offsets `off` (global or LDS): the chunk is
-// the smallest candidate length for which the partial results fit in p_cap.
-// Writes qoff, wstart, wlast, gstart, mstart, pbase and ubase (to global
-// memory, or with kMirror only to the LDS mirror m, for the fused routing
-// that uses them in the same block) and the plan. Clusters are split into contiguous
-// ranges, one per thread. Returns the chunk length (in every thread).
-template <bool kMirror, typename CntOf, typename LenOf>
+// through cnt_of) and the segment lengths (len_of): the chunk is the
+// smallest candidate length for which the partial results fit in p_cap.
+// Writes qoff, wstart, wlast, gstart, mstart, pbase and ubase to the LDS
+// mirror m (the fused routing uses them in the same block) and the plan.
+// Clusters are split into contiguous ranges, one per thread. Returns the
+// chunk length (in every thread).
+template <typename CntOf, typename LenOf>
 __device__ int64_t plan_chunks(const PlanArgs &pa, CntOf cnt_of, LenOf len_of, int64_t *s,
                                PlanMirror m) {
     const int t = threadIdx.x;
@@ -348,26 +348,13 @@ __device__ int64_t plan_chunks(const PlanArgs &pa, CntOf cnt_of, LenOf len_of, i
             for (int i = 0; i < kItemBuckets; ++i)
                 if (b == i) wl = bnext[i]++;
         }
-        const int32_t ws = (int32_t)(w[0] & 0xffffffff), gs = (int32_t)(w[0] >> 32);
-        // the tables go to global memory for the multi-block routing kernels,
-        // or only to the LDS mirror when the same block goes on to use them
-        if (!kMirror) {
-            pa.qoff[g] = (int32_t)qrun;
-            pa.wstart[g] = ws;
-            pa.wlast[g] = wl;
-            pa.pbase[g] = w[1];
-            pa.gstart[g] = gs;
-            pa.ubase[g] = w[2];
-            pa.mstart[g] = (int32_t)w[3];
-        } else {
-            m.qoff[g] = (int32_t)qrun;
-            m.wstart[g] = ws;
-            m.wlast[g] = wl;
-            m.pbase[g] = w[1];
-            m.gstart[g] = gs;
-            m.ubase[g] = w[2];
-            m.mstart[g] = (int32_t)w[3];
-        }
+        m.qoff[g] = (int32_t)qrun;
+        m.wstart[g] = (int32_t)(w[0] & 0xffffffff);
+        m.wlast[g] = wl;
+        m.pbase[g] = w[1];
+        m.gstart[g] = (int32_t)(w[0] >> 32);
+        m.ubase[g] = w[2];
+        m.mstart[g] = (int32_t)w[3];
         qrun += c;
         w[0] += nfull + (ng << 32);
         w[1] += nch * c;
@@ -375,17 +362,10 @@ __device__ int64_t plan_chunks(const PlanArgs &pa, CntOf cnt_of, LenOf len_of, i
         w[3] += nch != 1 ? c : 0;
     }
     if (t == kPlanThreads - 1) {
-        if (!kMirror) {
-            pa.qoff[G] = (int32_t)qtot[0];
-            pa.wstart[G] = (int32_t)n_full;
-            pa.gstart[G] = (int32_t)(wt[0] >> 32);
-            pa.mstart[G] = (int32_t)wt[3];
-        } else {
-            m.qoff[G] = (int32_t)qtot[0];
-            m.wstart[G] = (int32_t)n_full;
-            m.gstart[G] = (int32_t)(wt[0] >> 32);
-            m.mstart[G] = (int32_t)wt[3];
-        }
+        m.qoff[G] = (int32_t)qtot[0];
+        m.wstart[G] = (int32_t)n_full;
+        m.gstart[G] = (int32_t)(wt[0] >> 32);
+        m.mstart[G] = (int32_t)wt[3];
         pa.plan->chunk = ch;
         pa.plan->n_parts = wt[1];
         pa.plan->n_groups = wt[0] >> 32;
@@ -393,6 +373,176 @@ __device__ int64_t plan_chunks(const PlanArgs &pa, CntOf cnt_of, LenOf len_of, i
         pa.plan->n_merge = wt[3];
     }
     return ch;
+}
+
+// The same plan with the clusters interleaved over the lanes: wave w takes a
+// contiguous range of clusters, 64 at a time, one per lane. Reads and the
+// per-cluster table writes are then coalesced (one thread per contiguous run
+// of clusters made every store instruction touch 64 lines: most of the
+// planner's time on 16,384 clusters). The prefixes are taken per round with
+// DPP wave scans plus a running carry, from each wave's base (the totals of
+// the waves before it); a cluster's place among the last chunks of its
+// bucket comes from ballots. The result is the same plan, table for table.
+template <typename CntOf, typename LenOf>
+__device__ void plan_chunks_wave(const PlanArgs &pa, CntOf cnt_of, LenOf len_of, int64_t *s) {
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    constexpr int waves = kPlanThreads / kWave;
+    static_assert(kItemBuckets == 16, "the bucket bases are scanned by one 16-lane row");
+    constexpr int SW = 4 + kItemBuckets;            // LDS words per wave: totals, bucket counts
+    static_assert(waves * SW <= (waves + 1) * kChunkCands, "planner LDS");
+    const int32_t G = pa.G;
+    const int32_t per = (int32_t)(((int64_t)G + waves * kWave - 1) / (waves * kWave)) * kWave;
+    const int32_t gw0 = min(G, wave * per), gw1 = min(G, gw0 + per);
+    const int lmin = 63 - __builtin_clzll((unsigned long long)pa.chunk_min);   // chunk_min is a power of two
+    auto partials = [&](int i) {
+        int64_t p = 0;
+        for (int32_t g = gw0 + lane; g < gw1; g += kWave) {
+            const int64_t c = cnt_of(g), len = len_of(g);
+            if (c > 0 && len > 0) p += c * ((len + (int64_t(1) << (lmin + i)) - 1) >> (lmin + i));
+        }
+        return p;
+    };
+    // chunk length: the first four candidates in one pass, the rest by bisection
+    constexpr int kFirst = 4;
+    int64_t p4[kFirst];
+#pragma unroll
+    for (int i = 0; i < kFirst; ++i) p4[i] = 0;
+    for (int32_t g = gw0 + lane; g < gw1; g += kWave) {
+        const int64_t c = cnt_of(g), len = len_of(g);
+        if (c > 0 && len > 0) {
+#pragma unroll
+            for (int i = 0; i < kFirst; ++i)
+                p4[i] += c * ((len + (int64_t(1) << (lmin + i)) - 1) >> (lmin + i));
+        }
+    }
+    block_sum_n<kFirst>(p4, s);
+    int cand = -1;
+#pragma unroll
+    for (int i = kFirst - 1; i >= 0; --i)
+        if (p4[i] <= pa.p_cap) cand = i;
+    if (cand < 0) {
+        int lo = kFirst, hi = kChunkCands - 1;     // the answer is in [lo, hi]
+        while (lo < hi) {
+            const int mid = (lo + hi) >> 1;
+            int64_t pm[1] = {partials(mid)};
+            block_sum_n<1>(pm, s);
+            if (pm[0] <= pa.p_cap) hi = mid;
+            else lo = mid + 1;
+        }
+        cand = lo;
+    }
+    const int lch = lmin + cand;
+    const int64_t ch = int64_t(1) << lch;
+    const int64_t kp = pa.kp;
+
+    // Per cluster: v[0] = full items | level-one groups << 32, v[1] =
+    // partials, v[2] = level-one results, v[3] = queries | merge-list entries
+    // << 32 (each total below 2^31); returns the bucket of its last chunk, or
+    // -1 if its chunks are all full-length.
+    auto values = [&](int32_t g, int64_t (&v)[4]) {
+        const int64_t c = cnt_of(g), len = len_of(g);
+        const int64_t nch = (c > 0 && len > 0) ? (len + ch - 1) >> lch : 0;
+        const int64_t nfull = c > 0 ? len >> lch : 0;
+        const int64_t ng = group_count(nch, kp, pa.direct);
+        v[0] = nfull + (ng << 32);
+        v[1] = nch * c;
+        v[2] = ng * c;
+        v[3] = c + ((nch != 1 ? c : 0) << 32);     // empty segments are finished by the merge too
+        return nch > nfull ? item_bucket(len - (nfull << lch), lch, c) : -1;
+    };
+    // this wave's totals, and (lane b) its last chunks in bucket b
+    int64_t tot[4] = {0, 0, 0, 0};
+    int64_t bcnt = 0;
+    for (int32_t gr = gw0; gr < gw1; gr += kWave) {
+        const int32_t g = gr + lane;
+        int64_t v[4] = {0, 0, 0, 0};
+        const int b = g < gw1 ? values(g, v) : -1;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) tot[i] += v[i];
+#pragma unroll
+        for (int bb = 0; bb < kItemBuckets; ++bb) {
+            const uint64_t m = __ballot(b == bb);
+            if (lane == bb) bcnt += __popcll(m);
+        }
+    }
+    __syncthreads();                          // s is free again
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int64_t x = wave_sum64(tot[i]);
+        if (lane == 0) s[wave * SW + i] = x;
+    }
+    if (lane < kItemBuckets) s[wave * SW + 4 + lane] = bcnt;
+    __syncthreads();
+    // bases of this wave (the waves before it) and the totals
+    // (lane w < 16 reads wave w's totals: one row scan per value)
+    int64_t carry[4], grand[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int64_t x = lane < waves ? s[lane * SW + i] : 0;
+        const int64_t incl = row_scan64(x);
+        carry[i] = __shfl(incl - x, wave);
+        grand[i] = __shfl(incl, waves - 1);
+    }
+    int64_t bbase = 0, bgrand = 0;
+    if (lane < kItemBuckets) {
+#pragma unroll 1
+        for (int w = 0; w < waves; ++w) {
+            const int64_t x = s[w * SW + 4 + lane];
+            bbase += w < wave ? x : 0;
+            bgrand += x;
+        }
+    }
+    // items: every full-length chunk first, then the last chunks bucket by
+    // bucket (lanes 0..15, one row, hold the buckets)
+    const int64_t n_full = grand[0] & 0xffffffff;
+    const int64_t bincl = row_scan64(lane < kItemBuckets ? bgrand : 0);
+    int64_t bnext = n_full + bincl - bgrand + bbase;     // lane b: this wave's next item of bucket b
+    const int64_t n_items = n_full + __shfl(bincl, kItemBuckets - 1);
+    const uint64_t lt = (uint64_t(1) << lane) - 1;
+    for (int32_t gr = gw0; gr < gw1; gr += kWave) {
+        const int32_t g = gr + lane;
+        const bool valid = g < gw1;
+        int64_t v[4] = {0, 0, 0, 0};
+        const int b = valid ? values(g, v) : -1;
+        int64_t ex[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int64_t incl = wave_scan64(v[i]);
+            ex[i] = carry[i] + incl - v[i];
+            carry[i] += __shfl(incl, kWave - 1);
+        }
+        int32_t wl = -1;
+#pragma unroll
+        for (int bb = 0; bb < kItemBuckets; ++bb) {
+            const uint64_t m = __ballot(b == bb);
+            if (m) {
+                const int64_t bn = __shfl(bnext, bb);
+                if (b == bb) wl = (int32_t)(bn + __popcll(m & lt));
+                if (lane == bb) bnext += __popcll(m);
+            }
+        }
+        if (valid) {
+            pa.qoff[g] = (int32_t)(ex[3] & 0xffffffff);
+            pa.wstart[g] = (int32_t)(ex[0] & 0xffffffff);
+            pa.wlast[g] = wl;
+            pa.pbase[g] = ex[1];
+            pa.gstart[g] = (int32_t)(ex[0] >> 32);
+            pa.ubase[g] = ex[2];
+            pa.mstart[g] = (int32_t)(ex[3] >> 32);
+        }
+    }
+    if (t == 0) {
+        pa.qoff[G] = (int32_t)(grand[3] & 0xffffffff);
+        pa.wstart[G] = (int32_t)n_full;
+        pa.gstart[G] = (int32_t)(grand[0] >> 32);
+        pa.mstart[G] = (int32_t)(grand[3] >> 32);
+        pa.plan->chunk = ch;
+        pa.plan->n_items = n_items;
+        pa.plan->n_parts = grand[1];
+        pa.plan->n_groups = grand[0] >> 32;
+        pa.plan->n_l1 = grand[2];
+        pa.plan->n_merge = grand[3] >> 32;
+    }
 }
 
 struct GlobalCnt {
@@ -413,20 +563,6 @@ struct LdsLen {
     const int32_t *len;
     __device__ int64_t operator()(int32_t g) const { return len[g]; }
 };
-// Staged planner tables: one pad word per 16 clusters. A thread plans a
-// contiguous run of clusters (16 of them at G = 16384), so a wave's reads
-// are that run length apart; padded, the stride is odd and the 64 lanes
-// spread over all 32 banks instead of hitting two.
-__device__ __forceinline__ int32_t pad16(int32_t g) { return g + (g >> 4); }
-struct PadCnt {
-    const int32_t *cnt;
-    __device__ int64_t operator()(int32_t g) const { return cnt[pad16(g)]; }
-};
-struct PadLen {
-    const int32_t *len;
-    __device__ int64_t operator()(int32_t g) const { return len[pad16(g)]; }
-};
-
 // Outputs of the fine stage, for pairs the routing finishes itself: a
 // selected cluster id out of range gives an empty slot (no candidates).
 struct SlotOut {
@@ -500,23 +636,23 @@ __global__ __launch_bounds__(kPlanThreads) void route_plan(PlanArgs pa, const in
             if (t == 0) plan_nothing(pa.plan);
             return;
         }
-        int32_t *lcnt = stage, *llen = stage + pad16(G) + 1;
+        int32_t *lcnt = stage, *llen = stage + G;
 #pragma unroll
         for (int i = 0; i < kStagePer; ++i) {
             const int32_t g = t + i * kPlanThreads;
             if (g < G) {
-                lcnt[pad16(g)] = c[i];
-                llen[pad16(g)] = (int32_t)(o1[i] - o0[i]);      // N < 2^31
+                lcnt[g] = c[i];
+                llen[g] = (int32_t)(o1[i] - o0[i]);      // N < 2^31
             }
         }
         __syncthreads();
-        plan_chunks<false>(pa, PadCnt{lcnt}, PadLen{llen}, s, PlanMirror{});
+        plan_chunks_wave(pa, LdsCnt{lcnt}, LdsLen{llen}, s);
     } else {
         if (offsets_bad(pa.off, pa.G, pa.n_rows)) {
             if (threadIdx.x == 0) plan_nothing(pa.plan);
             return;
         }
-        plan_chunks<false>(pa, GlobalCnt{cnt}, OffLen{pa.off}, s, PlanMirror{});
+        plan_chunks_wave(pa, GlobalCnt{cnt}, OffLen{pa.off}, s);
     }
 }
 
@@ -647,7 +783,7 @@ __global__ __launch_bounds__(kPlanThreads) void route_fused(PlanArgs pa, const i
     }
     if (bad) atomicAdd(&s_bad, bad);
     __syncthreads();
-    const int64_t ch = plan_chunks<true>(pa, LdsCnt{lcnt}, OffLen{loff}, s, m);
+    const int64_t ch = plan_chunks(pa, LdsCnt{lcnt}, OffLen{loff}, s, m);
     const int lch = 63 - __builtin_clzll((unsigned long long)ch);
     if (t == 0) {
         pa.plan->next = 0;
@@ -1246,7 +1382,7 @@ hipError_t launch_attend(int32_t key_dtype, int32_t compute_dtype, int32_t d, in
         hipLaunchKernelGGL(route_init, dim3((G + 255) / 256 < 1024 ? (G + 255) / 256 : 1024),
                            dim3(256), 0, s, G, w.cnt, w.cursor, w.plan);
         hipLaunchKernelGGL(route_count, dim3(gblocks), dim3(256), 0, s, sel, bc, G, w.cnt, w.plan);
-        const size_t stage = ((size_t)G + G / 16 + 1) * 8;
+        const size_t stage = (size_t)G * 8;          // query counts and segment lengths
         if (G <= kStagePer * kPlanThreads && stage + 8 * 1024 <= lds_budget()) {
             hipError_t e1 = hipFuncSetAttribute((const void *)route_plan<true>,
                                                 hipFuncAttributeMaxDynamicSharedMemorySize,
