@@ -1296,6 +1296,21 @@ static hipError_t launch_stream(int32_t key_dtype, int32_t compute_dtype, const 
         l.smem = l.qs_bytes + fine_state_bytes(ql, fa0.cap, l.fa.ntile);
         // two blocks per CU when two blocks' LDS fits (and the buffers leave the registers)
         const bool two = npl <= 4 && 2 * (l.smem + 256) <= budget + 256;
+        // two blocks per CU with half of d's query fragments staged at a time
+        // (one query tile per pass: when the load needs no more), so that one
+        // block's staging, epilogues and pass ends overlap the other's loads
+        if (!two && ql == 16 && npl <= 4 && fa0.d % (key_dtype == kF32 ? 256 : 512) == 0) {
+            const int32_t qs_half = (int32_t)fine_qs_bytes(fa0.d / 2, 16);
+            const size_t sm2 = qs_half + fine_state_bytes(16, fa0.cap, 2);
+            if (2 * (sm2 + 256) <= budget + 256) {
+                l.ksplit = true;
+                l.fa.ntile = 2;
+                l.qs_bytes = qs_half;
+                l.smem = sm2;
+                return key_dtype == kF32 ? launch_stream_lds_f32(npl, false, l)
+                                         : launch_stream_lds_bf16(npl, false, l);
+            }
+        }
         // one block per CU: producer/consumer blocks (their load units are
         // 8 k-steps for bf16 keys, 4 for fp32: d % 256 or d % 128)
         l.producer_consumer = !two && npl <= 4;

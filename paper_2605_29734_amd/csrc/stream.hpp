@@ -108,6 +108,7 @@ struct StreamLaunch {
     size_t smem;
     int32_t qs_bytes;
     bool producer_consumer;       // eight-wave producer/consumer blocks (one block per CU)
+    bool ksplit;                  // two blocks per CU, half the query fragments staged at a time
     KernelEvents ev;
     hipStream_t stream;
 };
@@ -905,6 +906,180 @@ __global__ __launch_bounds__(2 * kFineThreads) void stream_pc(FineArgs a, int32_
     stream_lds_body<KT, sizeof(KT) == 4 ? 4 : 8, NPL, true, true>(a, qs_bytes, smem_raw, s_next);
 }
 
+// ---- split pass: the query fragments staged half of d at a time ------------
+// When two blocks fit on a CU only with half the query fragments in LDS, a
+// pass runs over its rows in groups of up to kSplitSteps steps, each group
+// twice: first over the k-steps of the first half of d, keeping every step's
+// partial scores in registers, then over the second half, which completes
+// the scores and runs the step ends. Each half of every key row is read once;
+// the queries are staged twice per group. With two blocks per CU, one
+// block's staging, epilogues and pass ends overlap the other's key loads.
+constexpr int kSplitSteps = 4;
+
+// Unit u of a half (NGH units of U k-steps per step, k-steps from k0) of the
+// row group starting at bank row g0: loads clamped into the chunk.
+template <typename KT, int U>
+__device__ __forceinline__ void split_load_unit(LoadUnit<KT, U> &lu, const KT *__restrict__ K,
+                                                const int32_t *__restrict__ tid_src, int d,
+                                                int NGH, int k0, int u, int64_t g0, int64_t r1) {
+    const int lane = threadIdx.x & 63, wave = fine_wave(), r16 = lane & 15, kg = lane >> 4;
+    const int tt = u / NGH, gi = u - tt * NGH;
+    const int64_t base = g0 + (int64_t)tt * kRowsPerStep;
+    const int64_t row = min(base + wave * kRowsPerWave + r16, r1 - 1);
+    const KT *kp = K + row * d + 32 * (k0 + U * gi) + 8 * kg;
+#pragma unroll
+    for (int uu = 0; uu < U; ++uu) lu.f[uu].load(kp + 32 * uu);
+    lu.tid = step_tid_load(tid_src, base, r1);
+}
+
+// Multiplies unit u (in lu) of half h and requests unit nu into nx. A step
+// starts from zero in the first half and from its partial scores in the
+// second; it ends by saving them (first half) or with the step end.
+template <typename KT, int U, int NQT, int NPL>
+__device__ __forceinline__ void split_compute_unit(
+    const FineArgs &a, const FineSmem &sm, const LoadUnit<KT, U> &lu, LoadUnit<KT, U> &nx,
+    const KT *__restrict__ K, int nu, int NGH, int k0, int u, bool valid, int h, int64_t g0,
+    int64_t r1, int step0, int nqg, f32x4_t (&acc)[NQT], f32x4_t (&part)[kSplitSteps][NQT],
+    OwnedLane &o, Stats<NQT> &st) {
+    const int lane = threadIdx.x & 63;
+    const int tt = u / NGH, gi = u - tt * NGH;
+    if (gi == 0) {
+#pragma unroll
+        for (int qt = 0; qt < NQT; ++qt) acc[qt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        if (h == 1) {
+#pragma unroll
+            for (int i = 0; i < kSplitSteps; ++i)
+                if (i == tt) {
+#pragma unroll
+                    for (int qt = 0; qt < NQT; ++qt) acc[qt] = part[i][qt];
+                }
+        }
+    }
+    split_load_unit<KT, U>(nx, K, a.tid_src, a.d, NGH, k0, nu, g0, r1);
+    const bf16x8_t *qs = sm.qs + (size_t)gi * U * NQT * kWave + lane;
+#pragma unroll
+    for (int uu = 0; uu < U; ++uu) {
+        const bf16x8_t A = lu.f[uu].bf16();
+#pragma unroll
+        for (int qt = 0; qt < NQT; ++qt)
+            acc[qt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, qs[(uu * NQT + qt) * kWave],
+                                                              acc[qt], 0, 0, 0);
+        if ((uu & 3) == 3) __builtin_amdgcn_sched_barrier(0);
+    }
+    if (valid && gi == NGH - 1) {
+        if (h == 0) {
+#pragma unroll
+            for (int i = 0; i < kSplitSteps; ++i)
+                if (i == tt) {
+#pragma unroll
+                    for (int qt = 0; qt < NQT; ++qt) part[i][qt] = acc[qt];
+                }
+        } else {
+            const int64_t base = g0 + (int64_t)tt * kRowsPerStep;
+            const int32_t tid = tid_value(lu.tid, a.tid == nullptr, base, r1);
+            step_end<NQT, NPL>(a, sm, acc, step0 + tt, base, r1, nqg, tid, o, st);
+        }
+    }
+}
+
+template <typename KT, int U, int NQT, int NPL>
+__device__ __forceinline__ void pass_split(const FineArgs &a, const FineSmem &sm, int64_t p0,
+                                           bool single, int64_t r0, int64_t r1, int32_t qbeg,
+                                           int32_t qg0, int32_t nqg) {
+    const int t = threadIdx.x;
+    const int d = a.d;
+    const KT *__restrict__ K = static_cast<const KT *>(a.keys);
+    const KT *__restrict__ Q = static_cast<const KT *>(a.q);
+    const int KH = d >> 6;             // k-steps per half of d
+    const int NGH = KH / U;            // units per step and half
+    const int T = (int)((r1 - r0 + kRowsPerStep - 1) / kRowsPerStep);
+    constexpr int R = kRing;
+    const PassBound pb = pass_begin<true>(a, sm, qbeg, qg0, nqg, single);
+    OwnedLane o;
+    Stats<NQT> st;
+    stats_reset<NQT>(st);
+    for (int tg = 0; tg < T; tg += kSplitSteps) {
+        const int Tg = min(kSplitSteps, T - tg);
+        const int64_t g0 = r0 + (int64_t)tg * kRowsPerStep;
+        f32x4_t part[kSplitSteps][NQT];
+#pragma unroll
+        for (int i = 0; i < kSplitSteps; ++i)
+#pragma unroll
+            for (int qt = 0; qt < NQT; ++qt) part[i][qt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        for (int h = 0; h < 2; ++h) {
+            const int k0 = h * KH;
+            const int total = Tg * NGH;
+            LoadUnit<KT, U> ring[R];
+#pragma unroll
+            for (int j = 0; j < R - 1; ++j)
+                split_load_unit<KT, U>(ring[j], K, a.tid_src, d, NGH, k0, min(j, total - 1), g0, r1);
+            // every wave is done with the fragments of the previous half
+            block_lds_barrier();
+            // this half's query fragments: [k-step][query tile][lane], as in
+            // the full staging (padding columns zeroed at the store); fp32
+            // queries in batches of four fragments (registers)
+            {
+                constexpr int kBatch = sizeof(KT) == 4 ? 4 : 8;
+                const int nfrag = KH * NQT * kWave;
+                const int nt = blockDim.x;
+                for (int i0 = t; i0 < nfrag; i0 += nt * kBatch) {
+                    bf16x8_t f[kBatch];
+#pragma unroll
+                    for (int b = 0; b < kBatch; ++b) {
+                        const int idx = min(i0 + b * nt, nfrag - 1);
+                        const int s2 = idx / (NQT * kWave), rem = idx - s2 * NQT * kWave;
+                        const int qt = rem >> 6, ln = rem & 63;
+                        const int n = qt * 16 + (ln & 15), k = 32 * (k0 + s2) + 8 * (ln >> 4);
+                        f[b] = load8(Q + (int64_t)sm.qrow[n < nqg ? n : 0] * d + k);
+                    }
+#pragma unroll
+                    for (int b = 0; b < kBatch; ++b) {
+                        const int idx = min(i0 + b * nt, nfrag - 1);
+                        const int rem = idx % (NQT * kWave);
+                        const int n = (rem >> 6) * 16 + (rem & 15);
+                        sm.qs[idx] = n < nqg ? f[b] : zero8();
+                    }
+                }
+            }
+            if (tg == 0 && h == 0) pass_bound(sm, pb);
+            wait_vmcnt<0>();
+            __syncthreads();
+            if (tg == 0 && h == 0) owned_begin<NQT>(sm, nqg, o);
+            f32x4_t acc[NQT];
+#pragma unroll
+            for (int qt = 0; qt < NQT; ++qt) acc[qt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+            for (int u = 0; u < total; u += R) {
+#pragma unroll
+                for (int j = 0; j < R; ++j)
+                    split_compute_unit<KT, U, NQT, NPL>(
+                        a, sm, ring[j], ring[(j + R - 1) % R], K, min(u + j + R - 1, total - 1),
+                        NGH, k0, u + j, u + j < total, h, g0, r1, tg, nqg, acc, part, o, st);
+            }
+        }
+    }
+    // the ring's last loads (re-reads of the last unit) are not used
+    wait_vmcnt<0>();
+    pass_end<NQT, NPL, false>(a, sm, p0, qbeg, single, qg0, nqg, o, st);
+}
+
+// Two blocks per CU with half the query fragments staged at a time (see
+// pass_split): registers capped at two waves per SIMD (the partial scores of
+// a group take 16 of them: one query tile per pass, qmax == 16);
+// d % (64 U) == 0.
+template <typename KT, int NPL>
+__global__ __launch_bounds__(kFineThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void stream_split(FineArgs a, int32_t qs_bytes) {
+    extern __shared__ __align__(16) unsigned char smem_raw[];
+    __shared__ int32_t s_next[2];
+    constexpr int U = sizeof(KT) == 4 ? 4 : 8;
+    const FineSmem sm = fine_carve(smem_raw, qs_bytes, a.qmax, a.cap, a.ntile);
+    for_each_item(a, s_next, [&](const ItemPass &it) {
+        for (int32_t qg0 = 0; qg0 < it.nq; qg0 += a.qmax)
+            pass_split<KT, U, 1, NPL>(a, sm, it.p0, it.single, it.r0, it.r1, it.qbeg, qg0,
+                                      min(a.qmax, it.nq - qg0));
+    });
+}
+
 template <typename T, bool BF16, int NPL>
 __global__ __launch_bounds__(kFineThreads) void stream_generic(FineArgs a) {
     extern __shared__ __align__(16) unsigned char smem_raw[];
@@ -947,6 +1122,13 @@ hipError_t launch_stream_kernel(Kern kern, const StreamLaunch &l, Args... args) 
 
 template <typename KT>
 hipError_t launch_stream_lds_t(int npl, bool two_per_cu, const StreamLaunch &l) {
+    if (l.ksplit) {
+        switch (npl) {
+            case 2: return launch_stream_kernel(stream_split<KT, 2>, l, l.fa, l.qs_bytes);
+            case 4: return launch_stream_kernel(stream_split<KT, 4>, l, l.fa, l.qs_bytes);
+        }
+        return hipErrorInvalidValue;
+    }
     if (l.producer_consumer) {
         switch (npl) {
             case 2: return launch_stream_kernel_n(stream_pc<KT, 2>, 2 * kFineThreads, l, l.fa,

@@ -36,7 +36,10 @@ template <int NPL>
 __global__ __launch_bounds__(kWave * kTopkWaves) void topk_rows(TopkArgs a) {
     extern __shared__ __align__(16) uint64_t tbuf[];
     constexpr int cap = NPL * kWave;
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63;
+    // the wave index as a uniform value: the unit's row, segment and bounds,
+    // and every address derived from them, then live in scalar registers
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int64_t row = (int64_t)blockIdx.x * kTopkWaves + wave;
     if (row >= a.rows) return;              // no block-wide synchronisation below
     uint64_t *buf = tbuf + wave * cap;
@@ -129,7 +132,8 @@ __global__ __launch_bounds__(kWave * kTopkWaves) void topk_rows(TopkArgs a) {
 // select over the lane maxima, one ballot per bit. Random scores leave a few
 // more than top_k candidates; each is written straight to the unit's output
 // list (k_slot >= top_k slots, unsorted, padded with (-inf, -1)) at its
-// ballot prefix position. A superset of the segment's top-k is all the row
+// lane's place (a prefix sum of the lanes' counts) in register order. A
+// superset of the segment's top-k is all the row
 // merge (topk_rows) needs. Only if the candidates overflow the list (many
 // ties, or top_k > 64 where no bound is taken) does the unit fall back to
 // the LDS buffer with radix-select compaction of topk_rows and write its
@@ -176,7 +180,10 @@ template <int NPL, bool IDS>
 __global__ __launch_bounds__(kWave * kTopkWaves) void seg_topk(SegArgs a) {
     extern __shared__ __align__(16) uint64_t tbuf[];
     constexpr int cap = NPL * kWave;
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63;
+    // the wave index as a uniform value: the unit's row, segment and bounds,
+    // and every address derived from them, then live in scalar registers
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int64_t u = (int64_t)blockIdx.x * kTopkWaves + wave;
     if (u >= a.units) return;               // no block-wide synchronisation below
     const int64_t row = u / a.n_seg, seg = u - row * a.n_seg;
@@ -192,13 +199,24 @@ __global__ __launch_bounds__(kWave * kTopkWaves) void seg_topk(SegArgs a) {
     // the segment; past-the-end columns become -inf and are never candidates)
     float s[kSegPer];
     int32_t id[IDS ? kSegPer : 1];
+    if (len == kSegCols) {
+        // a whole segment: one base address, the rest are instruction offsets
+        const float *sl = sc + lane;
 #pragma unroll
-    for (int j = 0; j < kSegPer; ++j) s[j] = sc[min(j * kWave + lane, len - 1)];
-    if constexpr (IDS) {
+        for (int j = 0; j < kSegPer; ++j) s[j] = sl[j * kWave];
+        if constexpr (IDS) {
+            const int32_t *il = a.col_id + c0 + lane;
 #pragma unroll
-        for (int j = 0; j < kSegPer; ++j) id[j] = a.col_id[c0 + min(j * kWave + lane, len - 1)];
-    }
-    if (len < kSegCols) {
+            for (int j = 0; j < kSegPer; ++j) id[j] = il[j * kWave];
+        }
+    } else {
+#pragma unroll
+        for (int j = 0; j < kSegPer; ++j) s[j] = sc[min(j * kWave + lane, len - 1)];
+        if constexpr (IDS) {
+#pragma unroll
+            for (int j = 0; j < kSegPer; ++j) id[j] = a.col_id[c0 + min(j * kWave + lane, len - 1)];
+        }
+        // past-the-end columns
 #pragma unroll
         for (int j = 0; j < kSegPer; ++j)
             if (j * kWave + lane >= len) s[j] = -INFINITY;
@@ -223,22 +241,30 @@ __global__ __launch_bounds__(kWave * kTopkWaves) void seg_topk(SegArgs a) {
         }
         if (t) T = score_of_ord(t);
     }
-    // candidates straight to the output list
-    int cnt = 0;
+    // candidates straight to the output list: a lane's passing registers as
+    // a bit mask, its first place the sum of the counts of the lanes below
+    // it (one ballot per bit of the counts, which are at most 32)
+    uint32_t pm = 0;
 #pragma unroll
-    for (int j = 0; j < kSegPer; ++j) {
-        const bool pass = s[j] >= T && s[j] != -INFINITY;
-        const uint64_t mask = __ballot(pass);
-        if (mask) {
-            const int pos = cnt + __popcll(mask & lt_mask);
-            if (pass && pos < a.k_slot) {
-                os[pos] = s[j];
-                oi[pos] = IDS ? id[j] : (int32_t)(a.id_base + c0 + j * kWave + lane);
-            }
-            cnt += __popcll(mask);
-        }
+    for (int j = 0; j < kSegPer; ++j) pm |= (s[j] >= T && s[j] != -INFINITY) ? (1u << j) : 0u;
+    const int mine = __popc(pm);
+    int first = 0, cnt = 0;
+#pragma unroll
+    for (int b = 0; b < 6; ++b) {
+        const uint64_t mb = __ballot((mine >> b) & 1);
+        first += __popcll(mb & lt_mask) << b;
+        cnt += __popcll(mb) << b;
     }
     if (cnt <= a.k_slot) {
+        int pos = first;
+#pragma unroll
+        for (int j = 0; j < kSegPer; ++j) {
+            if ((pm >> j) & 1) {
+                os[pos] = s[j];
+                oi[pos] = IDS ? id[j] : (int32_t)(a.id_base + c0 + j * kWave + lane);
+                ++pos;
+            }
+        }
         for (int r = cnt + lane; r < a.k_slot; r += kWave) {
             os[r] = -INFINITY;
             oi[r] = -1;
