@@ -1274,8 +1274,8 @@ static int qmax_for_load(int qmax, int64_t bc, int32_t G) {
 }
 
 static hipError_t launch_stream(int32_t key_dtype, int32_t compute_dtype, const FineArgs &fa0,
-                                int64_t bc, int n_cu, int64_t w_max, KernelEvents ev,
-                                hipStream_t s) {
+                                int64_t bc, int64_t n_rows, int n_cu, int64_t w_max,
+                                KernelEvents ev, hipStream_t s) {
     const size_t budget = lds_budget();
     const int npl = fa0.cap / kWave;
     StreamLaunch l{};
@@ -1298,8 +1298,11 @@ static hipError_t launch_stream(int32_t key_dtype, int32_t compute_dtype, const 
         const bool two = npl <= 4 && 2 * (l.smem + 256) <= budget + 256;
         // two blocks per CU with half of d's query fragments staged at a time
         // (one query tile per pass: when the load needs no more), so that one
-        // block's staging, epilogues and pass ends overlap the other's loads
-        if (!two && ql == 16 && npl <= 4 && fa0.d % (key_dtype == kF32 ? 256 : 512) == 0) {
+        // block's staging, epilogues and pass ends overlap the other's loads;
+        // for short segments (at most two four-step row groups on average:
+        // the queries are staged again for every group)
+        if (!two && ql == 16 && npl <= 4 && fa0.d % (key_dtype == kF32 ? 256 : 512) == 0 &&
+            n_rows <= (int64_t)fa0.G * 2 * kSplitSteps * kRowsPerStep) {
             const int32_t qs_half = (int32_t)fine_qs_bytes(fa0.d / 2, 16);
             const size_t sm2 = qs_half + fine_state_bytes(16, fa0.cap, 2);
             if (2 * (sm2 + 256) <= budget + 256) {
@@ -1439,7 +1442,7 @@ hipError_t launch_attend(int32_t key_dtype, int32_t compute_dtype, int32_t d, in
     fa.slot_sum = slot_sum;
     fa.cand_score = cand_score;
     fa.cand_id = cand_id;
-    err = launch_stream(key_dtype, compute_dtype, fa, bc, n_cu, w.w_max, ev, s);
+    err = launch_stream(key_dtype, compute_dtype, fa, bc, N, n_cu, w.w_max, ev, s);
     if (err != hipSuccess) return err;
 
     MergeArgs ma{};

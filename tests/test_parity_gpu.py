@@ -39,16 +39,16 @@ def test_before_after_reduced():
     run_case(synth.scaled(S["before_after_f32"], B=96, G=256, N=65536))
 
 
-@pytest.mark.parametrize("storage,N,top_k,min_size", [
-    ("f32", 200000, 128, 50),      # long segments: chunks of several four-step row groups
-    ("bf16", 100000, 64, 50),
-    ("f32", 6000, 128, 1),         # short and ragged segments: groups of fewer than four steps
+@pytest.mark.parametrize("storage,B,G,N,top_k,min_size", [
+    ("f32", 512, 512, 200000, 128, 20),   # Zipf segments (mean 390 rows, 1024-row chunks):
+    ("bf16", 512, 512, 200000, 64, 20),   # long ones of several four-step row groups per chunk
+    ("f32", 128, 64, 6000, 128, 1),       # short and ragged segments: groups under four steps
 ])
-def test_split_stream_kernel(storage, N, top_k, min_size):
+def test_split_stream_kernel(storage, B, G, N, top_k, min_size):
     """The two-blocks-per-CU stream kernel that stages half of d's query
-    fragments at a time (d = 2048, one query tile per pass: about eight
-    queries per selected cluster)."""
-    run_case(synth.Spec("split", B=128, d=2048, G=64, N=N, top_c=4, top_k=top_k, tau=0.5,
+    fragments at a time (d = 2048, short segments on average, one query tile
+    per pass: at most about eight queries per selected cluster)."""
+    run_case(synth.Spec("split", B=B, d=2048, G=G, N=N, top_c=4, top_k=top_k, tau=0.5,
                         storage=storage, compute="bf16", sizes="zipf", zipf_s=1.0,
                         min_size=min_size), gen_device="cuda", check_build=False)
 
