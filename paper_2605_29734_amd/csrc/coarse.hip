@@ -58,6 +58,13 @@ __device__ __forceinline__ void gemm_tile(int b, int nb, int tm, int tn, int &mt
     nt = in / gm;
 }
 
+// x from the lane N places before this one within its 16-lane row, rotating
+// (DPP row_ror).
+template <int N>
+__device__ __forceinline__ float row_ror_f32(float x) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x120 + N, 0xF, 0xF, false));
+}
+
 // Stage layout in LDS: the stacked [Q tile; C tile] rows (512 of them), 64
 // bytes each = four 16-byte chunks, chunk c of row r stored in slot
 // c ^ ((r >> 2) & 3). A fragment read (16 rows, one chunk each) then touches
@@ -90,7 +97,8 @@ __device__ __forceinline__ void gemm_issue_stage(const __bf16 *__restrict__ q,
 __global__ __launch_bounds__(kGemmThreads) void coarse_gemm(const __bf16 *__restrict__ q,
                                                             const __bf16 *__restrict__ ck,
                                                             int32_t B, int32_t G, int32_t d,
-                                                            float *__restrict__ S) {
+                                                            float *__restrict__ S,
+                                                            float *__restrict__ tmax) {
     extern __shared__ __align__(16) unsigned char lds[];
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
     const int r16 = lane & 15, kg = lane >> 4;
@@ -180,6 +188,31 @@ __global__ __launch_bounds__(kGemmThreads) void coarse_gemm(const __bf16 *__rest
                 const int64_t c = n0 + wn * 64 + j * 16 + r16;
                 if (r < B && c < G) S[r * G + c] = acc[i][j][e];
             }
+    if (tmax) {
+        // Each row's maximum over this wave's 64 columns (a 64-column tile of
+        // the score row): over the lane's four columns, then the 16 lanes of
+        // its row group (lanes 16 kg .. 16 kg + 15 hold one row's 16-column
+        // slices), by DPP row rotations; no LDS, no barrier.
+        const int n64 = (G + 63) / 64;
+        const int tcol = nt * (BN / 64) + wn;
+        if (tcol < n64) {
+#pragma unroll
+            for (int i = 0; i < 8; ++i)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    float m = -INFINITY;
+#pragma unroll
+                    for (int j = 0; j < 4; ++j)
+                        if (n0 + wn * 64 + j * 16 + r16 < G) m = fmaxf(m, acc[i][j][e]);
+                    m = fmaxf(m, row_ror_f32<8>(m));
+                    m = fmaxf(m, row_ror_f32<4>(m));
+                    m = fmaxf(m, row_ror_f32<2>(m));
+                    m = fmaxf(m, row_ror_f32<1>(m));
+                    const int64_t r = m0 + wm * 128 + i * 16 + 4 * kg + e;
+                    if (r16 == 0 && r < B) tmax[r * n64 + tcol] = m;
+                }
+        }
+    }
 }
 
 // Small problems (fewer 256 x 256 tiles than compute units): one wave per
@@ -315,14 +348,19 @@ CoarseWs coarse_layout(void *ws, int32_t B, int32_t G, int32_t d, int32_t key_dt
     const size_t np = w.n_seg > 1 ? (size_t)B * w.n_seg * seg_topk_slots(top_c) : 0;
     w.p_score = np ? cv.take<float>(np) : nullptr;
     w.p_id = np ? cv.take<int32_t>(np) : nullptr;
+    // 64-column tile maxima for the selection that reads only the tiles that matter
+    w.n_tile = (G + 63) / 64;
+    w.tmax = w.n_seg > 1 && compute_dtype == kBF16 ? cv.take<float>((size_t)B * w.n_tile) : nullptr;
     if (bytes) *bytes = cv.off + 256;
     return w;
 }
 
 hipError_t launch_scores(int32_t key_dtype, int32_t compute_dtype, int32_t d, int64_t n,
                          const void *keys, const void *q, int32_t B, float *S, __bf16 *q16,
-                         __bf16 *k16, bool convert_q, int n_cu, KernelEvents ev, hipStream_t s) {
+                         __bf16 *k16, bool convert_q, int n_cu, KernelEvents ev, hipStream_t s,
+                         float *tmax, bool *tiled) {
     const int32_t G = (int32_t)n;
+    if (tiled) *tiled = false;
     if (compute_dtype == kF32) {
         launch_timed(coarse_f32, dim3((G + 63) / 64, (B + 63) / 64), dim3(256), 0, s, ev,
                      static_cast<const float *>(q), static_cast<const float *>(keys), B, G, d, S);
@@ -359,7 +397,8 @@ hipError_t launch_scores(int32_t key_dtype, int32_t compute_dtype, int32_t d, in
         if (err != hipSuccess) return err;
         const int tiles = ((B + BM - 1) / BM) * ((G + BN - 1) / BN);
         launch_timed(coarse_gemm, dim3(tiles), dim3(kGemmThreads), kGemmLds, s, ev, qa, ka, B, G,
-                     d, S);
+                     d, S, tmax);
+        if (tiled) *tiled = tmax != nullptr;
     }
     return hipGetLastError();
 }
@@ -368,15 +407,21 @@ hipError_t launch_coarse(int32_t key_dtype, int32_t compute_dtype, int32_t d, in
                          const void *coarse_keys, const void *q, int32_t B, int32_t top_c,
                          int32_t *sel, float *sel_score, const CoarseWs &w, int n_cu,
                          KernelEvents ev, hipStream_t s) {
+    // tile maxima only where the selection can prune with them
+    bool tiled = false;
+    float *tmax = top_c <= kWave && top_c < w.n_tile ? w.tmax : nullptr;
     hipError_t err = launch_scores(key_dtype, compute_dtype, d, G, coarse_keys, q, B, w.scores,
-                                   w.q16, w.c16, true, n_cu, ev, s);
+                                   w.q16, w.c16, true, n_cu, ev, s, tmax, &tiled);
     if (err != hipSuccess) return err;
-    return launch_select(B, G, top_c, sel, sel_score, w, s);
+    return launch_select(B, G, top_c, sel, sel_score, w, s, tiled ? tmax : nullptr);
 }
 
 hipError_t launch_select(int32_t B, int32_t G, int32_t top_c, int32_t *sel, float *sel_score,
-                         const CoarseWs &w, hipStream_t s) {
+                         const CoarseWs &w, hipStream_t s, const float *tmax) {
     hipError_t err = hipSuccess;
+    // enough tiles for the bound to prune: read only the tiles that can hold the top_c
+    if (tmax && top_c <= kWave && top_c < (G + 63) / 64)
+        return launch_tile_topk(B, G, w.scores, tmax, top_c, sel, sel_score, s);
     if (w.n_seg == 1)
         return launch_topk(B, 1, G, w.scores, nullptr, nullptr, nullptr, 1.0f, top_c, sel,
                            sel_score, nullptr, nullptr, nullptr, nullptr, s);

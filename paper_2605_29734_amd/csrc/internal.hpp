@@ -112,6 +112,8 @@ struct CoarseWs {
     int32_t n_seg;     // segments per score row in the top-c selection
     float *p_score;    // [B][n_seg][top_c] per-segment selections (n_seg > 1)
     int32_t *p_id;
+    float *tmax;       // [B][n_tile] each row's maximum over each 64-column tile (n_seg > 1)
+    int32_t n_tile;
 };
 CoarseWs coarse_layout(void *ws, int32_t B, int32_t G, int32_t d, int32_t key_dtype,
                        int32_t compute_dtype, int32_t top_c, size_t *bytes);
@@ -121,8 +123,10 @@ hipError_t launch_coarse(int32_t key_dtype, int32_t compute_dtype, int32_t d, in
                          KernelEvents ev, hipStream_t s);
 
 // The top_c of each score row of w.scores [B][G] (descending, ties to the lower id).
+// With tmax (the rows' 256-column tile maxima of these scores) only the tiles
+// that can hold a row's top_c are read.
 hipError_t launch_select(int32_t B, int32_t G, int32_t top_c, int32_t *sel, float *sel_score,
-                         const CoarseWs &w, hipStream_t s);
+                         const CoarseWs &w, hipStream_t s, const float *tmax = nullptr);
 
 // ---- prefix-aware coarse scoring ----------------------------------------------
 struct PrefixWs {
@@ -229,6 +233,14 @@ hipError_t launch_attend(int32_t key_dtype, int32_t compute_dtype, int32_t d, in
 // there too. Column j's id is col_id[j] (or id_base + j without col_id).
 int32_t seg_topk_cols();
 int32_t seg_topk_slots(int32_t top_k);
+
+// Row top-k over score rows [rows][n] that come with their 64-column tile
+// maxima tmax [rows][ceil(n / 64)] (top_k <= 64): the top_k-th largest
+// tile maximum bounds the row's top_k from below, so only the tiles whose
+// maximum reaches it are read. Writes out_id / out_score [rows][top_k]
+// (descending, ties to the lower column), padded with (-1, -inf).
+hipError_t launch_tile_topk(int64_t rows, int64_t n, const float *score, const float *tmax,
+                            int32_t top_k, int32_t *out_id, float *out_score, hipStream_t s);
 hipError_t launch_seg_topk(int64_t rows, int64_t row_stride, int64_t n, const float *score,
                            const int32_t *col_id, int64_t id_base, int32_t top_k, float tau,
                            float *o_score, int32_t *o_id, float *o_m, float *o_z, int64_t o_lists,
@@ -236,10 +248,13 @@ hipError_t launch_seg_topk(int64_t rows, int64_t row_stride, int64_t n, const fl
 
 // S[B][n] = Q K^T over n key rows (row stride n), on the coarse GEMM kernels.
 // With fp32 storage and bf16 arithmetic the 256 x 256-tile kernel reads bf16
-// copies: k16 [n][d] is made here, q16 [B][d] too when convert_q.
+// copies: k16 [n][d] is made here, q16 [B][d] too when convert_q. Given tmax
+// ([B][ceil(n / 64)]), the 256 x 256-tile kernel also writes each row's
+// maximum over each 64-column tile there and sets *tiled (else false).
 hipError_t launch_scores(int32_t key_dtype, int32_t compute_dtype, int32_t d, int64_t n,
                          const void *keys, const void *q, int32_t B, float *S, __bf16 *q16,
-                         __bf16 *k16, bool convert_q, int n_cu, KernelEvents ev, hipStream_t s);
+                         __bf16 *k16, bool convert_q, int n_cu, KernelEvents ev, hipStream_t s,
+                         float *tmax = nullptr, bool *tiled = nullptr);
 
 // ---- flat retrieval (every record a candidate) --------------------------------
 struct FlatWs {

@@ -325,6 +325,103 @@ __global__ __launch_bounds__(kWave * kTopkWaves) void seg_topk(SegArgs a) {
     }
 }
 
+// Row top-k with tile maxima (the coarse selection after the 256 x 256-tile
+// GEMM, which writes each row's maximum over each 64-column tile). One wave
+// per row. T, the top_k-th largest of the lanes' maxima of the row's tile
+// maxima (lane l holds tiles l, l + 64, ...), is the maximum of top_k
+// distinct entries, so at most the row's top_k-th score: the top_k lie in
+// the tiles whose maximum reaches T and score at least T. Those tiles are
+// read four at a time (one score per lane each) and their entries of at
+// least T appended to the wave's LDS buffer as in topk_rows, compacted when
+// it fills.
+constexpr int kTileCols = 64;
+
+struct TileArgs {
+    int64_t rows, n;
+    int32_t n_tile, top_k;
+    const float *score, *tmax;
+    int32_t *out_id;
+    float *out_score;
+};
+
+template <int NPL>
+__global__ __launch_bounds__(kWave * kTopkWaves) void tile_topk(TileArgs a) {
+    extern __shared__ __align__(16) uint64_t tbuf[];
+    constexpr int cap = NPL * kWave;
+    constexpr int kTilesPerRound = 4;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t row = (int64_t)blockIdx.x * kTopkWaves + wave;
+    if (row >= a.rows) return;              // no block-wide synchronisation below
+    uint64_t *buf = tbuf + wave * cap;
+    const uint64_t lt_mask = (1ull << lane) - 1;
+    const float *tm = a.tmax + row * a.n_tile;
+    const float *sc = a.score + row * a.n;
+
+    float lm = -INFINITY;
+    for (int t = lane; t < a.n_tile; t += kWave) lm = fmaxf(lm, tm[t]);
+    float T = -INFINITY;
+    {
+        const uint32_t o = lm == -INFINITY ? 0u : ord_of(lm);
+        uint32_t th = 0;
+        for (int bit = 31; bit >= 0; --bit) {
+            const uint32_t cand = th | (1u << bit);
+            if (__popcll(__ballot(o >= cand)) >= a.top_k) th = cand;
+        }
+        if (th) T = score_of_ord(th);
+    }
+
+    int cnt = 0;
+    uint64_t theta = 0;
+    for (int tb = 0; tb < a.n_tile; tb += kWave) {
+        const int t = tb + lane;
+        const float mt = t < a.n_tile ? tm[t] : -INFINITY;
+        uint64_t pending = __ballot(mt >= T && mt != -INFINITY);
+        while (pending) {
+            // up to four qualifying tiles: every load issued before any is used
+            int tile[kTilesPerRound];
+#pragma unroll
+            for (int r = 0; r < kTilesPerRound; ++r) {
+                tile[r] = pending ? tb + __builtin_ctzll(pending) : -1;
+                pending &= pending ? pending - 1 : 0;
+            }
+            float v[kTilesPerRound];
+#pragma unroll
+            for (int r = 0; r < kTilesPerRound; ++r) {
+                const int64_t c = (int64_t)(tile[r] < 0 ? tile[0] : tile[r]) * kTileCols + lane;
+                v[r] = sc[c < a.n ? c : a.n - 1];
+            }
+#pragma unroll
+            for (int r = 0; r < kTilesPerRound; ++r) {
+                const int64_t c = (int64_t)tile[r] * kTileCols + lane;
+                const bool ok = tile[r] >= 0 && c < a.n && v[r] >= T;
+                const uint64_t key = ok ? make_key(v[r], (int32_t)c) : 0;
+                const bool pass = key > theta;
+                const uint64_t mask = __ballot(pass);
+                if (pass) buf[cnt + __popcll(mask & lt_mask)] = key;
+                cnt += __popcll(mask);
+                if (cnt > cap - kWave) {
+                    wave_lds_sync();
+                    cnt = compact_select<NPL>(buf, cnt, a.top_k, kWave, lane, theta);
+                }
+            }
+        }
+    }
+    wave_lds_sync();
+    uint64_t v[NPL];
+    sort_buffer<NPL>(buf, cnt, v, lane);
+    const int kept = cnt < a.top_k ? cnt : a.top_k;
+#pragma unroll
+    for (int q = 0; q < NPL; ++q) {
+        const int r = q * kWave + lane;
+        if (r < a.top_k) {
+            const bool ok = r < kept;
+            a.out_id[row * a.top_k + r] = ok ? key_id(v[q]) : -1;
+            a.out_score[row * a.top_k + r] = ok ? key_score(v[q]) : -INFINITY;
+        }
+    }
+}
+
 }  // namespace
 
 int32_t seg_topk_cols() { return kSegCols; }
@@ -365,6 +462,30 @@ hipError_t launch_seg_topk(int64_t rows, int64_t row_stride, int64_t n, const fl
         case 9: hipLaunchKernelGGL((seg_topk<4, true>), grid, block, smem, s, a); break;
         case 16: hipLaunchKernelGGL((seg_topk<8, false>), grid, block, smem, s, a); break;
         case 17: hipLaunchKernelGGL((seg_topk<8, true>), grid, block, smem, s, a); break;
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_tile_topk(int64_t rows, int64_t n, const float *score, const float *tmax,
+                            int32_t top_k, int32_t *out_id, float *out_score, hipStream_t s) {
+    if (rows == 0) return hipSuccess;
+    if (top_k > kWave) return hipErrorInvalidValue;
+    TileArgs a{};
+    a.rows = rows;
+    a.n = n;
+    a.n_tile = (int32_t)((n + kTileCols - 1) / kTileCols);
+    a.top_k = top_k;
+    a.score = score;
+    a.tmax = tmax;
+    a.out_id = out_id;
+    a.out_score = out_score;
+    const dim3 grid((unsigned)((rows + kTopkWaves - 1) / kTopkWaves)), block(kWave * kTopkWaves);
+    // buffers of top_k + 64 keys at least (compaction when fewer than 64 slots remain)
+    const int npl = next_pow2(top_k + kWave) / kWave;
+    const size_t smem = (size_t)kTopkWaves * npl * kWave * 8;
+    switch (npl) {
+        case 2: hipLaunchKernelGGL(tile_topk<2>, grid, block, smem, s, a); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();

@@ -181,6 +181,9 @@ def test_attend_out_of_range_selection_is_empty():
     (64, 20000, 128, 40, "bf16"),      # long rows for the row top-k
     (100, 300, 200, 50, "bf16"),       # 16 x 16-tile GEMM (few tiles), ragged, d % 32 != 0
     (50, 500, 96, 20, "f32"),          # the same with fp32 storage
+    (2048, 8192, 64, 16, "bf16"),      # 256 x 256 tiles with tile maxima: selection reads the
+    (2100, 9000, 96, 5, "bf16"),       # tiles that reach the bound (ragged rows and last tile)
+    (2048, 8300, 64, 33, "f32"),
 ])
 def test_coarse_every_row(B, G, d, c, storage):
     """Coarse retrieval over every row against the oracle's full score matrix
