@@ -375,193 +375,14 @@ __device__ int64_t plan_chunks(const PlanArgs &pa, CntOf cnt_of, LenOf len_of, i
     return ch;
 }
 
-// The same plan with the clusters interleaved over the lanes: wave w takes a
-// contiguous range of clusters, 64 at a time, one per lane. Reads and the
-// per-cluster table writes are then coalesced (one thread per contiguous run
-// of clusters made every store instruction touch 64 lines: most of the
-// planner's time on 16,384 clusters). The prefixes are taken per round with
-// DPP wave scans plus a running carry, from each wave's base (the totals of
-// the waves before it); a cluster's place among the last chunks of its
-// bucket comes from ballots. The result is the same plan, table for table.
-template <typename CntOf, typename LenOf>
-__device__ void plan_chunks_wave(const PlanArgs &pa, CntOf cnt_of, LenOf len_of, int64_t *s) {
-    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-    constexpr int waves = kPlanThreads / kWave;
-    static_assert(kItemBuckets == 16, "the bucket bases are scanned by one 16-lane row");
-    constexpr int SW = 4 + kItemBuckets;            // LDS words per wave: totals, bucket counts
-    static_assert(waves * SW <= (waves + 1) * kChunkCands, "planner LDS");
-    const int32_t G = pa.G;
-    const int32_t per = (int32_t)(((int64_t)G + waves * kWave - 1) / (waves * kWave)) * kWave;
-    const int32_t gw0 = min(G, wave * per), gw1 = min(G, gw0 + per);
-    const int lmin = 63 - __builtin_clzll((unsigned long long)pa.chunk_min);   // chunk_min is a power of two
-    auto partials = [&](int i) {
-        int64_t p = 0;
-        for (int32_t g = gw0 + lane; g < gw1; g += kWave) {
-            const int64_t c = cnt_of(g), len = len_of(g);
-            if (c > 0 && len > 0) p += c * ((len + (int64_t(1) << (lmin + i)) - 1) >> (lmin + i));
-        }
-        return p;
-    };
-    // chunk length: the first four candidates in one pass, the rest by bisection
-    constexpr int kFirst = 4;
-    int64_t p4[kFirst];
-#pragma unroll
-    for (int i = 0; i < kFirst; ++i) p4[i] = 0;
-    for (int32_t g = gw0 + lane; g < gw1; g += kWave) {
-        const int64_t c = cnt_of(g), len = len_of(g);
-        if (c > 0 && len > 0) {
-#pragma unroll
-            for (int i = 0; i < kFirst; ++i)
-                p4[i] += c * ((len + (int64_t(1) << (lmin + i)) - 1) >> (lmin + i));
-        }
-    }
-    block_sum_n<kFirst>(p4, s);
-    int cand = -1;
-#pragma unroll
-    for (int i = kFirst - 1; i >= 0; --i)
-        if (p4[i] <= pa.p_cap) cand = i;
-    if (cand < 0) {
-        int lo = kFirst, hi = kChunkCands - 1;     // the answer is in [lo, hi]
-        while (lo < hi) {
-            const int mid = (lo + hi) >> 1;
-            int64_t pm[1] = {partials(mid)};
-            block_sum_n<1>(pm, s);
-            if (pm[0] <= pa.p_cap) hi = mid;
-            else lo = mid + 1;
-        }
-        cand = lo;
-    }
-    const int lch = lmin + cand;
-    const int64_t ch = int64_t(1) << lch;
-    const int64_t kp = pa.kp;
-
-    // Per cluster: v[0] = full items | level-one groups << 32, v[1] =
-    // partials, v[2] = level-one results, v[3] = queries | merge-list entries
-    // << 32 (each total below 2^31); returns the bucket of its last chunk, or
-    // -1 if its chunks are all full-length.
-    auto values = [&](int32_t g, int64_t (&v)[4]) {
-        const int64_t c = cnt_of(g), len = len_of(g);
-        const int64_t nch = (c > 0 && len > 0) ? (len + ch - 1) >> lch : 0;
-        const int64_t nfull = c > 0 ? len >> lch : 0;
-        const int64_t ng = group_count(nch, kp, pa.direct);
-        v[0] = nfull + (ng << 32);
-        v[1] = nch * c;
-        v[2] = ng * c;
-        v[3] = c + ((nch != 1 ? c : 0) << 32);     // empty segments are finished by the merge too
-        return nch > nfull ? item_bucket(len - (nfull << lch), lch, c) : -1;
-    };
-    // this wave's totals, and (lane b) its last chunks in bucket b
-    int64_t tot[4] = {0, 0, 0, 0};
-    int64_t bcnt = 0;
-    for (int32_t gr = gw0; gr < gw1; gr += kWave) {
-        const int32_t g = gr + lane;
-        int64_t v[4] = {0, 0, 0, 0};
-        const int b = g < gw1 ? values(g, v) : -1;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) tot[i] += v[i];
-#pragma unroll
-        for (int bb = 0; bb < kItemBuckets; ++bb) {
-            const uint64_t m = __ballot(b == bb);
-            if (lane == bb) bcnt += __popcll(m);
-        }
-    }
-    __syncthreads();                          // s is free again
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int64_t x = wave_sum64(tot[i]);
-        if (lane == 0) s[wave * SW + i] = x;
-    }
-    if (lane < kItemBuckets) s[wave * SW + 4 + lane] = bcnt;
-    __syncthreads();
-    // bases of this wave (the waves before it) and the totals
-    // (lane w < 16 reads wave w's totals: one row scan per value)
-    int64_t carry[4], grand[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int64_t x = lane < waves ? s[lane * SW + i] : 0;
-        const int64_t incl = row_scan64(x);
-        carry[i] = __shfl(incl - x, wave);
-        grand[i] = __shfl(incl, waves - 1);
-    }
-    int64_t bbase = 0, bgrand = 0;
-    if (lane < kItemBuckets) {
-#pragma unroll 1
-        for (int w = 0; w < waves; ++w) {
-            const int64_t x = s[w * SW + 4 + lane];
-            bbase += w < wave ? x : 0;
-            bgrand += x;
-        }
-    }
-    // items: every full-length chunk first, then the last chunks bucket by
-    // bucket (lanes 0..15, one row, hold the buckets)
-    const int64_t n_full = grand[0] & 0xffffffff;
-    const int64_t bincl = row_scan64(lane < kItemBuckets ? bgrand : 0);
-    int64_t bnext = n_full + bincl - bgrand + bbase;     // lane b: this wave's next item of bucket b
-    const int64_t n_items = n_full + __shfl(bincl, kItemBuckets - 1);
-    const uint64_t lt = (uint64_t(1) << lane) - 1;
-    for (int32_t gr = gw0; gr < gw1; gr += kWave) {
-        const int32_t g = gr + lane;
-        const bool valid = g < gw1;
-        int64_t v[4] = {0, 0, 0, 0};
-        const int b = valid ? values(g, v) : -1;
-        int64_t ex[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int64_t incl = wave_scan64(v[i]);
-            ex[i] = carry[i] + incl - v[i];
-            carry[i] += __shfl(incl, kWave - 1);
-        }
-        int32_t wl = -1;
-#pragma unroll
-        for (int bb = 0; bb < kItemBuckets; ++bb) {
-            const uint64_t m = __ballot(b == bb);
-            if (m) {
-                const int64_t bn = __shfl(bnext, bb);
-                if (b == bb) wl = (int32_t)(bn + __popcll(m & lt));
-                if (lane == bb) bnext += __popcll(m);
-            }
-        }
-        if (valid) {
-            pa.qoff[g] = (int32_t)(ex[3] & 0xffffffff);
-            pa.wstart[g] = (int32_t)(ex[0] & 0xffffffff);
-            pa.wlast[g] = wl;
-            pa.pbase[g] = ex[1];
-            pa.gstart[g] = (int32_t)(ex[0] >> 32);
-            pa.ubase[g] = ex[2];
-            pa.mstart[g] = (int32_t)(ex[3] >> 32);
-        }
-    }
-    if (t == 0) {
-        pa.qoff[G] = (int32_t)(grand[3] & 0xffffffff);
-        pa.wstart[G] = (int32_t)n_full;
-        pa.gstart[G] = (int32_t)(grand[0] >> 32);
-        pa.mstart[G] = (int32_t)(grand[3] >> 32);
-        pa.plan->chunk = ch;
-        pa.plan->n_items = n_items;
-        pa.plan->n_parts = grand[1];
-        pa.plan->n_groups = grand[0] >> 32;
-        pa.plan->n_l1 = grand[2];
-        pa.plan->n_merge = grand[3] >> 32;
-    }
-}
-
-struct GlobalCnt {
-    const int32_t *cnt;
-    __device__ int64_t operator()(int32_t g) const { return cnt[g]; }
-};
 struct LdsCnt {
     const int32_t *cnt;
     __device__ int64_t operator()(int32_t g) const { return cnt[g]; }
 };
-// Segment length of cluster g from the offsets (global or an LDS copy) ...
+// Segment length of cluster g from the offsets (an LDS copy).
 struct OffLen {
     const int64_t *off;
     __device__ int64_t operator()(int32_t g) const { return off[g + 1] - off[g]; }
-};
-// ... or from an LDS table of lengths.
-struct LdsLen {
-    const int32_t *len;
-    __device__ int64_t operator()(int32_t g) const { return len[g]; }
 };
 // Outputs of the fine stage, for pairs the routing finishes itself: a
 // selected cluster id out of range gives an empty slot (no candidates).
@@ -602,57 +423,244 @@ __device__ __forceinline__ void plan_nothing(Plan *plan) {
     plan->bad_off = 1;
 }
 
-// Planning step of the multi-kernel routing. With kStage the clusters'
-// query counts and segment lengths are first staged in LDS (8 bytes per
-// cluster, coalesced loads all in flight together), so that the planning
-// passes over each thread's clusters read LDS instead of waiting on L2 in
-// every iteration; otherwise (too many clusters for the LDS) they read
-// global memory. With malformed offsets the plan is empty and the scatter
-// gives every pair an empty slot.
-constexpr int kStagePer = 16;    // clusters per thread the staged planner loads at once
+// ---- planning step of the multi-kernel routing ------------------------------
+// Three kernels over many blocks of 16 waves; each wave plans a contiguous
+// range of per_wave clusters, 64 at a time, one per lane, so that every
+// per-cluster load and table store is coalesced:
+//   route_plan_partials: each block's sums of the partial results at every
+//       candidate chunk length, and the offsets check;
+//   route_plan_totals: every block sums those and chooses the same chunk
+//       length, then writes its totals of the four scanned values and of the
+//       last chunks in each length bucket;
+//   route_plan_apply: each block's base is the totals of the blocks before
+//       it, each wave's the totals of the waves before it in the block; the
+//       per-cluster prefixes come from DPP wave scans with a running carry,
+//       and a cluster's place among the last chunks of its bucket from
+//       ballots.
+// The plan is the one route_fused makes, table for table.
+constexpr int kPlanSW = 4 + kItemBuckets;    // scanned values, then bucket counts
+constexpr int kMaxPlanBlocks = 64;
 
-template <bool kStage>
-__global__ __launch_bounds__(kPlanThreads) void route_plan(PlanArgs pa, const int32_t *cnt) {
+// Per-cluster values at chunk 2^lch: v[0] = full items | level-one groups
+// << 32, v[1] = partials, v[2] = level-one results, v[3] = queries |
+// merge-list entries << 32 (each total below 2^31); returns the bucket of
+// the cluster's shorter last chunk, or -1 if all its chunks are full-length.
+__device__ __forceinline__ int plan_values(const PlanArgs &pa, int64_t c, int64_t len, int lch,
+                                           int64_t (&v)[4]) {
+    const int64_t ch = int64_t(1) << lch;
+    const int64_t nch = (c > 0 && len > 0) ? (len + ch - 1) >> lch : 0;
+    const int64_t nfull = c > 0 ? len >> lch : 0;
+    const int64_t ng = group_count(nch, pa.kp, pa.direct);
+    v[0] = nfull + (ng << 32);
+    v[1] = nch * c;
+    v[2] = ng * c;
+    v[3] = c + ((nch != 1 ? c : 0) << 32);     // empty segments are finished by the merge too
+    return nch > nfull ? item_bucket(len - (nfull << lch), lch, c) : -1;
+}
+
+__device__ __forceinline__ int32_t plan_wave_start(int32_t per_wave) {
+    return (int32_t)(blockIdx.x * (kPlanThreads / kWave) + (threadIdx.x >> 6)) * per_wave;
+}
+
+// Partial results at chunk chunk_min * 2^i, i < kChunkCands, summed over this
+// block's clusters: part[block][i]. The offsets are checked by every block
+// over its own clusters (off[0] and off[G] by block 0); a failure sets
+// plan->bad_off, which the later kernels read.
+__global__ __launch_bounds__(kPlanThreads) void route_plan_partials(PlanArgs pa, const int32_t *cnt,
+                                                                    int32_t per_wave, int64_t *part) {
     __shared__ int64_t s[(kPlanThreads / kWave + 1) * kChunkCands];
-    extern __shared__ int32_t stage[];
-    if constexpr (kStage) {
-        // every load requested before any is used (G <= kStagePer * threads):
-        // one round trip, and the offsets are checked from the same registers
-        const int t = threadIdx.x;
-        const int32_t G = pa.G;
-        int64_t o0[kStagePer], o1[kStagePer];
-        int32_t c[kStagePer];
+    const int lane = threadIdx.x & 63;
+    const int32_t G = pa.G;
+    const int lmin = 63 - __builtin_clzll((unsigned long long)pa.chunk_min);
+    const int32_t gw0 = min(G, plan_wave_start(per_wave)), gw1 = min(G, gw0 + per_wave);
+    int64_t p[kChunkCands];
 #pragma unroll
-        for (int i = 0; i < kStagePer; ++i) {
-            const int32_t g = min(t + i * kPlanThreads, G - 1);
-            o0[i] = pa.off[g];
-            o1[i] = pa.off[g + 1];
-            c[i] = cnt[g];
+    for (int i = 0; i < kChunkCands; ++i) p[i] = 0;
+    int bad = blockIdx.x == 0 && threadIdx.x == 0 && (pa.off[0] != 0 || pa.off[G] != pa.n_rows);
+    for (int32_t g = gw0 + lane; g < gw1; g += kWave) {
+        const int64_t a0 = pa.off[g], a1 = pa.off[g + 1];
+        bad |= a0 > a1;
+        const int64_t c = cnt[g], len = a1 - a0;
+        if (c > 0 && len > 0) {
+#pragma unroll
+            for (int i = 0; i < kChunkCands; ++i)
+                p[i] += c * ((len + (int64_t(1) << (lmin + i)) - 1) >> (lmin + i));
         }
-        int bad = t == 0 && (o0[0] != 0 || pa.off[G] != pa.n_rows);
+    }
+    if (__syncthreads_or(bad) && threadIdx.x == 0) pa.plan->bad_off = 1;
+    block_sum_n<kChunkCands>(p, s);
+    if (threadIdx.x == 0) {
 #pragma unroll
-        for (int i = 0; i < kStagePer; ++i) bad |= o0[i] > o1[i];
-        if (__syncthreads_or(bad)) {
-            if (t == 0) plan_nothing(pa.plan);
-            return;
+        for (int i = 0; i < kChunkCands; ++i) part[(int64_t)blockIdx.x * kChunkCands + i] = p[i];
+    }
+}
+
+// The chunk length (log2), the same in every block: the smallest candidate
+// whose partials (summed over the blocks) fit in p_cap; the last always fits.
+__device__ __forceinline__ int plan_chunk_log2(const PlanArgs &pa, const int64_t *part, int32_t nb,
+                                               int64_t *s) {
+    const int lmin = 63 - __builtin_clzll((unsigned long long)pa.chunk_min);
+    if (threadIdx.x < kChunkCands) {
+        int64_t sum = 0;
+        for (int32_t b = 0; b < nb; ++b) sum += part[(int64_t)b * kChunkCands + threadIdx.x];
+        s[threadIdx.x] = sum;
+    }
+    __syncthreads();
+    int cand = kChunkCands - 1;
+    for (int i = kChunkCands - 1; i >= 0; --i)
+        if (s[i] <= pa.p_cap) cand = i;
+    __syncthreads();
+    return lmin + cand;
+}
+
+// This wave's totals of the scanned values and (lane b) of its last chunks
+// in bucket b.
+__device__ __forceinline__ void plan_wave_totals(const PlanArgs &pa, const int32_t *cnt, int lch,
+                                                 int32_t gw0, int32_t gw1, int64_t (&tot)[4],
+                                                 int64_t &bcnt) {
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) tot[i] = 0;
+    bcnt = 0;
+    for (int32_t gr = gw0; gr < gw1; gr += kWave) {
+        const int32_t g = gr + lane;
+        int64_t v[4] = {0, 0, 0, 0};
+        const int b = g < gw1 ? plan_values(pa, cnt[g], pa.off[g + 1] - pa.off[g], lch, v) : -1;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) tot[i] += v[i];
+#pragma unroll
+        for (int bb = 0; bb < kItemBuckets; ++bb) {
+            const uint64_t m = __ballot(b == bb);
+            if (lane == bb) bcnt += __popcll(m);
         }
-        int32_t *lcnt = stage, *llen = stage + G;
+    }
+}
+
+// The wave totals of this block into sw[wave][kPlanSW] (LDS).
+__device__ __forceinline__ void plan_block_waves(const PlanArgs &pa, const int32_t *cnt, int lch,
+                                                 int32_t per_wave, int64_t *sw) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int32_t gw0 = min(pa.G, plan_wave_start(per_wave)), gw1 = min(pa.G, gw0 + per_wave);
+    int64_t tot[4], bcnt;
+    plan_wave_totals(pa, cnt, lch, gw0, gw1, tot, bcnt);
 #pragma unroll
-        for (int i = 0; i < kStagePer; ++i) {
-            const int32_t g = t + i * kPlanThreads;
-            if (g < G) {
-                lcnt[g] = c[i];
-                llen[g] = (int32_t)(o1[i] - o0[i]);      // N < 2^31
+    for (int i = 0; i < 4; ++i) {
+        const int64_t x = wave_sum64(tot[i]);
+        if (lane == 0) sw[wave * kPlanSW + i] = x;
+    }
+    if (lane < kItemBuckets) sw[wave * kPlanSW + 4 + lane] = bcnt;
+    __syncthreads();
+}
+
+// This block's totals: tot[block][kPlanSW]; block 0 also stores the chunk.
+__global__ __launch_bounds__(kPlanThreads) void route_plan_totals(PlanArgs pa, const int32_t *cnt,
+                                                                  int32_t per_wave, int32_t nb,
+                                                                  const int64_t *part, int64_t *tot) {
+    __shared__ int64_t s[kChunkCands];
+    __shared__ int64_t sw[(kPlanThreads / kWave) * kPlanSW];
+    if (pa.plan->bad_off) {                    // malformed offsets: no work
+        if (blockIdx.x == 0 && threadIdx.x == 0) plan_nothing(pa.plan);
+        return;
+    }
+    const int lch = plan_chunk_log2(pa, part, nb, s);
+    if (blockIdx.x == 0 && threadIdx.x == 0) pa.plan->chunk = int64_t(1) << lch;
+    plan_block_waves(pa, cnt, lch, per_wave, sw);
+    if (threadIdx.x < kPlanSW) {
+        int64_t x = 0;
+        for (int w = 0; w < kPlanThreads / kWave; ++w) x += sw[w * kPlanSW + threadIdx.x];
+        tot[(int64_t)blockIdx.x * kPlanSW + threadIdx.x] = x;
+    }
+}
+
+// The per-cluster tables and the plan.
+__global__ __launch_bounds__(kPlanThreads) void route_plan_apply(PlanArgs pa, const int32_t *cnt,
+                                                                 int32_t per_wave, int32_t nb,
+                                                                 const int64_t *tot) {
+    constexpr int waves = kPlanThreads / kWave;
+    static_assert(kItemBuckets == 16, "the bucket bases are scanned by one 16-lane row");
+    __shared__ int64_t sw[waves * kPlanSW];
+    __shared__ int64_t sb[2 * kPlanSW];        // this block's base, the totals
+    if (pa.plan->bad_off) return;
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    const int32_t G = pa.G;
+    const int lch = 63 - __builtin_clzll((unsigned long long)pa.plan->chunk);
+    if (t < kPlanSW) {
+        int64_t base = 0, grand = 0;
+        for (int32_t b = 0; b < nb; ++b) {
+            const int64_t x = tot[(int64_t)b * kPlanSW + t];
+            base += b < (int32_t)blockIdx.x ? x : 0;
+            grand += x;
+        }
+        sb[t] = base;
+        sb[kPlanSW + t] = grand;
+    }
+    plan_block_waves(pa, cnt, lch, per_wave, sw);      // ends with a barrier
+    // this wave's base (lane w < 16 reads wave w's totals: one row scan per value)
+    int64_t carry[4], grand[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int64_t x = lane < waves ? sw[lane * kPlanSW + i] : 0;
+        const int64_t incl = row_scan64(x);
+        carry[i] = sb[i] + __shfl(incl - x, wave);
+        grand[i] = sb[kPlanSW + i];
+    }
+    int64_t bbase = 0, bgrand = 0;
+    if (lane < kItemBuckets) {
+        bbase = sb[4 + lane];
+        bgrand = sb[kPlanSW + 4 + lane];
+#pragma unroll 1
+        for (int w = 0; w < wave; ++w) bbase += sw[w * kPlanSW + 4 + lane];
+    }
+    // items: every full-length chunk first, then the last chunks bucket by
+    // bucket (lanes 0..15, one row, hold the buckets)
+    const int64_t n_full = grand[0] & 0xffffffff;
+    const int64_t bincl = row_scan64(lane < kItemBuckets ? bgrand : 0);
+    int64_t bnext = n_full + bincl - bgrand + bbase;     // lane b: this wave's next item of bucket b
+    const int64_t n_items = n_full + __shfl(bincl, kItemBuckets - 1);
+    const uint64_t lt = (uint64_t(1) << lane) - 1;
+    const int32_t gw0 = min(G, plan_wave_start(per_wave)), gw1 = min(G, gw0 + per_wave);
+    for (int32_t gr = gw0; gr < gw1; gr += kWave) {
+        const int32_t g = gr + lane;
+        const bool valid = g < gw1;
+        int64_t v[4] = {0, 0, 0, 0};
+        const int b = valid ? plan_values(pa, cnt[g], pa.off[g + 1] - pa.off[g], lch, v) : -1;
+        int64_t ex[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int64_t incl = wave_scan64(v[i]);
+            ex[i] = carry[i] + incl - v[i];
+            carry[i] += __shfl(incl, kWave - 1);
+        }
+        int32_t wl = -1;
+#pragma unroll
+        for (int bb = 0; bb < kItemBuckets; ++bb) {
+            const uint64_t m = __ballot(b == bb);
+            if (m) {
+                const int64_t bn = __shfl(bnext, bb);
+                if (b == bb) wl = (int32_t)(bn + __popcll(m & lt));
+                if (lane == bb) bnext += __popcll(m);
             }
         }
-        __syncthreads();
-        plan_chunks_wave(pa, LdsCnt{lcnt}, LdsLen{llen}, s);
-    } else {
-        if (offsets_bad(pa.off, pa.G, pa.n_rows)) {
-            if (threadIdx.x == 0) plan_nothing(pa.plan);
-            return;
+        if (valid) {
+            pa.qoff[g] = (int32_t)(ex[3] & 0xffffffff);
+            pa.wstart[g] = (int32_t)(ex[0] & 0xffffffff);
+            pa.wlast[g] = wl;
+            pa.pbase[g] = ex[1];
+            pa.gstart[g] = (int32_t)(ex[0] >> 32);
+            pa.ubase[g] = ex[2];
+            pa.mstart[g] = (int32_t)(ex[3] >> 32);
         }
-        plan_chunks_wave(pa, GlobalCnt{cnt}, OffLen{pa.off}, s);
+    }
+    if (blockIdx.x == 0 && t == 0) {
+        pa.qoff[G] = (int32_t)(grand[3] & 0xffffffff);
+        pa.wstart[G] = (int32_t)n_full;
+        pa.gstart[G] = (int32_t)(grand[0] >> 32);
+        pa.mstart[G] = (int32_t)(grand[3] >> 32);
+        pa.plan->n_items = n_items;
+        pa.plan->n_parts = grand[1];
+        pa.plan->n_groups = grand[0] >> 32;
+        pa.plan->n_l1 = grand[2];
+        pa.plan->n_merge = grand[3] >> 32;
     }
 }
 
@@ -1249,6 +1257,7 @@ AttendWs attend_layout(void *ws, int32_t d, int32_t G, int64_t N, int32_t key_by
     w.pos = cv.take<int32_t>(bc);
     w.bound = cv.take<uint64_t>(bc);
     w.plan = cv.take<Plan>(1);
+    w.ptot = cv.take<int64_t>(kMaxPlanBlocks * (kChunkCands + kPlanSW));
     w.items = cv.take<WorkItem>(w.w_max);
     w.groups = cv.take<MergeGroup>(w.g_max);
     w.pm = cv.take<float>(w.p_cap);
@@ -1400,16 +1409,18 @@ hipError_t launch_attend(int32_t key_dtype, int32_t compute_dtype, int32_t d, in
         hipLaunchKernelGGL(route_init, dim3((G + 255) / 256 < 1024 ? (G + 255) / 256 : 1024),
                            dim3(256), 0, s, G, w.cnt, w.cursor, w.plan);
         hipLaunchKernelGGL(route_count, dim3(gblocks), dim3(256), 0, s, sel, bc, G, w.cnt, w.plan);
-        const size_t stage = (size_t)G * 8;          // query counts and segment lengths
-        if (G <= kStagePer * kPlanThreads && stage + 8 * 1024 <= lds_budget()) {
-            hipError_t e1 = hipFuncSetAttribute((const void *)route_plan<true>,
-                                                hipFuncAttributeMaxDynamicSharedMemorySize,
-                                                (int)stage);
-            if (e1 != hipSuccess) return e1;
-            hipLaunchKernelGGL(route_plan<true>, dim3(1), dim3(kPlanThreads), stage, s, pa, w.cnt);
-        } else {
-            hipLaunchKernelGGL(route_plan<false>, dim3(1), dim3(kPlanThreads), 0, s, pa, w.cnt);
-        }
+        // planning over nb blocks of 16 waves, each wave per_wave clusters
+        const int64_t rounds = ((int64_t)G + kMaxPlanBlocks * kPlanThreads - 1) /
+                               (kMaxPlanBlocks * kPlanThreads);
+        const int32_t per_wave = (int32_t)(rounds * kWave);
+        const int32_t nb = (int32_t)(((int64_t)G + (int64_t)per_wave * (kPlanThreads / kWave) - 1) /
+                                     ((int64_t)per_wave * (kPlanThreads / kWave)));
+        hipLaunchKernelGGL(route_plan_partials, dim3(nb), dim3(kPlanThreads), 0, s, pa, w.cnt,
+                           per_wave, w.ptot);
+        hipLaunchKernelGGL(route_plan_totals, dim3(nb), dim3(kPlanThreads), 0, s, pa, w.cnt,
+                           per_wave, nb, w.ptot, w.ptot + kMaxPlanBlocks * kChunkCands);
+        hipLaunchKernelGGL(route_plan_apply, dim3(nb), dim3(kPlanThreads), 0, s, pa, w.cnt,
+                           per_wave, nb, w.ptot + kMaxPlanBlocks * kChunkCands);
         hipLaunchKernelGGL(route_scatter, dim3(gblocks), dim3(256), 0, s, sel, bc, G, w.qoff,
                            w.cursor, w.qlist, w.pos, w.bound, so, w.plan);
         hipLaunchKernelGGL(route_items, dim3((G + 3) / 4 < 2048 ? (G + 3) / 4 : 2048), dim3(256), 0,

@@ -201,6 +201,7 @@ struct AttendWs {
     int32_t *pos;      // [B*c] position of each entry inside its cluster's list
     uint64_t *bound;   // [B*c] per pair: a key at or below its k-th best, raised as chunks finish
     Plan *plan;
+    int64_t *ptot;     // planner: per-block partial sums and totals
     WorkItem *items;   // [w_max]
     MergeGroup *groups;// [g_max]
     float *pm;         // [p_cap] partial max
