@@ -192,25 +192,37 @@ __global__ __launch_bounds__(kGemmThreads) void coarse_gemm(const __bf16 *__rest
         // Each row's maximum over this wave's 64 columns (a 64-column tile of
         // the score row): over the lane's four columns, then the 16 lanes of
         // its row group (lanes 16 kg .. 16 kg + 15 hold one row's 16-column
-        // slices), by DPP row rotations; no LDS, no barrier.
+        // slices) by DPP row rotations; no LDS, no barrier. Lane r16 of a row
+        // group keeps the maxima of its rows r16 and 16 + r16 (in the order
+        // i * 4 + e), so that the wave stores them in two instructions.
         const int n64 = (G + 63) / 64;
         const int tcol = nt * (BN / 64) + wn;
         if (tcol < n64) {
+            bool ok[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) ok[j] = (int)n0 + wn * 64 + j * 16 + r16 < G;
+            float keep[2] = {-INFINITY, -INFINITY};
 #pragma unroll
             for (int i = 0; i < 8; ++i)
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    float m = -INFINITY;
-#pragma unroll
-                    for (int j = 0; j < 4; ++j)
-                        if (n0 + wn * 64 + j * 16 + r16 < G) m = fmaxf(m, acc[i][j][e]);
+                    float m = fmaxf(fmaxf(ok[0] ? acc[i][0][e] : -INFINITY,
+                                          ok[1] ? acc[i][1][e] : -INFINITY),
+                                    fmaxf(ok[2] ? acc[i][2][e] : -INFINITY,
+                                          ok[3] ? acc[i][3][e] : -INFINITY));
                     m = fmaxf(m, row_ror_f32<8>(m));
                     m = fmaxf(m, row_ror_f32<4>(m));
                     m = fmaxf(m, row_ror_f32<2>(m));
                     m = fmaxf(m, row_ror_f32<1>(m));
-                    const int64_t r = m0 + wm * 128 + i * 16 + 4 * kg + e;
-                    if (r16 == 0 && r < B) tmax[r * n64 + tcol] = m;
+                    const int idx = i * 4 + e;
+                    if ((idx & 15) == r16) keep[idx >> 4] = m;
                 }
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const int idx = 16 * h + r16, i = idx >> 2, e = idx & 3;
+                const int64_t r = m0 + wm * 128 + i * 16 + 4 * kg + e;
+                if (r < B) tmax[r * n64 + tcol] = keep[h];
+            }
         }
     }
 }
