@@ -55,13 +55,20 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
-def kernel_source_sha256() -> str:
-    """Hash of every device and host source of the library (a changed kernel
-    invalidates counter figures taken from an older build)."""
+# Sources of the bank-stream kernels and their launch (counter figures of the
+# stream stay valid while these are unchanged).
+STREAM_SOURCES = ("dev.hpp", "internal.hpp", "stream.hpp", "stream_lds_bf16.hip",
+                  "stream_lds_f32.hip", "stream_generic.hip", "fine.hip")
+
+
+def kernel_source_sha256(names=None) -> str:
+    """Hash of the library's device and host sources (all of them, or the
+    named files): a changed kernel invalidates counter figures taken from an
+    older build."""
     csrc = os.path.join(ROOT, "paper_2605_29734_amd", "csrc")
     h = hashlib.sha256()
     for name in sorted(os.listdir(csrc)):
-        if name.endswith((".hip", ".hpp", ".cpp", ".h")):
+        if name.endswith((".hip", ".hpp", ".cpp", ".h")) and (names is None or name in names):
             h.update(name.encode())
             h.update(open(os.path.join(csrc, name), "rb").read())
     return h.hexdigest()
@@ -71,13 +78,13 @@ def stream_kernel_traffic(workload: str):
     """Measured HBM bytes per launch of the bank-stream kernel (FETCH_SIZE +
     WRITE_SIZE, scaled by the same counters' reading for a plain copy of known
     size) from the committed rocprofv3 counter summary; None unless that
-    summary was taken from the current kernel sources."""
+    summary was taken from the current sources of the stream kernels."""
     path = os.path.join(ROOT, "profiles", "fine_stream_traffic.json")
     if not os.path.exists(path):
         return None
     try:
         rec = json.load(open(path))
-        if rec.get("source_sha256") != kernel_source_sha256():
+        if rec.get("source_sha256") != kernel_source_sha256(STREAM_SOURCES):
             return None
         return rec.get("workloads", {}).get(workload, {}).get("bytes_per_launch")
     except (OSError, ValueError, AttributeError):
