@@ -1230,8 +1230,6 @@ static size_t lds_budget() {
 
 AttendWs attend_layout(void *ws, int32_t d, int32_t G, int64_t N, int32_t key_bytes, int32_t B,
                        int32_t c, int32_t k, size_t *bytes) {
-    (void)d;
-    (void)key_bytes;
     AttendWs w{};
     Carve cv(ws);
     const int64_t bc = (int64_t)B * c;
@@ -1268,6 +1266,7 @@ AttendWs attend_layout(void *ws, int32_t d, int32_t G, int64_t N, int32_t key_by
     w.uz = cv.take<float>(w.u_cap);
     w.uc = cv.take<int32_t>(w.u_cap);
     w.uk = cv.take<uint64_t>(w.u_cap * k);
+    w.q16 = key_bytes == 4 ? cv.take<__bf16>((int64_t)B * d) : nullptr;
     if (bytes) *bytes = cv.off + 256;
     return w;
 }
@@ -1282,9 +1281,17 @@ static int qmax_for_load(int qmax, int64_t bc, int32_t G) {
     return want < qmax ? want : qmax;
 }
 
+// fp32 queries rounded to bf16 (to nearest even, as the LDS staging rounds
+// them), 8 elements per thread.
+__global__ void queries_to_bf16(const float *__restrict__ q, __bf16 *__restrict__ y, int64_t n8) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n8;
+         i += (int64_t)gridDim.x * blockDim.x)
+        reinterpret_cast<bf16x8_t *>(y)[i] = load8(q + i * 8);
+}
+
 static hipError_t launch_stream(int32_t key_dtype, int32_t compute_dtype, const FineArgs &fa0,
                                 int64_t bc, int64_t n_rows, int n_cu, int64_t w_max,
-                                KernelEvents ev, hipStream_t s) {
+                                int32_t B, __bf16 *q16, KernelEvents ev, hipStream_t s) {
     const size_t budget = lds_budget();
     const int npl = fa0.cap / kWave;
     StreamLaunch l{};
@@ -1315,6 +1322,15 @@ static hipError_t launch_stream(int32_t key_dtype, int32_t compute_dtype, const 
             const int32_t qs_half = (int32_t)fine_qs_bytes(fa0.d / 2, 16);
             const size_t sm2 = qs_half + fine_state_bytes(16, fa0.cap, 2);
             if (2 * (sm2 + 256) <= budget + 256) {
+                if (key_dtype == kF32) {
+                    // every half of every row group stages its queries: from a
+                    // bf16 copy, half the bytes and one round trip
+                    const int64_t n8 = (int64_t)B * fa0.d / 8;
+                    const int64_t nb = (n8 + 255) / 256;
+                    hipLaunchKernelGGL(queries_to_bf16, dim3((unsigned)(nb < 4096 ? nb : 4096)),
+                                       dim3(256), 0, s, static_cast<const float *>(fa0.q), q16, n8);
+                    l.fa.q16 = q16;
+                }
                 l.ksplit = true;
                 l.fa.ntile = 2;
                 l.qs_bytes = qs_half;
@@ -1453,7 +1469,7 @@ hipError_t launch_attend(int32_t key_dtype, int32_t compute_dtype, int32_t d, in
     fa.slot_sum = slot_sum;
     fa.cand_score = cand_score;
     fa.cand_id = cand_id;
-    err = launch_stream(key_dtype, compute_dtype, fa, bc, N, n_cu, w.w_max, ev, s);
+    err = launch_stream(key_dtype, compute_dtype, fa, bc, N, n_cu, w.w_max, B, w.q16, ev, s);
     if (err != hipSuccess) return err;
 
     MergeArgs ma{};

@@ -211,6 +211,7 @@ struct AttendWs {
     float *um, *uz;    // [u_cap] level-one merge results, same form as the partials
     int32_t *uc;
     uint64_t *uk;      // [u_cap][k]
+    __bf16 *q16;       // [B][d] the queries rounded to bf16 (fp32 keys; the split stream kernel)
     int64_t p_cap;     // partial results the workspace holds (>= B*c)
     int64_t w_max;     // bound on work items
     int64_t g_max;     // bound on level-one groups

@@ -54,6 +54,8 @@ struct FineArgs {
     const int32_t *tid;           // caller ids, or NULL: ids are bank rows
     const int32_t *tid_src;       // tid, or (when NULL) any readable array of >= N ints
     const void *q;
+    const __bf16 *q16;            // the queries rounded to bf16 ([B][d]) when the split
+                                  // kernel streams fp32 keys, else NULL
     int32_t d, c, G, k, cap, qmax;
     int32_t ntile;                // score tiles in LDS (1 or 2)
     float cexp;                   // log2(e) / tau
@@ -989,7 +991,10 @@ __device__ __forceinline__ void pass_split(const FineArgs &a, const FineSmem &sm
     const int t = threadIdx.x;
     const int d = a.d;
     const KT *__restrict__ K = static_cast<const KT *>(a.keys);
-    const KT *__restrict__ Q = static_cast<const KT *>(a.q);
+    // the queries in bf16: fp32 ones were rounded once per call (as the
+    // staging would round them), so each half is staged in one round trip
+    const __bf16 *__restrict__ Q =
+        sizeof(KT) == 4 ? a.q16 : reinterpret_cast<const __bf16 *>(a.q);
     const int KH = d >> 6;             // k-steps per half of d
     const int NGH = KH / U;            // units per step and half
     const int T = (int)((r1 - r0 + kRowsPerStep - 1) / kRowsPerStep);
@@ -1010,16 +1015,13 @@ __device__ __forceinline__ void pass_split(const FineArgs &a, const FineSmem &sm
             const int k0 = h * KH;
             const int total = Tg * NGH;
             LoadUnit<KT, U> ring[R];
-#pragma unroll
-            for (int j = 0; j < R - 1; ++j)
-                split_load_unit<KT, U>(ring[j], K, a.tid_src, d, NGH, k0, min(j, total - 1), g0, r1);
-            // every wave is done with the fragments of the previous half
-            block_lds_barrier();
             // this half's query fragments: [k-step][query tile][lane], as in
-            // the full staging (padding columns zeroed at the store); fp32
-            // queries in batches of four fragments (registers)
+            // the full staging (padding columns zeroed at the store). The
+            // ring's first units are requested behind the first batch, so that
+            // the staging waits for its own loads only, and the barrier after
+            // it waits for LDS only: the key loads stay in flight.
             {
-                constexpr int kBatch = sizeof(KT) == 4 ? 4 : 8;
+                constexpr int kBatch = 8;
                 const int nfrag = KH * NQT * kWave;
                 const int nt = blockDim.x;
                 for (int i0 = t; i0 < nfrag; i0 += nt * kBatch) {
@@ -1032,6 +1034,14 @@ __device__ __forceinline__ void pass_split(const FineArgs &a, const FineSmem &sm
                         const int n = qt * 16 + (ln & 15), k = 32 * (k0 + s2) + 8 * (ln >> 4);
                         f[b] = load8(Q + (int64_t)sm.qrow[n < nqg ? n : 0] * d + k);
                     }
+                    if (i0 == t) {
+#pragma unroll
+                        for (int j = 0; j < R - 1; ++j)
+                            split_load_unit<KT, U>(ring[j], K, a.tid_src, d, NGH, k0,
+                                                   min(j, total - 1), g0, r1);
+                        // every wave is done with the fragments of the previous half
+                        block_lds_barrier();
+                    }
 #pragma unroll
                     for (int b = 0; b < kBatch; ++b) {
                         const int idx = min(i0 + b * nt, nfrag - 1);
@@ -1042,8 +1052,7 @@ __device__ __forceinline__ void pass_split(const FineArgs &a, const FineSmem &sm
                 }
             }
             if (tg == 0 && h == 0) pass_bound(sm, pb);
-            wait_vmcnt<0>();
-            __syncthreads();
+            block_lds_barrier();
             if (tg == 0 && h == 0) owned_begin<NQT>(sm, nqg, o);
             f32x4_t acc[NQT];
 #pragma unroll
