@@ -1281,6 +1281,7 @@ static int qmax_for_load(int qmax, int64_t bc, int32_t G) {
     return want < qmax ? want : qmax;
 }
 
+namespace {
 // fp32 queries rounded to bf16 (to nearest even, as the LDS staging rounds
 // them), 8 elements per thread.
 __global__ void queries_to_bf16(const float *__restrict__ q, __bf16 *__restrict__ y, int64_t n8) {
@@ -1288,6 +1289,7 @@ __global__ void queries_to_bf16(const float *__restrict__ q, __bf16 *__restrict_
          i += (int64_t)gridDim.x * blockDim.x)
         reinterpret_cast<bf16x8_t *>(y)[i] = load8(q + i * 8);
 }
+}  // namespace
 
 static hipError_t launch_stream(int32_t key_dtype, int32_t compute_dtype, const FineArgs &fa0,
                                 int64_t bc, int64_t n_rows, int n_cu, int64_t w_max,
