@@ -12,6 +12,8 @@ d = 2,048 against 16,384 clusters and 4,194,304 fp32 records (a 34 GB bank,
 far beyond the last-level cache, so every step streams it from HBM). A bank
 that would fit the 256 MB last-level cache is timed over copies of itself
 that together exceed 1 GiB, one per step in turn (--no-rotate: one bank).
+The bank also carries its keys in the tiled order that the bank stream reads
+(htam_memory_tile, built with the bank, untimed; --no-tiled: row-major only).
 
 Prints one JSON line: queries/s for the workload (whole timed region), the
 roofline position of the dominant kernel (the bank stream, HBM-bound),
@@ -371,6 +373,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-rotate", action="store_true",
                     help="time one bank even when it fits the last-level cache")
+    ap.add_argument("--no-tiled", action="store_true",
+                    help="stream the row-major keys only (no tiled copy)")
     ap.add_argument("--event-every", type=int, default=4, metavar="E",
                     help="stamp the kernel and stage timing events on every E-th timed step")
     ap.add_argument("--path", default="hierarchical",
@@ -431,6 +435,13 @@ def main():
                       for _ in range(n_copies - 1)]
     if n_copies > 1:
         log(f"[bench] rotating over {n_copies} copies of the {bank_bytes / 2**20:.0f} MiB bank")
+    # the keys also in the tiled order of htam_memory_tile (built with the
+    # bank, untimed): the bank stream reads 1 KB of consecutive bytes per load
+    tiled = not args.no_tiled and spec.d % 32 == 0
+    if tiled:
+        banks = [htam.with_tiled_keys(b) for b in banks]
+        torch.cuda.synchronize()
+    r.bank = banks[0]
     log(f"[bench] warmup {args.warmup}")
     for i in range(max(args.warmup, n_copies)):
         r.bank = banks[i % n_copies]
@@ -524,7 +535,8 @@ def main():
         "config": {"workload": spec.name, "queries": spec.B, "d": spec.d, "clusters": spec.G,
                    "transitions": spec.N, "top_c": spec.top_c, "top_k": spec.top_k,
                    "tau": spec.tau, "key_storage": spec.storage,
-                   "bank_bytes": int(spec.N * spec.d * kb), "bank_copies": n_copies},
+                   "bank_bytes": int(spec.N * spec.d * kb), "bank_copies": n_copies,
+                   "tiled_keys": tiled},
         "roofline": {"bound": "hbm", "kernel": "fine_stream", "achieved": achieved,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "traffic": stream_kernel_traffic(spec.name),

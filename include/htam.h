@@ -97,6 +97,12 @@ typedef enum {
  *   transition_id  [N] int32 caller id of each row of fine_keys, or NULL for
  *                  the row index itself. Outputs report these ids, and ties
  *                  between equal scores go to the lower id.
+ *   fine_keys_tiled  NULL, or the copy written by htam_memory_tile for this
+ *                  bank (fine_keys and seg_offsets as they are now): an
+ *                  optional second copy of the keys that the bank stream of
+ *                  htam_attend_transitions reads instead of fine_keys where
+ *                  it can; results are identical either way. Requires
+ *                  d % 32 == 0; 16-byte aligned.
  */
 typedef struct htam_bank {
     int32_t d;
@@ -108,6 +114,7 @@ typedef struct htam_bank {
     const void *fine_keys;
     const int64_t *seg_offsets;
     const int32_t *transition_id;
+    const void *fine_keys_tiled;
 } htam_bank;
 
 /*
@@ -142,6 +149,36 @@ htam_status htam_memory_build(int64_t n, int32_t n_clusters, int32_t d, int32_t 
                               int64_t *seg_offsets, int32_t *transition_id, void *ws,
                               size_t ws_bytes, hipStream_t stream);
 size_t htam_memory_build_workspace_size(int64_t n, int32_t n_clusters);
+
+/*
+ * htam_memory_tile -- a copy of a bank's fine keys in the order the bank
+ * stream reads them (Eq. local policy scores every child of a selected
+ * cluster; this only changes where each key element is stored).
+ *
+ * The copy starts with a header of G + 1 int64: toff[g], the copy's row of
+ * segment g's first record (each segment padded to a multiple of 16 rows, so
+ * toff[g] % 16 == 0 and toff[G] is the padded total), the header padded to a
+ * multiple of 256 bytes. Then come the rows of the copy in tiles of 16, d cut
+ * into steps of 32: block (tile t, step s) holds copy rows 16 t .. 16 t + 15,
+ * elements 32 s .. 32 s + 31, at element offset (t * d / 32 + s) * 512 after
+ * the header. Inside a block, element 32 s + 8 c + e of copy row 16 t + i
+ * (c < 4, e < 8) sits at ((e / P) * 64 + c * 16 + i) * P + e % P, P = 16 /
+ * element bytes (4 for fp32, 8 for bf16): the 16-byte pieces of one
+ * matrix-core operand load of 16 rows lie next to each other, so a wave's
+ * load instruction reads 1 KB of consecutive bytes instead of 16 pieces of
+ * 16 rows. Copy row toff[g] + j holds bank row seg_offsets[g] + j (j below
+ * the segment's length); padding rows are zero.
+ *
+ *   bank         a bank with fine_keys (key_dtype HTAM_F32 or HTAM_BF16),
+ *                d % 32 == 0 and valid seg_offsets; its fine_keys_tiled is
+ *                ignored.
+ *   tiled_out    htam_memory_tile_bytes(bank) bytes (an upper bound:
+ *                N / 16 + G tiles), 16-byte aligned, not overlapping
+ *                fine_keys; receives the copy.
+ * Asynchronous on stream; allocates nothing.
+ */
+htam_status htam_memory_tile(const htam_bank *bank, void *tiled_out, hipStream_t stream);
+size_t htam_memory_tile_bytes(const htam_bank *bank);
 
 /*
  * htam_memory_merge -- online memory update, record side: fold a delta bank

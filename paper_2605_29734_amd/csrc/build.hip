@@ -137,7 +137,92 @@ __global__ void build_gather(const uint4 *keys_in, uint4 *keys_out, const int32_
     }
 }
 
+// The tiled copy of the keys (htam_memory_tile). Its header holds each
+// segment's first row in the copy, toff[g]: segments padded to multiples of
+// 16 rows, so that every segment, and every chunk of one (chunks are
+// multiples of 64 rows), starts on a tile.
+__global__ __launch_bounds__(kScanThreads) void tile_offsets(const int64_t *off, int32_t G,
+                                                             int64_t *toff) {
+    __shared__ int64_t s[kScanThreads];
+    const int t = threadIdx.x;
+    const int32_t per = (G + kScanThreads - 1) / kScanThreads;
+    const int32_t g0 = min(G, t * per), g1 = min(G, g0 + per);
+    int64_t local = 0;
+    for (int32_t g = g0; g < g1; ++g) local += (off[g + 1] - off[g] + 15) & ~int64_t(15);
+    s[t] = local;
+    __syncthreads();
+    for (int o = 1; o < kScanThreads; o <<= 1) {
+        const int64_t x = t >= o ? s[t - o] : 0;
+        __syncthreads();
+        s[t] += x;
+        __syncthreads();
+    }
+    int64_t run = s[t] - local;
+    for (int32_t g = g0; g < g1; ++g) {
+        toff[g] = run;
+        run += (off[g + 1] - off[g] + 15) & ~int64_t(15);
+    }
+    if (t == kScanThreads - 1) toff[G] = s[t];
+}
+
+// One block per tile of the copy (the grid is an upper bound on the tiles;
+// blocks past toff[G] / 16 return). The tile's segment g is found once, by
+// binary search over toff; then every 16-byte piece of the tile, in the
+// copy's order: piece w of block (tile, step) (`parts` pieces per 8-element
+// fragment) is part h = w / 64 of the fragment of group c = (w / 16) % 4 of
+// the tile's row i = w % 16, read from bank row off[g] + 16 tile + i -
+// toff[g] of the row-major keys, or zero past the segment's end.
+__global__ __launch_bounds__(256) void tile_keys(const uint4 *__restrict__ keys,
+                                                 const int64_t *__restrict__ off,
+                                                 const int64_t *__restrict__ toff, int32_t G,
+                                                 int32_t steps, int32_t parts,
+                                                 uint4 *__restrict__ tiles) {
+    __shared__ int32_t s_g;
+    const int64_t tile = blockIdx.x;
+    const int64_t row0 = tile * 16;
+    if (row0 >= toff[G]) return;                 // uniform across the block
+    if (threadIdx.x == 0) {
+        int32_t lo = 0, hi = G - 1;              // last g with toff[g] <= row0
+        while (lo < hi) {
+            const int32_t mid = (lo + hi + 1) >> 1;
+            if (toff[mid] <= row0) lo = mid; else hi = mid - 1;
+        }
+        s_g = lo;
+    }
+    __syncthreads();
+    const int32_t g = s_g;
+    const int64_t j0 = row0 - toff[g], len = off[g + 1] - off[g], src0 = off[g];
+    const int64_t per_block = (int64_t)parts * 64, per_row = (int64_t)steps * 4 * parts;
+    const int64_t n = (int64_t)steps * per_block;
+    uint4 *out = tiles + tile * n;
+    for (int64_t p = threadIdx.x; p < n; p += blockDim.x) {
+        const int64_t st = p / per_block;
+        const int w = (int)(p - st * per_block);
+        const int h = w >> 6, c = (w >> 4) & 3, i = w & 15;
+        const int64_t j = j0 + i;
+        uint4 v = make_uint4(0u, 0u, 0u, 0u);
+        if (j < len) v = keys[(src0 + j) * per_row + st * 4 * parts + c * parts + h];
+        out[p] = v;
+    }
+}
+
 }  // namespace
+
+size_t tile_header_bytes(int32_t G) { return ((size_t)(G + 1) * 8 + 255) / 256 * 256; }
+
+hipError_t launch_tile_keys(int64_t n_rows, int32_t G, int32_t d, int32_t elem_bytes,
+                            const void *keys, const int64_t *seg_offsets, void *out,
+                            hipStream_t s) {
+    int64_t *toff = static_cast<int64_t *>(out);
+    uint4 *tiles = reinterpret_cast<uint4 *>(static_cast<char *>(out) + tile_header_bytes(G));
+    hipLaunchKernelGGL(tile_offsets, dim3(1), dim3(kScanThreads), 0, s, seg_offsets, G, toff);
+    const int64_t max_tiles = (n_rows + 15) / 16 + G;
+    if (n_rows > 0)
+        hipLaunchKernelGGL(tile_keys, dim3((unsigned)max_tiles), dim3(256), 0, s,
+                           static_cast<const uint4 *>(keys), seg_offsets, toff, G, d / 32,
+                           elem_bytes == 4 ? 2 : 1, tiles);
+    return hipGetLastError();
+}
 
 BuildWs build_layout(void *ws, int64_t n, int32_t G, size_t *bytes) {
     Carve cv(ws);

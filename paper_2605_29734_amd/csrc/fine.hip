@@ -1382,7 +1382,8 @@ static hipError_t launch_merge(const MergeArgs &ma, int64_t u_cap, bool groups, 
 }
 
 hipError_t launch_attend(int32_t key_dtype, int32_t compute_dtype, int32_t d, int32_t G, int64_t N,
-                         const void *fine_keys, const int64_t *seg_offsets,
+                         const void *fine_keys, const void *fine_keys_tiled,
+                         const int64_t *seg_offsets,
                          const int32_t *transition_id, const void *q, int32_t B,
                          const int32_t *sel, int32_t c, float tau, int32_t k, float *slot_max,
                          float *slot_sum, float *cand_score, int32_t *cand_id, const AttendWs &w,
@@ -1449,6 +1450,11 @@ hipError_t launch_attend(int32_t key_dtype, int32_t compute_dtype, int32_t d, in
 
     FineArgs fa{};
     fa.keys = fine_keys;
+    if (fine_keys_tiled) {          // the header of segment starts, then the tiles
+        fa.toff = static_cast<const int64_t *>(fine_keys_tiled);
+        fa.keys_tiled = static_cast<const char *>(fine_keys_tiled) + tile_header_bytes(G);
+        fa.seg_off = seg_offsets;
+    }
     fa.tid = transition_id;
     // without ids the id loads read the key array (at least N ints) and are ignored
     fa.tid_src = transition_id ? transition_id : static_cast<const int32_t *>(fine_keys);

@@ -60,8 +60,10 @@ htam_status check_bank(const htam_bank *b) {
     if (!b->coarse_keys) return fail(HTAM_ERR_NULL, "bank->coarse_keys is NULL");
     if (!b->seg_offsets) return fail(HTAM_ERR_NULL, "bank->seg_offsets is NULL");
     if (b->n_transitions > 0 && !b->fine_keys) return fail(HTAM_ERR_NULL, "bank->fine_keys is NULL");
-    if (!aligned16(b->coarse_keys) || !aligned16(b->fine_keys))
+    if (!aligned16(b->coarse_keys) || !aligned16(b->fine_keys) || !aligned16(b->fine_keys_tiled))
         return fail(HTAM_ERR_ALIGN, "bank key arrays must be 16-byte aligned");
+    if (b->fine_keys_tiled && b->d % 32 != 0)
+        return fail(HTAM_ERR_SHAPE, "bank->fine_keys_tiled needs d %% 32 == 0 (d = %d)", b->d);
     return HTAM_OK;
 }
 
@@ -170,6 +172,36 @@ HTAM_API htam_status htam_memory_build(int64_t n, int32_t n_clusters, int32_t d,
 }
 
 // ---------------------------------------------------------------------------
+HTAM_API size_t htam_memory_tile_bytes(const htam_bank *bank) {
+    if (!bank || bank->d < 32 || bank->d > HTAM_MAX_DIM || bank->d % 32 != 0 ||
+        bank->n_transitions < 0 || !valid_dtype(bank->key_dtype))
+        return 0;
+    if (bank->n_clusters < 1) return 0;
+    // the header, then at most N / 16 + G tiles (each segment padded to 16 rows)
+    const size_t tiles = (size_t)((bank->n_transitions + 15) / 16) + (size_t)bank->n_clusters;
+    return htam::tile_header_bytes(bank->n_clusters) +
+           tiles * 16 * bank->d * dtype_bytes(bank->key_dtype);
+}
+
+HTAM_API htam_status htam_memory_tile(const htam_bank *bank, void *tiled_out, hipStream_t stream) {
+    if (!bank) return fail(HTAM_ERR_NULL, "bank is NULL");
+    htam_bank b = *bank;
+    b.fine_keys_tiled = nullptr;               // ignored here
+    HTAM_TRY(check_bank(&b));
+    if (b.d % 32 != 0) return fail(HTAM_ERR_SHAPE, "d = %d: the tiled copy needs d %% 32 == 0", b.d);
+    if (!tiled_out) return fail(HTAM_ERR_NULL, "tiled_out is NULL");
+    if (!aligned16(tiled_out)) return fail(HTAM_ERR_ALIGN, "tiled_out must be 16-byte aligned");
+    const size_t in_bytes = (size_t)b.n_transitions * b.d * dtype_bytes(b.key_dtype);
+    const char *a = static_cast<const char *>(b.fine_keys), *o = static_cast<const char *>(tiled_out);
+    if (a < o + htam_memory_tile_bytes(&b) && o < a + in_bytes)
+        return fail(HTAM_ERR_VALUE, "tiled_out overlaps bank->fine_keys");
+    return device_status(htam::launch_tile_keys(b.n_transitions, b.n_clusters, b.d,
+                                                dtype_bytes(b.key_dtype), b.fine_keys,
+                                                b.seg_offsets, tiled_out, stream),
+                         "htam_memory_tile");
+}
+
+// ---------------------------------------------------------------------------
 HTAM_API size_t htam_retrieve_coarse_workspace_size(const htam_bank *bank, int32_t n_queries,
                                                     int32_t top_c) {
     if (!bank || n_queries < 0 || bank->n_clusters < 1 || top_c < 1) return 0;
@@ -242,8 +274,9 @@ HTAM_API htam_status htam_attend_transitions(const htam_bank *bank, const void *
                             dtype_bytes(bank->key_dtype), n_queries, top_c, top_k, nullptr);
     const htam_status st = device_status(
         htam::launch_attend(bank->key_dtype, bank->compute_dtype, bank->d, bank->n_clusters,
-                            bank->n_transitions, bank->fine_keys, bank->seg_offsets,
-                            bank->transition_id, q, n_queries, sel_cluster, top_c, tau, top_k,
+                            bank->n_transitions, bank->fine_keys, bank->fine_keys_tiled,
+                            bank->seg_offsets, bank->transition_id, q, n_queries, sel_cluster,
+                            top_c, tau, top_k,
                             slot_max, slot_sum, cand_score, cand_id, w, n_cu,
                             g_events[HTAM_KERNEL_STREAM], stream),
         "htam_attend_transitions");

@@ -100,6 +100,12 @@ struct BuildWs {
     int32_t *err;      // [1] count of out-of-range cluster ids
 };
 BuildWs build_layout(void *ws, int64_t n, int32_t G, size_t *bytes);
+// The tiled copy of a bank's fine keys (d % 32 == 0): a header of G + 1
+// int64 segment starts in the copy (tile_header_bytes), then the tiles.
+size_t tile_header_bytes(int32_t G);
+hipError_t launch_tile_keys(int64_t n_rows, int32_t G, int32_t d, int32_t elem_bytes,
+                            const void *keys, const int64_t *seg_offsets, void *out,
+                            hipStream_t s);
 hipError_t launch_build(int64_t n, int32_t G, int32_t row_bytes, const int32_t *cluster_of,
                         const void *keys_in, void *keys_out, int64_t *seg_offsets,
                         int32_t *transition_id, const BuildWs &w, hipStream_t s);
@@ -221,7 +227,8 @@ struct AttendWs {
 AttendWs attend_layout(void *ws, int32_t d, int32_t G, int64_t N, int32_t key_bytes, int32_t B,
                        int32_t c, int32_t k, size_t *bytes);
 hipError_t launch_attend(int32_t key_dtype, int32_t compute_dtype, int32_t d, int32_t G,
-                         int64_t N, const void *fine_keys, const int64_t *seg_offsets,
+                         int64_t N, const void *fine_keys, const void *fine_keys_tiled,
+                         const int64_t *seg_offsets,
                          const int32_t *transition_id, const void *q, int32_t B,
                          const int32_t *sel, int32_t c, float tau, int32_t k, float *slot_max,
                          float *slot_sum, float *cand_score, int32_t *cand_id, const AttendWs &w,

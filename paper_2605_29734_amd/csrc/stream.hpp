@@ -51,6 +51,9 @@ constexpr int kRing = 3;               // key load units in the LDS kernel's pre
 
 struct FineArgs {
     const void *keys;
+    const void *keys_tiled;       // the tiles of the keys' tiled copy, or NULL (split kernel)
+    const int64_t *toff;          // the tiled copy's segment starts (its header)
+    const int64_t *seg_off;       // the bank's segment offsets
     const int32_t *tid;           // caller ids, or NULL: ids are bank rows
     const int32_t *tid_src;       // tid, or (when NULL) any readable array of >= N ints
     const void *q;
@@ -610,6 +613,8 @@ struct AFrag<__bf16> {
     static constexpr int U = 16;   // k-steps per load unit (one-block-per-CU kernels): 16 x 16 B per lane
     uint4 v;
     __device__ __forceinline__ void load(const __bf16 *p) { v = *reinterpret_cast<const uint4 *>(p); }
+    // in the tiled copy a fragment is one 16-byte piece
+    __device__ __forceinline__ void load_tiled(const __bf16 *p) { load(p); }
     __device__ __forceinline__ bf16x8_t bf16() const { return __builtin_bit_cast(bf16x8_t, v); }
 };
 template <>
@@ -619,6 +624,11 @@ struct AFrag<float> {
     __device__ __forceinline__ void load(const float *p) {
         lo = reinterpret_cast<const float4 *>(p)[0];
         hi = reinterpret_cast<const float4 *>(p)[1];
+    }
+    // in the tiled copy the fragment's second piece is 64 pieces after the first
+    __device__ __forceinline__ void load_tiled(const float *p) {
+        lo = reinterpret_cast<const float4 *>(p)[0];
+        hi = reinterpret_cast<const float4 *>(p)[64];
     }
     __device__ __forceinline__ bf16x8_t bf16() const {
         bf16x8_t r;
@@ -817,7 +827,7 @@ __device__ __forceinline__ void pass_lds(const FineArgs &a, const FineSmem &sm, 
 // ends; the queries of an item in passes of at most qmax.
 struct ItemPass {
     int64_t p0, r0, r1;
-    int32_t qbeg, nq;
+    int32_t qbeg, nq, g;
     bool single;
 };
 
@@ -828,6 +838,7 @@ __device__ __forceinline__ ItemPass item_pass(const WorkItem &wi) {
     it.r1 = wi.r0 + wi.len;
     it.qbeg = wi.qbeg;
     it.nq = wi.nq;
+    it.g = wi.g;
     // passes over one item cover disjoint queries, so a single-chunk item's results are final
     it.single = wi.single != 0;
     return it;
@@ -920,29 +931,43 @@ constexpr int kSplitSteps = 4;
 
 // Unit u of a half (NGH units of U k-steps per step, k-steps from k0) of the
 // row group starting at bank row g0: loads clamped into the chunk.
-template <typename KT, int U>
+template <typename KT, int U, bool TILED>
 __device__ __forceinline__ void split_load_unit(LoadUnit<KT, U> &lu, const KT *__restrict__ K,
                                                 const int32_t *__restrict__ tid_src, int d,
-                                                int NGH, int k0, int u, int64_t g0, int64_t r1) {
+                                                int NGH, int k0, int u, int64_t g0, int64_t r1,
+                                                int64_t shift) {
     const int lane = threadIdx.x & 63, wave = fine_wave(), r16 = lane & 15, kg = lane >> 4;
     const int tt = u / NGH, gi = u - tt * NGH;
     const int64_t base = g0 + (int64_t)tt * kRowsPerStep;
     const int64_t row = min(base + wave * kRowsPerWave + r16, r1 - 1);
-    const KT *kp = K + row * d + 32 * (k0 + U * gi) + 8 * kg;
+    const int ks0 = k0 + U * gi;
+    if constexpr (TILED) {
+        // K is the tiled copy, where bank row r of this segment is row r +
+        // shift (a segment starts on a tile, and so does a wave's 16 rows):
+        // block (row / 16, k-step) of 512 elements, this lane's first piece
+        // at (kg * 16 + row % 16) * P, P = 16 / element bytes
+        constexpr int P = 16 / (int)sizeof(KT);
+        const int64_t tr = row + shift;
+        const KT *kp = K + ((tr >> 4) * (d >> 5) + ks0) * 512 + (kg * 16 + (int)(tr & 15)) * P;
 #pragma unroll
-    for (int uu = 0; uu < U; ++uu) lu.f[uu].load(kp + 32 * uu);
+        for (int uu = 0; uu < U; ++uu) lu.f[uu].load_tiled(kp + 512 * uu);
+    } else {
+        const KT *kp = K + row * d + 32 * ks0 + 8 * kg;
+#pragma unroll
+        for (int uu = 0; uu < U; ++uu) lu.f[uu].load(kp + 32 * uu);
+    }
     lu.tid = step_tid_load(tid_src, base, r1);
 }
 
 // Multiplies unit u (in lu) of half h and requests unit nu into nx. A step
 // starts from zero in the first half and from its partial scores in the
 // second; it ends by saving them (first half) or with the step end.
-template <typename KT, int U, int NQT, int NPL>
+template <typename KT, int U, int NQT, int NPL, bool TILED>
 __device__ __forceinline__ void split_compute_unit(
     const FineArgs &a, const FineSmem &sm, const LoadUnit<KT, U> &lu, LoadUnit<KT, U> &nx,
     const KT *__restrict__ K, int nu, int NGH, int k0, int u, bool valid, int h, int64_t g0,
-    int64_t r1, int step0, int nqg, f32x4_t (&acc)[NQT], f32x4_t (&part)[kSplitSteps][NQT],
-    OwnedLane &o, Stats<NQT> &st) {
+    int64_t r1, int64_t shift, int step0, int nqg, f32x4_t (&acc)[NQT],
+    f32x4_t (&part)[kSplitSteps][NQT], OwnedLane &o, Stats<NQT> &st) {
     const int lane = threadIdx.x & 63;
     const int tt = u / NGH, gi = u - tt * NGH;
     if (gi == 0) {
@@ -957,7 +982,7 @@ __device__ __forceinline__ void split_compute_unit(
                 }
         }
     }
-    split_load_unit<KT, U>(nx, K, a.tid_src, a.d, NGH, k0, nu, g0, r1);
+    split_load_unit<KT, U, TILED>(nx, K, a.tid_src, a.d, NGH, k0, nu, g0, r1, shift);
     const bf16x8_t *qs = sm.qs + (size_t)gi * U * NQT * kWave + lane;
 #pragma unroll
     for (int uu = 0; uu < U; ++uu) {
@@ -984,13 +1009,15 @@ __device__ __forceinline__ void split_compute_unit(
     }
 }
 
-template <typename KT, int U, int NQT, int NPL>
+template <typename KT, int U, int NQT, int NPL, bool TILED>
 __device__ __forceinline__ void pass_split(const FineArgs &a, const FineSmem &sm, int64_t p0,
                                            bool single, int64_t r0, int64_t r1, int32_t qbeg,
-                                           int32_t qg0, int32_t nqg) {
+                                           int32_t qg0, int32_t nqg, int32_t g) {
     const int t = threadIdx.x;
+    // the tiled copy's row of bank row r of segment g is r + shift
+    const int64_t shift = TILED ? a.toff[g] - a.seg_off[g] : 0;
     const int d = a.d;
-    const KT *__restrict__ K = static_cast<const KT *>(a.keys);
+    const KT *__restrict__ K = static_cast<const KT *>(TILED ? a.keys_tiled : a.keys);
     // the queries in bf16: fp32 ones were rounded once per call (as the
     // staging would round them), so each half is staged in one round trip
     const __bf16 *__restrict__ Q =
@@ -1037,8 +1064,8 @@ __device__ __forceinline__ void pass_split(const FineArgs &a, const FineSmem &sm
                     if (i0 == t) {
 #pragma unroll
                         for (int j = 0; j < R - 1; ++j)
-                            split_load_unit<KT, U>(ring[j], K, a.tid_src, d, NGH, k0,
-                                                   min(j, total - 1), g0, r1);
+                            split_load_unit<KT, U, TILED>(ring[j], K, a.tid_src, d, NGH, k0,
+                                                          min(j, total - 1), g0, r1, shift);
                         // every wave is done with the fragments of the previous half
                         block_lds_barrier();
                     }
@@ -1060,9 +1087,10 @@ __device__ __forceinline__ void pass_split(const FineArgs &a, const FineSmem &sm
             for (int u = 0; u < total; u += R) {
 #pragma unroll
                 for (int j = 0; j < R; ++j)
-                    split_compute_unit<KT, U, NQT, NPL>(
+                    split_compute_unit<KT, U, NQT, NPL, TILED>(
                         a, sm, ring[j], ring[(j + R - 1) % R], K, min(u + j + R - 1, total - 1),
-                        NGH, k0, u + j, u + j < total, h, g0, r1, tg, nqg, acc, part, o, st);
+                        NGH, k0, u + j, u + j < total, h, g0, r1, shift, tg, nqg, acc, part, o,
+                        st);
             }
         }
     }
@@ -1075,7 +1103,7 @@ __device__ __forceinline__ void pass_split(const FineArgs &a, const FineSmem &sm
 // pass_split): registers capped at two waves per SIMD (the partial scores of
 // a group take 16 of them: one query tile per pass, qmax == 16);
 // d % (64 U) == 0.
-template <typename KT, int NPL>
+template <typename KT, int NPL, bool TILED>
 __global__ __launch_bounds__(kFineThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void stream_split(FineArgs a, int32_t qs_bytes) {
     extern __shared__ __align__(16) unsigned char smem_raw[];
@@ -1084,8 +1112,8 @@ void stream_split(FineArgs a, int32_t qs_bytes) {
     const FineSmem sm = fine_carve(smem_raw, qs_bytes, a.qmax, a.cap, a.ntile);
     for_each_item(a, s_next, [&](const ItemPass &it) {
         for (int32_t qg0 = 0; qg0 < it.nq; qg0 += a.qmax)
-            pass_split<KT, U, 1, NPL>(a, sm, it.p0, it.single, it.r0, it.r1, it.qbeg, qg0,
-                                      min(a.qmax, it.nq - qg0));
+            pass_split<KT, U, 1, NPL, TILED>(a, sm, it.p0, it.single, it.r0, it.r1, it.qbeg, qg0,
+                                             min(a.qmax, it.nq - qg0), it.g);
     });
 }
 
@@ -1133,8 +1161,12 @@ template <typename KT>
 hipError_t launch_stream_lds_t(int npl, bool two_per_cu, const StreamLaunch &l) {
     if (l.ksplit) {
         switch (npl) {
-            case 2: return launch_stream_kernel(stream_split<KT, 2>, l, l.fa, l.qs_bytes);
-            case 4: return launch_stream_kernel(stream_split<KT, 4>, l, l.fa, l.qs_bytes);
+            case 2: return l.fa.keys_tiled
+                               ? launch_stream_kernel(stream_split<KT, 2, true>, l, l.fa, l.qs_bytes)
+                               : launch_stream_kernel(stream_split<KT, 2, false>, l, l.fa, l.qs_bytes);
+            case 4: return l.fa.keys_tiled
+                               ? launch_stream_kernel(stream_split<KT, 4, true>, l, l.fa, l.qs_bytes)
+                               : launch_stream_kernel(stream_split<KT, 4, false>, l, l.fa, l.qs_bytes);
         }
         return hipErrorInvalidValue;
     }

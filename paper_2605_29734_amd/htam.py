@@ -44,7 +44,7 @@ class BankStruct(ctypes.Structure):
                 ("n_transitions", ctypes.c_int64), ("key_dtype", ctypes.c_int32),
                 ("compute_dtype", ctypes.c_int32), ("coarse_keys", ctypes.c_void_p),
                 ("fine_keys", ctypes.c_void_p), ("seg_offsets", ctypes.c_void_p),
-                ("transition_id", ctypes.c_void_p)]
+                ("transition_id", ctypes.c_void_p), ("fine_keys_tiled", ctypes.c_void_p)]
 
 
 def _load():
@@ -59,6 +59,8 @@ def _load():
     sig = {
         "htam_memory_build": ([i64, i32, i32, i32, P, P, P, P, P, P, sz, P], i32),
         "htam_memory_build_workspace_size": ([i64, i32], sz),
+        "htam_memory_tile": ([BP, P, P], i32),
+        "htam_memory_tile_bytes": ([BP], sz),
         "htam_retrieve_coarse": ([BP, P, i32, i32, i32, P, P, P, sz, P], i32),
         "htam_retrieve_coarse_workspace_size": ([BP, i32, i32], sz),
         "htam_attend_transitions": ([BP, P, i32, i32, P, i32, f32, i32, P, P, P, P, P, sz, P], i32),
@@ -124,6 +126,7 @@ class Bank:
     seg_offsets: torch.Tensor       # [G+1] int64
     transition_id: torch.Tensor | None   # [N] int32 or None (= row index)
     compute: str = "bf16"           # "f32" | "bf16"
+    fine_keys_tiled: torch.Tensor | None = None   # htam_memory_tile's copy, or None
 
     def __post_init__(self):
         self._s = BankStruct(
@@ -132,7 +135,8 @@ class Bank:
             compute_dtype=HTAM_BF16 if self.compute == "bf16" else HTAM_F32,
             coarse_keys=self.coarse_keys.data_ptr(), fine_keys=self.fine_keys.data_ptr(),
             seg_offsets=self.seg_offsets.data_ptr(),
-            transition_id=None if self.transition_id is None else self.transition_id.data_ptr())
+            transition_id=None if self.transition_id is None else self.transition_id.data_ptr(),
+            fine_keys_tiled=None if self.fine_keys_tiled is None else self.fine_keys_tiled.data_ptr())
 
     @property
     def struct(self) -> BankStruct:
@@ -425,12 +429,31 @@ def retrieve_two_banks(main: Bank, delta: Bank, q: torch.Tensor, top_c: int, top
                 m=row[3], Z=row[4], count=row[5])
 
 
+def htam_memory_tile(bank: Bank) -> torch.Tensor:
+    """The tiled copy of bank.fine_keys (htam_memory_tile), same dtype, flat."""
+    nbytes = lib.htam_memory_tile_bytes(ctypes.byref(bank.struct))
+    if nbytes == 0:
+        raise HtamError("htam_memory_tile", -2,
+                        f"no tiled copy for d = {bank.fine_keys.shape[1]} (needs d % 32 == 0)")
+    dev = bank.fine_keys.device
+    out = torch.empty(nbytes // bank.fine_keys.element_size(), dtype=bank.fine_keys.dtype, device=dev)
+    _check("htam_memory_tile", lib.htam_memory_tile(ctypes.byref(bank.struct), _ptr(out), _stream(dev)))
+    return out
+
+
+def with_tiled_keys(bank: Bank) -> Bank:
+    """The same bank with the tiled copy of its fine keys attached."""
+    return dataclasses.replace(bank, fine_keys_tiled=htam_memory_tile(bank))
+
+
 def build_bank(cluster_of: torch.Tensor, keys_in: torch.Tensor, coarse_keys: torch.Tensor,
-               compute: str) -> Bank:
-    """Run htam_memory_build on records in arrival order and wrap the result as a Bank."""
+               compute: str, tiled: bool = False) -> Bank:
+    """Run htam_memory_build on records in arrival order and wrap the result as a
+    Bank (with the tiled copy of the keys when tiled is set)."""
     keys_out, off, tid = htam_memory_build(cluster_of, keys_in, coarse_keys.shape[0])
-    return Bank(coarse_keys=coarse_keys, fine_keys=keys_out, seg_offsets=off, transition_id=tid,
+    bank = Bank(coarse_keys=coarse_keys, fine_keys=keys_out, seg_offsets=off, transition_id=tid,
                 compute=compute)
+    return with_tiled_keys(bank) if tiled else bank
 
 
 def retrieve(bank: Bank, q: torch.Tensor, top_c: int, top_k: int, tau: float) -> dict:

@@ -24,7 +24,7 @@ def to_np(t: torch.Tensor) -> np.ndarray:
 
 
 def run_case(spec, seed=0, rows=None, tau=None, gen_device="cpu", check_build=True,
-             determinism=False, identity_ids=False):
+             determinism=False, identity_ids=False, tiled=False):
     from paper_2605_29734_amd import htam
     dev = torch.device("cuda:0")
     tau = spec.tau if tau is None else tau
@@ -52,11 +52,23 @@ def run_case(spec, seed=0, rows=None, tau=None, gen_device="cpu", check_build=Tr
         bank = htam.Bank(coarse_keys=bank.coarse_keys, fine_keys=bank.fine_keys,
                          seg_offsets=bank.seg_offsets, transition_id=None, compute=bank.compute)
         tid = None
+    plain = None
+    if tiled:               # the same bank read through its tiled copy of the keys
+        say("[step] retrieve without the tiled copy")
+        plain = {k: to_np(v) for k, v in
+                 htam.Retriever(bank, spec.B, spec.top_c, spec.top_k, tau).run(q).items()}
+        torch.cuda.synchronize()
+        say("[step] htam_memory_tile")
+        bank = htam.with_tiled_keys(bank)
     say("[step] retrieve (coarse, attend, topk)")
     r = htam.Retriever(bank, spec.B, spec.top_c, spec.top_k, tau)
     out = r.run(q)
     torch.cuda.synchronize()
     gpu = {k: to_np(v) for k, v in out.items()}
+    if plain is not None:
+        for k in gpu:       # only where keys are read from changes: the same bits
+            assert np.array_equal(gpu[k], plain[k], equal_nan=True), f"{k}: tiled copy differs"
+        del plain
     if determinism:
         say("[step] second run for bitwise determinism")
         again = {k: to_np(v) for k, v in r.run(q).items()}

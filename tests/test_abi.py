@@ -109,6 +109,27 @@ def test_build_rejects_bad_arguments():
     assert mb(10, 4, 64, 1, FAKE, FAKE, FAKE * 4, FAKE, FAKE, FAKE, 8, None) == -5
 
 
+def test_tiled_copy_rejects_bad_arguments():
+    """htam_memory_tile and a bank carrying a tiled copy: validated on the host
+    (the tiled copy needs d % 32 == 0 and 16-byte alignment)."""
+    tile = htam.lib.htam_memory_tile
+    b = _bank(d=64, N=100, kd=htam.HTAM_F32, cd=htam.HTAM_BF16)
+    # header of G + 1 = 9 int64 (256 bytes), then at most N / 16 + G = 7 + 8 tiles of 16 rows
+    assert htam.lib.htam_memory_tile_bytes(ctypes.byref(b)) == 256 + 15 * 16 * 64 * 4
+    assert htam.lib.htam_memory_tile_bytes(ctypes.byref(_bank(d=40))) == 0
+    assert tile(None, FAKE, None) == -1
+    assert tile(ctypes.byref(_bank(d=40)), FAKE, None) == -2
+    assert tile(ctypes.byref(b), None, None) == -1
+    assert tile(ctypes.byref(b), FAKE + 8, None) == -6
+    assert tile(ctypes.byref(b), FAKE + 64, None) == -4            # overlaps fine_keys
+    bad = _bank(d=40)
+    bad.fine_keys_tiled = FAKE * 2
+    assert _coarse(bad) == -2 and _attend(bad) == -2
+    mis = _bank(d=64)
+    mis.fine_keys_tiled = FAKE * 2 + 8
+    assert _attend(mis) == -6
+
+
 def test_workspace_sizes():
     b = _bank(d=1024, G=4096, N=8388608)
     assert htam.lib.htam_memory_build_workspace_size(8388608, 4096) > 2048 * 4096 * 4

@@ -53,5 +53,5 @@ def test_full_size_zipf_large_subset():
 @pytest.mark.timeout(900)
 def test_full_size_before_after_subset():
     spec = S["before_after_f32"]
-    run_case(spec, rows=_subset(spec, 256), gen_device="cuda", check_build=False)
+    run_case(spec, rows=_subset(spec, 256), gen_device="cuda", check_build=False, tiled=True)
     torch.cuda.empty_cache()

@@ -35,22 +35,72 @@ def test_zipf_large_bf16_reduced():
     run_case(synth.scaled(S["zipf_large_bf16"], B=256, G=256, N=262144))
 
 
-def test_before_after_reduced():
-    run_case(synth.scaled(S["before_after_f32"], B=96, G=256, N=65536))
+@pytest.mark.parametrize("tiled", [False, True])
+def test_before_after_reduced(tiled):
+    run_case(synth.scaled(S["before_after_f32"], B=96, G=256, N=65536), tiled=tiled)
 
 
+@pytest.mark.parametrize("tiled", [False, True])
 @pytest.mark.parametrize("storage,B,G,N,top_k,min_size", [
     ("f32", 512, 512, 200000, 128, 20),   # Zipf segments (mean 390 rows, 1024-row chunks):
     ("bf16", 512, 512, 200000, 64, 20),   # long ones of several four-step row groups per chunk
     ("f32", 128, 64, 6000, 128, 1),       # short and ragged segments: groups under four steps
 ])
-def test_split_stream_kernel(storage, B, G, N, top_k, min_size):
+def test_split_stream_kernel(storage, B, G, N, top_k, min_size, tiled):
     """The two-blocks-per-CU stream kernel that stages half of d's query
     fragments at a time (d = 2048, short segments on average, one query tile
-    per pass: at most about eight queries per selected cluster)."""
+    per pass: at most about eight queries per selected cluster); with the
+    tiled copy of the keys (segments start anywhere in a 16-row tile) its
+    outputs must equal those of the row-major bank bit for bit."""
     run_case(synth.Spec("split", B=B, d=2048, G=G, N=N, top_c=4, top_k=top_k, tau=0.5,
                         storage=storage, compute="bf16", sizes="zipf", zipf_s=1.0,
-                        min_size=min_size), gen_device="cuda", check_build=False)
+                        min_size=min_size), gen_device="cuda", check_build=False, tiled=tiled)
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("sizes,d", [([1000], 64), ([16], 32), ([37, 0, 5, 16, 0, 33], 96),
+                                     ([0, 0], 32)])
+def test_tiled_copy_layout(sizes, d, dtype):
+    """htam_memory_tile against the layout written out in numpy: the header
+    of padded segment starts, then element 32 s + 8 c + e of copy row
+    16 t + i at block (t, s), piece (e // P) * 64 + c * 16 + i, offset e % P;
+    segment g's record j at copy row toff[g] + j, padding rows zero (empty
+    segments, segments that end inside a tile). Bit-exact."""
+    from paper_2605_29734_amd import htam
+    say(f"[case] tiled copy sizes={sizes} d={d} dtype={dtype}")
+    dev = torch.device("cuda:0")
+    G, N = len(sizes), sum(sizes)
+    off = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+    g = torch.Generator().manual_seed(N + d + G)
+    keys = torch.randn(max(N, 1), d, generator=g).to(dtype)[:N]
+    bank = htam.Bank(coarse_keys=torch.zeros(G, d, dtype=dtype, device=dev),
+                     fine_keys=keys.to(dev) if N else torch.zeros(1, d, dtype=dtype, device=dev),
+                     seg_offsets=torch.from_numpy(off).to(dev), transition_id=None,
+                     compute="bf16")
+    bank.struct.n_transitions = N
+    out = htam.htam_memory_tile(bank)
+    torch.cuda.synchronize()
+    raw = out.view(torch.uint8).cpu().numpy()
+    head = ((G + 1) * 8 + 255) // 256 * 256
+    toff = raw[:(G + 1) * 8].view(np.int64)
+    pad = [(n + 15) // 16 * 16 for n in sizes]
+    assert np.array_equal(toff, np.concatenate([[0], np.cumsum(pad)]).astype(np.int64))
+    P = 16 // keys.element_size()
+    T, S = int(toff[-1]) // 16, d // 32
+    ref = np.zeros((T, S, 8 // P, 4, 16, P), dtype=np.float32)
+    k = keys.float().numpy()
+    for gi in range(G):
+        for j in range(sizes[gi]):
+            t, i = divmod(int(toff[gi]) + j, 16)
+            for s_ in range(S):
+                for c in range(4):
+                    for e in range(8):
+                        ref[t, s_, e // P, c, i, e % P] = k[off[gi] + j, 32 * s_ + 8 * c + e]
+    if T == 0:
+        return
+    tiles = torch.from_numpy(raw[head:head + T * 16 * d * keys.element_size()].copy())
+    got = tiles.view(dtype).float().numpy()
+    np.testing.assert_array_equal(got, ref.reshape(-1))
 
 
 @pytest.mark.parametrize("compute", ["bf16", "f32"])
