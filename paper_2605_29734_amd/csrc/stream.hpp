@@ -648,24 +648,39 @@ struct LoadUnit {
 
 // Unconditional loads only (rows clamped into the chunk), so that the compiler
 // can count outstanding loads exactly and wait for one unit at a time.
-template <typename KT, int U>
+// The lane's first key fragment of unit u. With TILED, K is the keys' tiled
+// copy, where bank row r of the item's segment is row r + shift and the unit's
+// k-steps are blocks of 512 elements (unit_frag reads fragment uu).
+template <typename KT, int U, bool TILED>
 __device__ __forceinline__ const KT *unit_keys(const KT *__restrict__ K, int d, int NG, int u,
-                                               int64_t r0, int64_t r1, int64_t &base) {
+                                               int64_t r0, int64_t r1, int64_t shift,
+                                               int64_t &base) {
     const int lane = threadIdx.x & 63, wave = fine_wave(), r16 = lane & 15, kg = lane >> 4;
     const int tt = u / NG, gi = u - tt * NG;
     base = r0 + (int64_t)tt * kRowsPerStep;
     const int64_t row = min(base + wave * kRowsPerWave + r16, r1 - 1);
-    return K + row * d + 32 * U * gi + 8 * kg;
+    if constexpr (TILED) {
+        constexpr int P = 16 / (int)sizeof(KT);
+        const int64_t tr = row + shift;
+        return K + ((tr >> 4) * (d >> 5) + U * gi) * 512 + (kg * 16 + (int)(tr & 15)) * P;
+    } else {
+        return K + row * d + 32 * U * gi + 8 * kg;
+    }
+}
+template <typename KT, int U, bool TILED>
+__device__ __forceinline__ void unit_frag(AFrag<KT> &f, const KT *kp, int uu) {
+    if constexpr (TILED) f.load_tiled(kp + 512 * uu);
+    else f.load(kp + 32 * uu);
 }
 
-template <typename KT, int U>
+template <typename KT, int U, bool TILED>
 __device__ __forceinline__ void lds_load_unit(LoadUnit<KT, U> &lu, const KT *__restrict__ K,
                                               const int32_t *__restrict__ tid_src, int d, int NG,
-                                              int u, int64_t r0, int64_t r1) {
+                                              int u, int64_t r0, int64_t r1, int64_t shift) {
     int64_t base;
-    const KT *kp = unit_keys<KT, U>(K, d, NG, u, r0, r1, base);
+    const KT *kp = unit_keys<KT, U, TILED>(K, d, NG, u, r0, r1, shift, base);
 #pragma unroll
-    for (int uu = 0; uu < U; ++uu) lu.f[uu].load(kp + 32 * uu);
+    for (int uu = 0; uu < U; ++uu) unit_frag<KT, U, TILED>(lu.f[uu], kp, uu);
     lu.tid = step_tid_load(tid_src, base, r1);
 }
 
@@ -675,23 +690,24 @@ __device__ __forceinline__ void lds_load_unit(LoadUnit<KT, U> &lu, const KT *__r
 // while it multiplies, instead of issuing a whole unit at once and leaving
 // the pipeline to drain; without it (two blocks per CU, whose waves cover for
 // each other) the unit is requested before the MFMAs.
-template <typename KT, int U, int NQT, int NPL, bool SPREAD, bool PC = false>
+template <typename KT, int U, int NQT, int NPL, bool SPREAD, bool PC, bool TILED>
 __device__ __forceinline__ void lds_compute_unit(const FineArgs &a, const FineSmem &sm,
                                                  const LoadUnit<KT, U> &lu, LoadUnit<KT, U> &nx,
                                                  const KT *__restrict__ K, int nu, int NG, int u,
-                                                 bool valid, int64_t r0, int64_t r1, int nqg,
-                                                 f32x4_t (&acc)[NQT], OwnedLane &o, Stats<NQT> &st) {
+                                                 bool valid, int64_t r0, int64_t r1, int64_t shift,
+                                                 int nqg, f32x4_t (&acc)[NQT], OwnedLane &o,
+                                                 Stats<NQT> &st) {
     const int lane = threadIdx.x & 63;
     const int tt = u / NG, gi = u - tt * NG;
     const float keep = gi == 0 ? 0.0f : 1.0f;
 #pragma unroll
     for (int qt = 0; qt < NQT; ++qt) acc[qt] *= keep;
     int64_t nbase;
-    const KT *nkp = unit_keys<KT, U>(K, a.d, NG, nu, r0, r1, nbase);
+    const KT *nkp = unit_keys<KT, U, TILED>(K, a.d, NG, nu, r0, r1, shift, nbase);
     nx.tid = step_tid_load(a.tid_src, nbase, r1);
     if (!SPREAD) {
 #pragma unroll
-        for (int uu = 0; uu < U; ++uu) nx.f[uu].load(nkp + 32 * uu);
+        for (int uu = 0; uu < U; ++uu) unit_frag<KT, U, TILED>(nx.f[uu], nkp, uu);
     }
     const bf16x8_t *qs = sm.qs + (size_t)gi * U * NQT * kWave + lane;
     // Query fragments are read from LDS a few k-steps ahead of their MFMAs;
@@ -699,7 +715,7 @@ __device__ __forceinline__ void lds_compute_unit(const FineArgs &a, const FineSm
     // (4 registers each), or the next unit's loads, to the top of the unit.
 #pragma unroll
     for (int uu = 0; uu < U; ++uu) {
-        if (SPREAD) nx.f[uu].load(nkp + 32 * uu);
+        if (SPREAD) unit_frag<KT, U, TILED>(nx.f[uu], nkp, uu);
         const bf16x8_t A = lu.f[uu].bf16();
 #pragma unroll
         for (int qt = 0; qt < NQT; ++qt)
@@ -719,14 +735,16 @@ __device__ __forceinline__ void lds_compute_unit(const FineArgs &a, const FineSm
 // buffers; waves 4-7 run the owner epilogue of each step's tile while the
 // producers multiply the next. Both sides meet once per step at a barrier
 // (twice when only one score tile fits in LDS).
-template <typename KT, int U, int NQT, int NPL, bool SPREAD, bool PC = false>
+template <typename KT, int U, int NQT, int NPL, bool SPREAD, bool PC, bool TILED>
 __device__ __forceinline__ void pass_lds(const FineArgs &a, const FineSmem &sm, int64_t p0,
                                          bool single, int64_t r0, int64_t r1, int32_t qbeg,
-                                         int32_t qg0, int32_t nqg) {
+                                         int32_t qg0, int32_t nqg, int32_t g) {
     const int t = threadIdx.x;
     const bool producer = !PC || t < kFineThreads;
     const int d = a.d;
-    const KT *__restrict__ K = static_cast<const KT *>(a.keys);
+    const KT *__restrict__ K = static_cast<const KT *>(TILED ? a.keys_tiled : a.keys);
+    // the tiled copy's row of bank row r of segment g is r + shift
+    const int64_t shift = TILED ? a.toff[g] - a.seg_off[g] : 0;
     const KT *__restrict__ Q = static_cast<const KT *>(a.q);
     const int KS = d >> 5;
     const int NG = KS / U;
@@ -744,7 +762,8 @@ __device__ __forceinline__ void pass_lds(const FineArgs &a, const FineSmem &sm, 
     if (producer) {
 #pragma unroll
         for (int j = 0; j < R - 1; ++j)
-            lds_load_unit<KT, U>(ring[j], K, a.tid_src, d, NG, min(j, total - 1), r0, r1);
+            lds_load_unit<KT, U, TILED>(ring[j], K, a.tid_src, d, NG, min(j, total - 1), r0, r1,
+                                        shift);
     }
 
     const PassBound pb = pass_begin<true>(a, sm, qbeg, qg0, nqg, single);
@@ -800,9 +819,9 @@ __device__ __forceinline__ void pass_lds(const FineArgs &a, const FineSmem &sm, 
         for (int u = 0; u < total; u += R) {
 #pragma unroll
             for (int j = 0; j < R; ++j)
-                lds_compute_unit<KT, U, NQT, NPL, SPREAD, PC>(
+                lds_compute_unit<KT, U, NQT, NPL, SPREAD, PC, TILED>(
                     a, sm, ring[j], ring[(j + R - 1) % R], K, min(u + j + R - 1, total - 1), NG,
-                    u + j, u + j < total, r0, r1, nqg, acc, o, st);
+                    u + j, u + j < total, r0, r1, shift, nqg, acc, o, st);
         }
     } else {
         // consumers: one step's tile at a time, in step order
@@ -869,7 +888,7 @@ __device__ __forceinline__ void for_each_item(const FineArgs &a, int32_t *s_next
     }
 }
 
-template <typename KT, int U, int NPL, bool SPREAD, bool PC = false>
+template <typename KT, int U, int NPL, bool SPREAD, bool PC = false, bool TILED = false>
 __device__ __forceinline__ void stream_lds_body(const FineArgs &a, int32_t qs_bytes,
                                                 unsigned char *smem_raw, int32_t *s_next) {
     const FineSmem sm = fine_carve(smem_raw, qs_bytes, a.qmax, a.cap, a.ntile);
@@ -877,10 +896,10 @@ __device__ __forceinline__ void stream_lds_body(const FineArgs &a, int32_t qs_by
         for (int32_t qg0 = 0; qg0 < it.nq; qg0 += a.qmax) {
             const int32_t nqg = min(a.qmax, it.nq - qg0);
             switch ((nqg + 15) >> 4) {
-                case 1: pass_lds<KT, U, 1, NPL, SPREAD, PC>(a, sm, it.p0, it.single, it.r0, it.r1, it.qbeg, qg0, nqg); break;
-                case 2: pass_lds<KT, U, 2, NPL, SPREAD, PC>(a, sm, it.p0, it.single, it.r0, it.r1, it.qbeg, qg0, nqg); break;
-                case 3: pass_lds<KT, U, 3, NPL, SPREAD, PC>(a, sm, it.p0, it.single, it.r0, it.r1, it.qbeg, qg0, nqg); break;
-                default: pass_lds<KT, U, 4, NPL, SPREAD, PC>(a, sm, it.p0, it.single, it.r0, it.r1, it.qbeg, qg0, nqg); break;
+                case 1: pass_lds<KT, U, 1, NPL, SPREAD, PC, TILED>(a, sm, it.p0, it.single, it.r0, it.r1, it.qbeg, qg0, nqg, it.g); break;
+                case 2: pass_lds<KT, U, 2, NPL, SPREAD, PC, TILED>(a, sm, it.p0, it.single, it.r0, it.r1, it.qbeg, qg0, nqg, it.g); break;
+                case 3: pass_lds<KT, U, 3, NPL, SPREAD, PC, TILED>(a, sm, it.p0, it.single, it.r0, it.r1, it.qbeg, qg0, nqg, it.g); break;
+                default: pass_lds<KT, U, 4, NPL, SPREAD, PC, TILED>(a, sm, it.p0, it.single, it.r0, it.r1, it.qbeg, qg0, nqg, it.g); break;
             }
         }
     });
@@ -898,13 +917,14 @@ __global__ __launch_bounds__(kFineThreads) void stream_lds(FineArgs a, int32_t q
 // capped at two waves per SIMD, so that one block's latency-bound steps
 // (staging, epilogue, pass end) overlap the other's; shorter load units keep
 // the ring within that budget (d must be a multiple of 256).
-template <typename KT, int NPL>
+template <typename KT, int NPL, bool TILED>
 __global__ __launch_bounds__(kFineThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void stream_lds2(FineArgs a, int32_t qs_bytes) {
     extern __shared__ __align__(16) unsigned char smem_raw[];
     __shared__ int32_t s_next[2];
     // fp32 fragments take twice the registers: half-length units
-    stream_lds_body<KT, sizeof(KT) == 4 ? 4 : 8, NPL, false>(a, qs_bytes, smem_raw, s_next);
+    stream_lds_body<KT, sizeof(KT) == 4 ? 4 : 8, NPL, false, false, TILED>(a, qs_bytes, smem_raw,
+                                                                         s_next);
 }
 
 // Producer/consumer blocks of eight waves, one per CU (LDS-bound launches):
@@ -912,11 +932,12 @@ void stream_lds2(FineArgs a, int32_t qs_bytes) {
 // fragments take twice the registers) in a ring of four (spread between the
 // MFMAs), four keep the top-k buffers. Registers are capped at two waves per
 // SIMD, which the two roles share.
-template <typename KT, int NPL>
+template <typename KT, int NPL, bool TILED>
 __global__ __launch_bounds__(2 * kFineThreads) void stream_pc(FineArgs a, int32_t qs_bytes) {
     extern __shared__ __align__(16) unsigned char smem_raw[];
     __shared__ int32_t s_next[2];
-    stream_lds_body<KT, sizeof(KT) == 4 ? 4 : 8, NPL, true, true>(a, qs_bytes, smem_raw, s_next);
+    stream_lds_body<KT, sizeof(KT) == 4 ? 4 : 8, NPL, true, true, TILED>(a, qs_bytes, smem_raw,
+                                                                       s_next);
 }
 
 // ---- split pass: the query fragments staged half of d at a time ------------
@@ -1170,19 +1191,23 @@ hipError_t launch_stream_lds_t(int npl, bool two_per_cu, const StreamLaunch &l) 
         }
         return hipErrorInvalidValue;
     }
+    // the kernels that read the tiled copy of the keys when the bank has one
+    const bool tiled = l.fa.keys_tiled != nullptr;
     if (l.producer_consumer) {
+        const int th = 2 * kFineThreads;
         switch (npl) {
-            case 2: return launch_stream_kernel_n(stream_pc<KT, 2>, 2 * kFineThreads, l, l.fa,
-                                                  l.qs_bytes);
-            case 4: return launch_stream_kernel_n(stream_pc<KT, 4>, 2 * kFineThreads, l, l.fa,
-                                                  l.qs_bytes);
+            case 2: return tiled ? launch_stream_kernel_n(stream_pc<KT, 2, true>, th, l, l.fa, l.qs_bytes)
+                                 : launch_stream_kernel_n(stream_pc<KT, 2, false>, th, l, l.fa, l.qs_bytes);
+            case 4: return tiled ? launch_stream_kernel_n(stream_pc<KT, 4, true>, th, l, l.fa, l.qs_bytes)
+                                 : launch_stream_kernel_n(stream_pc<KT, 4, false>, th, l, l.fa, l.qs_bytes);
         }
         return hipErrorInvalidValue;
     }
     if (two_per_cu) {
+        // row-major keys only: with the tiled addressing the registers spill
         switch (npl) {
-            case 2: return launch_stream_kernel(stream_lds2<KT, 2>, l, l.fa, l.qs_bytes);
-            case 4: return launch_stream_kernel(stream_lds2<KT, 4>, l, l.fa, l.qs_bytes);
+            case 2: return launch_stream_kernel(stream_lds2<KT, 2, false>, l, l.fa, l.qs_bytes);
+            case 4: return launch_stream_kernel(stream_lds2<KT, 4, false>, l, l.fa, l.qs_bytes);
         }
         return hipErrorInvalidValue;
     }

@@ -43,7 +43,7 @@ def test_full_size_zipf_large_subset():
         chosen["big"], chosen["rows"] = big, r
         return r
 
-    rep = run_case(spec, rows=rows, gen_device="cuda", check_build=False)
+    rep = run_case(spec, rows=rows, gen_device="cuda", check_build=False, tiled=True)
     assert (rep["sel"] == chosen["big"]).any(), "the checked rows miss the largest cluster"
     say(f"[ok] largest cluster {chosen['big']} ({int(rep['sizes'][chosen['big']])} rows) "
         f"checked in {int((rep['sel'] == chosen['big']).any(axis=1).sum())} rows")

@@ -27,12 +27,14 @@ def test_zipf_bf16_full():
     run_case(S["zipf_bf16"])
 
 
-def test_mixture_bf16_reduced():
-    run_case(synth.scaled(S["mixture_bf16"], B=128, G=64, N=65536))
+@pytest.mark.parametrize("tiled", [False, True])
+def test_mixture_bf16_reduced(tiled):
+    run_case(synth.scaled(S["mixture_bf16"], B=128, G=64, N=65536), tiled=tiled)
 
 
-def test_zipf_large_bf16_reduced():
-    run_case(synth.scaled(S["zipf_large_bf16"], B=256, G=256, N=262144))
+@pytest.mark.parametrize("tiled", [False, True])
+def test_zipf_large_bf16_reduced(tiled):
+    run_case(synth.scaled(S["zipf_large_bf16"], B=256, G=256, N=262144), tiled=tiled)
 
 
 @pytest.mark.parametrize("tiled", [False, True])
