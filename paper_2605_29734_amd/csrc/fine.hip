@@ -86,6 +86,7 @@ struct PlanArgs {
     int32_t G;
     int64_t n_rows;           // N, the bank's rows
     const int64_t *off;
+    const int64_t *toff;      // [G+1] the tiled copy's segment starts, or NULL
     int32_t *qoff;            // [G+1]
     int32_t *wstart;          // [G+1] first full-length chunk item of each cluster
     int32_t *wlast;           // [G]   item of the cluster's shorter last chunk (-1: none)
@@ -404,10 +405,15 @@ struct SlotOut {
 // off[0] = 0, nondecreasing, off[G] = N (Eq. local nodes: every record has
 // one parent). Checked by the whole block before any row is indexed through
 // them; returns the verdict in every thread.
-__device__ __forceinline__ bool offsets_bad(const int64_t *off, int32_t G, int64_t N) {
+__device__ __forceinline__ bool offsets_bad(const int64_t *off, int32_t G, int64_t N,
+                                            const int64_t *toff) {
     int bad = 0;
-    for (int32_t g = threadIdx.x; g < G; g += blockDim.x) bad |= off[g] > off[g + 1];
-    if (threadIdx.x == 0) bad |= off[0] != 0 || off[G] != N;
+    for (int32_t g = threadIdx.x; g < G; g += blockDim.x) {
+        bad |= off[g] > off[g + 1];
+        // the tiled copy's header must match: segments padded to 16 rows
+        if (toff) bad |= toff[g + 1] - toff[g] != ((off[g + 1] - off[g] + 15) & ~int64_t(15));
+    }
+    if (threadIdx.x == 0) bad |= off[0] != 0 || off[G] != N || (toff && toff[0] != 0);
     return __syncthreads_or(bad) != 0;
 }
 
@@ -476,10 +482,13 @@ __global__ __launch_bounds__(kPlanThreads) void route_plan_partials(PlanArgs pa,
     int64_t p[kChunkCands];
 #pragma unroll
     for (int i = 0; i < kChunkCands; ++i) p[i] = 0;
-    int bad = blockIdx.x == 0 && threadIdx.x == 0 && (pa.off[0] != 0 || pa.off[G] != pa.n_rows);
+    int bad = blockIdx.x == 0 && threadIdx.x == 0 &&
+              (pa.off[0] != 0 || pa.off[G] != pa.n_rows || (pa.toff && pa.toff[0] != 0));
     for (int32_t g = gw0 + lane; g < gw1; g += kWave) {
         const int64_t a0 = pa.off[g], a1 = pa.off[g + 1];
         bad |= a0 > a1;
+        // the tiled copy's header must match: segments padded to 16 rows
+        if (pa.toff) bad |= pa.toff[g + 1] - pa.toff[g] != ((a1 - a0 + 15) & ~int64_t(15));
         const int64_t c = cnt[g], len = a1 - a0;
         if (c > 0 && len > 0) {
 #pragma unroll
@@ -772,7 +781,7 @@ __global__ __launch_bounds__(kPlanThreads) void route_fused(PlanArgs pa, const i
     for (int32_t g = t; g < G; g += kPlanThreads) lcnt[g] = 0;
     if (t == 0) s_bad = 0;
     __syncthreads();
-    if (offsets_bad(loff, G, pa.n_rows)) {     // before any row is indexed through them
+    if (offsets_bad(loff, G, pa.n_rows, pa.toff)) {   // before any row is indexed through them
         if (t == 0) {
             plan_nothing(pa.plan);
             pa.plan->bad_sel = 0;
@@ -1395,6 +1404,7 @@ hipError_t launch_attend(int32_t key_dtype, int32_t compute_dtype, int32_t d, in
     pa.G = G;
     pa.n_rows = N;
     pa.off = seg_offsets;
+    pa.toff = static_cast<const int64_t *>(fine_keys_tiled);   // its header, or NULL
     pa.qoff = w.qoff;
     pa.wstart = w.wstart;
     pa.wlast = w.wlast;

@@ -287,7 +287,8 @@ HTAM_API htam_status htam_attend_transitions(const htam_bank *bank, const void *
     if (e != hipSuccess) return device_status(e, "htam_attend_transitions (validation)");
     if (plan.bad_off)
         return fail(HTAM_ERR_VALUE, "bank->seg_offsets is not a partition of [0, %lld): need "
-                    "off[0] = 0, nondecreasing, off[G] = N (no record was read)",
+                    "off[0] = 0, nondecreasing, off[G] = N; or the header of "
+                    "bank->fine_keys_tiled does not match them (no record was read)",
                     (long long)bank->n_transitions);
     if (plan.bad_sel)
         return fail(HTAM_ERR_VALUE, "%d selected cluster ids lie outside [0, %d) (their slots are empty)",

@@ -1,5 +1,6 @@
 """Malformed banks through the C ABI: segment offsets that are not a partition
-of the bank's rows, and selected cluster ids out of range.
+of the bank's rows, a tiled copy of the keys whose header does not match
+them, and selected cluster ids out of range.
 
 The first kernel that reads the offsets (the routing's planning step) checks
 them before any record is indexed through them, so such a call reads no bank
@@ -79,3 +80,39 @@ def test_validate_mode_passes_good_banks_and_flags_bad_selections(B, monkeypatch
     with pytest.raises(htam.HtamError) as ei:
         htam.htam_attend_transitions(bank, q, bad_sel, spec.tau, spec.top_k)
     assert ei.value.status == -4 and "outside" in str(ei.value)
+
+
+@pytest.mark.parametrize("B", [40, 4200])          # one-block and multi-block routing
+@pytest.mark.parametrize("how", ["shifted_segment", "start_not_zero"])
+def test_tiled_copy_header_mismatch(B, how, monkeypatch):
+    """A tiled copy whose header of segment starts does not match the bank's
+    offsets (a stale copy): checked with the offsets, before any row is read
+    through it; a matching copy passes and gives the row-major results."""
+    import dataclasses
+    from paper_2605_29734_amd import htam
+    say(f"[case] tiled copy header ({how}), B={B}")
+    spec, bank, q = _bank_and_queries(B)
+    tb = htam.with_tiled_keys(bank)
+    sel, _ = htam.htam_retrieve_coarse(bank, q, spec.top_c)
+    monkeypatch.setenv("HTAM_VALIDATE", "1")
+    plain = [to_np(x) for x in htam.htam_attend_transitions(bank, q, sel, spec.tau, spec.top_k)]
+    tiled = [to_np(x) for x in htam.htam_attend_transitions(tb, q, sel, spec.tau, spec.top_k)]
+    for a, b in zip(plain, tiled):
+        np.testing.assert_array_equal(a, b)
+    raw = tb.fine_keys_tiled.clone()
+    head = raw.view(torch.uint8)[:(spec.G + 1) * 8].view(torch.int64)
+    if how == "shifted_segment":
+        head[3:] += 16
+    else:
+        head[0] = 16
+    bad = dataclasses.replace(tb, fine_keys_tiled=raw)
+    monkeypatch.delenv("HTAM_VALIDATE", raising=False)
+    smax, ssum, cs, ci = (to_np(x) for x in htam.htam_attend_transitions(bad, q, sel, spec.tau,
+                                                                           spec.top_k))
+    torch.cuda.synchronize()
+    assert np.all(smax == -np.inf) and np.all(ssum == 0.0)
+    assert np.all(ci == -1) and np.all(cs == -np.inf)
+    monkeypatch.setenv("HTAM_VALIDATE", "1")
+    with pytest.raises(htam.HtamError) as ei:
+        htam.htam_attend_transitions(bad, q, sel, spec.tau, spec.top_k)
+    assert ei.value.status == -4 and "fine_keys_tiled" in str(ei.value)
