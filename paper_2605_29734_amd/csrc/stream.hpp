@@ -648,6 +648,23 @@ struct LoadUnit {
 
 // Unconditional loads only (rows clamped into the chunk), so that the compiler
 // can count outstanding loads exactly and wait for one unit at a time.
+// The lane's first fragment in the keys' tiled copy for the 16 rows from bank
+// row `base + 16 * wave` of a segment (copy row = bank row + shift; the 16
+// rows are one tile) at k-step ks0. Rows past the item's last row read that
+// row, as in the row-major layout, so that no row outside the item is read
+// from memory; the tile index is then wave-uniform (scalar arithmetic) and
+// the lane adds its place in the block, (kg * 16 + row % 16) * P.
+template <typename KT>
+__device__ __forceinline__ const KT *tiled_frag(const KT *__restrict__ K, int d, int64_t base,
+                                                int64_t r1, int64_t shift, int ks0) {
+    constexpr int P = 16 / (int)sizeof(KT);
+    const int lane = threadIdx.x & 63, r16 = lane & 15, kg = lane >> 4;
+    const int64_t wave = __builtin_amdgcn_readfirstlane(fine_wave());
+    const int64_t t = min((base + shift) / 16 + wave, (r1 - 1 + shift) / 16);
+    const int i = (int)((min(base + 16 * wave + r16, r1 - 1) + shift) & 15);
+    return K + (t * (d >> 5) + ks0) * 512 + (kg * 16 + i) * P;
+}
+
 // The lane's first key fragment of unit u. With TILED, K is the keys' tiled
 // copy, where bank row r of the item's segment is row r + shift and the unit's
 // k-steps are blocks of 512 elements (unit_frag reads fragment uu).
@@ -658,12 +675,10 @@ __device__ __forceinline__ const KT *unit_keys(const KT *__restrict__ K, int d, 
     const int lane = threadIdx.x & 63, wave = fine_wave(), r16 = lane & 15, kg = lane >> 4;
     const int tt = u / NG, gi = u - tt * NG;
     base = r0 + (int64_t)tt * kRowsPerStep;
-    const int64_t row = min(base + wave * kRowsPerWave + r16, r1 - 1);
     if constexpr (TILED) {
-        constexpr int P = 16 / (int)sizeof(KT);
-        const int64_t tr = row + shift;
-        return K + ((tr >> 4) * (d >> 5) + U * gi) * 512 + (kg * 16 + (int)(tr & 15)) * P;
+        return tiled_frag<KT>(K, d, base, r1, shift, U * gi);
     } else {
+        const int64_t row = min(base + wave * kRowsPerWave + r16, r1 - 1);
         return K + row * d + 32 * U * gi + 8 * kg;
     }
 }
@@ -966,7 +981,9 @@ __device__ __forceinline__ void split_load_unit(LoadUnit<KT, U> &lu, const KT *_
         // K is the tiled copy, where bank row r of this segment is row r +
         // shift (a segment starts on a tile, and so does a wave's 16 rows):
         // block (row / 16, k-step) of 512 elements, this lane's first piece
-        // at (kg * 16 + row % 16) * P, P = 16 / element bytes
+        // at (kg * 16 + row % 16) * P, P = 16 / element bytes. (Per-lane
+        // arithmetic here: with tiled_frag's scalar tile index this kernel
+        // ran 1% slower.)
         constexpr int P = 16 / (int)sizeof(KT);
         const int64_t tr = row + shift;
         const KT *kp = K + ((tr >> 4) * (d >> 5) + ks0) * 512 + (kg * 16 + (int)(tr & 15)) * P;
@@ -1204,10 +1221,11 @@ hipError_t launch_stream_lds_t(int npl, bool two_per_cu, const StreamLaunch &l) 
         return hipErrorInvalidValue;
     }
     if (two_per_cu) {
-        // row-major keys only: with the tiled addressing the registers spill
         switch (npl) {
-            case 2: return launch_stream_kernel(stream_lds2<KT, 2, false>, l, l.fa, l.qs_bytes);
-            case 4: return launch_stream_kernel(stream_lds2<KT, 4, false>, l, l.fa, l.qs_bytes);
+            case 2: return tiled ? launch_stream_kernel(stream_lds2<KT, 2, true>, l, l.fa, l.qs_bytes)
+                                 : launch_stream_kernel(stream_lds2<KT, 2, false>, l, l.fa, l.qs_bytes);
+            case 4: return tiled ? launch_stream_kernel(stream_lds2<KT, 4, true>, l, l.fa, l.qs_bytes)
+                                 : launch_stream_kernel(stream_lds2<KT, 4, false>, l, l.fa, l.qs_bytes);
         }
         return hipErrorInvalidValue;
     }

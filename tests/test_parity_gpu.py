@@ -23,8 +23,9 @@ def test_tiny_f32():
     run_case(S["tiny_f32"], determinism=True)
 
 
-def test_zipf_bf16_full():
-    run_case(S["zipf_bf16"])
+@pytest.mark.parametrize("tiled", [False, True])
+def test_zipf_bf16_full(tiled):
+    run_case(S["zipf_bf16"], tiled=tiled)
 
 
 @pytest.mark.parametrize("tiled", [False, True])
