@@ -165,44 +165,49 @@ __global__ __launch_bounds__(kScanThreads) void tile_offsets(const int64_t *off,
     if (t == kScanThreads - 1) toff[G] = s[t];
 }
 
-// One block per tile of the copy (the grid is an upper bound on the tiles;
-// blocks past toff[G] / 16 return). The tile's segment g is found once, by
-// binary search over toff; then every 16-byte piece of the tile, in the
-// copy's order: piece w of block (tile, step) (`parts` pieces per 8-element
-// fragment) is part h = w / 64 of the fragment of group c = (w / 16) % 4 of
-// the tile's row i = w % 16, read from bank row off[g] + 16 tile + i -
-// toff[g] of the row-major keys, or zero past the segment's end.
-__global__ __launch_bounds__(256) void tile_keys(const uint4 *__restrict__ keys,
+// Blocks take the tiles of the copy in turn (tile = block index, then every
+// grid-th). A tile's segment g is found once, by binary search over toff;
+// then every 16-byte piece of the tile, in the copy's order: piece w of block
+// (tile, step) (`parts` pieces per 8-element fragment) is part h = w / 64 of
+// the fragment of group c = (w / 16) % 4 of the tile's row i = w % 16, read
+// from bank row off[g] + 16 tile + i - toff[g] of the row-major keys, or zero
+// past the segment's end. Malformed offsets give a wrong copy (the stream's
+// offset check rejects it) but no access outside the keys or the copy's
+// max_tiles tiles.
+__global__ __launch_bounds__(256) void tile_keys(const uint4 *__restrict__ keys, int64_t n_rows,
                                                  const int64_t *__restrict__ off,
                                                  const int64_t *__restrict__ toff, int32_t G,
-                                                 int32_t steps, int32_t parts,
+                                                 int32_t steps, int32_t parts, int64_t max_tiles,
                                                  uint4 *__restrict__ tiles) {
     __shared__ int32_t s_g;
-    const int64_t tile = blockIdx.x;
-    const int64_t row0 = tile * 16;
-    if (row0 >= toff[G]) return;                 // uniform across the block
-    if (threadIdx.x == 0) {
-        int32_t lo = 0, hi = G - 1;              // last g with toff[g] <= row0
-        while (lo < hi) {
-            const int32_t mid = (lo + hi + 1) >> 1;
-            if (toff[mid] <= row0) lo = mid; else hi = mid - 1;
-        }
-        s_g = lo;
-    }
-    __syncthreads();
-    const int32_t g = s_g;
-    const int64_t j0 = row0 - toff[g], len = off[g + 1] - off[g], src0 = off[g];
+    const int64_t n_tiles = min(toff[G] / 16, max_tiles);
     const int64_t per_block = (int64_t)parts * 64, per_row = (int64_t)steps * 4 * parts;
     const int64_t n = (int64_t)steps * per_block;
-    uint4 *out = tiles + tile * n;
-    for (int64_t p = threadIdx.x; p < n; p += blockDim.x) {
-        const int64_t st = p / per_block;
-        const int w = (int)(p - st * per_block);
-        const int h = w >> 6, c = (w >> 4) & 3, i = w & 15;
-        const int64_t j = j0 + i;
-        uint4 v = make_uint4(0u, 0u, 0u, 0u);
-        if (j < len) v = keys[(src0 + j) * per_row + st * 4 * parts + c * parts + h];
-        out[p] = v;
+    for (int64_t tile = blockIdx.x; tile < n_tiles; tile += gridDim.x) {   // uniform bounds
+        const int64_t row0 = tile * 16;
+        __syncthreads();                         // the previous tile is done with s_g
+        if (threadIdx.x == 0) {
+            int32_t lo = 0, hi = G - 1;          // last g with toff[g] <= row0
+            while (lo < hi) {
+                const int32_t mid = (lo + hi + 1) >> 1;
+                if (toff[mid] <= row0) lo = mid; else hi = mid - 1;
+            }
+            s_g = lo;
+        }
+        __syncthreads();
+        const int32_t g = s_g;
+        const int64_t j0 = row0 - toff[g], len = off[g + 1] - off[g], src0 = off[g];
+        uint4 *out = tiles + tile * n;
+        for (int64_t p = threadIdx.x; p < n; p += blockDim.x) {
+            const int64_t st = p / per_block;
+            const int w = (int)(p - st * per_block);
+            const int h = w >> 6, c = (w >> 4) & 3, i = w & 15;
+            const int64_t j = j0 + i;
+            uint4 v = make_uint4(0u, 0u, 0u, 0u);
+            if (j < len && src0 + j >= 0 && src0 + j < n_rows)
+                v = keys[(src0 + j) * per_row + st * 4 * parts + c * parts + h];
+            out[p] = v;
+        }
     }
 }
 
@@ -218,9 +223,10 @@ hipError_t launch_tile_keys(int64_t n_rows, int32_t G, int32_t d, int32_t elem_b
     hipLaunchKernelGGL(tile_offsets, dim3(1), dim3(kScanThreads), 0, s, seg_offsets, G, toff);
     const int64_t max_tiles = (n_rows + 15) / 16 + G;
     if (n_rows > 0)
-        hipLaunchKernelGGL(tile_keys, dim3((unsigned)max_tiles), dim3(256), 0, s,
-                           static_cast<const uint4 *>(keys), seg_offsets, toff, G, d / 32,
-                           elem_bytes == 4 ? 2 : 1, tiles);
+        hipLaunchKernelGGL(tile_keys, dim3((unsigned)(max_tiles < 65536 ? max_tiles : 65536)),
+                           dim3(256), 0, s,
+                           static_cast<const uint4 *>(keys), n_rows, seg_offsets, toff, G, d / 32,
+                           elem_bytes == 4 ? 2 : 1, max_tiles, tiles);
     return hipGetLastError();
 }
 
