@@ -13,7 +13,9 @@ far beyond the last-level cache, so every step streams it from HBM). A bank
 that would fit the 256 MB last-level cache is timed over copies of itself
 that together exceed 1 GiB, one per step in turn (--no-rotate: one bank).
 The bank also carries its keys in the tiled order that the bank stream reads
-(htam_memory_tile, built with the bank, untimed; --no-tiled: row-major only).
+(htam_memory_tile) and, for fp32 banks, its coarse keys rounded to bf16
+(htam_coarse_keys_bf16), both built with the bank, untimed (--no-tiled:
+neither).
 
 Prints one JSON line: queries/s for the workload (whole timed region), the
 roofline position of the dominant kernel (the bank stream, HBM-bound),
@@ -374,7 +376,8 @@ def main():
     ap.add_argument("--no-rotate", action="store_true",
                     help="time one bank even when it fits the last-level cache")
     ap.add_argument("--no-tiled", action="store_true",
-                    help="stream the row-major keys only (no tiled copy)")
+                    help="no prepared copies: the stream reads the row-major keys and the "
+                         "coarse scoring rounds fp32 coarse keys on every call")
     ap.add_argument("--event-every", type=int, default=4, metavar="E",
                     help="stamp the kernel and stage timing events on every E-th timed step")
     ap.add_argument("--path", default="hierarchical",
@@ -435,11 +438,12 @@ def main():
                       for _ in range(n_copies - 1)]
     if n_copies > 1:
         log(f"[bench] rotating over {n_copies} copies of the {bank_bytes / 2**20:.0f} MiB bank")
-    # the keys also in the tiled order of htam_memory_tile (built with the
-    # bank, untimed): the bank stream reads 1 KB of consecutive bytes per load
+    # the copies built with the bank, untimed: the fine keys in the tiled
+    # order of htam_memory_tile (the bank stream reads 1 KB of consecutive
+    # bytes per load) and fp32 coarse keys rounded to bf16 once
     tiled = not args.no_tiled and spec.d % 32 == 0
-    if tiled:
-        banks = [htam.with_tiled_keys(b) for b in banks]
+    if not args.no_tiled:
+        banks = [htam.prepared(b) for b in banks]
         torch.cuda.synchronize()
     r.bank = banks[0]
     log(f"[bench] warmup {args.warmup}")
@@ -536,7 +540,8 @@ def main():
                    "transitions": spec.N, "top_c": spec.top_c, "top_k": spec.top_k,
                    "tau": spec.tau, "key_storage": spec.storage,
                    "bank_bytes": int(spec.N * spec.d * kb), "bank_copies": n_copies,
-                   "tiled_keys": tiled},
+                   "tiled_keys": tiled,
+                   "coarse_keys_bf16": banks[0].coarse_keys_bf16 is not None},
         "roofline": {"bound": "hbm", "kernel": "fine_stream", "achieved": achieved,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "traffic": stream_kernel_traffic(spec.name),

@@ -103,6 +103,10 @@ typedef enum {
  *                  htam_attend_transitions reads instead of fine_keys where
  *                  it can; results are identical either way. Requires
  *                  d % 32 == 0; 16-byte aligned.
+ *   coarse_keys_bf16  NULL, or (fp32 banks computed in bf16) coarse_keys
+ *                  rounded to bf16 as htam_coarse_keys_bf16 writes them:
+ *                  the coarse scoring then rounds only the queries per call.
+ *                  Ignored for bf16 banks; 16-byte aligned.
  */
 typedef struct htam_bank {
     int32_t d;
@@ -115,6 +119,7 @@ typedef struct htam_bank {
     const int64_t *seg_offsets;
     const int32_t *transition_id;
     const void *fine_keys_tiled;
+    const void *coarse_keys_bf16;
 } htam_bank;
 
 /*
@@ -179,6 +184,18 @@ size_t htam_memory_build_workspace_size(int64_t n, int32_t n_clusters);
  */
 htam_status htam_memory_tile(const htam_bank *bank, void *tiled_out, hipStream_t stream);
 size_t htam_memory_tile_bytes(const htam_bank *bank);
+
+/*
+ * htam_coarse_keys_bf16 -- the bank's fp32 coarse keys rounded to bf16 (to
+ * nearest even), the operand of the bf16 coarse scores of Eq. score, for
+ * htam_bank.coarse_keys_bf16 (so that htam_retrieve_coarse does not round
+ * them on every call; its results are the same either way).
+ *
+ *   bank   a bank with key_dtype HTAM_F32; its coarse_keys_bf16 is ignored.
+ *   out    [G][d] bf16, 16-byte aligned, not overlapping coarse_keys.
+ * Asynchronous on stream; allocates nothing.
+ */
+htam_status htam_coarse_keys_bf16(const htam_bank *bank, void *out, hipStream_t stream);
 
 /*
  * htam_memory_merge -- online memory update, record side: fold a delta bank

@@ -370,7 +370,7 @@ CoarseWs coarse_layout(void *ws, int32_t B, int32_t G, int32_t d, int32_t key_dt
 hipError_t launch_scores(int32_t key_dtype, int32_t compute_dtype, int32_t d, int64_t n,
                          const void *keys, const void *q, int32_t B, float *S, __bf16 *q16,
                          __bf16 *k16, bool convert_q, int n_cu, KernelEvents ev, hipStream_t s,
-                         float *tmax, bool *tiled) {
+                         float *tmax, bool *tiled, const __bf16 *keys16) {
     const int32_t G = (int32_t)n;
     if (tiled) *tiled = false;
     if (compute_dtype == kF32) {
@@ -395,13 +395,16 @@ hipError_t launch_scores(int32_t key_dtype, int32_t compute_dtype, int32_t d, in
         const __bf16 *qa = static_cast<const __bf16 *>(q);
         const __bf16 *ka = static_cast<const __bf16 *>(keys);
         if (key_dtype == kF32) {
-            const int64_t nq = convert_q ? (int64_t)B * d / 8 : 0, nc = (int64_t)G * d / 8;
+            // the keys are rounded here unless the caller's bf16 copy is given
+            const int64_t nq = convert_q ? (int64_t)B * d / 8 : 0;
+            const int64_t nc = keys16 ? 0 : (int64_t)G * d / 8;
             const int64_t nb = (nq + nc + 255) / 256;
-            hipLaunchKernelGGL(to_bf16, dim3((unsigned)(nb < 8192 ? nb : 8192)), dim3(256), 0, s,
-                               static_cast<const float *>(q), q16, nq,
-                               static_cast<const float *>(keys), k16, nc);
+            if (nb > 0)
+                hipLaunchKernelGGL(to_bf16, dim3((unsigned)(nb < 8192 ? nb : 8192)), dim3(256), 0,
+                                   s, static_cast<const float *>(q), q16, nq,
+                                   static_cast<const float *>(keys), k16, nc);
             qa = q16;
-            ka = k16;
+            ka = keys16 ? keys16 : k16;
         }
         hipError_t err = hipFuncSetAttribute((const void *)coarse_gemm,
                                              hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -415,15 +418,24 @@ hipError_t launch_scores(int32_t key_dtype, int32_t compute_dtype, int32_t d, in
     return hipGetLastError();
 }
 
+hipError_t launch_round_bf16(const float *x, __bf16 *y, int64_t n, hipStream_t s) {
+    const int64_t n8 = n / 8, nb = (n8 + 255) / 256;
+    if (nb > 0)
+        hipLaunchKernelGGL(to_bf16, dim3((unsigned)(nb < 8192 ? nb : 8192)), dim3(256), 0, s, x, y,
+                           n8, nullptr, nullptr, (int64_t)0);
+    return hipGetLastError();
+}
+
 hipError_t launch_coarse(int32_t key_dtype, int32_t compute_dtype, int32_t d, int32_t G,
-                         const void *coarse_keys, const void *q, int32_t B, int32_t top_c,
-                         int32_t *sel, float *sel_score, const CoarseWs &w, int n_cu,
-                         KernelEvents ev, hipStream_t s) {
+                         const void *coarse_keys, const void *coarse_keys_bf16, const void *q,
+                         int32_t B, int32_t top_c, int32_t *sel, float *sel_score,
+                         const CoarseWs &w, int n_cu, KernelEvents ev, hipStream_t s) {
     // tile maxima only where the selection can prune with them
     bool tiled = false;
     float *tmax = top_c <= kWave && top_c < w.n_tile ? w.tmax : nullptr;
     hipError_t err = launch_scores(key_dtype, compute_dtype, d, G, coarse_keys, q, B, w.scores,
-                                   w.q16, w.c16, true, n_cu, ev, s, tmax, &tiled);
+                                   w.q16, w.c16, true, n_cu, ev, s, tmax, &tiled,
+                                   static_cast<const __bf16 *>(coarse_keys_bf16));
     if (err != hipSuccess) return err;
     return launch_select(B, G, top_c, sel, sel_score, w, s, tiled ? tmax : nullptr);
 }

@@ -60,7 +60,8 @@ htam_status check_bank(const htam_bank *b) {
     if (!b->coarse_keys) return fail(HTAM_ERR_NULL, "bank->coarse_keys is NULL");
     if (!b->seg_offsets) return fail(HTAM_ERR_NULL, "bank->seg_offsets is NULL");
     if (b->n_transitions > 0 && !b->fine_keys) return fail(HTAM_ERR_NULL, "bank->fine_keys is NULL");
-    if (!aligned16(b->coarse_keys) || !aligned16(b->fine_keys) || !aligned16(b->fine_keys_tiled))
+    if (!aligned16(b->coarse_keys) || !aligned16(b->fine_keys) || !aligned16(b->fine_keys_tiled) ||
+        !aligned16(b->coarse_keys_bf16))
         return fail(HTAM_ERR_ALIGN, "bank key arrays must be 16-byte aligned");
     if (b->fine_keys_tiled && b->d % 32 != 0)
         return fail(HTAM_ERR_SHAPE, "bank->fine_keys_tiled needs d %% 32 == 0 (d = %d)", b->d);
@@ -201,6 +202,22 @@ HTAM_API htam_status htam_memory_tile(const htam_bank *bank, void *tiled_out, hi
                          "htam_memory_tile");
 }
 
+HTAM_API htam_status htam_coarse_keys_bf16(const htam_bank *bank, void *out, hipStream_t stream) {
+    if (!bank) return fail(HTAM_ERR_NULL, "bank is NULL");
+    htam_bank b = *bank;
+    b.coarse_keys_bf16 = nullptr;              // ignored here
+    HTAM_TRY(check_bank(&b));
+    if (b.key_dtype != HTAM_F32) return fail(HTAM_ERR_DTYPE, "the bank's keys are not fp32");
+    if (!out) return fail(HTAM_ERR_NULL, "out is NULL");
+    if (!aligned16(out)) return fail(HTAM_ERR_ALIGN, "out must be 16-byte aligned");
+    const size_t n = (size_t)b.n_clusters * b.d;
+    const char *a = static_cast<const char *>(b.coarse_keys), *o = static_cast<const char *>(out);
+    if (a < o + 2 * n && o < a + 4 * n) return fail(HTAM_ERR_VALUE, "out overlaps bank->coarse_keys");
+    return device_status(htam::launch_round_bf16(static_cast<const float *>(b.coarse_keys),
+                                                 static_cast<__bf16 *>(out), (int64_t)n, stream),
+                         "htam_coarse_keys_bf16");
+}
+
 // ---------------------------------------------------------------------------
 HTAM_API size_t htam_retrieve_coarse_workspace_size(const htam_bank *bank, int32_t n_queries,
                                                     int32_t top_c) {
@@ -228,9 +245,10 @@ HTAM_API htam_status htam_retrieve_coarse(const htam_bank *bank, const void *q, 
     const htam::CoarseWs w = htam::coarse_layout(ws, n_queries, bank->n_clusters, bank->d,
                                                  bank->key_dtype, bank->compute_dtype, top_c,
                                                  nullptr);
+    const void *ck16 = bank->key_dtype == HTAM_F32 ? bank->coarse_keys_bf16 : nullptr;
     return device_status(htam::launch_coarse(bank->key_dtype, bank->compute_dtype, bank->d,
-                                             bank->n_clusters, bank->coarse_keys, q, n_queries,
-                                             top_c, sel_cluster, sel_score, w, n_cu,
+                                             bank->n_clusters, bank->coarse_keys, ck16, q,
+                                             n_queries, top_c, sel_cluster, sel_score, w, n_cu,
                                              g_events[HTAM_KERNEL_COARSE], stream),
                          "htam_retrieve_coarse");
 }

@@ -123,10 +123,12 @@ struct CoarseWs {
 };
 CoarseWs coarse_layout(void *ws, int32_t B, int32_t G, int32_t d, int32_t key_dtype,
                        int32_t compute_dtype, int32_t top_c, size_t *bytes);
+// fp32 -> bf16, round to nearest even (n % 8 == 0).
+hipError_t launch_round_bf16(const float *x, __bf16 *y, int64_t n, hipStream_t s);
 hipError_t launch_coarse(int32_t key_dtype, int32_t compute_dtype, int32_t d, int32_t G,
-                         const void *coarse_keys, const void *q, int32_t B, int32_t top_c,
-                         int32_t *sel, float *sel_score, const CoarseWs &w, int n_cu,
-                         KernelEvents ev, hipStream_t s);
+                         const void *coarse_keys, const void *coarse_keys_bf16, const void *q,
+                         int32_t B, int32_t top_c, int32_t *sel, float *sel_score,
+                         const CoarseWs &w, int n_cu, KernelEvents ev, hipStream_t s);
 
 // The top_c of each score row of w.scores [B][G] (descending, ties to the lower id).
 // With tmax (the rows' 256-column tile maxima of these scores) only the tiles
@@ -263,7 +265,8 @@ hipError_t launch_seg_topk(int64_t rows, int64_t row_stride, int64_t n, const fl
 hipError_t launch_scores(int32_t key_dtype, int32_t compute_dtype, int32_t d, int64_t n,
                          const void *keys, const void *q, int32_t B, float *S, __bf16 *q16,
                          __bf16 *k16, bool convert_q, int n_cu, KernelEvents ev, hipStream_t s,
-                         float *tmax = nullptr, bool *tiled = nullptr);
+                         float *tmax = nullptr, bool *tiled = nullptr,
+                         const __bf16 *keys16 = nullptr);
 
 // ---- flat retrieval (every record a candidate) --------------------------------
 struct FlatWs {

@@ -44,7 +44,8 @@ class BankStruct(ctypes.Structure):
                 ("n_transitions", ctypes.c_int64), ("key_dtype", ctypes.c_int32),
                 ("compute_dtype", ctypes.c_int32), ("coarse_keys", ctypes.c_void_p),
                 ("fine_keys", ctypes.c_void_p), ("seg_offsets", ctypes.c_void_p),
-                ("transition_id", ctypes.c_void_p), ("fine_keys_tiled", ctypes.c_void_p)]
+                ("transition_id", ctypes.c_void_p), ("fine_keys_tiled", ctypes.c_void_p),
+                ("coarse_keys_bf16", ctypes.c_void_p)]
 
 
 def _load():
@@ -61,6 +62,7 @@ def _load():
         "htam_memory_build_workspace_size": ([i64, i32], sz),
         "htam_memory_tile": ([BP, P, P], i32),
         "htam_memory_tile_bytes": ([BP], sz),
+        "htam_coarse_keys_bf16": ([BP, P, P], i32),
         "htam_retrieve_coarse": ([BP, P, i32, i32, i32, P, P, P, sz, P], i32),
         "htam_retrieve_coarse_workspace_size": ([BP, i32, i32], sz),
         "htam_attend_transitions": ([BP, P, i32, i32, P, i32, f32, i32, P, P, P, P, P, sz, P], i32),
@@ -127,6 +129,7 @@ class Bank:
     transition_id: torch.Tensor | None   # [N] int32 or None (= row index)
     compute: str = "bf16"           # "f32" | "bf16"
     fine_keys_tiled: torch.Tensor | None = None   # htam_memory_tile's copy, or None
+    coarse_keys_bf16: torch.Tensor | None = None  # htam_coarse_keys_bf16's copy, or None
 
     def __post_init__(self):
         self._s = BankStruct(
@@ -136,7 +139,8 @@ class Bank:
             coarse_keys=self.coarse_keys.data_ptr(), fine_keys=self.fine_keys.data_ptr(),
             seg_offsets=self.seg_offsets.data_ptr(),
             transition_id=None if self.transition_id is None else self.transition_id.data_ptr(),
-            fine_keys_tiled=None if self.fine_keys_tiled is None else self.fine_keys_tiled.data_ptr())
+            fine_keys_tiled=None if self.fine_keys_tiled is None else self.fine_keys_tiled.data_ptr(),
+            coarse_keys_bf16=None if self.coarse_keys_bf16 is None else self.coarse_keys_bf16.data_ptr())
 
     @property
     def struct(self) -> BankStruct:
@@ -444,6 +448,24 @@ def htam_memory_tile(bank: Bank) -> torch.Tensor:
 def with_tiled_keys(bank: Bank) -> Bank:
     """The same bank with the tiled copy of its fine keys attached."""
     return dataclasses.replace(bank, fine_keys_tiled=htam_memory_tile(bank))
+
+
+def htam_coarse_keys_bf16(bank: Bank) -> torch.Tensor:
+    """The bank's fp32 coarse keys rounded to bf16 (htam_coarse_keys_bf16)."""
+    out = torch.empty(bank.coarse_keys.shape, dtype=torch.bfloat16, device=bank.coarse_keys.device)
+    _check("htam_coarse_keys_bf16", lib.htam_coarse_keys_bf16(ctypes.byref(bank.struct), _ptr(out),
+                                                              _stream(out.device)))
+    return out
+
+
+def prepared(bank: Bank) -> Bank:
+    """The bank with the copies the retrieval calls read when present: the
+    tiled fine keys (d % 32 == 0) and, for fp32 keys, the bf16 coarse keys."""
+    if bank.fine_keys.shape[1] % 32 == 0 and bank.fine_keys_tiled is None:
+        bank = with_tiled_keys(bank)
+    if bank.fine_keys.dtype == torch.float32 and bank.coarse_keys_bf16 is None:
+        bank = dataclasses.replace(bank, coarse_keys_bf16=htam_coarse_keys_bf16(bank))
+    return bank
 
 
 def build_bank(cluster_of: torch.Tensor, keys_in: torch.Tensor, coarse_keys: torch.Tensor,

@@ -53,13 +53,13 @@ def run_case(spec, seed=0, rows=None, tau=None, gen_device="cpu", check_build=Tr
                          seg_offsets=bank.seg_offsets, transition_id=None, compute=bank.compute)
         tid = None
     plain = None
-    if tiled:               # the same bank read through its tiled copy of the keys
-        say("[step] retrieve without the tiled copy")
+    if tiled:               # the same bank read through its prepared copies
+        say("[step] retrieve without the prepared copies")
         plain = {k: to_np(v) for k, v in
                  htam.Retriever(bank, spec.B, spec.top_c, spec.top_k, tau).run(q).items()}
         torch.cuda.synchronize()
-        say("[step] htam_memory_tile")
-        bank = htam.with_tiled_keys(bank)
+        say("[step] htam_memory_tile, htam_coarse_keys_bf16")
+        bank = htam.prepared(bank)
     say("[step] retrieve (coarse, attend, topk)")
     r = htam.Retriever(bank, spec.B, spec.top_c, spec.top_k, tau)
     out = r.run(q)
@@ -67,7 +67,7 @@ def run_case(spec, seed=0, rows=None, tau=None, gen_device="cpu", check_build=Tr
     gpu = {k: to_np(v) for k, v in out.items()}
     if plain is not None:
         for k in gpu:       # only where keys are read from changes: the same bits
-            assert np.array_equal(gpu[k], plain[k], equal_nan=True), f"{k}: tiled copy differs"
+            assert np.array_equal(gpu[k], plain[k], equal_nan=True), f"{k}: prepared bank differs"
         del plain
     if determinism:
         say("[step] second run for bitwise determinism")

@@ -128,6 +128,15 @@ def test_tiled_copy_rejects_bad_arguments():
     mis = _bank(d=64)
     mis.fine_keys_tiled = FAKE * 2 + 8
     assert _attend(mis) == -6
+    ck = _bank(d=64, kd=htam.HTAM_F32, cd=htam.HTAM_BF16)
+    ck.coarse_keys_bf16 = FAKE * 2 + 8
+    assert _coarse(ck, qd=htam.HTAM_F32) == -6
+    c16 = htam.lib.htam_coarse_keys_bf16
+    assert c16(None, FAKE, None) == -1
+    assert c16(ctypes.byref(_bank(d=64)), FAKE * 2, None) == -3        # bf16 keys: nothing to round
+    assert c16(ctypes.byref(ck), None, None) == -1
+    assert c16(ctypes.byref(ck), FAKE * 2 + 8, None) == -6
+    assert c16(ctypes.byref(ck), FAKE + 16, None) == -4                # overlaps coarse_keys
 
 
 def test_workspace_sizes():

@@ -269,6 +269,32 @@ def test_coarse_every_row(B, G, d, c, storage):
     np.testing.assert_allclose(ss, top, rtol=0, atol=1e-4)
 
 
+@pytest.mark.parametrize("B,G,d,c", [(2048, 8300, 64, 33), (1024, 4096, 96, 16)])
+def test_coarse_with_bf16_coarse_keys(B, G, d, c):
+    """An fp32 bank with its coarse keys rounded to bf16 once
+    (htam_coarse_keys_bf16): the 256 x 256-tile GEMM then rounds only the
+    queries, and the selection and scores equal those of the bank without
+    the copy bit for bit (the same rounding, done earlier)."""
+    import dataclasses
+    from paper_2605_29734_amd import htam
+    say(f"[case] coarse with a bf16 coarse-key copy B={B} G={G} d={d} c={c}")
+    rng = np.random.default_rng(B + G + d)
+    dev = torch.device("cuda:0")
+    q = torch.from_numpy(rng.standard_normal((B, d)).astype(np.float32)).to(dev)
+    ck = torch.from_numpy(rng.standard_normal((G, d)).astype(np.float32)).to(dev)
+    bank = htam.Bank(coarse_keys=ck, fine_keys=torch.zeros(1, d, device=dev),
+                     seg_offsets=torch.zeros(G + 1, dtype=torch.int64, device=dev),
+                     transition_id=None, compute="bf16")
+    c16 = htam.htam_coarse_keys_bf16(bank)
+    assert torch.equal(c16, ck.to(torch.bfloat16))          # round to nearest even
+    a = [to_np(x) for x in htam.htam_retrieve_coarse(bank, q, c)]
+    b = [to_np(x) for x in htam.htam_retrieve_coarse(
+        dataclasses.replace(bank, coarse_keys_bf16=c16), q, c)]
+    torch.cuda.synchronize()
+    for x, y in zip(a, b):
+        np.testing.assert_array_equal(x, y)
+
+
 def test_level_one_merge_groups():
     """A bank large enough for two merge levels (level-one groups of chunk
     partials): one 1.5M-row cluster next to 15 of 33K rows, k = 128. The
