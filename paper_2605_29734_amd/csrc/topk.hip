@@ -512,7 +512,13 @@ hipError_t launch_topk(int32_t rows, int32_t lists, int32_t k_in, const float *s
     a.row_max = row_max;
     a.row_sum = row_sum;
     a.out_count = out_count;
-    const int npl = next_pow2(top_k + kWave) / kWave;
+    // the smallest buffer that holds top_k + 64 keys; twice that when a row
+    // offers at least 16 times as many entries (zipf_large_bf16's final merge:
+    // 2048 entries, k = 64: 64 -> 39 us): a compaction every 64 entries that
+    // pass the threshold becomes one every 192, while for shorter rows the
+    // larger sort costs more than it saves
+    const int npl0 = next_pow2(top_k + kWave) / kWave;
+    const int npl = npl0 < 8 && a.n >= (int64_t)16 * kWave * npl0 ? 2 * npl0 : npl0;
     const dim3 grid((unsigned)((rows + kTopkWaves - 1) / kTopkWaves)), block(kWave * kTopkWaves);
     const size_t smem = (size_t)kTopkWaves * npl * kWave * 8;
     switch (npl) {
