@@ -1511,8 +1511,11 @@ hipError_t launch_attend(int32_t key_dtype, int32_t compute_dtype, int32_t d, in
     ma.slot_sum = slot_sum;
     ma.cand_score = cand_score;
     ma.cand_id = cand_id;
+    // a buffer of 128 keys for k >= 48 would leave at most 80 free after each
+    // compaction: 256 (zipf_large_bf16, k = 64: merges 89 -> 56 us)
     switch (next_pow2(k + kWave) / kWave) {
-        case 2: return launch_merge<2>(ma, w.u_cap, groups, n_cu, s);
+        case 2: return k >= 48 ? launch_merge<4>(ma, w.u_cap, groups, n_cu, s)
+                               : launch_merge<2>(ma, w.u_cap, groups, n_cu, s);
         case 4: return launch_merge<4>(ma, w.u_cap, groups, n_cu, s);
         default: return launch_merge<8>(ma, w.u_cap, groups, n_cu, s);
     }
