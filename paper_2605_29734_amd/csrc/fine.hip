@@ -4,7 +4,8 @@
 // statistics and the top-k kept per (query, selected cluster).
 //
 // Kernels, in launch order:
-//   route_init / route_count / route_plan / route_scatter
+//   route_fused (few pairs: one block), or route_zero / route_count /
+//   route_plan / route_emit
 //       group the (query, slot) pairs by selected cluster, choose the chunk
 //       length that splits long segments, and number the work items
 //       (cluster, chunk) and their partial results;
@@ -51,34 +52,86 @@ __host__ __device__ inline int64_t group_span(int64_t nch, int64_t kp, int64_t d
     }
     return r < 2 ? 2 : r;
 }
+// ceil(a / b) for 0 <= a < 2^31 and 1 <= b < 2^31, in 32-bit arithmetic
+// (chunk and group counts: the plan numbers its items in 32 bits)
+__host__ __device__ inline int64_t div_up32(int64_t a, int64_t b) {
+    return (int64_t)(((uint32_t)a + (uint32_t)b - 1u) / (uint32_t)b);
+}
 __host__ __device__ inline int64_t group_count(int64_t nch, int64_t kp, int64_t direct) {
     const int64_t r = group_span(nch, kp, direct);
-    return r ? (nch + r - 1) / r : 0;
+    return r ? div_up32(nch, r) : 0;
 }
 
 // ---------------------------------------------------------------------------
 // routing
 // ---------------------------------------------------------------------------
-__global__ void route_init(int32_t G, int32_t *cnt, int32_t *cursor, Plan *plan) {
-    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < G;
-         i += (int64_t)gridDim.x * blockDim.x) {
-        cnt[i] = 0;
-        cursor[i] = 0;
-    }
-    if (blockIdx.x == 0 && threadIdx.x == 0) {
+// Clears the per-cluster pair counters and the plan's flags; with q16 given,
+// also rounds the fp32 queries to bf16 (to nearest even, as the LDS staging
+// rounds them), 8 elements per thread, for the streaming kernel.
+__global__ void route_zero(int32_t G, int32_t *cnt, Plan *plan, const float *__restrict__ q,
+                           __bf16 *__restrict__ q16, int64_t n8) {
+    const int64_t i0 = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = i0; i < G; i += stride) cnt[i] = 0;
+    if (i0 == 0) {
         plan->next = 0;
         plan->bad_sel = 0;
         plan->bad_off = 0;
     }
+    for (int64_t i = i0; i < n8; i += stride)
+        reinterpret_cast<bf16x8_t *>(q16)[i] = load8(q + i * 8);
 }
 
-__global__ void route_count(const int32_t *sel, int64_t n, int32_t G, int32_t *cnt, Plan *plan) {
-    for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < n;
-         e += (int64_t)gridDim.x * blockDim.x) {
-        const int32_t g = sel[e];
-        if (g >= 0 && g < G) atomicAdd(&cnt[g], 1);
-        else atomicAdd(&plan->bad_sel, 1);
+// Most blocks of the planning kernel (one wave scans their totals) and of
+// the counting kernel (one pair per thread up to 131,072 pairs).
+constexpr int kRouteBlocks = 64;
+constexpr int kCountBlocks = 128;
+constexpr int kCountThreads = 1024;
+constexpr int kRouteThreads = 256;
+
+// Counts the (query, slot) pairs of each cluster; a pair's place in its
+// cluster's list is the count its atomic increment returns. For the choice
+// of the chunk length, each block also counts, over its pairs with a
+// nonempty segment of len rows, how many have bit b of len - 1 set (b >=
+// lmin; the partial results at chunk 2^j then sum exactly from these:
+// ceil(len / 2^j) = 1 + sum over b >= j of bit b times 2^(b-j)), and lane 63
+// how many such pairs there are: bits[block][64].
+__global__ __launch_bounds__(kCountThreads) void route_count(const int32_t *sel, int64_t n, int32_t G,
+                                                            const int64_t *off, int lmin,
+                                                            int32_t *cnt, int32_t *pos, Plan *plan,
+                                                            uint32_t *bits) {
+    __shared__ uint32_t s_bits[kWave];
+    const int t = threadIdx.x, lane = t & 63;
+    if (t < kWave) s_bits[t] = 0;
+    __syncthreads();
+    uint32_t acc = 0;      // lane b: pairs with bit b of len - 1 set; lane 63: pairs with len > 0
+    int32_t nbad = 0;
+    for (int64_t e0 = (int64_t)blockIdx.x * kCountThreads; e0 < n;
+         e0 += (int64_t)gridDim.x * kCountThreads) {
+        const int64_t e = e0 + t;
+        const int32_t g = e < n ? sel[e] : 0;
+        const bool valid = e < n && g >= 0 && g < G;
+        uint64_t hi = 0;
+        bool has = false;
+        if (valid) {
+            pos[e] = atomicAdd(&cnt[g], 1);
+            const int64_t len = off[g + 1] - off[g];
+            has = len > 0;
+            hi = has ? (uint64_t)(len - 1) >> lmin : 0;
+        }
+        const uint64_t bm = __ballot(e < n && !valid);
+        if (lane == 0) nbad += __popcll(bm);
+        const uint64_t hm = __ballot(has);
+        if (lane == kWave - 1) acc += __popcll(hm);
+        for (int b = lmin; b < kWave - 1 && __ballot(hi != 0) != 0; ++b, hi >>= 1) {
+            const uint64_t m = __ballot((hi & 1) != 0);
+            if (lane == b) acc += __popcll(m);
+        }
     }
+    if (acc) atomicAdd(&s_bits[lane], acc);
+    if (nbad) atomicAdd(&plan->bad_sel, nbad);
+    __syncthreads();
+    if (t < kWave) bits[(int64_t)blockIdx.x * kWave + t] = s_bits[t];
 }
 
 // Inputs and outputs of the planning step (device pointers).
@@ -429,23 +482,17 @@ __device__ __forceinline__ void plan_nothing(Plan *plan) {
     plan->bad_off = 1;
 }
 
-// ---- planning step of the multi-kernel routing ------------------------------
-// Three kernels over many blocks of 16 waves; each wave plans a contiguous
-// range of per_wave clusters, 64 at a time, one per lane, so that every
-// per-cluster load and table store is coalesced:
-//   route_plan_partials: each block's sums of the partial results at every
-//       candidate chunk length, and the offsets check;
-//   route_plan_totals: every block sums those and chooses the same chunk
-//       length, then writes its totals of the four scanned values and of the
-//       last chunks in each length bucket;
-//   route_plan_apply: each block's base is the totals of the blocks before
-//       it, each wave's the totals of the waves before it in the block; the
-//       per-cluster prefixes come from DPP wave scans with a running carry,
-//       and a cluster's place among the last chunks of its bucket from
-//       ballots.
-// The plan is the one route_fused makes, table for table.
-constexpr int kPlanSW = 4 + kItemBuckets;    // scanned values, then bucket counts
-constexpr int kMaxPlanBlocks = 64;
+// ---- planning step of the multi-block routing -------------------------------
+// route_plan: every block takes the same chunk length from the bit counts of
+// route_count, then plans its own range of clusters (rounds x 256 of them;
+// each wave a contiguous run, 64 at a time, one per lane, so that the
+// per-cluster loads and stores are coalesced): the block-local exclusive
+// prefixes of the four scanned values, and each cluster's rank among the
+// block's last chunks of its length bucket; agg[block] holds the block's
+// totals and its offsets check. route_emit adds the bases of the blocks
+// before (a scan of agg). The plan is the one route_fused makes, table for
+// table.
+constexpr int kAgg = 4 + kItemBuckets + 1;   // scanned values, last chunks per bucket, bad offsets
 
 // Per-cluster values at chunk 2^lch: v[0] = full items | level-one groups
 // << 32, v[1] = partials, v[2] = level-one results, v[3] = queries |
@@ -464,212 +511,167 @@ __device__ __forceinline__ int plan_values(const PlanArgs &pa, int64_t c, int64_
     return nch > nfull ? item_bucket(len - (nfull << lch), lch, c) : -1;
 }
 
-__device__ __forceinline__ int32_t plan_wave_start(int32_t per_wave) {
-    return (int32_t)(blockIdx.x * (kPlanThreads / kWave) + (threadIdx.x >> 6)) * per_wave;
-}
-
-// Partial results at chunk chunk_min * 2^i, i < kChunkCands, summed over this
-// block's clusters: part[block][i]. The offsets are checked by every block
-// over its own clusters (off[0] and off[G] by block 0); a failure sets
-// plan->bad_off, which the later kernels read.
-__global__ __launch_bounds__(kPlanThreads) void route_plan_partials(PlanArgs pa, const int32_t *cnt,
-                                                                    int32_t per_wave, int64_t *part) {
-    __shared__ int64_t s[(kPlanThreads / kWave + 1) * kChunkCands];
-    const int lane = threadIdx.x & 63;
-    const int32_t G = pa.G;
-    const int lmin = 63 - __builtin_clzll((unsigned long long)pa.chunk_min);
-    const int32_t gw0 = min(G, plan_wave_start(per_wave)), gw1 = min(G, gw0 + per_wave);
-    int64_t p[kChunkCands];
-#pragma unroll
-    for (int i = 0; i < kChunkCands; ++i) p[i] = 0;
-    int bad = blockIdx.x == 0 && threadIdx.x == 0 &&
-              (pa.off[0] != 0 || pa.off[G] != pa.n_rows || (pa.toff && pa.toff[0] != 0));
-    for (int32_t g = gw0 + lane; g < gw1; g += kWave) {
-        const int64_t a0 = pa.off[g], a1 = pa.off[g + 1];
-        bad |= a0 > a1;
-        // the tiled copy's header must match: segments padded to 16 rows
-        if (pa.toff) bad |= pa.toff[g + 1] - pa.toff[g] != ((a1 - a0 + 15) & ~int64_t(15));
-        const int64_t c = cnt[g], len = a1 - a0;
-        if (c > 0 && len > 0) {
-#pragma unroll
-            for (int i = 0; i < kChunkCands; ++i)
-                p[i] += c * ((len + (int64_t(1) << (lmin + i)) - 1) >> (lmin + i));
-        }
-    }
-    if (__syncthreads_or(bad) && threadIdx.x == 0) pa.plan->bad_off = 1;
-    block_sum_n<kChunkCands>(p, s);
-    if (threadIdx.x == 0) {
-#pragma unroll
-        for (int i = 0; i < kChunkCands; ++i) part[(int64_t)blockIdx.x * kChunkCands + i] = p[i];
-    }
-}
-
-// The chunk length (log2), the same in every block: the smallest candidate
-// whose partials (summed over the blocks) fit in p_cap; the last always fits.
-__device__ __forceinline__ int plan_chunk_log2(const PlanArgs &pa, const int64_t *part, int32_t nb,
-                                               int64_t *s) {
-    const int lmin = 63 - __builtin_clzll((unsigned long long)pa.chunk_min);
-    if (threadIdx.x < kChunkCands) {
-        int64_t sum = 0;
-        for (int32_t b = 0; b < nb; ++b) sum += part[(int64_t)b * kChunkCands + threadIdx.x];
-        s[threadIdx.x] = sum;
-    }
-    __syncthreads();
-    int cand = kChunkCands - 1;
-    for (int i = kChunkCands - 1; i >= 0; --i)
-        if (s[i] <= pa.p_cap) cand = i;
-    __syncthreads();
-    return lmin + cand;
-}
-
-// This wave's totals of the scanned values and (lane b) of its last chunks
-// in bucket b.
-__device__ __forceinline__ void plan_wave_totals(const PlanArgs &pa, const int32_t *cnt, int lch,
-                                                 int32_t gw0, int32_t gw1, int64_t (&tot)[4],
-                                                 int64_t &bcnt) {
-    const int lane = threadIdx.x & 63;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) tot[i] = 0;
-    bcnt = 0;
-    for (int32_t gr = gw0; gr < gw1; gr += kWave) {
-        const int32_t g = gr + lane;
-        int64_t v[4] = {0, 0, 0, 0};
-        const int b = g < gw1 ? plan_values(pa, cnt[g], pa.off[g + 1] - pa.off[g], lch, v) : -1;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) tot[i] += v[i];
-#pragma unroll
-        for (int bb = 0; bb < kItemBuckets; ++bb) {
-            const uint64_t m = __ballot(b == bb);
-            if (lane == bb) bcnt += __popcll(m);
-        }
-    }
-}
-
-// The wave totals of this block into sw[wave][kPlanSW] (LDS).
-__device__ __forceinline__ void plan_block_waves(const PlanArgs &pa, const int32_t *cnt, int lch,
-                                                 int32_t per_wave, int64_t *sw) {
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int32_t gw0 = min(pa.G, plan_wave_start(per_wave)), gw1 = min(pa.G, gw0 + per_wave);
-    int64_t tot[4], bcnt;
-    plan_wave_totals(pa, cnt, lch, gw0, gw1, tot, bcnt);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int64_t x = wave_sum64(tot[i]);
-        if (lane == 0) sw[wave * kPlanSW + i] = x;
-    }
-    if (lane < kItemBuckets) sw[wave * kPlanSW + 4 + lane] = bcnt;
-    __syncthreads();
-}
-
-// This block's totals: tot[block][kPlanSW]; block 0 also stores the chunk.
-__global__ __launch_bounds__(kPlanThreads) void route_plan_totals(PlanArgs pa, const int32_t *cnt,
-                                                                  int32_t per_wave, int32_t nb,
-                                                                  const int64_t *part, int64_t *tot) {
-    __shared__ int64_t s[kChunkCands];
-    __shared__ int64_t sw[(kPlanThreads / kWave) * kPlanSW];
-    if (pa.plan->bad_off) {                    // malformed offsets: no work
-        if (blockIdx.x == 0 && threadIdx.x == 0) plan_nothing(pa.plan);
-        return;
-    }
-    const int lch = plan_chunk_log2(pa, part, nb, s);
-    if (blockIdx.x == 0 && threadIdx.x == 0) pa.plan->chunk = int64_t(1) << lch;
-    plan_block_waves(pa, cnt, lch, per_wave, sw);
-    if (threadIdx.x < kPlanSW) {
-        int64_t x = 0;
-        for (int w = 0; w < kPlanThreads / kWave; ++w) x += sw[w * kPlanSW + threadIdx.x];
-        tot[(int64_t)blockIdx.x * kPlanSW + threadIdx.x] = x;
-    }
-}
-
-// The per-cluster tables and the plan.
-__global__ __launch_bounds__(kPlanThreads) void route_plan_apply(PlanArgs pa, const int32_t *cnt,
-                                                                 int32_t per_wave, int32_t nb,
-                                                                 const int64_t *tot) {
-    constexpr int waves = kPlanThreads / kWave;
-    static_assert(kItemBuckets == 16, "the bucket bases are scanned by one 16-lane row");
-    __shared__ int64_t sw[waves * kPlanSW];
-    __shared__ int64_t sb[2 * kPlanSW];        // this block's base, the totals
-    if (pa.plan->bad_off) return;
+// Chunk length (log2), the same in every block: the smallest candidate
+// chunk_min * 2^i whose partial results fit in p_cap (the last always fits).
+__device__ __forceinline__ int route_chunk_log2(const PlanArgs &pa, const uint32_t *bits, int32_t nb2) {
+    __shared__ unsigned long long s_bits[kWave];
+    __shared__ int32_t s_cand;
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-    const int32_t G = pa.G;
-    const int lch = 63 - __builtin_clzll((unsigned long long)pa.plan->chunk);
-    if (t < kPlanSW) {
-        int64_t base = 0, grand = 0;
-        for (int32_t b = 0; b < nb; ++b) {
-            const int64_t x = tot[(int64_t)b * kPlanSW + t];
-            base += b < (int32_t)blockIdx.x ? x : 0;
-            grand += x;
-        }
-        sb[t] = base;
-        sb[kPlanSW + t] = grand;
-    }
-    plan_block_waves(pa, cnt, lch, per_wave, sw);      // ends with a barrier
-    // this wave's base (lane w < 16 reads wave w's totals: one row scan per value)
-    int64_t carry[4], grand[4];
+    if (t < kWave) s_bits[t] = 0;
+    __syncthreads();
+    constexpr int per = kCountBlocks / (kRouteThreads / kWave);
+    uint32_t x[per];                           // every load in flight at once
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int64_t x = lane < waves ? sw[lane * kPlanSW + i] : 0;
-        const int64_t incl = row_scan64(x);
-        carry[i] = sb[i] + __shfl(incl - x, wave);
-        grand[i] = sb[kPlanSW + i];
+    for (int i = 0; i < per; ++i) {
+        const int32_t r = wave + i * (kRouteThreads / kWave);
+        x[i] = r < nb2 ? bits[(int64_t)r * kWave + lane] : 0;
     }
-    int64_t bbase = 0, bgrand = 0;
-    if (lane < kItemBuckets) {
-        bbase = sb[4 + lane];
-        bgrand = sb[kPlanSW + 4 + lane];
+    unsigned long long acc = 0;
+#pragma unroll
+    for (int i = 0; i < per; ++i) acc += x[i];
+    if (acc) atomicAdd(&s_bits[lane], acc);
+    __syncthreads();
+    const int lmin = 63 - __builtin_clzll((unsigned long long)pa.chunk_min);
+    if (wave == 0) {
+        // candidates in order, one wave sum each (the first usually fits):
+        // lane b < 63 adds its count times 2^(b-j) for b >= j, lane 63 the
+        // pairs; a term above cap rules the candidate out, so the sum of at
+        // most 64 terms of at most cap each cannot overflow
+        const uint64_t cb = s_bits[lane], cap = (uint64_t)pa.p_cap;
+        int cand = kChunkCands - 1;
 #pragma unroll 1
-        for (int w = 0; w < wave; ++w) bbase += sw[w * kPlanSW + 4 + lane];
-    }
-    // items: every full-length chunk first, then the last chunks bucket by
-    // bucket (lanes 0..15, one row, hold the buckets)
-    const int64_t n_full = grand[0] & 0xffffffff;
-    const int64_t bincl = row_scan64(lane < kItemBuckets ? bgrand : 0);
-    int64_t bnext = n_full + bincl - bgrand + bbase;     // lane b: this wave's next item of bucket b
-    const int64_t n_items = n_full + __shfl(bincl, kItemBuckets - 1);
-    const uint64_t lt = (uint64_t(1) << lane) - 1;
-    const int32_t gw0 = min(G, plan_wave_start(per_wave)), gw1 = min(G, gw0 + per_wave);
-    for (int32_t gr = gw0; gr < gw1; gr += kWave) {
-        const int32_t g = gr + lane;
-        const bool valid = g < gw1;
-        int64_t v[4] = {0, 0, 0, 0};
-        const int b = valid ? plan_values(pa, cnt[g], pa.off[g + 1] - pa.off[g], lch, v) : -1;
-        int64_t ex[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int64_t incl = wave_scan64(v[i]);
-            ex[i] = carry[i] + incl - v[i];
-            carry[i] += __shfl(incl, kWave - 1);
-        }
-        int32_t wl = -1;
-#pragma unroll
-        for (int bb = 0; bb < kItemBuckets; ++bb) {
-            const uint64_t m = __ballot(b == bb);
-            if (m) {
-                const int64_t bn = __shfl(bnext, bb);
-                if (b == bb) wl = (int32_t)(bn + __popcll(m & lt));
-                if (lane == bb) bnext += __popcll(m);
+        for (int i = 0; i < kChunkCands - 1; ++i) {
+            const int j = lmin + i;
+            uint64_t term = lane == kWave - 1 ? cb : 0;
+            bool over = false;
+            if (lane < kWave - 1 && lane >= j) {
+                const int sh = lane - j;
+                over = cb > (cap >> sh);
+                term = over ? 0 : cb << sh;
+            }
+            if (__ballot(over) == 0 && (uint64_t)wave_sum64((int64_t)term) <= cap) {
+                cand = i;
+                break;
             }
         }
-        if (valid) {
-            pa.qoff[g] = (int32_t)(ex[3] & 0xffffffff);
-            pa.wstart[g] = (int32_t)(ex[0] & 0xffffffff);
-            pa.wlast[g] = wl;
-            pa.pbase[g] = ex[1];
-            pa.gstart[g] = (int32_t)(ex[0] >> 32);
-            pa.ubase[g] = ex[2];
-            pa.mstart[g] = (int32_t)(ex[3] >> 32);
-        }
+        if (lane == 0) s_cand = cand;
     }
-    if (blockIdx.x == 0 && t == 0) {
-        pa.qoff[G] = (int32_t)(grand[3] & 0xffffffff);
-        pa.wstart[G] = (int32_t)n_full;
-        pa.gstart[G] = (int32_t)(grand[0] >> 32);
-        pa.mstart[G] = (int32_t)(grand[3] >> 32);
-        pa.plan->n_items = n_items;
-        pa.plan->n_parts = grand[1];
-        pa.plan->n_groups = grand[0] >> 32;
-        pa.plan->n_l1 = grand[2];
-        pa.plan->n_merge = grand[3] >> 32;
+    __syncthreads();
+    return lmin + s_cand;
+}
+
+// A cluster's count and segment, and the offsets check of cluster g.
+struct ClusterIn {
+    int64_t c, len;
+    bool bad;
+};
+__device__ __forceinline__ ClusterIn cluster_in(const PlanArgs &pa, const int32_t *cnt, int32_t g) {
+    ClusterIn ci;
+    const int64_t a0 = pa.off[g], a1 = pa.off[g + 1];
+    ci.c = cnt[g];
+    ci.len = a1 - a0;
+    ci.bad = a0 > a1;
+    // the tiled copy's header must match: segments padded to 16 rows
+    if (pa.toff) ci.bad |= pa.toff[g + 1] - pa.toff[g] != ((a1 - a0 + 15) & ~int64_t(15));
+    return ci;
+}
+
+__global__ __launch_bounds__(kRouteThreads) void route_plan(PlanArgs pa, const int32_t *cnt,
+                                                           const uint32_t *bits, int32_t nb2,
+                                                           int32_t rounds, int64_t *agg) {
+    constexpr int waves = kRouteThreads / kWave;
+    __shared__ int64_t sw[waves * kAgg];
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    const int32_t G = pa.G;
+    const int32_t per_wave = rounds * kWave;
+    const int32_t gw0 = min(G, (int32_t)(blockIdx.x * waves + wave) * per_wave);
+    const int32_t gw1 = min(G, gw0 + per_wave);
+    // the first round's cluster, loaded while the chunk length is chosen
+    // (and kept for the second pass)
+    ClusterIn c0{0, 0, false};
+    if (gw0 + lane < gw1) c0 = cluster_in(pa, cnt, gw0 + lane);
+    const int lch = route_chunk_log2(pa, bits, nb2);
+    if (blockIdx.x == 0 && t == 0) pa.plan->chunk = int64_t(1) << lch;
+    // pass 0: this wave's totals (lane b: its last chunks in bucket b);
+    // pass 1: block-local exclusive prefixes, from the waves before this one.
+    // One copy of the per-cluster code for both (it runs once per call: its
+    // instructions are fetched cold)
+    int64_t tot[4] = {0, 0, 0, 0}, carry[4] = {0, 0, 0, 0}, bcnt = 0, bnext = 0;
+    int bad = blockIdx.x == 0 && t == 0 &&
+              (pa.off[0] != 0 || pa.off[G] != pa.n_rows || (pa.toff && pa.toff[0] != 0));
+    const uint64_t lt = (uint64_t(1) << lane) - 1;
+#pragma unroll 1
+    for (int pass = 0; pass < 2; ++pass) {
+        if (pass == 1) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int64_t x = wave_sum64(tot[i]);
+                if (lane == 0) sw[wave * kAgg + i] = x;
+            }
+            if (lane < kItemBuckets) sw[wave * kAgg + 4 + lane] = bcnt;
+            const uint64_t bm = __ballot(bad != 0);
+            if (lane == 0) sw[wave * kAgg + kAgg - 1] = bm != 0;
+            __syncthreads();
+            if (t < kAgg) {
+                int64_t x = 0;
+#pragma unroll
+                for (int w = 0; w < waves; ++w) x += sw[w * kAgg + t];
+                agg[(int64_t)blockIdx.x * kAgg + t] = x;
+            }
+            for (int w = 0; w < wave; ++w) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) carry[i] += sw[w * kAgg + i];
+                if (lane < kItemBuckets) bnext += sw[w * kAgg + 4 + lane];
+            }
+        }
+        for (int32_t gr = gw0; gr < gw1; gr += kWave) {
+            const int32_t g = gr + lane;
+            const bool valid = g < gw1;
+            int64_t v[4] = {0, 0, 0, 0};
+            int b = -1;
+            if (valid) {
+                const ClusterIn ci = gr == gw0 ? c0 : cluster_in(pa, cnt, g);
+                bad |= ci.bad;
+                b = plan_values(pa, ci.c, ci.len, lch, v);
+            }
+            const bool any_last = __ballot(b >= 0) != 0;
+            if (pass == 0) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) tot[i] += v[i];
+#pragma unroll 1
+                for (int bb = 0; bb < (any_last ? kItemBuckets : 0); ++bb) {
+                    const uint64_t m = __ballot(b == bb);
+                    if (lane == bb) bcnt += __popcll(m);
+                }
+                continue;
+            }
+            int64_t ex[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int64_t incl = wave_scan64(v[i]);
+                ex[i] = carry[i] + incl - v[i];
+                carry[i] += __shfl(incl, kWave - 1);
+            }
+            int32_t wl = -1;                   // rank among the block's last chunks of bucket b, | b
+#pragma unroll 1
+            for (int bb = 0; bb < (any_last ? kItemBuckets : 0); ++bb) {
+                const uint64_t m = __ballot(b == bb);
+                if (m) {
+                    const int64_t bn = __shfl(bnext, bb);
+                    if (b == bb) wl = (int32_t)((bn + __popcll(m & lt)) << 4) | bb;
+                    if (lane == bb) bnext += __popcll(m);
+                }
+            }
+            if (valid) {
+                pa.qoff[g] = (int32_t)(ex[3] & 0xffffffff);
+                pa.mstart[g] = (int32_t)(ex[3] >> 32);
+                pa.wstart[g] = (int32_t)(ex[0] & 0xffffffff);
+                pa.gstart[g] = (int32_t)(ex[0] >> 32);
+                pa.pbase[g] = ex[1];
+                pa.ubase[g] = ex[2];
+                pa.wlast[g] = wl;
+            }
+        }
     }
 }
 
@@ -690,7 +692,7 @@ __device__ __forceinline__ MergeSlot merge_slot(int64_t e, int32_t i, int64_t nc
     ms.e = (int32_t)e;
     ms.stride = nq;
     ms.level = r > 0;
-    ms.n = (int32_t)(r > 0 ? (nch + r - 1) / r : nch);
+    ms.n = (int32_t)(r > 0 ? div_up32(nch, r) : nch);
     ms.p0 = (r > 0 ? ub : pb) + i;
     return ms;
 }
@@ -713,7 +715,15 @@ __device__ __forceinline__ MergeGroup merge_group_of(int32_t jg, int64_t nch, in
 // table, so that the blocks reach a cluster's chunks at different times and
 // the later ones start from the bounds the earlier ones published.
 __device__ __forceinline__ int32_t full_slot(int32_t w, int32_t n_full) {
-    return (int32_t)(((uint64_t)w * 2147483629ull) % (uint64_t)n_full);
+    // w p mod n = w (p mod n) mod n; the product of two values below n <
+    // 2^31 is reduced with a quotient estimated in double precision (off by
+    // at most one: the quotient is below 2^31) and corrected
+    const int64_t n = n_full, pm = (int64_t)(2147483629u % (uint32_t)n_full);
+    const int64_t x = (int64_t)w * pm;
+    int64_t r = x - (int64_t)((double)x / (double)n) * n;
+    r += r < 0 ? n : 0;
+    r -= r >= n ? n : 0;
+    return (int32_t)r;
 }
 
 // Work item j (a chunk of ch = 2^lch rows) of cluster g, whose segment starts
@@ -866,64 +876,110 @@ __global__ __launch_bounds__(kPlanThreads) void route_fused(PlanArgs pa, const i
     }
 }
 
-// Fills, from the plan and the per-cluster query lists, the item table of the
-// bank stream, the level-one merge groups and their work units, and the list
-// of pairs the merge finishes (clusters of several chunks, and empty ones):
-// one wave per cluster, spread over the lanes.
-__global__ __launch_bounds__(256) void route_items(PlanArgs pa, const int32_t *qlist,
-                                                   WorkItem *items, MergeGroup *groups,
-                                                   int2 *units, MergeSlot *mlist) {
-    const int lane = threadIdx.x & 63;
-    if (pa.plan->bad_off) return;              // malformed offsets: no work
-    const int64_t ch = pa.plan->chunk;
-    const int lch = 63 - __builtin_clzll((unsigned long long)ch);
-    const int64_t kp = pa.kp;
-    for (int64_t g = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); g < pa.G;
-         g += (int64_t)gridDim.x * 4) {
-        const int32_t qb = pa.qoff[g], nq = pa.qoff[g + 1] - qb;
-        if (nq == 0) continue;
-        const int64_t a = pa.off[g], len = pa.off[g + 1] - a;
-        const int64_t nch = (len + ch - 1) >> lch;
-        const int64_t r = group_span(nch, kp, pa.direct);
-        if (nch != 1) {
-            const int32_t m0 = pa.mstart[g];
-            const int64_t pb = pa.pbase[g], ub = pa.ubase[g];
-            for (int32_t i = lane; i < nq; i += kWave)
-                mlist[m0 + i] = merge_slot(qlist[qb + i], i, nch, r, nq, pb, ub);
-        }
-        if (nch == 0) continue;
-        const int32_t w0 = pa.wstart[g], wl = pa.wlast[g];
-        const int32_t gs = pa.gstart[g], ng = pa.gstart[g + 1] - gs;
-        const int64_t pb = pa.pbase[g], ub = pa.ubase[g];
-        const int64_t nfull = len >> lch;
-        const int32_t n_full = pa.wstart[pa.G];
-        for (int64_t j = lane; j < nch; j += kWave)
-            items[j < nfull ? full_slot(w0 + (int32_t)j, n_full) : wl] =
-                make_item((int32_t)g, j, a, len, lch, qb, nq, pb);
-        for (int32_t jg = lane; jg < ng; jg += kWave)
-            groups[gs + jg] = merge_group_of(jg, nch, r, nq, pb, ub);
-        for (int64_t x = lane; x < (int64_t)ng * nq; x += kWave) {
-            const int32_t jg = (int32_t)(x / nq), i = (int32_t)(x - (int64_t)jg * nq);
-            units[ub + x] = make_int2(gs + jg, i);
+// Finishes the routing, one thread per pair: the bases of each planning
+// block (a scan of agg, one lane per block) turn its local tables into
+// global ones; pair e, place i in the list of its cluster g (nq pairs), writes its list
+// entry, its merge-list entry and level-one units, and the cluster's work
+// items j and level-one groups jg with j, jg = i mod nq (a cluster's pairs
+// share its tables). Block 0 writes the plan's totals. Malformed offsets:
+// every slot is empty and the plan has no work.
+__global__ __launch_bounds__(kRouteThreads) void route_emit(PlanArgs pa, const int32_t *sel, int64_t n,
+                                                           const int32_t *cnt, const int32_t *pos,
+                                                           const int64_t *agg, int32_t nb3,
+                                                           int32_t per_block, int32_t *qlist,
+                                                           uint64_t *bound, SlotOut out,
+                                                           WorkItem *items, MergeGroup *groups,
+                                                           int2 *units, MergeSlot *mlist) {
+    constexpr int NB = kAgg - 1;               // per-block bases: the scanned values, the buckets
+    __shared__ int64_t s_base[kRouteBlocks * NB];
+    __shared__ int64_t s_tot[kAgg];
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    const int32_t G = pa.G;
+    const int64_t chunk = pa.plan->chunk;
+    // this thread's pair and its cluster's tables, loaded before the scan
+    const int64_t e = blockIdx.x * (int64_t)kRouteThreads + t;
+    const int32_t g = e < n ? sel[e] : -1;
+    const bool valid = g >= 0 && g < G;
+    int32_t i = 0, nq = 0, qoff = 0, mst = 0, wst = 0, gst = 0, code = -1;
+    int64_t a0 = 0, len = 0, pb = 0, ub = 0;
+    if (valid) {
+        i = pos[e];
+        nq = cnt[g];
+        a0 = pa.off[g];
+        len = pa.off[g + 1] - a0;
+        qoff = pa.qoff[g];
+        mst = pa.mstart[g];
+        wst = pa.wstart[g];
+        gst = pa.gstart[g];
+        code = pa.wlast[g];
+        pb = pa.pbase[g];
+        ub = pa.ubase[g];
+    }
+    constexpr int per = (kAgg + kRouteThreads / kWave - 1) / (kRouteThreads / kWave);
+    int64_t x[per];
+#pragma unroll
+    for (int j = 0; j < per; ++j) {
+        const int v = wave + j * (kRouteThreads / kWave);
+        x[j] = v < kAgg && lane < nb3 ? agg[(int64_t)lane * kAgg + v] : 0;
+    }
+#pragma unroll
+    for (int j = 0; j < per; ++j) {
+        const int v = wave + j * (kRouteThreads / kWave);
+        if (v < kAgg) {
+            const int64_t incl = wave_scan64(x[j]);
+            if (v < NB) s_base[lane * NB + v] = incl - x[j];
+            if (lane == kWave - 1) s_tot[v] = incl;
         }
     }
-}
-
-__global__ void route_scatter(const int32_t *sel, int64_t n, int32_t G, const int32_t *qoff,
-                              int32_t *cursor, int32_t *qlist, int32_t *pos, uint64_t *bound,
-                              SlotOut out, const Plan *plan) {
-    const bool none = plan->bad_off != 0;      // malformed offsets: every slot empty
-    for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < n;
-         e += (int64_t)gridDim.x * blockDim.x) {
-        const int32_t g = sel[e];
-        bound[e] = 0;
-        if (!none && g >= 0 && g < G) {
-            const int32_t slot = atomicAdd(&cursor[g], 1);
-            qlist[qoff[g] + slot] = (int32_t)e;
-            pos[e] = slot;
+    __syncthreads();
+    const int64_t n_full = s_tot[0] & 0xffffffff;
+    // items: every full-length chunk, then bucket by bucket (lane b of each
+    // row: the first item of bucket b)
+    const int64_t bt = s_tot[4 + (lane & 15)];
+    const int64_t bstart = n_full + row_scan64(bt) - bt;
+    const bool bad = s_tot[kAgg - 1] != 0;
+    if (blockIdx.x == 0 && t == kItemBuckets - 1) {
+        if (bad) {
+            plan_nothing(pa.plan);
         } else {
-            out.empty(e);
+            pa.plan->n_items = bstart + bt;
+            pa.plan->n_parts = s_tot[1];
+            pa.plan->n_groups = s_tot[0] >> 32;
+            pa.plan->n_l1 = s_tot[2];
+            pa.plan->n_merge = s_tot[3] >> 32;
         }
+    }
+    const int64_t bstart_b = __shfl(bstart, code & 15);   // lanes without a last chunk: unused
+    if (e >= n) return;
+    bound[e] = 0;
+    if (bad || !valid) {
+        out.empty(e);
+        return;
+    }
+    const int lch = 63 - __builtin_clzll((unsigned long long)chunk);
+    const int64_t ch = int64_t(1) << lch, kp = pa.kp;
+    const int64_t *bs = s_base + (g / per_block) * NB;
+    const int32_t qb = qoff + (int32_t)(bs[3] & 0xffffffff);
+    qlist[qb + i] = (int32_t)e;
+    const int64_t nch = len > 0 ? (len + ch - 1) >> lch : 0;
+    const int64_t r = group_span(nch, kp, pa.direct);
+    pb += bs[1];
+    ub += bs[2];
+    if (nch != 1) mlist[mst + (int32_t)(bs[3] >> 32) + i] = merge_slot(e, i, nch, r, nq, pb, ub);
+    if (r > 0) {                               // this pair's level-one units, one per group
+        const int32_t gs = gst + (int32_t)(bs[0] >> 32);
+        const int32_t ng = (int32_t)div_up32(nch, r);
+        for (int32_t jg = 0; jg < ng; ++jg) units[ub + (int64_t)jg * nq + i] = make_int2(gs + jg, i);
+        for (int32_t jg = i; jg < ng; jg += nq) groups[gs + jg] = merge_group_of(jg, nch, r, nq, pb, ub);
+    }
+    if (i < nch) {
+        const int64_t nfull = len >> lch;
+        const int32_t w0 = wst + (int32_t)(bs[0] & 0xffffffff);
+        const int32_t wl =
+            code < 0 ? -1 : (int32_t)(bstart_b + bs[4 + (code & 15)] + (code >> 4));
+        for (int64_t j = i; j < nch; j += nq)
+            items[j < nfull ? full_slot(w0 + (int32_t)j, (int32_t)n_full) : wl] =
+                make_item(g, j, a0, len, lch, qb, nq, pb);
     }
 }
 
@@ -1250,7 +1306,6 @@ AttendWs attend_layout(void *ws, int32_t d, int32_t G, int64_t N, int32_t key_by
     w.g_max = w.w_max / 2 + G + 1;
     w.u_cap = w.p_cap / 2 + bc;
     w.cnt = cv.take<int32_t>(G);
-    w.cursor = cv.take<int32_t>(G);
     w.qoff = cv.take<int32_t>(G + 1);
     w.wstart = cv.take<int32_t>(G + 1);
     w.wlast = cv.take<int32_t>(G);
@@ -1264,7 +1319,8 @@ AttendWs attend_layout(void *ws, int32_t d, int32_t G, int64_t N, int32_t key_by
     w.pos = cv.take<int32_t>(bc);
     w.bound = cv.take<uint64_t>(bc);
     w.plan = cv.take<Plan>(1);
-    w.ptot = cv.take<int64_t>(kMaxPlanBlocks * (kChunkCands + kPlanSW));
+    w.rbits = cv.take<uint32_t>(kCountBlocks * kWave);
+    w.ragg = cv.take<int64_t>(kRouteBlocks * kAgg);
     w.items = cv.take<WorkItem>(w.w_max);
     w.groups = cv.take<MergeGroup>(w.g_max);
     w.pm = cv.take<float>(w.p_cap);
@@ -1300,12 +1356,23 @@ __global__ void queries_to_bf16(const float *__restrict__ q, __bf16 *__restrict_
 }
 }  // namespace
 
-static hipError_t launch_stream(int32_t key_dtype, int32_t compute_dtype, const FineArgs &fa0,
-                                int64_t bc, int64_t n_rows, int n_cu, int64_t w_max,
-                                int32_t B, __bf16 *q16, KernelEvents ev, hipStream_t s) {
+// The streaming kernel and its launch shape for one call (nothing launched).
+struct StreamChoice {
+    StreamLaunch l;
+    int npl;
+    bool lds;          // an LDS-staged kernel (else the generic one)
+    bool two;          // two blocks per CU
+    bool q16;          // the split kernel with fp32 keys: stages a bf16 copy of the queries
+};
+
+static StreamChoice choose_stream(int32_t key_dtype, int32_t compute_dtype, const FineArgs &fa0,
+                                  int64_t bc, int64_t n_rows, int n_cu, int64_t w_max,
+                                  KernelEvents ev, hipStream_t s) {
     const size_t budget = lds_budget();
-    const int npl = fa0.cap / kWave;
-    StreamLaunch l{};
+    StreamChoice c{};
+    c.npl = fa0.cap / kWave;
+    const int npl = c.npl;
+    StreamLaunch &l = c.l;
     l.fa = fa0;
     l.ev = ev;
     l.stream = s;
@@ -1333,36 +1400,39 @@ static hipError_t launch_stream(int32_t key_dtype, int32_t compute_dtype, const 
             const int32_t qs_half = (int32_t)fine_qs_bytes(fa0.d / 2, 16);
             const size_t sm2 = qs_half + fine_state_bytes(16, fa0.cap, 2);
             if (2 * (sm2 + 256) <= budget + 256) {
-                if (key_dtype == kF32) {
-                    // every half of every row group stages its queries: from a
-                    // bf16 copy, half the bytes and one round trip
-                    const int64_t n8 = (int64_t)B * fa0.d / 8;
-                    const int64_t nb = (n8 + 255) / 256;
-                    hipLaunchKernelGGL(queries_to_bf16, dim3((unsigned)(nb < 4096 ? nb : 4096)),
-                                       dim3(256), 0, s, static_cast<const float *>(fa0.q), q16, n8);
-                    l.fa.q16 = q16;
-                }
+                // every half of every row group stages its queries: with fp32
+                // keys from a bf16 copy, half the bytes and one round trip
+                c.q16 = key_dtype == kF32;
                 l.ksplit = true;
                 l.fa.ntile = 2;
                 l.qs_bytes = qs_half;
                 l.smem = sm2;
-                return key_dtype == kF32 ? launch_stream_lds_f32(npl, false, l)
-                                         : launch_stream_lds_bf16(npl, false, l);
+                c.lds = true;
+                return c;
             }
         }
         // one block per CU: producer/consumer blocks (their load units are
         // 8 k-steps for bf16 keys, 4 for fp32: d % 256 or d % 128)
         l.producer_consumer = !two && npl <= 4;
         const int unit_k = key_dtype == kF32 ? 8 : 16;
-        if (two || l.producer_consumer || fa0.d % (32 * unit_k) == 0)
-            return key_dtype == kF32 ? launch_stream_lds_f32(npl, two, l)
-                                     : launch_stream_lds_bf16(npl, two, l);
+        if (two || l.producer_consumer || fa0.d % (32 * unit_k) == 0) {
+            c.lds = true;
+            c.two = two;
+            return c;
+        }
     }
     l.fa.qmax = qmax_generic(fa0.cap);
     l.fa.ntile = 2;
     l.qs_bytes = 0;
     l.smem = fine_state_bytes(l.fa.qmax, fa0.cap, 2);
-    return launch_stream_generic(key_dtype, compute_dtype, npl, l);
+    return c;
+}
+
+static hipError_t launch_stream(int32_t key_dtype, int32_t compute_dtype, const StreamChoice &c) {
+    if (c.lds)
+        return key_dtype == kF32 ? launch_stream_lds_f32(c.npl, c.two, c.l)
+                                 : launch_stream_lds_bf16(c.npl, c.two, c.l);
+    return launch_stream_generic(key_dtype, compute_dtype, c.npl, c.l);
 }
 
 // Merge grids: enough resident waves to cover the GPU several times over, or
@@ -1399,7 +1469,6 @@ hipError_t launch_attend(int32_t key_dtype, int32_t compute_dtype, int32_t d, in
                          int n_cu, KernelEvents ev, hipStream_t s) {
     const int64_t bc = (int64_t)B * c;
     const float cexp = 1.4426950408889634f / tau;
-    const int gblocks = (int)((bc + 255) / 256 < 4096 ? (bc + 255) / 256 : 4096);
     PlanArgs pa{};
     pa.G = G;
     pa.n_rows = N;
@@ -1426,38 +1495,6 @@ hipError_t launch_attend(int32_t key_dtype, int32_t compute_dtype, int32_t d, in
     const bool groups = group_span(nch_max, pa.kp, kMergeDirectSmall * req) > 0;
     pa.direct = (groups ? kMergeDirect : kMergeDirectSmall) * req;
     const SlotOut so{slot_max, slot_sum, cand_score, cand_id, k};
-    const size_t route_lds = route_fused_lds(G, bc);
-    static_assert((3 * (size_t)kNoCluster + 1) * 8 > kRouteLdsBytes, "fused routing keeps cluster ids in 16 bits");
-    if (bc <= kFusedRoutePairs && route_lds <= kRouteLdsBytes) {
-        hipError_t e0 = hipFuncSetAttribute((const void *)route_fused,
-                                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)route_lds);
-        if (e0 != hipSuccess) return e0;
-        hipLaunchKernelGGL(route_fused, dim3(1), dim3(kPlanThreads), route_lds, s, pa, sel, bc,
-                           w.qlist, w.pos, w.bound, so, w.items, w.groups, w.units, w.mlist);
-    } else {
-        hipLaunchKernelGGL(route_init, dim3((G + 255) / 256 < 1024 ? (G + 255) / 256 : 1024),
-                           dim3(256), 0, s, G, w.cnt, w.cursor, w.plan);
-        hipLaunchKernelGGL(route_count, dim3(gblocks), dim3(256), 0, s, sel, bc, G, w.cnt, w.plan);
-        // planning over nb blocks of 16 waves, each wave per_wave clusters
-        const int64_t rounds = ((int64_t)G + kMaxPlanBlocks * kPlanThreads - 1) /
-                               (kMaxPlanBlocks * kPlanThreads);
-        const int32_t per_wave = (int32_t)(rounds * kWave);
-        const int32_t nb = (int32_t)(((int64_t)G + (int64_t)per_wave * (kPlanThreads / kWave) - 1) /
-                                     ((int64_t)per_wave * (kPlanThreads / kWave)));
-        hipLaunchKernelGGL(route_plan_partials, dim3(nb), dim3(kPlanThreads), 0, s, pa, w.cnt,
-                           per_wave, w.ptot);
-        hipLaunchKernelGGL(route_plan_totals, dim3(nb), dim3(kPlanThreads), 0, s, pa, w.cnt,
-                           per_wave, nb, w.ptot, w.ptot + kMaxPlanBlocks * kChunkCands);
-        hipLaunchKernelGGL(route_plan_apply, dim3(nb), dim3(kPlanThreads), 0, s, pa, w.cnt,
-                           per_wave, nb, w.ptot + kMaxPlanBlocks * kChunkCands);
-        hipLaunchKernelGGL(route_scatter, dim3(gblocks), dim3(256), 0, s, sel, bc, G, w.qoff,
-                           w.cursor, w.qlist, w.pos, w.bound, so, w.plan);
-        hipLaunchKernelGGL(route_items, dim3((G + 3) / 4 < 2048 ? (G + 3) / 4 : 2048), dim3(256), 0,
-                           s, pa, w.qlist, w.items, w.groups, w.units, w.mlist);
-    }
-    hipError_t err = hipGetLastError();
-    if (err != hipSuccess) return err;
-
     FineArgs fa{};
     fa.keys = fine_keys;
     if (fine_keys_tiled) {          // the header of segment starts, then the tiles
@@ -1487,7 +1524,48 @@ hipError_t launch_attend(int32_t key_dtype, int32_t compute_dtype, int32_t d, in
     fa.slot_sum = slot_sum;
     fa.cand_score = cand_score;
     fa.cand_id = cand_id;
-    err = launch_stream(key_dtype, compute_dtype, fa, bc, N, n_cu, w.w_max, B, w.q16, ev, s);
+    StreamChoice sc = choose_stream(key_dtype, compute_dtype, fa, bc, N, n_cu, w.w_max, ev, s);
+    const int64_t n8 = sc.q16 ? (int64_t)B * d / 8 : 0;
+    if (sc.q16) sc.l.fa.q16 = w.q16;
+
+    const size_t route_lds = route_fused_lds(G, bc);
+    static_assert((3 * (size_t)kNoCluster + 1) * 8 > kRouteLdsBytes, "fused routing keeps cluster ids in 16 bits");
+    if (bc <= kFusedRoutePairs && route_lds <= kRouteLdsBytes) {
+        hipError_t e0 = hipFuncSetAttribute((const void *)route_fused,
+                                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)route_lds);
+        if (e0 != hipSuccess) return e0;
+        hipLaunchKernelGGL(route_fused, dim3(1), dim3(kPlanThreads), route_lds, s, pa, sel, bc,
+                           w.qlist, w.pos, w.bound, so, w.items, w.groups, w.units, w.mlist);
+        if (sc.q16) {
+            const int64_t nb = (n8 + 255) / 256;
+            hipLaunchKernelGGL(queries_to_bf16, dim3((unsigned)(nb < 8192 ? nb : 8192)), dim3(256),
+                               0, s, static_cast<const float *>(q), w.q16, n8);
+        }
+    } else {
+        // zero the counters (and round the queries), count the pairs, plan per
+        // block of clusters, then emit the lists and tables pair by pair
+        const int64_t nz = (n8 > G ? n8 : (int64_t)G) + 255;
+        hipLaunchKernelGGL(route_zero, dim3((unsigned)(nz / 256 < 8192 ? nz / 256 : 8192)), dim3(256),
+                           0, s, G, w.cnt, w.plan, static_cast<const float *>(q), w.q16, n8);
+        const int64_t nb2 = (bc + kCountThreads - 1) / kCountThreads;
+        const int32_t nc2 = (int32_t)(nb2 < kCountBlocks ? nb2 : kCountBlocks);
+        const int lmin = 63 - __builtin_clzll((unsigned long long)pa.chunk_min);
+        hipLaunchKernelGGL(route_count, dim3(nc2), dim3(kCountThreads), 0, s, sel, bc, G, seg_offsets,
+                           lmin, w.cnt, w.pos, w.plan, w.rbits);
+        const int32_t rounds = (int32_t)(((int64_t)G + kRouteBlocks * kRouteThreads - 1) /
+                                         ((int64_t)kRouteBlocks * kRouteThreads));
+        const int32_t per_block = rounds * kRouteThreads;
+        const int32_t nb3 = (int32_t)(((int64_t)G + per_block - 1) / per_block);
+        hipLaunchKernelGGL(route_plan, dim3(nb3), dim3(kRouteThreads), 0, s, pa, w.cnt, w.rbits, nc2,
+                           rounds, w.ragg);
+        const int64_t nb4 = (bc + kRouteThreads - 1) / kRouteThreads;
+        hipLaunchKernelGGL(route_emit, dim3((unsigned)nb4), dim3(kRouteThreads),
+                           0, s, pa, sel, bc, w.cnt, w.pos, w.ragg, nb3, per_block, w.qlist,
+                           w.bound, so, w.items, w.groups, w.units, w.mlist);
+    }
+    hipError_t err = hipGetLastError();
+    if (err != hipSuccess) return err;
+    err = launch_stream(key_dtype, compute_dtype, sc);
     if (err != hipSuccess) return err;
 
     MergeArgs ma{};
@@ -1511,8 +1589,8 @@ hipError_t launch_attend(int32_t key_dtype, int32_t compute_dtype, int32_t d, in
     ma.slot_sum = slot_sum;
     ma.cand_score = cand_score;
     ma.cand_id = cand_id;
-    // a buffer of 128 keys for k >= 48 would leave at most 80 free after each
-    // compaction: 256 (zipf_large_bf16, k = 64: merges 89 -> 56 us)
+    // k >= 48: 256-key buffers (a 128-key one has at most 80 free slots
+    // after each compaction; zipf_large_bf16, k = 64: merges 89 -> 56 us)
     switch (next_pow2(k + kWave) / kWave) {
         case 2: return k >= 48 ? launch_merge<4>(ma, w.u_cap, groups, n_cu, s)
                                : launch_merge<2>(ma, w.u_cap, groups, n_cu, s);

@@ -195,10 +195,11 @@ hipError_t launch_sampled(int32_t key_dtype, int32_t compute_dtype, int32_t d, i
 // ---- fine stage (routing + bank stream + per-slot merge) ----------------------
 struct AttendWs {
     int32_t *cnt;      // [G] queries per cluster
-    int32_t *cursor;   // [G]
+    // per-cluster tables of the routing (block-local prefixes on the
+    // multi-block path, which adds the planning blocks' bases as it reads them)
     int32_t *qoff;     // [G+1]
     int32_t *wstart;   // [G+1] first full-length chunk item of each cluster
-    int32_t *wlast;    // [G]   item of each cluster's shorter last chunk (-1: none)
+    int32_t *wlast;    // [G]   the cluster's shorter last chunk (-1: none)
     int32_t *gstart;   // [G+1] first level-one merge group of each cluster
     int64_t *pbase;    // [G]   first partial of each cluster
     int64_t *ubase;    // [G]   first level-one merge result of each cluster
@@ -209,7 +210,8 @@ struct AttendWs {
     int32_t *pos;      // [B*c] position of each entry inside its cluster's list
     uint64_t *bound;   // [B*c] per pair: a key at or below its k-th best, raised as chunks finish
     Plan *plan;
-    int64_t *ptot;     // planner: per-block partial sums and totals
+    uint32_t *rbits;   // multi-block routing: per counting block, bit counts of segment lengths
+    int64_t *ragg;     //   and per planning block, its totals
     WorkItem *items;   // [w_max]
     MergeGroup *groups;// [g_max]
     float *pm;         // [p_cap] partial max
