@@ -65,11 +65,24 @@ __host__ __device__ inline int64_t group_count(int64_t nch, int64_t kp, int64_t 
 // ---------------------------------------------------------------------------
 // routing
 // ---------------------------------------------------------------------------
-// Clears the per-cluster pair counters and the plan's flags; with q16 given,
-// also rounds the fp32 queries to bf16 (to nearest even, as the LDS staging
-// rounds them), 8 elements per thread, for the streaming kernel.
-__global__ void route_zero(int32_t G, int32_t *cnt, Plan *plan, const float *__restrict__ q,
-                           __bf16 *__restrict__ q16, int64_t n8) {
+// A slice of the fp32 queries' bf16 copy (8-element groups [begin, end),
+// rounded to nearest even as the LDS staging rounds them). The routing
+// kernels wait mostly on memory latency on a few blocks; blocks past their
+// routing grid copy a slice each, so the copy's bandwidth hides in that wait.
+struct QCopy {
+    const float *q;
+    __bf16 *q16;
+    int64_t begin, end;
+};
+__device__ __forceinline__ void copy_queries(const QCopy &qc, int64_t blk, int64_t nblk) {
+    for (int64_t i = qc.begin + blk * blockDim.x + threadIdx.x; i < qc.end;
+         i += nblk * blockDim.x)
+        reinterpret_cast<bf16x8_t *>(qc.q16)[i] = load8(qc.q + i * 8);
+}
+
+// Clears the per-cluster pair counters and the plan's flags (and copies a
+// slice of the queries).
+__global__ void route_zero(int32_t G, int32_t *cnt, Plan *plan, QCopy qc) {
     const int64_t i0 = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t i = i0; i < G; i += stride) cnt[i] = 0;
@@ -78,8 +91,7 @@ __global__ void route_zero(int32_t G, int32_t *cnt, Plan *plan, const float *__r
         plan->bad_sel = 0;
         plan->bad_off = 0;
     }
-    for (int64_t i = i0; i < n8; i += stride)
-        reinterpret_cast<bf16x8_t *>(q16)[i] = load8(q + i * 8);
+    copy_queries(qc, blockIdx.x, gridDim.x);
 }
 
 // Most blocks of the planning kernel (one wave scans their totals) and of
@@ -99,7 +111,11 @@ constexpr int kRouteThreads = 256;
 __global__ __launch_bounds__(kCountThreads) void route_count(const int32_t *sel, int64_t n, int32_t G,
                                                             const int64_t *off, int lmin,
                                                             int32_t *cnt, int32_t *pos, Plan *plan,
-                                                            uint32_t *bits) {
+                                                            uint32_t *bits, int32_t n_route, QCopy qc) {
+    if ((int32_t)blockIdx.x >= n_route) {
+        copy_queries(qc, blockIdx.x - n_route, gridDim.x - n_route);
+        return;
+    }
     __shared__ uint32_t s_bits[kWave];
     const int t = threadIdx.x, lane = t & 63;
     if (t < kWave) s_bits[t] = 0;
@@ -107,7 +123,7 @@ __global__ __launch_bounds__(kCountThreads) void route_count(const int32_t *sel,
     uint32_t acc = 0;      // lane b: pairs with bit b of len - 1 set; lane 63: pairs with len > 0
     int32_t nbad = 0;
     for (int64_t e0 = (int64_t)blockIdx.x * kCountThreads; e0 < n;
-         e0 += (int64_t)gridDim.x * kCountThreads) {
+         e0 += (int64_t)n_route * kCountThreads) {
         const int64_t e = e0 + t;
         const int32_t g = e < n ? sel[e] : 0;
         const bool valid = e < n && g >= 0 && g < G;
@@ -578,7 +594,12 @@ __device__ __forceinline__ ClusterIn cluster_in(const PlanArgs &pa, const int32_
 
 __global__ __launch_bounds__(kRouteThreads) void route_plan(PlanArgs pa, const int32_t *cnt,
                                                            const uint32_t *bits, int32_t nb2,
-                                                           int32_t rounds, int64_t *agg) {
+                                                           int32_t rounds, int64_t *agg,
+                                                           int32_t n_route, QCopy qc) {
+    if ((int32_t)blockIdx.x >= n_route) {
+        copy_queries(qc, blockIdx.x - n_route, gridDim.x - n_route);
+        return;
+    }
     constexpr int waves = kRouteThreads / kWave;
     __shared__ int64_t sw[waves * kAgg];
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
@@ -889,7 +910,12 @@ __global__ __launch_bounds__(kRouteThreads) void route_emit(PlanArgs pa, const i
                                                            int32_t per_block, int32_t *qlist,
                                                            uint64_t *bound, SlotOut out,
                                                            WorkItem *items, MergeGroup *groups,
-                                                           int2 *units, MergeSlot *mlist) {
+                                                           int2 *units, MergeSlot *mlist,
+                                                           int32_t n_route, QCopy qc) {
+    if ((int32_t)blockIdx.x >= n_route) {
+        copy_queries(qc, blockIdx.x - n_route, gridDim.x - n_route);
+        return;
+    }
     constexpr int NB = kAgg - 1;               // per-block bases: the scanned values, the buckets
     __shared__ int64_t s_base[kRouteBlocks * NB];
     __shared__ int64_t s_tot[kAgg];
@@ -1542,26 +1568,36 @@ hipError_t launch_attend(int32_t key_dtype, int32_t compute_dtype, int32_t d, in
                                0, s, static_cast<const float *>(q), w.q16, n8);
         }
     } else {
-        // zero the counters (and round the queries), count the pairs, plan per
-        // block of clusters, then emit the lists and tables pair by pair
-        const int64_t nz = (n8 > G ? n8 : (int64_t)G) + 255;
-        hipLaunchKernelGGL(route_zero, dim3((unsigned)(nz / 256 < 8192 ? nz / 256 : 8192)), dim3(256),
-                           0, s, G, w.cnt, w.plan, static_cast<const float *>(q), w.q16, n8);
+        // zero the counters, count the pairs, plan per block of clusters, then
+        // emit the lists and tables pair by pair; each launch also copies a
+        // quarter of the queries to bf16 on blocks past its routing grid
+        QCopy qc[4];
+        unsigned ncopy[4];
+        for (int j = 0; j < 4; ++j) {
+            qc[j] = QCopy{static_cast<const float *>(q), w.q16, n8 * j / 4, n8 * (j + 1) / 4};
+            const int64_t nb = (qc[j].end - qc[j].begin + 1023) / 1024;   // 4 groups per thread
+            ncopy[j] = (unsigned)(nb < 2048 ? nb : 2048);
+        }
+        const int64_t nz = ((int64_t)G + 255) / 256;
+        hipLaunchKernelGGL(route_zero, dim3((unsigned)(nz < 1024 ? nz : 1024) + ncopy[0]), dim3(256), 0,
+                           s, G, w.cnt, w.plan, qc[0]);
         const int64_t nb2 = (bc + kCountThreads - 1) / kCountThreads;
         const int32_t nc2 = (int32_t)(nb2 < kCountBlocks ? nb2 : kCountBlocks);
         const int lmin = 63 - __builtin_clzll((unsigned long long)pa.chunk_min);
-        hipLaunchKernelGGL(route_count, dim3(nc2), dim3(kCountThreads), 0, s, sel, bc, G, seg_offsets,
-                           lmin, w.cnt, w.pos, w.plan, w.rbits);
+        // the copy blocks of the counting kernel are 1024 threads too: a
+        // quarter as many
+        hipLaunchKernelGGL(route_count, dim3((unsigned)nc2 + (ncopy[1] + 3) / 4), dim3(kCountThreads), 0,
+                           s, sel, bc, G, seg_offsets, lmin, w.cnt, w.pos, w.plan, w.rbits, nc2, qc[1]);
         const int32_t rounds = (int32_t)(((int64_t)G + kRouteBlocks * kRouteThreads - 1) /
                                          ((int64_t)kRouteBlocks * kRouteThreads));
         const int32_t per_block = rounds * kRouteThreads;
         const int32_t nb3 = (int32_t)(((int64_t)G + per_block - 1) / per_block);
-        hipLaunchKernelGGL(route_plan, dim3(nb3), dim3(kRouteThreads), 0, s, pa, w.cnt, w.rbits, nc2,
-                           rounds, w.ragg);
+        hipLaunchKernelGGL(route_plan, dim3((unsigned)nb3 + ncopy[2]), dim3(kRouteThreads), 0, s, pa,
+                           w.cnt, w.rbits, nc2, rounds, w.ragg, nb3, qc[2]);
         const int64_t nb4 = (bc + kRouteThreads - 1) / kRouteThreads;
-        hipLaunchKernelGGL(route_emit, dim3((unsigned)nb4), dim3(kRouteThreads),
-                           0, s, pa, sel, bc, w.cnt, w.pos, w.ragg, nb3, per_block, w.qlist,
-                           w.bound, so, w.items, w.groups, w.units, w.mlist);
+        hipLaunchKernelGGL(route_emit, dim3((unsigned)nb4 + ncopy[3]), dim3(kRouteThreads), 0, s, pa,
+                           sel, bc, w.cnt, w.pos, w.ragg, nb3, per_block, w.qlist, w.bound, so,
+                           w.items, w.groups, w.units, w.mlist, (int32_t)nb4, qc[3]);
     }
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
