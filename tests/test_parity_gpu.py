@@ -307,6 +307,35 @@ def test_level_one_merge_groups():
     run_case(spec, gen_device="cuda", check_build=False)
 
 
+def test_chunk_choice_many_blocks():
+    """The multi-block routing (more than 8,192 (query, slot) pairs) choosing
+    a chunk past its first candidates: one 200K-row cluster next to 15 of 10K
+    rows, 4,200 queries, c = 2. At the shortest candidate chunk the partial
+    results would exceed the buffer (4 B c of them; asserted here from the
+    selection), so the chunk comes from the length-bit counts at a later
+    candidate. Every row that selected the large cluster (up to 256) and 256
+    seeded others are checked against the oracle."""
+    sizes = tuple([200_000] + [10_000] * 15)
+    spec = synth.Spec("chunks", B=4200, d=64, G=len(sizes), N=sum(sizes), top_c=2, top_k=128,
+                      tau=0.5, storage="bf16", compute="bf16", sizes="fixed", fixed_sizes=sizes)
+    n_cu = torch.cuda.get_device_properties(0).multi_processor_count
+    chunk_min = 64
+    while chunk_min * 2 <= spec.N // n_cu and chunk_min * 2 <= 4096:
+        chunk_min *= 2
+
+    def pick(gpu, seg):
+        sel = gpu["sel"]
+        parts = int(np.sum(-(-seg[sel] // chunk_min)))
+        assert parts > 4 * sel.size, "the shortest chunk must not fit the partial buffer"
+        big = np.flatnonzero((sel == 0).any(axis=1))
+        assert big.size >= 16, "the large cluster must be selected"
+        rest = np.setdiff1d(np.arange(spec.B), big)
+        rng = np.random.default_rng(0)
+        return np.sort(np.concatenate([big[:256], rng.choice(rest, 256, replace=False)]))
+
+    run_case(spec, gen_device="cuda", check_build=False, rows=pick)
+
+
 def test_level_one_merge_groups_selected():
     """The workload above selects its large cluster (so the two-level merge ran)."""
     from paper_2605_29734_amd import htam
