@@ -204,7 +204,8 @@ def bench_alt(args, spec, w, bank):
                                              out=r.sel, ws=wsp)
             marks[i][1].record()
             htam.htam_attend_transitions(bank, q, r.sel[0], r.tau, r.k, out=r.slots, ws=r.ws_attend)
-            htam.htam_topk(r.slots[2], r.slots[3], r.k, r.slots[0], r.slots[1], r.tau, out=r.rows)
+            htam.htam_topk(r.slots[2], r.slots[3], r.k, r.slots[0], r.slots[1], r.tau, out=r.rows,
+                           sorted_lists=True)
     marks = [[mk(), mk()] for _ in range(K)] + [[mk()]]
     ev = [(mk(), mk()) for _ in range((K + E - 1) // E)]
     for a, b in ev:
@@ -486,7 +487,8 @@ def main():
         htam.htam_attend_transitions(bk, q, r.sel[0], r.tau, r.k, out=r.slots, ws=r.ws_attend)
         if stamped:
             marks[i][2].record()
-        htam.htam_topk(r.slots[2], r.slots[3], r.k, r.slots[0], r.slots[1], r.tau, out=r.rows)
+        htam.htam_topk(r.slots[2], r.slots[3], r.k, r.slots[0], r.slots[1], r.tau, out=r.rows,
+                       sorted_lists=True)
     marks[K][0].record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0

@@ -439,6 +439,27 @@ htam_status htam_topk(int32_t n_rows, int32_t n_lists, int32_t k_in, const float
                       hipStream_t stream);
 
 /*
+ * htam_topk_sorted -- htam_topk for lists that are each sorted, as
+ * htam_attend_transitions returns its per-slot lists: by descending score,
+ * ties to the lower id, padding (id -1) only at the end of a list (with
+ * cand_id NULL: by descending score, ties to the lower position). The same
+ * arguments and the same outputs as htam_topk on such lists, bit for bit.
+ * With m = ceil(top_k / n_lists), at least top_k entries score at least the
+ * lowest of the lists' m-th entries, so no entry below it can be among the
+ * top_k (the argmax of Eq. local policy widened to top_k needs only the best
+ * entries of each list); each list is read only as far as its entries can
+ * still reach the row's top_k. Lists that are not sorted give undefined
+ * (but in-bounds) results. Rows of more than 64 lists, or of lists shorter
+ * than 128 entries, are merged as by htam_topk.
+ */
+htam_status htam_topk_sorted(int32_t n_rows, int32_t n_lists, int32_t k_in,
+                             const float *cand_score, const int32_t *cand_id,
+                             const float *slot_max, const float *slot_sum, float tau,
+                             int32_t top_k, int32_t *out_id, float *out_score, float *out_weight,
+                             float *row_max, float *row_sum, int32_t *out_count,
+                             hipStream_t stream);
+
+/*
  * htam_retrieve_flat -- flat memory retrieval: the baseline without a
  * hierarchy, in which every record of the memory is a candidate of every
  * query (the "Flat Memory Retrieval" row of Table 1 and App. C.4; the

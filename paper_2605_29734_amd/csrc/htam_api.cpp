@@ -534,12 +534,12 @@ HTAM_API htam_status htam_retrieve_flat(const htam_bank *bank, const void *q, in
 }
 
 // ---------------------------------------------------------------------------
-HTAM_API htam_status htam_topk(int32_t n_rows, int32_t n_lists, int32_t k_in,
-                               const float *cand_score, const int32_t *cand_id,
-                               const float *slot_max, const float *slot_sum, float tau,
-                               int32_t top_k, int32_t *out_id, float *out_score,
-                               float *out_weight, float *row_max, float *row_sum,
-                               int32_t *out_count, hipStream_t stream) {
+static htam_status topk_entry(int32_t n_rows, int32_t n_lists, int32_t k_in,
+                              const float *cand_score, const int32_t *cand_id,
+                              const float *slot_max, const float *slot_sum, float tau,
+                              int32_t top_k, int32_t *out_id, float *out_score, float *out_weight,
+                              float *row_max, float *row_sum, int32_t *out_count,
+                              hipStream_t stream, bool sorted_lists, const char *name) {
     if (n_rows < 0 || n_lists < 1 || k_in < 1)
         return fail(HTAM_ERR_SHAPE, "n_rows %d, n_lists %d, k_in %d: need n_rows >= 0, n_lists >= 1, k_in >= 1",
                     n_rows, n_lists, k_in);
@@ -557,8 +557,30 @@ HTAM_API htam_status htam_topk(int32_t n_rows, int32_t n_lists, int32_t k_in,
     return device_status(htam::launch_topk(n_rows, n_lists, k_in, cand_score, cand_id, slot_max,
                                            slot_sum, slot_max ? tau : 1.0f, top_k, out_id,
                                            out_score, out_weight, row_max, row_sum, out_count,
-                                           stream),
-                         "htam_topk");
+                                           stream, sorted_lists),
+                         name);
+}
+
+HTAM_API htam_status htam_topk(int32_t n_rows, int32_t n_lists, int32_t k_in,
+                               const float *cand_score, const int32_t *cand_id,
+                               const float *slot_max, const float *slot_sum, float tau,
+                               int32_t top_k, int32_t *out_id, float *out_score,
+                               float *out_weight, float *row_max, float *row_sum,
+                               int32_t *out_count, hipStream_t stream) {
+    return topk_entry(n_rows, n_lists, k_in, cand_score, cand_id, slot_max, slot_sum, tau, top_k,
+                      out_id, out_score, out_weight, row_max, row_sum, out_count, stream, false,
+                      "htam_topk");
+}
+
+HTAM_API htam_status htam_topk_sorted(int32_t n_rows, int32_t n_lists, int32_t k_in,
+                                      const float *cand_score, const int32_t *cand_id,
+                                      const float *slot_max, const float *slot_sum, float tau,
+                                      int32_t top_k, int32_t *out_id, float *out_score,
+                                      float *out_weight, float *row_max, float *row_sum,
+                                      int32_t *out_count, hipStream_t stream) {
+    return topk_entry(n_rows, n_lists, k_in, cand_score, cand_id, slot_max, slot_sum, tau, top_k,
+                      out_id, out_score, out_weight, row_max, row_sum, out_count, stream, true,
+                      "htam_topk_sorted");
 }
 
 // ---------------------------------------------------------------------------

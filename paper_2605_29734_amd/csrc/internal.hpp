@@ -292,9 +292,13 @@ hipError_t launch_flat(int32_t key_dtype, int32_t compute_dtype, int32_t d, int6
 int32_t report_error(int32_t status, const char *msg);
 
 // ---- top-k merge -----------------------------------------------------------
+// sorted_lists: every list is sorted by descending (score, lower id) with its
+// padding at the end (htam_attend_transitions' per-slot lists), so a row
+// reads each list only as far as its entries can still reach the top_k.
 hipError_t launch_topk(int32_t rows, int32_t lists, int32_t k_in, const float *score,
                        const int32_t *id, const float *slot_max, const float *slot_sum, float tau,
                        int32_t top_k, int32_t *out_id, float *out_score, float *out_weight,
-                       float *row_max, float *row_sum, int32_t *out_count, hipStream_t s);
+                       float *row_max, float *row_sum, int32_t *out_count, hipStream_t s,
+                       bool sorted_lists = false);
 
 }  // namespace htam

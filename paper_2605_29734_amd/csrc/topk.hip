@@ -31,6 +31,48 @@ struct TopkArgs {
     int32_t *out_count;
 };
 
+// The end of a row's merge, common to the row kernels: the merged softmax
+// statistics of the row's lists (lane l holds list l's (lm, lz) for l < 64;
+// more lists are read here), then the buffer's top_k sorted and written with
+// their weights.
+template <int NPL>
+__device__ __forceinline__ void finish_row(const TopkArgs &a, int64_t row, uint64_t *buf, int cnt,
+                                           int total, float lm, float lz, int lane) {
+    static_assert(kTopkStatLists == 1, "one 64-list group of statistics loaded with the keys");
+    float M = -INFINITY, Z = 0.0f;
+    if (a.slot_max) {
+        mz_merge(M, Z, lm, lz, a.cexp);
+        for (int l = kWave + lane; l < a.lists; l += kWave)
+            mz_merge(M, Z, a.slot_max[row * a.lists + l], a.slot_sum[row * a.lists + l], a.cexp);
+        for (int sh = 32; sh >= 1; sh >>= 1) {
+            const float m2 = __shfl_xor(M, sh), z2 = __shfl_xor(Z, sh);
+            mz_merge(M, Z, m2, z2, a.cexp);
+        }
+    }
+
+    wave_lds_sync();
+    uint64_t v[NPL];
+    sort_buffer<NPL>(buf, cnt, v, lane);
+    const int kept = cnt < a.top_k ? cnt : a.top_k;
+#pragma unroll
+    for (int q = 0; q < NPL; ++q) {
+        const int r = q * kWave + lane;
+        if (r < a.top_k) {
+            const bool ok = r < kept;
+            const float sv = ok ? key_score(v[q]) : -INFINITY;
+            a.out_id[row * a.top_k + r] = ok ? key_id(v[q]) : -1;
+            if (a.out_score) a.out_score[row * a.top_k + r] = sv;
+            if (a.out_weight)
+                a.out_weight[row * a.top_k + r] = ok ? exp2f((sv - M) * a.cexp) / Z : 0.0f;
+        }
+    }
+    if (lane == 0) {
+        if (a.row_max) a.row_max[row] = M;
+        if (a.row_sum) a.row_sum[row] = Z;
+        if (a.out_count) a.out_count[row] = total < a.top_k ? total : a.top_k;
+    }
+}
+
 // cap = 64 * NPL >= top_k + 64 keys of LDS per wave.
 template <int NPL>
 __global__ __launch_bounds__(kWave * kTopkWaves) void topk_rows(TopkArgs a) {
@@ -85,40 +127,127 @@ __global__ __launch_bounds__(kWave * kTopkWaves) void topk_rows(TopkArgs a) {
         }
     }
 
-    // merged softmax statistics of the row's lists
-    float M = -INFINITY, Z = 0.0f;
-    if (a.slot_max) {
-#pragma unroll
-        for (int i = 0; i < kTopkStatLists; ++i) mz_merge(M, Z, lm[i], lz[i], a.cexp);
-        for (int l = kTopkStatLists * kWave + lane; l < a.lists; l += kWave)
-            mz_merge(M, Z, a.slot_max[row * a.lists + l], a.slot_sum[row * a.lists + l], a.cexp);
-        for (int sh = 32; sh >= 1; sh >>= 1) {
-            const float m2 = __shfl_xor(M, sh), z2 = __shfl_xor(Z, sh);
-            mz_merge(M, Z, m2, z2, a.cexp);
-        }
-    }
+    finish_row<NPL>(a, row, buf, cnt, total, lm[0], lz[0], lane);
+}
 
-    wave_lds_sync();
-    uint64_t v[NPL];
-    sort_buffer<NPL>(buf, cnt, v, lane);
-    const int kept = cnt < a.top_k ? cnt : a.top_k;
+// Row top-k over lists that are each sorted by descending key (score, then
+// the lower id) with their padding (id < 0) at the end, as
+// htam_attend_transitions writes them. With m = ceil(top_k / lists), each
+// list's first m keys are at least its m-th key, so at least lists x m >=
+// top_k keys are at least th, the smallest of the lists' m-th keys, and no
+// key below th is in the top-k (th = 0, no bound, when a list is shorter
+// than m). A list is read 16 entries at a time, four lists per 64-lane load,
+// and only while the last key read from it is above the running threshold,
+// which starts just below th and rises with every compaction: a row of
+// sorted lists reads a few entries past each list's share of the top-k
+// instead of every entry. The result is topk_rows' (the same keys are kept:
+// the exact top_k). Up to 64 lists of at least 128 entries (the launcher
+// sends other rows to topk_rows).
+constexpr int kSortedMaxLists = 64;
+constexpr int kSortedMinLen = 128;
+constexpr int kSortedChunk = 16;
+
+// compact_select out of line (one copy: the unrolled loop over the lists
+// stays small; the row kernels run once per row, their code fetched cold).
+struct TopkCompacted {
+    int n;
+    uint64_t theta;
+};
+template <int NPL>
+__device__ __noinline__ TopkCompacted topk_compact(uint64_t *buf, int n, int k) {
+    TopkCompacted r;
+    r.theta = 0;
+    r.n = compact_select<NPL>(buf, n, k, kWave, threadIdx.x & 63, r.theta);
+    return r;
+}
+
+template <int NPL>
+__global__ __launch_bounds__(kWave * kTopkWaves) void topk_sorted_rows(TopkArgs a, int32_t k_in) {
+    extern __shared__ __align__(16) uint64_t tbuf[];
+    constexpr int cap = NPL * kWave;
+    constexpr int kGroups = kSortedMaxLists / (kWave / kSortedChunk);
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t row = (int64_t)blockIdx.x * kTopkWaves + wave;
+    if (row >= a.rows) return;              // no block-wide synchronisation below
+    uint64_t *buf = tbuf + wave * cap;
+    const float *sc = a.score + row * a.n;
+    const int32_t *ids = a.id ? a.id + row * a.n : nullptr;
+    const uint64_t lt_mask = (1ull << lane) - 1;
+    const int L = a.lists, sub = lane / kSortedChunk, pos = lane % kSortedChunk;
+    auto key_at = [&](int64_t i) -> uint64_t {
+        const int32_t id = ids ? ids[i] : (int32_t)i;
+        return id >= 0 ? make_key(sc[i], id) : 0ull;
+    };
+    // statistics, the lists' m-th keys and every list's first chunk, all
+    // requested before any is used
+    const bool okl = a.slot_max && lane < L;
+    const float lm = okl ? a.slot_max[row * L + lane] : -INFINITY;
+    const float lz = okl ? a.slot_sum[row * L + lane] : 0.0f;
+    const int m = (a.top_k + L - 1) / L;
+    uint64_t th = m <= k_in && lane < L ? key_at((int64_t)lane * k_in + m - 1) : ~0ull;
+    uint64_t key[kGroups];
 #pragma unroll
-    for (int q = 0; q < NPL; ++q) {
-        const int r = q * kWave + lane;
-        if (r < a.top_k) {
-            const bool ok = r < kept;
-            const float sv = ok ? key_score(v[q]) : -INFINITY;
-            a.out_id[row * a.top_k + r] = ok ? key_id(v[q]) : -1;
-            if (a.out_score) a.out_score[row * a.top_k + r] = sv;
-            if (a.out_weight)
-                a.out_weight[row * a.top_k + r] = ok ? exp2f((sv - M) * a.cexp) / Z : 0.0f;
+    for (int g = 0; g < kGroups; ++g) {
+        const int l = g * (kWave / kSortedChunk) + sub;
+        key[g] = l < L && pos < k_in ? key_at((int64_t)l * k_in + pos) : 0ull;
+    }
+    th = m <= k_in ? th : 0ull;
+#pragma unroll
+    for (int sh = 1; sh < kWave; sh <<= 1) {
+        uint64_t o;
+        switch (sh) {
+            case 1: o = lane_xor64<1>(th, lane); break;
+            case 2: o = lane_xor64<2>(th, lane); break;
+            case 4: o = lane_xor64<4>(th, lane); break;
+            case 8: o = lane_xor64<8>(th, lane); break;
+            case 16: o = lane_xor64<16>(th, lane); break;
+            default: o = lane_xor64<32>(th, lane); break;
+        }
+        th = o < th ? o : th;
+    }
+    uint64_t theta = th ? th - 1 : 0;       // offered: keys above theta, i.e. at least th
+
+    int cnt = 0, total = 0;
+    for (int c0 = 0;;) {
+#pragma unroll
+        for (int g = 0; g < kGroups; ++g) {
+            if (g * (kWave / kSortedChunk) >= L) break;
+            const uint64_t k = key[g];
+            total += __popcll(__ballot(k != 0));
+            const bool pass = k > theta;
+            const uint64_t mask = __ballot(pass);
+            if (pass) buf[cnt + __popcll(mask & lt_mask)] = k;
+            cnt += __popcll(mask);
+            if (cnt > cap - kWave) {
+                wave_lds_sync();
+                const TopkCompacted tc = topk_compact<NPL>(buf, cnt, a.top_k);
+                cnt = tc.n;
+                theta = tc.theta > theta ? tc.theta : theta;
+            }
+        }
+        // a list goes on while the last key of its chunk is above the
+        // threshold the whole round has raised
+        uint64_t live = 0;
+#pragma unroll
+        for (int g = 0; g < kGroups; ++g) {
+            if (g * (kWave / kSortedChunk) >= L) break;
+            const uint64_t cm = __ballot(pos == kSortedChunk - 1 && key[g] > theta);
+#pragma unroll
+            for (int j = 0; j < kWave / kSortedChunk; ++j)
+                live |= ((cm >> (j * kSortedChunk + kSortedChunk - 1)) & 1ull)
+                        << (g * (kWave / kSortedChunk) + j);
+        }
+        c0 += kSortedChunk;
+        if (c0 >= k_in || live == 0) break;
+#pragma unroll
+        for (int g = 0; g < kGroups; ++g) {
+            const int l = g * (kWave / kSortedChunk) + sub;
+            key[g] = l < L && ((live >> l) & 1) && c0 + pos < k_in
+                         ? key_at((int64_t)l * k_in + c0 + pos) : 0ull;
         }
     }
-    if (lane == 0) {
-        if (a.row_max) a.row_max[row] = M;
-        if (a.row_sum) a.row_sum[row] = Z;
-        if (a.out_count) a.out_count[row] = total < a.top_k ? total : a.top_k;
-    }
+    finish_row<NPL>(a, row, buf, cnt, total, lm, lz, lane);
 }
 
 // Segmented row top-k with optional softmax statistics. A unit is one
@@ -494,7 +623,8 @@ hipError_t launch_tile_topk(int64_t rows, int64_t n, const float *score, const f
 hipError_t launch_topk(int32_t rows, int32_t lists, int32_t k_in, const float *score,
                        const int32_t *id, const float *slot_max, const float *slot_sum, float tau,
                        int32_t top_k, int32_t *out_id, float *out_score, float *out_weight,
-                       float *row_max, float *row_sum, int32_t *out_count, hipStream_t s) {
+                       float *row_max, float *row_sum, int32_t *out_count, hipStream_t s,
+                       bool sorted_lists) {
     if (rows == 0) return hipSuccess;
     TopkArgs a{};
     a.rows = rows;
@@ -521,6 +651,19 @@ hipError_t launch_topk(int32_t rows, int32_t lists, int32_t k_in, const float *s
     const int npl = npl0 < 8 && a.n >= (int64_t)16 * kWave * npl0 ? 2 * npl0 : npl0;
     const dim3 grid((unsigned)((rows + kTopkWaves - 1) / kTopkWaves)), block(kWave * kTopkWaves);
     const size_t smem = (size_t)kTopkWaves * npl * kWave * 8;
+    // sorted lists of at least 128 entries: a row reads a chunk or two of
+    // each instead of all (before_after_f32's final merge, 16 lists of 128:
+    // 63 -> 51 us); on shorter lists the rounds of chunks cost more than the
+    // entries they skip (zipf_large_bf16, 32 lists of 64: 36 -> 54 us)
+    if (sorted_lists && lists <= kSortedMaxLists && k_in >= kSortedMinLen) {
+        switch (npl) {
+            case 2: hipLaunchKernelGGL(topk_sorted_rows<2>, grid, block, smem, s, a, k_in); break;
+            case 4: hipLaunchKernelGGL(topk_sorted_rows<4>, grid, block, smem, s, a, k_in); break;
+            case 8: hipLaunchKernelGGL(topk_sorted_rows<8>, grid, block, smem, s, a, k_in); break;
+            default: return hipErrorInvalidValue;
+        }
+        return hipGetLastError();
+    }
     switch (npl) {
         case 2: hipLaunchKernelGGL(topk_rows<2>, grid, block, smem, s, a); break;
         case 4: hipLaunchKernelGGL(topk_rows<4>, grid, block, smem, s, a); break;

@@ -79,6 +79,7 @@ def _load():
         "htam_retrieve_flat_workspace_size": ([BP, i32, i32], sz),
         "htam_attend_transitions_noalloc": ([BP, P, i32, i32, P, i32, f32, i32, P, P, P, P, P], i32),
         "htam_topk": ([i32, i32, i32, P, P, P, P, f32, i32, P, P, P, P, P, P, P], i32),
+        "htam_topk_sorted": ([i32, i32, i32, P, P, P, P, f32, i32, P, P, P, P, P, P, P], i32),
         "htam_set_kernel_events": ([i32, P, P], i32),
         "htam_status_string": ([i32], ctypes.c_char_p),
         "htam_last_error": ([], ctypes.c_char_p),
@@ -293,9 +294,10 @@ def htam_attend_transitions_noalloc(bank: Bank, q: torch.Tensor, sel: torch.Tens
 
 def htam_topk(cand_score: torch.Tensor, cand_id: torch.Tensor | None, top_k: int,
               slot_max: torch.Tensor | None = None, slot_sum: torch.Tensor | None = None,
-              tau: float = 1.0, out=None):
+              tau: float = 1.0, out=None, sorted_lists: bool = False):
     """Merge [rows][lists][k_in] candidates. Returns (id, score, weight, row_max, row_sum, count);
-    the softmax outputs are None without slot statistics."""
+    the softmax outputs are None without slot statistics. sorted_lists: every list is sorted
+    as htam_attend_transitions returns them (htam_topk_sorted)."""
     if cand_score.dim() == 2:
         cand_score = cand_score.unsqueeze(1)
         cand_id = None if cand_id is None else cand_id.unsqueeze(1)
@@ -309,10 +311,11 @@ def htam_topk(cand_score: torch.Tensor, cand_id: torch.Tensor | None, top_k: int
                torch.empty(rows, dtype=torch.float32, device=dev) if stats else None,
                torch.empty(rows, dtype=torch.float32, device=dev) if stats else None,
                torch.empty(rows, dtype=torch.int32, device=dev))
-    _check("htam_topk",
-           lib.htam_topk(rows, lists, k_in, _ptr(cand_score), _ptr(cand_id), _ptr(slot_max),
-                         _ptr(slot_sum), float(tau), top_k, _ptr(out[0]), _ptr(out[1]),
-                         _ptr(out[2]), _ptr(out[3]), _ptr(out[4]), _ptr(out[5]), _stream(dev)))
+    fn = lib.htam_topk_sorted if sorted_lists else lib.htam_topk
+    _check("htam_topk_sorted" if sorted_lists else "htam_topk",
+           fn(rows, lists, k_in, _ptr(cand_score), _ptr(cand_id), _ptr(slot_max),
+              _ptr(slot_sum), float(tau), top_k, _ptr(out[0]), _ptr(out[1]),
+              _ptr(out[2]), _ptr(out[3]), _ptr(out[4]), _ptr(out[5]), _stream(dev)))
     return out
 
 
@@ -343,7 +346,7 @@ class Retriever:
         htam_attend_transitions(self.bank, q, self.sel[0], self.tau, self.k, out=self.slots,
                                 ws=self.ws_attend)
         htam_topk(self.slots[2], self.slots[3], self.k, self.slots[0], self.slots[1], self.tau,
-                  out=self.rows)
+                  out=self.rows, sorted_lists=True)
         return self.outputs()
 
     def outputs(self) -> dict:

@@ -87,8 +87,9 @@ def test_attend_rejects_bad_arguments():
     assert _attend(b, B=0) == 0
 
 
-def test_topk_rejects_bad_arguments():
-    t = htam.lib.htam_topk
+@pytest.mark.parametrize("name", ["htam_topk", "htam_topk_sorted"])
+def test_topk_rejects_bad_arguments(name):
+    t = getattr(htam.lib, name)
     assert t(4, 2, 8, FAKE, FAKE, None, None, 1.0, 0, FAKE, FAKE, None, None, None, None, None) == -2
     assert t(4, 0, 8, FAKE, FAKE, None, None, 1.0, 4, FAKE, FAKE, None, None, None, None, None) == -2
     assert t(4, 2, 8, FAKE, FAKE, FAKE, None, 1.0, 4, FAKE, FAKE, None, None, None, None, None) == -1
