@@ -551,6 +551,104 @@ __global__ __launch_bounds__(kWave * kTopkWaves) void tile_topk(TileArgs a) {
     }
 }
 
+// The same selection for rows of 65 to 512 tiles, in about three memory
+// round trips instead of one per round of tile maxima and per four tiles:
+// every tile maximum is held in registers (eight per lane), T is the exact
+// top_k-th largest of them (a radix select, one ballot per register and
+// bit), so that hardly more than top_k tiles reach it; their ids are listed
+// in LDS and the tiles read sixteen at a time.
+constexpr int kHeldPer = 8;
+constexpr int kHeldTiles = kHeldPer * kWave;
+constexpr int kHeldBatch = 16;
+
+template <int NPL>
+__global__ __launch_bounds__(kWave * kTopkWaves) void tile_topk_held(TileArgs a) {
+    extern __shared__ __align__(16) uint64_t tbuf[];
+    constexpr int cap = NPL * kWave;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t row = (int64_t)blockIdx.x * kTopkWaves + wave;
+    if (row >= a.rows) return;              // no block-wide synchronisation below
+    uint64_t *buf = tbuf + wave * cap;
+    int32_t *list = reinterpret_cast<int32_t *>(tbuf + kTopkWaves * cap) + wave * kHeldTiles;
+    const uint64_t lt_mask = (1ull << lane) - 1;
+    const float *tm = a.tmax + row * a.n_tile;
+    const float *sc = a.score + row * a.n;
+    const int R = (a.n_tile + kWave - 1) / kWave;        // registers in use, at most kHeldPer
+    uint32_t o[kHeldPer];                                // ordered tile maxima, 0: none
+#pragma unroll
+    for (int r = 0; r < kHeldPer; ++r) {
+        const int t = r * kWave + lane;
+        const float m = r < R && t < a.n_tile ? tm[t] : -INFINITY;
+        o[r] = m == -INFINITY ? 0u : ord_of(m);
+    }
+    uint32_t th = 0;                                     // the top_k-th largest (0: fewer tiles)
+    for (int bit = 31; bit >= 0; --bit) {
+        const uint32_t cand = th | (1u << bit);
+        int c = 0;
+#pragma unroll
+        for (int r = 0; r < kHeldPer; ++r)
+            if (r < R) c += __popcll(__ballot(o[r] >= cand));
+        if (c >= a.top_k) th = cand;
+    }
+    const float T = th ? score_of_ord(th) : -INFINITY;
+    const uint32_t lo = th ? th : 1u;
+    int n_list = 0;
+#pragma unroll
+    for (int r = 0; r < kHeldPer; ++r) {
+        if (r < R) {
+            const bool q = o[r] >= lo;
+            const uint64_t m = __ballot(q);
+            if (q) list[n_list + __popcll(m & lt_mask)] = r * kWave + lane;
+            n_list += __popcll(m);
+        }
+    }
+    wave_lds_sync();
+
+    int cnt = 0;
+    uint64_t theta = 0;
+    for (int b0 = 0; b0 < n_list; b0 += kHeldBatch) {
+        int tile[kHeldBatch];
+        float v[kHeldBatch];
+#pragma unroll
+        for (int j = 0; j < kHeldBatch; ++j) tile[j] = b0 + j < n_list ? list[b0 + j] : -1;
+#pragma unroll
+        for (int j = 0; j < kHeldBatch; ++j) {           // every load in flight at once
+            const int64_t c = (int64_t)(tile[j] < 0 ? tile[0] : tile[j]) * kTileCols + lane;
+            v[j] = sc[c < a.n ? c : a.n - 1];
+        }
+#pragma unroll
+        for (int j = 0; j < kHeldBatch; ++j) {
+            const int64_t c = (int64_t)tile[j] * kTileCols + lane;
+            const bool ok = tile[j] >= 0 && c < a.n && v[j] >= T;
+            const uint64_t key = ok ? make_key(v[j], (int32_t)c) : 0;
+            const bool pass = key > theta;
+            const uint64_t mask = __ballot(pass);
+            if (pass) buf[cnt + __popcll(mask & lt_mask)] = key;
+            cnt += __popcll(mask);
+            if (cnt > cap - kWave) {
+                wave_lds_sync();
+                const TopkCompacted tc = topk_compact<NPL>(buf, cnt, a.top_k);
+                cnt = tc.n;
+                theta = tc.theta > theta ? tc.theta : theta;
+            }
+        }
+    }
+    wave_lds_sync();
+    uint64_t w[NPL];
+    sort_buffer<NPL>(buf, cnt, w, lane);
+    const int kept = cnt < a.top_k ? cnt : a.top_k;
+#pragma unroll
+    for (int q = 0; q < NPL; ++q) {
+        const int r = q * kWave + lane;
+        if (r < a.top_k) {
+            const bool ok = r < kept;
+            a.out_id[row * a.top_k + r] = ok ? key_id(w[q]) : -1;
+            a.out_score[row * a.top_k + r] = ok ? key_score(w[q]) : -INFINITY;
+        }
+    }
+}
+
 }  // namespace
 
 int32_t seg_topk_cols() { return kSegCols; }
@@ -613,6 +711,18 @@ hipError_t launch_tile_topk(int64_t rows, int64_t n, const float *score, const f
     // buffers of top_k + 64 keys at least (compaction when fewer than 64 slots remain)
     const int npl = next_pow2(top_k + kWave) / kWave;
     const size_t smem = (size_t)kTopkWaves * npl * kWave * 8;
+    // more tiles than lanes: a lane's maximum merges several tiles and its
+    // bound admits more tiles than the exact one (before_after_f32, 256
+    // tiles: 32 -> 28 us); up to 64 tiles both bounds are the same and the
+    // exact one costs its radix select (zipf_large_bf16: 16.5 -> 19 us)
+    if (a.n_tile > kWave && a.n_tile <= kHeldTiles) {
+        const size_t sm2 = smem + (size_t)kTopkWaves * kHeldTiles * 4;   // and the tile lists
+        switch (npl) {
+            case 2: hipLaunchKernelGGL(tile_topk_held<2>, grid, block, sm2, s, a); break;
+            default: return hipErrorInvalidValue;
+        }
+        return hipGetLastError();
+    }
     switch (npl) {
         case 2: hipLaunchKernelGGL(tile_topk<2>, grid, block, smem, s, a); break;
         default: return hipErrorInvalidValue;
