@@ -606,13 +606,25 @@ __device__ __forceinline__ void pass_generic(const FineArgs &a, const FineSmem &
 // ---- LDS pass: query fragments staged in LDS, key fragments prefetched -------
 // A key fragment (8 elements of one row) as it is loaded: bf16 storage is used
 // as is, fp32 storage is rounded to bf16 when the fragment is consumed.
+// Key loads are non-temporal (streaming cache policy): a call reads each key
+// row once, and HBM delivers such reads faster (a read probe of the stream's
+// tiled units: 6.23 -> 6.70 TB/s; the stream 5.69 -> 5.36 ms on
+// before_after_f32, 3.20 -> 3.02 ms on zipf_large_bf16).
+typedef unsigned int ntu32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 nt_load16(const void *p) {
+    return __builtin_bit_cast(uint4, __builtin_nontemporal_load(reinterpret_cast<const ntu32x4 *>(p)));
+}
+__device__ __forceinline__ float4 nt_load16f(const void *p) {
+    return __builtin_bit_cast(float4, __builtin_nontemporal_load(reinterpret_cast<const ntu32x4 *>(p)));
+}
+
 template <typename KT>
 struct AFrag;
 template <>
 struct AFrag<__bf16> {
     static constexpr int U = 16;   // k-steps per load unit (one-block-per-CU kernels): 16 x 16 B per lane
     uint4 v;
-    __device__ __forceinline__ void load(const __bf16 *p) { v = *reinterpret_cast<const uint4 *>(p); }
+    __device__ __forceinline__ void load(const __bf16 *p) { v = nt_load16(p); }
     // in the tiled copy a fragment is one 16-byte piece
     __device__ __forceinline__ void load_tiled(const __bf16 *p) { load(p); }
     __device__ __forceinline__ bf16x8_t bf16() const { return __builtin_bit_cast(bf16x8_t, v); }
@@ -622,13 +634,14 @@ struct AFrag<float> {
     static constexpr int U = 8;    // k-steps per load unit: 8 x 32 B per lane
     float4 lo, hi;
     __device__ __forceinline__ void load(const float *p) {
-        lo = reinterpret_cast<const float4 *>(p)[0];
-        hi = reinterpret_cast<const float4 *>(p)[1];
+        lo = nt_load16f(p);
+        hi = nt_load16f(p + 4);
     }
-    // in the tiled copy the fragment's second piece is 64 pieces after the first
+    // in the tiled copy the fragment's second piece is 64 pieces (256 floats)
+    // after the first
     __device__ __forceinline__ void load_tiled(const float *p) {
-        lo = reinterpret_cast<const float4 *>(p)[0];
-        hi = reinterpret_cast<const float4 *>(p)[64];
+        lo = nt_load16f(p);
+        hi = nt_load16f(p + 256);
     }
     __device__ __forceinline__ bf16x8_t bf16() const {
         bf16x8_t r;
