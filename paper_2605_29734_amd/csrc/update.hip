@@ -47,6 +47,9 @@ __global__ void merge_offsets(const int64_t *off_a, const int64_t *off_b, int32_
 // Rows of one source bank to their merged positions: row r of cluster g goes
 // to r + shift[g + step] (step 0: the main bank, shift = delta offsets;
 // step 1: the delta bank, shift = main offsets).
+typedef unsigned int ucopy_t __attribute__((ext_vector_type(4)));
+constexpr int kCopyPer = 16;
+
 __global__ __launch_bounds__(256) void merge_rows(const uint4 *__restrict__ keys,
                                                   const int32_t *__restrict__ ids,
                                                   const int64_t *__restrict__ off, int64_t n,
@@ -70,11 +73,29 @@ __global__ __launch_bounds__(256) void merge_rows(const uint4 *__restrict__ keys
             dst = r + shift[lo + step];
             ids_out[dst] = ids[r];
         }
+        // the wave's rows as one run of 16-byte elements, 16 per lane in
+        // flight (element e: row e / vpr, its destination row from the lane
+        // that holds it), with non-temporal loads and stores: each byte is
+        // moved once (mixture_bf16's bank and delta: 4.46 -> 4.94 TB/s,
+        // against one row at a time with ordinary loads)
         const int rows = (int)min((int64_t)kWave, n - r0);
-        for (int i = 0; i < rows; ++i) {
-            const int64_t di = __shfl(dst, i);
-            for (int v = lane; v < vpr; v += kWave)
-                keys_out[di * vpr + v] = keys[(r0 + i) * vpr + v];
+        const int32_t total = rows * vpr;
+        for (int32_t e0 = 0; e0 < total; e0 += kCopyPer * kWave) {
+            ucopy_t x[kCopyPer];
+            int64_t to[kCopyPer];
+#pragma unroll
+            for (int j = 0; j < kCopyPer; ++j) {
+                const int32_t e = e0 + j * kWave + lane;
+                const uint32_t ec = (uint32_t)(e < total ? e : total - 1);
+                const uint32_t i = ec / (uint32_t)vpr, v = ec - i * (uint32_t)vpr;
+                x[j] = __builtin_nontemporal_load(
+                    reinterpret_cast<const ucopy_t *>(keys + (r0 + i) * vpr + v));
+                to[j] = __shfl(dst, (int)i) * vpr + v;
+            }
+#pragma unroll
+            for (int j = 0; j < kCopyPer; ++j)
+                if (e0 + j * kWave + lane < total)
+                    __builtin_nontemporal_store(x[j], reinterpret_cast<ucopy_t *>(keys_out + to[j]));
         }
     }
 }
