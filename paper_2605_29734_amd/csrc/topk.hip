@@ -212,18 +212,19 @@ __global__ __launch_bounds__(kWave * kTopkWaves) void topk_sorted_rows(TopkArgs 
     for (int c0 = 0;;) {
 #pragma unroll
         for (int g = 0; g < kGroups; ++g) {
-            if (g * (kWave / kSortedChunk) >= L) break;
-            const uint64_t k = key[g];
-            total += __popcll(__ballot(k != 0));
-            const bool pass = k > theta;
-            const uint64_t mask = __ballot(pass);
-            if (pass) buf[cnt + __popcll(mask & lt_mask)] = k;
-            cnt += __popcll(mask);
-            if (cnt > cap - kWave) {
-                wave_lds_sync();
-                const TopkCompacted tc = topk_compact<NPL>(buf, cnt, a.top_k);
-                cnt = tc.n;
-                theta = tc.theta > theta ? tc.theta : theta;
+            if (g * (kWave / kSortedChunk) < L) {       // groups past the lists: nothing
+                const uint64_t k = key[g];
+                total += __popcll(__ballot(k != 0));
+                const bool pass = k > theta;
+                const uint64_t mask = __ballot(pass);
+                if (pass) buf[cnt + __popcll(mask & lt_mask)] = k;
+                cnt += __popcll(mask);
+                if (cnt > cap - kWave) {
+                    wave_lds_sync();
+                    const TopkCompacted tc = topk_compact<NPL>(buf, cnt, a.top_k);
+                    cnt = tc.n;
+                    theta = tc.theta > theta ? tc.theta : theta;
+                }
             }
         }
         // a list goes on while the last key of its chunk is above the
@@ -231,12 +232,13 @@ __global__ __launch_bounds__(kWave * kTopkWaves) void topk_sorted_rows(TopkArgs 
         uint64_t live = 0;
 #pragma unroll
         for (int g = 0; g < kGroups; ++g) {
-            if (g * (kWave / kSortedChunk) >= L) break;
-            const uint64_t cm = __ballot(pos == kSortedChunk - 1 && key[g] > theta);
+            if (g * (kWave / kSortedChunk) < L) {
+                const uint64_t cm = __ballot(pos == kSortedChunk - 1 && key[g] > theta);
 #pragma unroll
-            for (int j = 0; j < kWave / kSortedChunk; ++j)
-                live |= ((cm >> (j * kSortedChunk + kSortedChunk - 1)) & 1ull)
-                        << (g * (kWave / kSortedChunk) + j);
+                for (int j = 0; j < kWave / kSortedChunk; ++j)
+                    live |= ((cm >> (j * kSortedChunk + kSortedChunk - 1)) & 1ull)
+                            << (g * (kWave / kSortedChunk) + j);
+            }
         }
         c0 += kSortedChunk;
         if (c0 >= k_in || live == 0) break;
